@@ -1,0 +1,273 @@
+"""Benchmark: one GPU's share of a training step of the encoder-decoder.
+
+A step is one pass of the whole hot path over one synthetic batch: the
+forward pass of the 13 layers (fused ReLU), the loss-scaled L2 head
+gradient, the backward pass (kernel and input gradients, fused ReLU
+gradient) and, as each group of weight gradients completes, fusion-buffer
+pack, unscale with overflow check and unpack into fp32 master gradients
+(25 MiB groups). Inputs are resident in HBM before the timed region.
+
+value = algorithmic convolution flops of the step (3 passes x 13 layers,
+direct-convolution count, 5.528 TFLOP) / wall time of the step, in TFLOP/s.
+The JSON line also carries the roofline of the dominant kernel (timed with
+HIP events on its own stream inside the timed region), the gradient-path
+bandwidths and the CPU oracle timed on a bounded sample of the same work.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+MFMA_F16_PEAK_TFLOPS = 2500.0      # MI355X dense fp16 MFMA
+HBM_PEAK_GBPS = 8000.0             # MI355X HBM3E
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu", action="store_true",
+                    help="skip the CPU oracle baseline leg")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="approximate CPU work of the oracle sample")
+    ap.add_argument("--detail", default=None,
+                    help="write per-op timings (JSON) to this path")
+    return ap.parse_args()
+
+
+class TimedChain:
+    """Wraps Chain so every library call in a step records HIP events on the
+    stream it is launched on (the current stream)."""
+
+    def __init__(self, chain):
+        self.ch = chain
+        self.records = []   # (label, kernel, flops_or_bytes, ev0, ev1)
+
+    def _ev(self):
+        import torch
+        return torch.cuda.Event(enable_timing=True)
+
+    def call(self, label, kernel, work, fn, *a, **k):
+        e0, e1 = self._ev(), self._ev()
+        e0.record()
+        fn(*a, **k)
+        e1.record()
+        self.records.append((label, kernel, work, e0, e1))
+
+    def step(self, target):
+        import paper_1909_11150_amd as fg
+        from paper_1909_11150_amd import fcn
+        ch = self.ch
+        # forward
+        for i, L in enumerate(ch.layers):
+            epi = fg.EPI_RELU if L.relu else fg.EPI_NONE
+            d = fcn.fwd_desc(L)
+            if L.kind == "conv":
+                self.call(f"{L.name}.fwd", fg.kernel_name(d, fg.OP_FWD), L.flops,
+                          fg.conv2d_fwd, d, ch.acts[i], ch.w[i], ch.acts[i + 1], epi)
+            else:
+                self.call(f"{L.name}.fwd", fg.kernel_name(d, fg.OP_CONVT), L.flops,
+                          fg.conv_transpose2d_fwd, d, ch.acts[i], ch.w[i],
+                          ch.acts[i + 1], epi)
+        y = ch.acts[-1]
+        self.call("head_grad", "head_grad_kernel", y.numel() * 6, fg.l2_head_grad,
+                  y, target, 2.0 * ch.loss_scale / y.numel(), ch.g[-1])
+        ch.flags.zero_()
+        for i in reversed(range(len(ch.layers))):
+            L = ch.layers[i]
+            dy = ch.g[i + 1]
+            gate = i > 0 and ch.layers[i - 1].relu
+            epi = fg.EPI_GATE if gate else fg.EPI_NONE
+            gt = ch.acts[i] if gate else None
+            if L.kind == "conv":
+                d = fcn.fwd_desc(L)
+                self.call(f"{L.name}.dW", fg.kernel_name(d, fg.OP_BWD_WEIGHT), L.flops,
+                          fg.conv2d_bwd_weight, d, ch.acts[i], dy, ch.dw[i], ch.ws)
+                self.call(f"{L.name}.dx", fg.kernel_name(d, fg.OP_BWD_DATA), L.flops,
+                          fg.conv2d_bwd_data, d, dy, ch.w[i], ch.g[i], epi, gt)
+            else:
+                dd = fcn.convt_dx_desc(L)
+                self.call(f"{L.name}.dW", fg.kernel_name(dd, fg.OP_BWD_WEIGHT), L.flops,
+                          fg.conv2d_bwd_weight, dd, dy, ch.acts[i], ch.dw[i], ch.ws)
+                self.call(f"{L.name}.dx", fg.kernel_name(dd, fg.OP_FWD), L.flops,
+                          fg.conv2d_fwd, dd, dy, ch.w[i], ch.g[i], epi, gt)
+            gi = ch._group_done_at.get(i)
+            if gi is not None:
+                g = ch.groups[gi]
+                n = g["numel"]
+                self.call(f"G{gi}.pack", "copy_pieces_kernel<2>", 4 * n,
+                          fg.grad_group_pack, [ch.dw[m] for m in g["members"]],
+                          g["offsets"], ch.gbuf16[gi])
+                self.call(f"G{gi}.unscale", "unscale_vec_kernel", 6 * n,
+                          fg.grad_unscale_check, ch.gbuf16[gi], 1.0 / ch.loss_scale,
+                          ch.gbuf32[gi], ch.flags[gi:gi + 1])
+                self.call(f"G{gi}.unpack", "copy_pieces_kernel<4>", 8 * n,
+                          fg.grad_group_unpack, ch.gbuf32[gi],
+                          [ch.master[m] for m in g["members"]], g["offsets"])
+
+
+def cpu_baseline(layers, seconds):
+    """Time the fp64 oracle on a bounded sample of the step's convolutions:
+    the same seeded full-size inputs, a random sample of output elements of
+    every layer's three passes, sized so the whole sample takes roughly
+    `seconds`. Reported as algorithmic TFLOP/s (flops per output element x
+    elements computed / time)."""
+    import oracle
+    threads = int(os.environ.get("OMP_NUM_THREADS", len(os.sched_getaffinity(0))))
+    rng = np.random.default_rng(123)
+    per_task = seconds / (3 * len(layers))
+    flops_done, t_total = 0.0, 0.0
+    for L in layers:
+        xs = np.maximum(rng.standard_normal(L.x_shape), 0.0)
+        ws = rng.standard_normal(L.w_shape)
+        dys = rng.standard_normal(L.y_shape)
+        ny = int(np.prod(L.y_shape))
+        nx = int(np.prod(L.x_shape))
+        nw = int(np.prod(L.w_shape))
+        if L.kind == "conv":
+            tasks = [
+                (ny, lambda i: oracle.conv2d_fwd_points(xs, ws, i, L.stride, L.pad)),
+                (nx, lambda i: oracle.conv2d_bwd_data_points(dys, ws, L.x_shape, i,
+                                                             L.stride, L.pad)),
+                (nw, lambda i: oracle.conv2d_bwd_weight_points(xs, dys, L.r, L.s, i,
+                                                               L.stride, L.pad))]
+        else:
+            tasks = [
+                (ny, lambda i: oracle.conv_transpose2d_fwd_points(xs, ws, i, 2, 1)),
+                (nx, lambda i: oracle.conv2d_fwd_points(dys, ws, i, 2, 1)),
+                (nw, lambda i: oracle.conv2d_bwd_weight_points(dys, xs, L.r, L.s, i,
+                                                               2, 1))]
+        for total, fn in tasks:
+            fpe = L.flops / total   # algorithmic flops per output element
+            probe = rng.choice(total, size=min(total, 16), replace=False)
+            t0 = time.perf_counter()
+            fn(probe)
+            dt = max(time.perf_counter() - t0, 1e-6)
+            k = int(min(total, max(16, 16 * per_task / dt)))
+            idx = rng.choice(total, size=k, replace=False)
+            t0 = time.perf_counter()
+            fn(idx)
+            t_total += time.perf_counter() - t0
+            flops_done += fpe * k
+        del xs, ws, dys
+    return {"value": flops_done / t_total / 1e12, "unit": "TFLOP/s",
+            "cores": threads, "kind": "oracle",
+            "sample": (f"fp64 oracle on random output elements of all 39 conv "
+                       f"passes of the full network (full-size seeded inputs), "
+                       f"{flops_done / 1e9:.1f} GFLOP algorithmic in {t_total:.1f} s")}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; "
+                          "--gpus must be 1 (multi-GPU sharding is design-only)"}))
+        sys.exit(2)
+    import torch
+
+    import synth
+    from paper_1909_11150_amd.fcn import Chain
+
+    wl = synth.fcn()
+    layers = wl.layers
+    ch = Chain(layers, wl.weights, wl.x, loss_scale=synth.LOSS_SCALE,
+               group_cap_bytes=synth.GROUP_CAP_BYTES)
+    target = torch.from_numpy(wl.target).cuda()
+    torch.cuda.synchronize()
+    tc = TimedChain(ch)
+    for _ in range(args.warmup):
+        tc.step(target)
+    torch.cuda.synchronize()
+    tc.records.clear()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record()
+    for _ in range(args.steps):
+        tc.step(target)
+    ev1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = ev0.elapsed_time(ev1) / args.steps
+    flops_step = sum(3 * L.flops for L in layers)
+    value = flops_step / (ms_step * 1e-3) / 1e12
+
+    # per-kernel aggregation of the event timings
+    per_kernel, per_op = {}, {}
+    for label, kern, work, e0, e1 in tc.records:
+        t = e0.elapsed_time(e1)
+        k = per_kernel.setdefault(kern, [0, 0.0, 0.0])
+        k[0] += 1
+        k[1] += t
+        k[2] += work
+        o = per_op.setdefault(label, [0, 0.0, work])
+        o[0] += 1
+        o[1] += t
+    conv_kernels = {k: v for k, v in per_kernel.items()
+                    if k.startswith(("data_conv", "wgrad", "head_fwd", "head_bwd",
+                                     "head_wgrad"))}
+    conv_ms = sum(v[1] for v in conv_kernels.values()) / args.steps
+    dom = max((k for k in conv_kernels if k.startswith("data_conv")),
+              key=lambda k: conv_kernels[k][1])
+    n, tsum, fsum = conv_kernels[dom]
+    avg_s = tsum / n * 1e-3
+    achieved = fsum / n / avg_s / 1e12
+    roof = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),
+            "peak": MFMA_F16_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(achieved / MFMA_F16_PEAK_TFLOPS, 4),
+            "avg_launch_us": round(avg_s * 1e6, 2), "launches_per_step": n // args.steps,
+            "traffic": None}
+
+    def bw(name):
+        v = per_kernel.get(name)
+        return None if not v else round(v[2] / (v[1] * 1e-3) / 1e9, 1)
+
+    out = {
+        "metric": "fp16 conv fwd+bwd TFLOP/s per MI355X (% MFMA peak); grad pack GB/s",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {"workload": "fcn encoder-decoder step, N=4 x 256x256 x 256ch input, "
+                               "13 layers (99,483,904 weights), L2 head, loss scale 2^15, "
+                               "25 MiB gradient groups (9)",
+                   "global_batch": 4, "conv_tflop_per_step": round(flops_step / 1e12, 4)},
+        "mfma_peak_frac": round(value / MFMA_F16_PEAK_TFLOPS, 4),
+        "conv_kernels_tflops": round(flops_step / (conv_ms * 1e-3) / 1e12, 2),
+        "grad_pack_GBps": bw("copy_pieces_kernel<2>"),
+        "grad_unscale_GBps": bw("unscale_vec_kernel"),
+        "grad_unpack_GBps": bw("copy_pieces_kernel<4>"),
+        "wall_s_timed": round(wall, 3),
+        "roofline": roof,
+    }
+    if args.detail:
+        det = {"per_kernel": {k: {"launches": v[0], "ms_total": v[1], "work": v[2]}
+                              for k, v in per_kernel.items()},
+               "per_op_ms": {k: v[1] / v[0] for k, v in per_op.items()},
+               "per_op_tflops_or_gbps": {k: v[2] / (v[1] / v[0] * 1e-3) / 1e12
+                                         for k, v in per_op.items()}}
+        with open(args.detail, "w") as f:
+            json.dump(det, f, indent=1)
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(layers, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

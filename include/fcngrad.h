@@ -1,0 +1,235 @@
+/*
+ * fcngrad — one GPU's share of a data-parallel training step of a fully
+ * convolutional encoder-decoder in fp16 (Laanait et al., "Exascale Deep
+ * Learning for Scientific Inverse Problems", arXiv 1909.11150), for AMD
+ * Instinct MI355X (gfx950).
+ *
+ * The step has two halves:
+ *   1. the three convolution passes of every layer — forward, gradient with
+ *      respect to the kernel, gradient with respect to the input (Section
+ *      5.2: the passes counted by the factor 3 in the Sustained and Peak
+ *      performance equations; the operation count of each is the
+ *      direct-convolution count OPS_conv of that section) — plus the
+ *      transposed convolution of the decoder (Section 6.2, Figure workflow
+ *      (B): encoder-decoder network) and the ReLU after each layer (Section
+ *      6.2, Neural Network Architecture), fused into the convolutions;
+ *   2. the gradient path between back-propagation and the optimizer: the
+ *      weight gradients are fused into contiguous group buffers (Section
+ *      4.2, Grouping: only complete groups are fused into one message), the
+ *      loss scale is removed and overflow is detected (Section 6.2, Model
+ *      Implementation: loss scaling keeps values inside the float16 range),
+ *      and the fp32 gradients are scattered back to per-tensor buffers.
+ * On more than one GPU a sum-allreduce of each packed group sits between
+ * grad_group_pack and grad_unscale_check; this library is the per-GPU part.
+ *
+ * Conventions (all entry points)
+ *   - fp16 data is passed as uint16_t bit patterns (IEEE binary16).
+ *     Activations are NHWC. Convolution weights are KRSC (out channel,
+ *     kernel row, kernel column, in channel). Transposed-convolution weights
+ *     are C_in x R x S x C_out. Convolution is cross-correlation (no flip);
+ *     padding is symmetric zero padding; forward output size is
+ *     P = (H + 2*pad_h - R)/stride_h + 1 (floor), likewise Q.
+ *   - Every device pointer (x, w, y, gate, ws, group buffers, flags, segment
+ *     targets) is owned by the caller. The library never allocates or frees
+ *     device memory and keeps no state between calls.
+ *   - GPU work is enqueued on `stream` (0 = the null stream) and the call
+ *     returns without synchronising; results are valid once the caller has
+ *     synchronised the stream. Device faults surface at that synchronisation.
+ *   - Arguments are validated on the host before any HIP call:
+ *       FG_EINVAL        null pointer, non-positive size, empty output,
+ *                        gate missing for FG_EPI_GATE, an output aliasing an
+ *                        input, an unknown enum value;
+ *       FG_EUNSUPPORTED  a valid shape outside what the kernels implement
+ *                        (listed per call);
+ *       FG_EWORKSPACE    ws_bytes below fg_conv_workspace_bytes();
+ *       FG_ELAUNCH       the HIP runtime rejected a launch.
+ *     No exception crosses the interface. On any error nothing is launched
+ *     (FG_ELAUNCH: kernels launched before the failing one stay queued).
+ *   - Results are bit-reproducible for a fixed device, shape and input:
+ *     every sum is evaluated in a fixed order (no floating-point atomics).
+ *   - Tensor sizes must stay below 2^31 elements per tensor.
+ */
+#ifndef FCNGRAD_H
+#define FCNGRAD_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    FG_OK = 0,
+    FG_EINVAL = 1,
+    FG_EUNSUPPORTED = 2,
+    FG_EWORKSPACE = 3,
+    FG_ELAUNCH = 4
+} fg_status;
+
+/* Epilogue fused into the convolution's output.
+ *   FG_EPI_NONE  out = fp16(acc)
+ *   FG_EPI_RELU  out = fp16(acc > 0 ? acc : +0)          (forward ReLU)
+ *   FG_EPI_GATE  out = fp16(gate > 0 ? acc : +0)         (ReLU backward;
+ *                gate = the forward ReLU output at the same index, an fp16
+ *                tensor with the output's shape)
+ * acc is the fp32 accumulator; fp16() rounds to nearest-even with overflow
+ * to +-infinity (no saturation) and keeps subnormals. */
+typedef enum { FG_EPI_NONE = 0, FG_EPI_RELU = 1, FG_EPI_GATE = 2 } fg_epilogue;
+
+/* Shape of a convolution, always described by its forward direction:
+ *   n, h, w, c   the input image (NHWC); for the transposed convolution, its
+ *                (smaller) input with c = C_in;
+ *   k            output channels (transposed convolution: C_out);
+ *   r, s         kernel height and width;
+ *   stride_*, pad_*  stride and symmetric zero padding. */
+typedef struct {
+    int32_t n, h, w, c;
+    int32_t k, r, s;
+    int32_t stride_h, stride_w, pad_h, pad_w;
+} fg_conv_desc;
+
+/* One member of a gradient group: `ptr` is a device address (fp16 dW for
+ * pack, fp32 destination for unpack), `numel` its element count and
+ * `offset` the element offset of its first element inside the group. */
+typedef struct {
+    uint64_t ptr;
+    uint64_t numel;
+    uint64_t offset;
+} fg_segment;
+
+enum { FG_OP_FWD = 0, FG_OP_BWD_DATA = 1, FG_OP_BWD_WEIGHT = 2, FG_OP_CONVT = 3 };
+
+/* Maximum number of members in one pack / unpack call. */
+#define FG_MAX_SEGMENTS 64
+
+/* ---- convolution passes (Section 5.2, OPS_conv and the factor 3) -------- */
+
+/* Forward convolution: y[n,p,q,k] = epi(sum_{r,s,c} x~[n, p*sh-ph+r,
+ * q*sw-pw+s, c] * w[k,r,s,c]), x~ = x extended by zeros outside the image.
+ * x: n*h*w*c fp16; w_krsc: k*r*s*c fp16; y: n*P*Q*k fp16 (written);
+ * gate: n*P*Q*k fp16 for FG_EPI_GATE, else ignored (may be NULL).
+ * ws: device workspace of at least fg_conv_workspace_bytes(d, FG_OP_FWD)
+ * bytes (may be NULL when that is 0); its contents are scratch.
+ * FG_EUNSUPPORTED unless c % 8 == 0 and either k % 8 == 0, or k == 1 with a
+ * 1x1 stride-1 unpadded kernel. Kernel sizes up to 4x4 (at most 16 taps). */
+fg_status conv2d_fwd(const fg_conv_desc *d, const uint16_t *x,
+                     const uint16_t *w_krsc, uint16_t *y, fg_epilogue epi,
+                     const uint16_t *gate, void *ws, size_t ws_bytes,
+                     hipStream_t stream);
+
+/* Input gradient (adjoint of conv2d_fwd with respect to x):
+ * dx[n,h,w,c] = epi(sum over k and the taps (r,s) with h + ph - r = p*sh and
+ * w + pw - s = q*sw for some output position (p,q), of dy[n,p,q,k] *
+ * w[k,r,s,c]); zero where no term lands. dy: n*P*Q*k; dx: n*h*w*c written;
+ * gate: n*h*w*c for FG_EPI_GATE. Strided cases are evaluated per output
+ * phase (h mod sh, w mod sw) over the taps that reach it only.
+ * FG_EUNSUPPORTED unless c % 8 == 0 and (k % 8 == 0, or k == 1 with a 1x1
+ * stride-1 unpadded kernel). */
+fg_status conv2d_bwd_data(const fg_conv_desc *d, const uint16_t *dy,
+                          const uint16_t *w_krsc, uint16_t *dx,
+                          fg_epilogue epi, const uint16_t *gate, void *ws,
+                          size_t ws_bytes, hipStream_t stream);
+
+/* Kernel gradient: dw[k,r,s,c] = sum_{n,p,q} dy[n,p,q,k] *
+ * x~[n, p*sh-ph+r, q*sw-pw+s, c], accumulated in fp32 and rounded once to
+ * fp16. x: n*h*w*c; dy: n*P*Q*k; dw_krsc: k*r*s*c written. The reduction
+ * over n*P*Q may be split across workgroups (fp32 partials in ws, summed in
+ * a fixed order). FG_EUNSUPPORTED unless c % 8 == 0 and (k % 8 == 0, or
+ * k == 1 with a 1x1 stride-1 unpadded kernel). */
+fg_status conv2d_bwd_weight(const fg_conv_desc *d, const uint16_t *x,
+                            const uint16_t *dy, uint16_t *dw_krsc, void *ws,
+                            size_t ws_bytes, hipStream_t stream);
+
+/* Transposed convolution (decoder upsampling):
+ * y[n,o,u,k] = epi(sum over c and the taps (r,s) with o + ph - r = i*sh and
+ * u + pw - s = j*sw for an input position (i,j), of x[n,i,j,c] *
+ * w[c,r,s,k]). Output size (h-1)*sh - 2*ph + r by (w-1)*sw - 2*pw + s.
+ * x: n*h*w*c (c = C_in); w_crsk: c*r*s*k; y written; gate shaped like y.
+ * Its backward passes are conv2d_fwd (input gradient: dy convolved with
+ * w_crsk read as a KRSC weight with K = C_in, C = C_out) and
+ * conv2d_bwd_weight (x := dy, dy := x). FG_EUNSUPPORTED unless c % 8 == 0,
+ * k % 8 == 0 and the kernel is 4x4 with stride 2 and padding 1. */
+fg_status conv_transpose2d_fwd(const fg_conv_desc *d, const uint16_t *x,
+                               const uint16_t *w_crsk, uint16_t *y,
+                               fg_epilogue epi, const uint16_t *gate,
+                               void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* ---- gradient path (Section 4.2 Grouping; Section 6.2 loss scaling) ----- */
+
+/* Fusion-buffer copy-in: group[seg.offset + j] = src[j] (bit copy) for every
+ * segment, and every element of [0, group_numel) not covered by a segment
+ * is set to 0x0000. segs: host array of nseg (1..FG_MAX_SEGMENTS) fp16
+ * sources, read during the call only; segments must lie inside the group
+ * and must not overlap each other (FG_EINVAL). group: group_numel fp16. */
+fg_status grad_group_pack(const fg_segment *segs, int32_t nseg,
+                          uint16_t *group, uint64_t group_numel,
+                          hipStream_t stream);
+
+/* Loss-scale removal with overflow detection:
+ * out_f32[j] = fp32(value(group[j]) * inv_scale), one nearest-even rounding
+ * of the exact product, for j < numel; and *found_nonfinite is set to 1 if
+ * any group[j] has an all-ones exponent field (+-inf or NaN). The flag is
+ * only ever written with 1: the caller zeroes it before the step and may
+ * share one flag between several calls. */
+fg_status grad_unscale_check(const uint16_t *group, uint64_t numel,
+                             float inv_scale, float *out_f32,
+                             int32_t *found_nonfinite, hipStream_t stream);
+
+/* Fusion-buffer copy-out: dst[j] = group_f32[seg.offset + j] (bit copy) for
+ * every segment; seg.ptr is the fp32 destination. Same segment rules as
+ * grad_group_pack (group_numel bounds the offsets). */
+fg_status grad_group_unpack(const float *group_f32, uint64_t group_numel,
+                            const fg_segment *segs, int32_t nseg,
+                            hipStream_t stream);
+
+/* ---- network glue (Section 6.2, Model Implementation) -------------------- */
+
+/* Gradient of the loss-scaled mean squared error at the network output:
+ * dy[j] = fp16(scale * (y[j] - t[j])), evaluated in fp64 and rounded once
+ * to fp16 (nearest-even, overflow to infinity); for loss S * mean((y-t)^2)
+ * over numel outputs the caller passes scale = 2*S/numel. y fp16, t fp32. */
+fg_status l2_head_grad(const uint16_t *y, const float *t, uint64_t numel,
+                       double scale, uint16_t *dy, hipStream_t stream);
+
+/* Gradient through a ReLU where no convolution follows to fuse it into:
+ * out[j] = act[j] > 0 ? dy[j] : +0 (bit copy of dy when passed). */
+fg_status relu_backward(const uint16_t *dy, const uint16_t *act,
+                        uint64_t numel, uint16_t *out, hipStream_t stream);
+
+/* ---- host-only helpers (no device access) ------------------------------- */
+
+/* Workspace in bytes that the given pass needs for this shape (0 if none). */
+size_t fg_conv_workspace_bytes(const fg_conv_desc *d, int op);
+
+/* Output spatial size: transpose = 0 gives the forward P, Q; 1 gives the
+ * transposed convolution's output size. FG_EINVAL if it is not positive. */
+fg_status fg_conv_out_dims(const fg_conv_desc *d, int transpose, int32_t *p,
+                           int32_t *q);
+
+/* Group planner (Section 4.2, Grouping; Figure grouping). Tensors are given
+ * in backward-completion order (numel[i] elements of elem_bytes each). A
+ * tensor joins the open group at the next multiple of align_bytes unless
+ * its end would pass cap_bytes, in which case the open group is closed
+ * first; a tensor larger than the cap forms a group of its own. Outputs:
+ * group_of[i], offset_of[i] (elements), *ngroups and group_numel[g] (the
+ * end of the group's last member; arrays sized ntensors). */
+fg_status grad_group_plan(const uint64_t *numel, int32_t ntensors,
+                          uint64_t cap_bytes, uint32_t align_bytes,
+                          uint32_t elem_bytes, int32_t *group_of,
+                          uint64_t *offset_of, int32_t *ngroups,
+                          uint64_t *group_numel);
+
+/* Name of the main GPU kernel the given pass launches for this shape (a
+ * static string; "" for an invalid or unsupported shape). Lets a profiler
+ * or benchmark group launches the way a kernel trace does. */
+const char *fg_conv_kernel_name(const fg_conv_desc *d, int op);
+
+/* Human-readable name of a status code (static string). */
+const char *fg_status_string(fg_status s);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FCNGRAD_H */

@@ -45,15 +45,21 @@ def layer_backward(L, x16, w16, dy16, gate_input):
     return dx, dw
 
 
-def forward(layers, x16, weights):
-    """fp16 activations [x, a1, ..., aL] (a_i rounded once to fp16)."""
-    acts = [x16]
+def _store(a, fp16):
+    return _f16(a) if fp16 else np.asarray(a, dtype=np.float64)
+
+
+def forward(layers, x16, weights, store_fp16=True):
+    """Activations [x, a1, ..., aL]; each a_i rounded once to fp16 (the
+    network's storage format) unless store_fp16 is False, in which case the
+    chain runs entirely in fp64 (used to measure what fp16 storage costs)."""
+    acts = [x16 if store_fp16 else np.asarray(x16, dtype=np.float64)]
     for L, w in zip(layers, weights):
-        acts.append(_f16(layer_forward(L, acts[-1], w)))
+        acts.append(_store(layer_forward(L, acts[-1], w), store_fp16))
     return acts
 
 
-def backward(layers, acts, weights, dy_out16):
+def backward(layers, acts, weights, dy_out16, store_fp16=True):
     """fp16 weight gradients in forward order and fp16 input gradients.
 
     dy_out16 is the gradient w.r.t. the last layer's pre-activation output.
@@ -67,11 +73,14 @@ def backward(layers, acts, weights, dy_out16):
         L = layers[i]
         gate = i > 0 and layers[i - 1].relu
         dx, dw = layer_backward(L, acts[i], weights[i], dy, gate)
-        dws[i] = _f16(dw)
-        dxs[i] = _f16(dx)
+        dws[i] = _store(dw, store_fp16)
+        dxs[i] = _store(dx, store_fp16)
         dy = dxs[i]
     return dws, dxs
 
 
-def head_grad(y16, target, loss_scale):
-    return _grad.head_grad(y16, target, loss_scale)
+def head_grad(y16, target, loss_scale, store_fp16=True):
+    if store_fp16:
+        return _grad.head_grad(y16, target, loss_scale)
+    y = np.asarray(y16, dtype=np.float64)
+    return loss_scale * 2.0 * (y - np.asarray(target, np.float64)) / y.size

@@ -1,0 +1,224 @@
+"""Python binding of libfcngrad (fp16 FCN training-step hot path, gfx950).
+
+Argument marshalling only: every call forwards device pointers of torch
+tensors and the current HIP stream to the C ABI declared in
+``include/fcngrad.h``; all arithmetic runs in the library's HIP kernels.
+PyTorch provides device memory and streams. The library is loaded from
+this directory; a missing library raises ``LibraryNotBuilt`` — there is no
+fallback path.
+"""
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libfcngrad.so")
+
+FG_OK, FG_EINVAL, FG_EUNSUPPORTED, FG_EWORKSPACE, FG_ELAUNCH = range(5)
+EPI_NONE, EPI_RELU, EPI_GATE = 0, 1, 2
+OP_FWD, OP_BWD_DATA, OP_BWD_WEIGHT, OP_CONVT = 0, 1, 2, 3
+MAX_SEGMENTS = 64
+
+ENTRY_POINTS = (
+    "conv2d_fwd", "conv2d_bwd_data", "conv2d_bwd_weight",
+    "conv_transpose2d_fwd", "grad_group_pack", "grad_unscale_check",
+    "grad_group_unpack", "l2_head_grad", "relu_backward",
+    "fg_conv_workspace_bytes", "fg_conv_out_dims", "grad_group_plan",
+    "fg_conv_kernel_name", "fg_status_string",
+)
+
+
+class LibraryNotBuilt(RuntimeError):
+    pass
+
+
+class FgError(RuntimeError):
+    def __init__(self, fn, status):
+        self.status = status
+        super().__init__(f"{fn}: {status_string(status)}")
+
+
+class ConvDesc(ctypes.Structure):
+    _fields_ = [(f, ctypes.c_int32) for f in
+                ("n", "h", "w", "c", "k", "r", "s", "stride_h", "stride_w",
+                 "pad_h", "pad_w")]
+
+    @classmethod
+    def make(cls, n, h, w, c, k, r, s, stride=1, pad=0):
+        return cls(n, h, w, c, k, r, s, stride, stride, pad, pad)
+
+
+class Segment(ctypes.Structure):
+    _fields_ = [("ptr", ctypes.c_uint64), ("numel", ctypes.c_uint64),
+                ("offset", ctypes.c_uint64)]
+
+
+_lib = None
+
+
+def lib():
+    """Load libfcngrad.so (once) and declare every entry point."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise LibraryNotBuilt(
+            f"{LIB_PATH} is missing; build it with "
+            "`python -m paper_1909_11150_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, u64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint64, ctypes.c_size_t
+    pdesc = ctypes.POINTER(ConvDesc)
+    pseg = ctypes.POINTER(Segment)
+    sigs = {
+        "conv2d_fwd": [pdesc, vp, vp, vp, i32, vp, vp, sz, vp],
+        "conv2d_bwd_data": [pdesc, vp, vp, vp, i32, vp, vp, sz, vp],
+        "conv2d_bwd_weight": [pdesc, vp, vp, vp, vp, sz, vp],
+        "conv_transpose2d_fwd": [pdesc, vp, vp, vp, i32, vp, vp, sz, vp],
+        "grad_group_pack": [pseg, i32, vp, u64, vp],
+        "grad_unscale_check": [vp, u64, ctypes.c_float, vp, vp, vp],
+        "grad_group_unpack": [vp, u64, pseg, i32, vp],
+        "l2_head_grad": [vp, vp, u64, ctypes.c_double, vp, vp],
+        "relu_backward": [vp, vp, u64, vp, vp],
+        "fg_conv_out_dims": [pdesc, ctypes.c_int, ctypes.POINTER(i32),
+                             ctypes.POINTER(i32)],
+        "grad_group_plan": [ctypes.POINTER(u64), i32, u64, ctypes.c_uint32,
+                            ctypes.c_uint32, ctypes.POINTER(i32),
+                            ctypes.POINTER(u64), ctypes.POINTER(i32),
+                            ctypes.POINTER(u64)],
+    }
+    for name, args in sigs.items():
+        fn = getattr(L, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_int
+    L.fg_conv_workspace_bytes.argtypes = [pdesc, ctypes.c_int]
+    L.fg_conv_workspace_bytes.restype = ctypes.c_size_t
+    L.fg_conv_kernel_name.argtypes = [pdesc, ctypes.c_int]
+    L.fg_conv_kernel_name.restype = ctypes.c_char_p
+    L.fg_status_string.argtypes = [ctypes.c_int]
+    L.fg_status_string.restype = ctypes.c_char_p
+    _lib = L
+    return L
+
+
+def status_string(status):
+    return lib().fg_status_string(status).decode()
+
+
+def _check(fn, status):
+    if status != FG_OK:
+        raise FgError(fn, status)
+
+
+def _p(t):
+    """Device pointer of a tensor (None -> NULL)."""
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensors passed to libfcngrad must be contiguous")
+    return t.data_ptr()
+
+
+def _s(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    return stream
+
+
+# ---- convolution passes ---------------------------------------------------
+def kernel_name(desc, op):
+    """Main kernel the pass launches for this shape (for grouping timings)."""
+    return lib().fg_conv_kernel_name(ctypes.byref(desc), op).decode()
+
+
+def workspace_bytes(desc, op):
+    return lib().fg_conv_workspace_bytes(ctypes.byref(desc), op)
+
+
+def out_dims(desc, transpose=False):
+    p, q = ctypes.c_int32(), ctypes.c_int32()
+    _check("fg_conv_out_dims", lib().fg_conv_out_dims(
+        ctypes.byref(desc), int(transpose), ctypes.byref(p), ctypes.byref(q)))
+    return p.value, q.value
+
+
+def _ws(ws):
+    return (None, 0) if ws is None else (ws.data_ptr(), ws.numel() * ws.element_size())
+
+
+def conv2d_fwd(desc, x, w, y, epi=EPI_NONE, gate=None, ws=None, stream=None):
+    wp, wb = _ws(ws)
+    _check("conv2d_fwd", lib().conv2d_fwd(
+        ctypes.byref(desc), _p(x), _p(w), _p(y), epi, _p(gate), wp, wb, _s(stream)))
+
+
+def conv2d_bwd_data(desc, dy, w, dx, epi=EPI_NONE, gate=None, ws=None,
+                    stream=None):
+    wp, wb = _ws(ws)
+    _check("conv2d_bwd_data", lib().conv2d_bwd_data(
+        ctypes.byref(desc), _p(dy), _p(w), _p(dx), epi, _p(gate), wp, wb,
+        _s(stream)))
+
+
+def conv2d_bwd_weight(desc, x, dy, dw, ws=None, stream=None):
+    wp, wb = _ws(ws)
+    _check("conv2d_bwd_weight", lib().conv2d_bwd_weight(
+        ctypes.byref(desc), _p(x), _p(dy), _p(dw), wp, wb, _s(stream)))
+
+
+def conv_transpose2d_fwd(desc, x, w, y, epi=EPI_NONE, gate=None, ws=None,
+                         stream=None):
+    wp, wb = _ws(ws)
+    _check("conv_transpose2d_fwd", lib().conv_transpose2d_fwd(
+        ctypes.byref(desc), _p(x), _p(w), _p(y), epi, _p(gate), wp, wb,
+        _s(stream)))
+
+
+# ---- gradient path --------------------------------------------------------
+def _segments(tensors, offsets):
+    arr = (Segment * len(tensors))()
+    for i, (t, off) in enumerate(zip(tensors, offsets)):
+        arr[i] = Segment(_p(t), t.numel(), off)
+    return arr
+
+
+def grad_group_pack(srcs, offsets, group, stream=None):
+    segs = _segments(srcs, offsets)
+    _check("grad_group_pack", lib().grad_group_pack(
+        segs, len(srcs), _p(group), group.numel(), _s(stream)))
+
+
+def grad_unscale_check(group, inv_scale, out_f32, flag, numel=None,
+                       stream=None):
+    n = group.numel() if numel is None else numel
+    _check("grad_unscale_check", lib().grad_unscale_check(
+        _p(group), n, float(inv_scale), _p(out_f32), _p(flag), _s(stream)))
+
+
+def grad_group_unpack(group_f32, dsts, offsets, stream=None):
+    segs = _segments(dsts, offsets)
+    _check("grad_group_unpack", lib().grad_group_unpack(
+        _p(group_f32), group_f32.numel(), segs, len(dsts), _s(stream)))
+
+
+def l2_head_grad(y, t, scale, dy, stream=None):
+    _check("l2_head_grad", lib().l2_head_grad(
+        _p(y), _p(t), y.numel(), float(scale), _p(dy), _s(stream)))
+
+
+def relu_backward(dy, act, out, stream=None):
+    _check("relu_backward", lib().relu_backward(
+        _p(dy), _p(act), dy.numel(), _p(out), _s(stream)))
+
+
+def grad_group_plan(numels, cap_bytes, align_bytes=256, elem_bytes=2):
+    """Host planner in the library: returns (group_of, offset_of, group_numel)."""
+    n = len(numels)
+    u64a = (ctypes.c_uint64 * n)(*numels)
+    gof = (ctypes.c_int32 * n)()
+    oof = (ctypes.c_uint64 * n)()
+    gnum = (ctypes.c_uint64 * n)()
+    ng = ctypes.c_int32()
+    _check("grad_group_plan", lib().grad_group_plan(
+        u64a, n, cap_bytes, align_bytes, elem_bytes, gof, oof,
+        ctypes.byref(ng), gnum))
+    return list(gof), list(oof), list(gnum[:ng.value])

@@ -1,0 +1,472 @@
+// C-ABI entry points of libfcngrad: host-side validation, the lowering of
+// each convolution pass onto the implicit-GEMM kernels, and the host-only
+// helpers. Every check runs before the first HIP call, so an invalid call
+// returns without touching the device.
+#include <string.h>
+
+#include "internal.h"
+
+using namespace fg;
+
+namespace {
+
+constexpr int64_t kMaxElems = (int64_t)1 << 31;
+
+bool pos(int32_t v) { return v > 0; }
+
+int64_t elems4(int64_t a, int64_t b, int64_t c, int64_t d) {
+  return a * b * c * d;
+}
+
+// Forward output size; <= 0 when the kernel does not fit.
+int32_t fwd_out(int32_t in, int32_t pad, int32_t ker, int32_t str) {
+  int64_t t = (int64_t)in + 2 * (int64_t)pad - ker;
+  if (t < 0) return 0;
+  return (int32_t)(t / str + 1);
+}
+
+int32_t convt_out(int32_t in, int32_t pad, int32_t ker, int32_t str) {
+  int64_t o = ((int64_t)in - 1) * str - 2 * (int64_t)pad + ker;
+  return o > 0 && o < kMaxElems ? (int32_t)o : 0;
+}
+
+fg_status check_desc(const fg_conv_desc *d) {
+  if (!d) return FG_EINVAL;
+  if (!pos(d->n) || !pos(d->h) || !pos(d->w) || !pos(d->c) || !pos(d->k) ||
+      !pos(d->r) || !pos(d->s) || !pos(d->stride_h) || !pos(d->stride_w) ||
+      d->pad_h < 0 || d->pad_w < 0)
+    return FG_EINVAL;
+  return FG_OK;
+}
+
+// K == 1 is served by the bandwidth kernels of the 1x1 head only.
+bool is_head(const fg_conv_desc *d) {
+  return d->k == 1 && d->r == 1 && d->s == 1 && d->stride_h == 1 &&
+         d->stride_w == 1 && d->pad_h == 0 && d->pad_w == 0;
+}
+
+fg_status check_conv_support(const fg_conv_desc *d) {
+  if (d->c % 8 != 0) return FG_EUNSUPPORTED;
+  if (d->k == 1) return is_head(d) && d->c <= 2048 ? FG_OK : FG_EUNSUPPORTED;
+  if (d->k % 8 != 0) return FG_EUNSUPPORTED;
+  if (d->r * d->s > 16) return FG_EUNSUPPORTED;
+  return FG_OK;
+}
+
+// Byte ranges [a, a+na) and [b, b+nb) overlap.
+bool overlap(const void *a, size_t na, const void *b, size_t nb) {
+  uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+  return x < y + nb && y < x + na;
+}
+
+bool sizes_ok(int64_t a, int64_t b, int64_t c) {
+  return a < kMaxElems && b < kMaxElems && c < kMaxElems;
+}
+
+fg_status launch_status(hipError_t e) {
+  return e == hipSuccess ? FG_OK : FG_ELAUNCH;
+}
+
+// Phase description for an input-gradient style convolution (scatter form
+// evaluated per output phase). Dimension of size `out` with stride `str`,
+// padding `pad`, kernel `ker`, input (gathered) size `in`: for output
+// positions o = a*str + ph, the taps are r = r0, r0+str, ... with
+// (ph + pad - r) divisible by str, reading input row a + (ph + pad - r)/str.
+struct Dim1 {
+  int32_t m, r0, n, d0;
+};
+
+Dim1 phase_dim(int32_t out, int32_t str, int32_t pad, int32_t ker,
+               int32_t ph) {
+  Dim1 d{0, 0, 0, 0};
+  d.m = ph < out ? (out - ph + str - 1) / str : 0;
+  int32_t r0 = ((ph + pad) % str + str) % str;
+  d.r0 = r0;
+  d.n = r0 < ker ? (ker - r0 + str - 1) / str : 0;
+  d.d0 = (ph + pad - r0) / str;  // exact: ph + pad - r0 is a multiple of str
+  return d;
+}
+
+// Fill the phases of an input-gradient style lowering. Returns the count.
+int make_phases(DataConvArgs &a, int32_t ho, int32_t wo, int32_t sh,
+                int32_t sw, int32_t pad_h, int32_t pad_w, int32_t r,
+                int32_t s) {
+  int np = 0;
+  for (int ph = 0; ph < sh; ++ph)
+    for (int pw = 0; pw < sw; ++pw) {
+      Dim1 dh = phase_dim(ho, sh, pad_h, r, ph);
+      Dim1 dw = phase_dim(wo, sw, pad_w, s, pw);
+      Phase &P = a.ph[np++];
+      P.mh = dh.m;
+      P.mw = dw.m;
+      P.ooh = ph;
+      P.oow = pw;
+      P.nr = dh.n;
+      P.ns = dw.n;
+      P.dh0 = dh.d0;
+      P.dw0 = dw.d0;
+      P.dstep = -1;
+      P.r0 = dh.r0;
+      P.s0 = dw.r0;
+      P.rstep = sh;  // equal strides only (checked by the callers)
+    }
+  return np;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+extern "C" {
+
+const char *fg_status_string(fg_status s) {
+  switch (s) {
+    case FG_OK: return "FG_OK";
+    case FG_EINVAL: return "FG_EINVAL: invalid argument";
+    case FG_EUNSUPPORTED: return "FG_EUNSUPPORTED: shape not implemented";
+    case FG_EWORKSPACE: return "FG_EWORKSPACE: workspace too small";
+    case FG_ELAUNCH: return "FG_ELAUNCH: kernel launch failed";
+  }
+  return "unknown fg_status";
+}
+
+fg_status fg_conv_out_dims(const fg_conv_desc *d, int transpose, int32_t *p,
+                           int32_t *q) {
+  if (check_desc(d) != FG_OK || !p || !q || (transpose != 0 && transpose != 1))
+    return FG_EINVAL;
+  int32_t pp, qq;
+  if (transpose) {
+    pp = convt_out(d->h, d->pad_h, d->r, d->stride_h);
+    qq = convt_out(d->w, d->pad_w, d->s, d->stride_w);
+  } else {
+    pp = fwd_out(d->h, d->pad_h, d->r, d->stride_h);
+    qq = fwd_out(d->w, d->pad_w, d->s, d->stride_w);
+  }
+  if (pp <= 0 || qq <= 0) return FG_EINVAL;
+  *p = pp;
+  *q = qq;
+  return FG_OK;
+}
+
+size_t fg_conv_workspace_bytes(const fg_conv_desc *d, int op) {
+  if (check_desc(d) != FG_OK) return 0;
+  if (op == FG_OP_BWD_WEIGHT) {
+    int32_t p, q;
+    if (fg_conv_out_dims(d, 0, &p, &q) != FG_OK) return 0;
+    if (is_head(d)) return head_wgrad_ws_bytes(*d);
+    return plan_wgrad(*d, p, q).ws_bytes;
+  }
+  return 0;
+}
+
+const char *fg_conv_kernel_name(const fg_conv_desc *d, int op) {
+  if (check_desc(d) != FG_OK) return "";
+  switch (op) {
+    case FG_OP_FWD:
+      if (check_conv_support(d) != FG_OK) return "";
+      return d->k == 1 ? "head_fwd_kernel" : data_conv_kernel_name(d->c, true);
+    case FG_OP_BWD_DATA:
+      if (check_conv_support(d) != FG_OK) return "";
+      return d->k == 1 ? "head_bwd_data_kernel"
+                       : data_conv_kernel_name(d->k, false);
+    case FG_OP_BWD_WEIGHT:
+      if (check_conv_support(d) != FG_OK) return "";
+      return d->k == 1 ? "head_wgrad_kernel" : wgrad_kernel_name();
+    case FG_OP_CONVT:
+      return data_conv_kernel_name(d->c, false);
+  }
+  return "";
+}
+
+fg_status conv2d_fwd(const fg_conv_desc *d, const uint16_t *x,
+                     const uint16_t *w_krsc, uint16_t *y, fg_epilogue epi,
+                     const uint16_t *gate, void *ws, size_t ws_bytes,
+                     hipStream_t stream) {
+  (void)ws;
+  (void)ws_bytes;
+  fg_status st = check_desc(d);
+  if (st != FG_OK) return st;
+  if (!x || !w_krsc || !y) return FG_EINVAL;
+  if (epi != FG_EPI_NONE && epi != FG_EPI_RELU && epi != FG_EPI_GATE)
+    return FG_EINVAL;
+  if (epi == FG_EPI_GATE && !gate) return FG_EINVAL;
+  int32_t P, Q;
+  if (fg_conv_out_dims(d, 0, &P, &Q) != FG_OK) return FG_EINVAL;
+  const int64_t nx = elems4(d->n, d->h, d->w, d->c);
+  const int64_t nw = elems4(d->k, d->r, d->s, d->c);
+  const int64_t ny = elems4(d->n, P, Q, d->k);
+  if (!sizes_ok(nx, nw, ny)) return FG_EUNSUPPORTED;
+  if (overlap(y, ny * 2, x, nx * 2) || overlap(y, ny * 2, w_krsc, nw * 2))
+    return FG_EINVAL;
+  if ((st = check_conv_support(d)) != FG_OK) return st;
+  // one input step per output position for both image axes
+  if (d->stride_h != d->stride_w) return FG_EUNSUPPORTED;
+
+  if (d->k == 1)
+    return launch_status(launch_head_fwd(x, w_krsc, y, (int64_t)d->n * P * Q,
+                                         d->c, epi, gate, stream));
+  DataConvArgs a;
+  memset(&a, 0, sizeof(a));
+  a.act = x;
+  a.wgt = w_krsc;
+  a.out = y;
+  a.gate = gate;
+  a.n = d->n; a.hi = d->h; a.wi = d->w; a.cr = d->c;
+  a.ho = P; a.wo = Q; a.co = d->k;
+  a.istr = d->stride_h;
+  a.ostr = 1;
+  a.s = d->s;
+  a.ldw = d->r * d->s * d->c;
+  a.epi = epi;
+  a.nphase = 1;
+  Phase &ph = a.ph[0];
+  ph.mh = P; ph.mw = Q; ph.ooh = 0; ph.oow = 0;
+  ph.nr = d->r; ph.ns = d->s;
+  ph.dh0 = -d->pad_h; ph.dw0 = -d->pad_w; ph.dstep = 1;
+  ph.r0 = 0; ph.s0 = 0; ph.rstep = 1;
+  return launch_status(launch_data_conv(a, true, stream));
+}
+
+fg_status conv2d_bwd_data(const fg_conv_desc *d, const uint16_t *dy,
+                          const uint16_t *w_krsc, uint16_t *dx,
+                          fg_epilogue epi, const uint16_t *gate, void *ws,
+                          size_t ws_bytes, hipStream_t stream) {
+  (void)ws;
+  (void)ws_bytes;
+  fg_status st = check_desc(d);
+  if (st != FG_OK) return st;
+  if (!dy || !w_krsc || !dx) return FG_EINVAL;
+  if (epi != FG_EPI_NONE && epi != FG_EPI_RELU && epi != FG_EPI_GATE)
+    return FG_EINVAL;
+  if (epi == FG_EPI_GATE && !gate) return FG_EINVAL;
+  int32_t P, Q;
+  if (fg_conv_out_dims(d, 0, &P, &Q) != FG_OK) return FG_EINVAL;
+  const int64_t nx = elems4(d->n, d->h, d->w, d->c);
+  const int64_t nw = elems4(d->k, d->r, d->s, d->c);
+  const int64_t ny = elems4(d->n, P, Q, d->k);
+  if (!sizes_ok(nx, nw, ny)) return FG_EUNSUPPORTED;
+  if (overlap(dx, nx * 2, dy, ny * 2) || overlap(dx, nx * 2, w_krsc, nw * 2))
+    return FG_EINVAL;
+  if ((st = check_conv_support(d)) != FG_OK) return st;
+  if (d->stride_h != d->stride_w || d->stride_h > 2) return FG_EUNSUPPORTED;
+
+  if (d->k == 1)
+    return launch_status(launch_head_bwd_data(
+        dy, w_krsc, dx, (int64_t)d->n * d->h * d->w, d->c, epi, gate, stream));
+  DataConvArgs a;
+  memset(&a, 0, sizeof(a));
+  a.act = dy;
+  a.wgt = w_krsc;
+  a.out = dx;
+  a.gate = gate;
+  a.n = d->n; a.hi = P; a.wi = Q; a.cr = d->k;
+  a.ho = d->h; a.wo = d->w; a.co = d->c;
+  a.istr = 1;
+  a.ostr = d->stride_h;
+  a.s = d->s;
+  a.w_red = d->r * d->s * d->c;  // W[k][r][s][c]: reduction index k
+  a.w_tap = d->c;
+  a.epi = epi;
+  a.nphase = make_phases(a, d->h, d->w, d->stride_h, d->stride_w, d->pad_h,
+                         d->pad_w, d->r, d->s);
+  return launch_status(launch_data_conv(a, false, stream));
+}
+
+fg_status conv_transpose2d_fwd(const fg_conv_desc *d, const uint16_t *x,
+                               const uint16_t *w_crsk, uint16_t *y,
+                               fg_epilogue epi, const uint16_t *gate,
+                               void *ws, size_t ws_bytes, hipStream_t stream) {
+  (void)ws;
+  (void)ws_bytes;
+  fg_status st = check_desc(d);
+  if (st != FG_OK) return st;
+  if (!x || !w_crsk || !y) return FG_EINVAL;
+  if (epi != FG_EPI_NONE && epi != FG_EPI_RELU && epi != FG_EPI_GATE)
+    return FG_EINVAL;
+  if (epi == FG_EPI_GATE && !gate) return FG_EINVAL;
+  int32_t HO, WO;
+  if (fg_conv_out_dims(d, 1, &HO, &WO) != FG_OK) return FG_EINVAL;
+  const int64_t nx = elems4(d->n, d->h, d->w, d->c);
+  const int64_t nw = elems4(d->c, d->r, d->s, d->k);
+  const int64_t ny = elems4(d->n, HO, WO, d->k);
+  if (!sizes_ok(nx, nw, ny)) return FG_EUNSUPPORTED;
+  if (overlap(y, ny * 2, x, nx * 2) || overlap(y, ny * 2, w_crsk, nw * 2))
+    return FG_EINVAL;
+  if (d->c % 8 != 0 || d->k % 8 != 0 || d->r != 4 || d->s != 4 ||
+      d->stride_h != 2 || d->stride_w != 2 || d->pad_h != 1 || d->pad_w != 1)
+    return FG_EUNSUPPORTED;
+
+  DataConvArgs a;
+  memset(&a, 0, sizeof(a));
+  a.act = x;
+  a.wgt = w_crsk;
+  a.out = y;
+  a.gate = gate;
+  a.n = d->n; a.hi = d->h; a.wi = d->w; a.cr = d->c;
+  a.ho = HO; a.wo = WO; a.co = d->k;
+  a.istr = 1;
+  a.ostr = d->stride_h;
+  a.s = d->s;
+  a.w_red = d->r * d->s * d->k;  // Wt[c][r][s][k]: reduction index c
+  a.w_tap = d->k;
+  a.epi = epi;
+  a.nphase = make_phases(a, HO, WO, d->stride_h, d->stride_w, d->pad_h,
+                         d->pad_w, d->r, d->s);
+  return launch_status(launch_data_conv(a, false, stream));
+}
+
+fg_status conv2d_bwd_weight(const fg_conv_desc *d, const uint16_t *x,
+                            const uint16_t *dy, uint16_t *dw_krsc, void *ws,
+                            size_t ws_bytes, hipStream_t stream) {
+  fg_status st = check_desc(d);
+  if (st != FG_OK) return st;
+  if (!x || !dy || !dw_krsc) return FG_EINVAL;
+  int32_t P, Q;
+  if (fg_conv_out_dims(d, 0, &P, &Q) != FG_OK) return FG_EINVAL;
+  const int64_t nx = elems4(d->n, d->h, d->w, d->c);
+  const int64_t nw = elems4(d->k, d->r, d->s, d->c);
+  const int64_t ny = elems4(d->n, P, Q, d->k);
+  if (!sizes_ok(nx, nw, ny)) return FG_EUNSUPPORTED;
+  if (overlap(dw_krsc, nw * 2, x, nx * 2) ||
+      overlap(dw_krsc, nw * 2, dy, ny * 2))
+    return FG_EINVAL;
+  if ((st = check_conv_support(d)) != FG_OK) return st;
+  const size_t need = fg_conv_workspace_bytes(d, FG_OP_BWD_WEIGHT);
+  if (need > 0 && (!ws || ws_bytes < need)) return FG_EWORKSPACE;
+  if (need > 0 && (overlap(ws, need, dw_krsc, nw * 2) ||
+                   overlap(ws, need, x, nx * 2) || overlap(ws, need, dy, ny * 2)))
+    return FG_EINVAL;
+
+  if (d->k == 1)
+    return launch_status(launch_head_wgrad(x, dy, dw_krsc,
+                                           (int64_t)d->n * d->h * d->w, d->c,
+                                           (float *)ws, stream));
+  WgradPlan pl = plan_wgrad(*d, P, Q);
+  WgradArgs a;
+  memset(&a, 0, sizeof(a));
+  a.x = x;
+  a.dy = dy;
+  a.dw = dw_krsc;
+  a.part = (float *)ws;
+  a.n = d->n; a.h = d->h; a.w = d->w; a.c = d->c; a.k = d->k;
+  a.r = d->r; a.s = d->s; a.p = P; a.q = Q;
+  a.sh = d->stride_h; a.sw = d->stride_w; a.ph = d->pad_h; a.pw = d->pad_w;
+  a.mtot = d->n * P * Q;
+  a.mchunk = pl.mchunk;
+  a.nsplit = pl.nsplit;
+  return launch_status(launch_wgrad(a, stream));
+}
+
+// ---------------------------------------------------------------------------
+// Segments must lie inside the group and not overlap there; with
+// distinct_ptrs (unpack destinations) their device ranges must not overlap
+// either.
+static fg_status check_segments(const fg_segment *segs, int32_t nseg,
+                                uint64_t group_numel, size_t esz,
+                                bool distinct_ptrs) {
+  if (!segs || nseg < 1) return FG_EINVAL;
+  if (nseg > FG_MAX_SEGMENTS) return FG_EUNSUPPORTED;
+  if (group_numel >= (uint64_t)kMaxElems) return FG_EUNSUPPORTED;
+  for (int i = 0; i < nseg; ++i) {
+    const fg_segment &s = segs[i];
+    if (!s.ptr && s.numel) return FG_EINVAL;
+    if (s.offset > group_numel || s.numel > group_numel - s.offset)
+      return FG_EINVAL;
+    for (int j = 0; j < i; ++j) {
+      const fg_segment &t = segs[j];
+      if (s.numel && t.numel && s.offset < t.offset + t.numel &&
+          t.offset < s.offset + s.numel)
+        return FG_EINVAL;
+      if (distinct_ptrs && s.numel && t.numel &&
+          overlap((void *)s.ptr, s.numel * esz, (void *)t.ptr, t.numel * esz))
+        return FG_EINVAL;
+    }
+  }
+  return FG_OK;
+}
+
+fg_status grad_group_pack(const fg_segment *segs, int32_t nseg,
+                          uint16_t *group, uint64_t group_numel,
+                          hipStream_t stream) {
+  if (!group || group_numel == 0) return FG_EINVAL;
+  fg_status st = check_segments(segs, nseg, group_numel, 2, false);
+  if (st != FG_OK) return st;
+  for (int i = 0; i < nseg; ++i)
+    if (overlap((void *)segs[i].ptr, segs[i].numel * 2, group, group_numel * 2))
+      return FG_EINVAL;
+  return launch_status(launch_pack(segs, nseg, group, group_numel, stream));
+}
+
+fg_status grad_group_unpack(const float *group_f32, uint64_t group_numel,
+                            const fg_segment *segs, int32_t nseg,
+                            hipStream_t stream) {
+  if (!group_f32 || group_numel == 0) return FG_EINVAL;
+  fg_status st = check_segments(segs, nseg, group_numel, 4, true);
+  if (st != FG_OK) return st;
+  for (int i = 0; i < nseg; ++i)
+    if (overlap((void *)segs[i].ptr, segs[i].numel * 4, group_f32,
+                group_numel * 4))
+      return FG_EINVAL;
+  return launch_status(launch_unpack(group_f32, segs, nseg, stream));
+}
+
+fg_status grad_unscale_check(const uint16_t *group, uint64_t numel,
+                             float inv_scale, float *out_f32,
+                             int32_t *found_nonfinite, hipStream_t stream) {
+  if (!group || !out_f32 || !found_nonfinite || numel == 0) return FG_EINVAL;
+  if (numel >= (uint64_t)kMaxElems) return FG_EUNSUPPORTED;
+  if (overlap(group, numel * 2, out_f32, numel * 4) ||
+      overlap(found_nonfinite, 4, out_f32, numel * 4) ||
+      overlap(found_nonfinite, 4, group, numel * 2))
+    return FG_EINVAL;
+  return launch_status(launch_unscale(group, numel, inv_scale, out_f32,
+                                      found_nonfinite, stream));
+}
+
+fg_status l2_head_grad(const uint16_t *y, const float *t, uint64_t numel,
+                       double scale, uint16_t *dy, hipStream_t stream) {
+  if (!y || !t || !dy || numel == 0) return FG_EINVAL;
+  if (numel >= (uint64_t)kMaxElems) return FG_EUNSUPPORTED;
+  if (overlap(dy, numel * 2, y, numel * 2) || overlap(dy, numel * 2, t, numel * 4))
+    return FG_EINVAL;
+  return launch_status(launch_head_grad(y, t, numel, scale, dy, stream));
+}
+
+fg_status relu_backward(const uint16_t *dy, const uint16_t *act,
+                        uint64_t numel, uint16_t *out, hipStream_t stream) {
+  if (!dy || !act || !out || numel == 0) return FG_EINVAL;
+  if (numel >= (uint64_t)kMaxElems) return FG_EUNSUPPORTED;
+  if (overlap(out, numel * 2, act, numel * 2)) return FG_EINVAL;
+  if (out != dy && overlap(out, numel * 2, dy, numel * 2)) return FG_EINVAL;
+  return launch_status(launch_relu_backward(dy, act, numel, out, stream));
+}
+
+fg_status grad_group_plan(const uint64_t *numel, int32_t ntensors,
+                          uint64_t cap_bytes, uint32_t align_bytes,
+                          uint32_t elem_bytes, int32_t *group_of,
+                          uint64_t *offset_of, int32_t *ngroups,
+                          uint64_t *group_numel) {
+  if (!numel || ntensors < 1 || !group_of || !offset_of || !ngroups ||
+      !group_numel || cap_bytes == 0 || align_bytes == 0 || elem_bytes == 0 ||
+      align_bytes % elem_bytes != 0)
+    return FG_EINVAL;
+  const uint64_t align = align_bytes / elem_bytes;
+  int32_t g = 0;
+  uint64_t end = 0;
+  bool open = false;
+  for (int32_t i = 0; i < ntensors; ++i) {
+    uint64_t start = (end + align - 1) / align * align;
+    if (open && (start + numel[i]) * elem_bytes > cap_bytes) {
+      group_numel[g++] = end;
+      start = 0;
+    }
+    group_of[i] = g;
+    offset_of[i] = start;
+    end = start + numel[i];
+    open = true;
+  }
+  group_numel[g++] = end;
+  *ngroups = g;
+  return FG_OK;
+}
+
+}  // extern "C"

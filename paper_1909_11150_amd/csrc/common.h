@@ -1,0 +1,46 @@
+// Device-side helpers shared by the fcngrad kernels (gfx950 / CDNA4).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fg {
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kWave = 64;
+
+// fp32 -> fp16 bits, round to nearest even, overflow to infinity.
+__device__ __forceinline__ uint16_t f32_to_h(float v) {
+  _Float16 h = (_Float16)v;
+  return __builtin_bit_cast(uint16_t, h);
+}
+
+__device__ __forceinline__ float h_to_f32(uint16_t b) {
+  return (float)__builtin_bit_cast(_Float16, b);
+}
+
+// 32x32x16 fp16 MFMA with fp32 accumulate. Operand lane layout: lane l holds
+// row (A) / column (B) l % 32 and the 8 reduction elements 8*(l/32)..+7.
+// Accumulator layout: lane l, register v holds C[8*(v/4) + 4*(l/32) + v%4]
+// [l % 32].
+__device__ __forceinline__ f32x16 mfma32(const u32x4 &a, const u32x4 &b,
+                                         const f32x16 &c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(half8, a),
+                                                __builtin_bit_cast(half8, b),
+                                                c, 0, 0, 0);
+}
+
+// Select the low (sel=0) or high (sel=1) 16-bit half of each of two words
+// and pack them as (lo_word_part, hi_word_part).
+__device__ __forceinline__ uint32_t pack_lo(uint32_t a, uint32_t b) {
+  return (a & 0xFFFFu) | (b << 16);
+}
+__device__ __forceinline__ uint32_t pack_hi(uint32_t a, uint32_t b) {
+  return (a >> 16) | (b & 0xFFFF0000u);
+}
+
+}  // namespace fg

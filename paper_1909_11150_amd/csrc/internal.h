@@ -1,0 +1,94 @@
+// Host-side interface between the C-ABI layer (abi.hip) and the kernel
+// launchers. Not part of the public API.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "fcngrad.h"
+
+namespace fg {
+
+// One output phase of a data convolution (forward, input gradient or
+// transposed forward) written as an implicit GEMM over the taps that reach
+// it. Output positions (a, b) of the phase land at image position
+// (a*ostr + ooh, b*ostr + oow); tap (i, j) reads the input at
+// (a*istr + dh0 + dstep*i, b*istr + dw0 + dstep*j) and the kernel element
+// (r0 + rstep*i, s0 + rstep*j).
+struct Phase {
+  int32_t mh, mw;
+  int32_t ooh, oow;
+  int32_t nr, ns;
+  int32_t dh0, dw0, dstep;
+  int32_t r0, s0, rstep;
+};
+
+struct DataConvArgs {
+  const uint16_t *act;   // input image  [n][hi][wi][cr]
+  const uint16_t *wgt;   // weights (layout per w_kmajor)
+  uint16_t *out;         // output image [n][ho][wo][co]
+  const uint16_t *gate;  // shaped like out (FG_EPI_GATE) or null
+  int32_t n, hi, wi, cr;
+  int32_t ho, wo, co;
+  int32_t istr, ostr;
+  int32_t s;             // kernel width
+  // weight element (co, r, s, cr):
+  //   k-major:  wgt[co*ldw + (r*S + s)*cr_stride + cr]
+  //   mn-major: wgt[cr*w_red + (r*S + s)*w_tap + co]
+  int32_t ldw, w_red, w_tap;
+  int32_t epi;
+  int32_t nphase;
+  Phase ph[4];
+};
+
+struct WgradArgs {
+  const uint16_t *x;     // [n][h][w][c]
+  const uint16_t *dy;    // [n][p][q][k]
+  uint16_t *dw;          // [k][r][s][c] fp16 (single split)
+  float *part;           // [nsplit][k][r*s*c] fp32 partials (nsplit > 1)
+  int32_t n, h, w, c, k, r, s, p, q;
+  int32_t sh, sw, ph, pw;
+  int32_t mtot;          // n*p*q
+  int32_t mchunk;        // reduction rows per split, multiple of 64
+  int32_t nsplit;
+};
+
+// Kernel selection for a shape; pure host logic, shared by the workspace
+// query and the launchers so both always agree.
+struct WgradPlan {
+  int32_t nsplit, mchunk;
+  size_t ws_bytes;
+};
+WgradPlan plan_wgrad(const fg_conv_desc &d, int32_t p, int32_t q);
+size_t head_wgrad_ws_bytes(const fg_conv_desc &d);
+
+hipError_t launch_data_conv(const DataConvArgs &a, bool w_kmajor,
+                            hipStream_t st);
+const char *data_conv_kernel_name(int32_t cr, bool w_kmajor);
+const char *wgrad_kernel_name();
+hipError_t launch_wgrad(const WgradArgs &a, hipStream_t st);
+hipError_t launch_head_fwd(const uint16_t *x, const uint16_t *w, uint16_t *y,
+                           int64_t npix, int32_t c, int32_t epi,
+                           const uint16_t *gate, hipStream_t st);
+hipError_t launch_head_bwd_data(const uint16_t *dy, const uint16_t *w,
+                                uint16_t *dx, int64_t npix, int32_t c,
+                                int32_t epi, const uint16_t *gate,
+                                hipStream_t st);
+hipError_t launch_head_wgrad(const uint16_t *x, const uint16_t *dy,
+                             uint16_t *dw, int64_t npix, int32_t c,
+                             float *ws, hipStream_t st);
+
+hipError_t launch_pack(const fg_segment *segs, int32_t nseg, uint16_t *group,
+                       uint64_t group_numel, hipStream_t st);
+hipError_t launch_unscale(const uint16_t *group, uint64_t numel,
+                          float inv_scale, float *out, int32_t *flag,
+                          hipStream_t st);
+hipError_t launch_unpack(const float *group, const fg_segment *segs,
+                         int32_t nseg, hipStream_t st);
+hipError_t launch_head_grad(const uint16_t *y, const float *t, uint64_t numel,
+                            double scale, uint16_t *dy, hipStream_t st);
+hipError_t launch_relu_backward(const uint16_t *dy, const uint16_t *act,
+                                uint64_t numel, uint16_t *out,
+                                hipStream_t st);
+
+}  // namespace fg

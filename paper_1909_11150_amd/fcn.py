@@ -1,0 +1,165 @@
+"""One GPU's share of a training step of the fully convolutional network.
+
+``Chain`` sequences the library's calls for a chain of conv / transposed-conv
+layers (Section 6.2, Figure workflow (B): encoder-decoder): the forward pass
+with fused ReLUs, the loss-scaled L2 head gradient, the backward pass with
+fused ReLU gradients, and — per complete gradient group, in backward
+completion order — fusion-buffer pack, unscale with overflow check and
+unpack to fp32 master gradients (Section 4.2 Grouping; Section 6.2 loss
+scaling). Device memory comes from torch; every step is a libfcngrad call.
+
+Layers are duck-typed: ``kind`` ("conv" | "convT"), ``x_shape``/``y_shape``
+(NHWC), ``r``, ``s``, ``stride``, ``pad``, ``relu`` and ``w_shape``.
+"""
+import torch
+
+from . import (EPI_GATE, EPI_NONE, EPI_RELU, OP_BWD_WEIGHT, ConvDesc,
+               conv2d_bwd_data, conv2d_bwd_weight, conv2d_fwd,
+               conv_transpose2d_fwd, grad_group_pack, grad_group_plan,
+               grad_group_unpack, grad_unscale_check, l2_head_grad,
+               relu_backward, workspace_bytes)
+
+F16 = torch.float16
+
+
+def fwd_desc(L):
+    """Descriptor of the layer's forward op (convT: its own input/output)."""
+    n, h, w, c = L.x_shape
+    k = L.y_shape[3]
+    return ConvDesc.make(n, h, w, c, k, L.r, L.s, L.stride, L.pad)
+
+
+def convt_dx_desc(L):
+    """Input gradient of a transposed conv: a forward conv of dy (the big
+    image) with Wt read as KRSC (K = C_in, C = C_out)."""
+    n, ho, wo, co = L.y_shape
+    ci = L.x_shape[3]
+    return ConvDesc.make(n, ho, wo, co, ci, L.r, L.s, L.stride, L.pad)
+
+
+def convt_dw_desc(L):
+    """Kernel gradient of a transposed conv: the conv kernel gradient with
+    x := dy (big image, C = C_out channels) and dy := x (K = C_in)."""
+    return convt_dx_desc(L)
+
+
+class Chain:
+    def __init__(self, layers, weights, x, device="cuda", loss_scale=2.0 ** 15,
+                 group_cap_bytes=None, group_align_bytes=256, stream=None):
+        self.layers = list(layers)
+        self.dev = torch.device(device)
+        self.stream = stream
+        self.loss_scale = float(loss_scale)
+        self.w = [torch.as_tensor(w).to(self.dev).contiguous() for w in weights]
+        self.x = torch.as_tensor(x).to(self.dev).contiguous()
+        nl = len(self.layers)
+        self.acts = [self.x] + [torch.empty(L.y_shape, dtype=F16, device=self.dev)
+                                for L in self.layers]
+        # g[i]: gradient w.r.t. the pre-activation output of layer i-1 (g[0]
+        # is the input gradient of the network)
+        self.g = [torch.empty(L.x_shape, dtype=F16, device=self.dev)
+                  for L in self.layers] + \
+                 [torch.empty(self.layers[-1].y_shape, dtype=F16, device=self.dev)]
+        self.dw = [torch.empty(L.w_shape, dtype=F16, device=self.dev)
+                   for L in self.layers]
+        ws = 0
+        for L in self.layers:
+            d = fwd_desc(L) if L.kind == "conv" else convt_dw_desc(L)
+            ws = max(ws, workspace_bytes(d, OP_BWD_WEIGHT))
+        self.ws = torch.empty(max(ws, 16), dtype=torch.uint8, device=self.dev)
+        self.groups = None
+        if group_cap_bytes is not None:
+            self._plan_groups(group_cap_bytes, group_align_bytes)
+        self._nl = nl
+
+    # ---- gradient groups ---------------------------------------------------
+    def _plan_groups(self, cap, align):
+        order = list(reversed(range(len(self.layers))))  # completion order
+        numels = [self.dw[i].numel() for i in order]
+        gof, oof, gnum = grad_group_plan(numels, cap, align, 2)
+        groups = []
+        for g, n in enumerate(gnum):
+            mem = [(order[j], oof[j]) for j in range(len(order)) if gof[j] == g]
+            groups.append({"members": [m for m, _ in mem],
+                           "offsets": [o for _, o in mem], "numel": n})
+        self.groups = groups
+        self.gbuf16 = [torch.empty(g["numel"], dtype=F16, device=self.dev)
+                       for g in groups]
+        self.gbuf32 = [torch.empty(g["numel"], dtype=torch.float32, device=self.dev)
+                       for g in groups]
+        self.flags = torch.zeros(len(groups), dtype=torch.int32, device=self.dev)
+        self.master = [torch.empty(L.w_shape, dtype=torch.float32, device=self.dev)
+                       for L in self.layers]
+        # the layer whose dW completes each group (last member in order)
+        self._group_done_at = {g["members"][-1]: gi for gi, g in enumerate(groups)}
+
+    def run_group(self, gi):
+        g = self.groups[gi]
+        grad_group_pack([self.dw[m] for m in g["members"]], g["offsets"],
+                        self.gbuf16[gi], stream=self.stream)
+        grad_unscale_check(self.gbuf16[gi], 1.0 / self.loss_scale,
+                           self.gbuf32[gi], self.flags[gi:gi + 1],
+                           stream=self.stream)
+        grad_group_unpack(self.gbuf32[gi], [self.master[m] for m in g["members"]],
+                          g["offsets"], stream=self.stream)
+
+    # ---- passes --------------------------------------------------------------
+    def forward(self):
+        for i, L in enumerate(self.layers):
+            epi = EPI_RELU if L.relu else EPI_NONE
+            if L.kind == "conv":
+                conv2d_fwd(fwd_desc(L), self.acts[i], self.w[i], self.acts[i + 1],
+                           epi, stream=self.stream)
+            else:
+                conv_transpose2d_fwd(fwd_desc(L), self.acts[i], self.w[i],
+                                     self.acts[i + 1], epi, stream=self.stream)
+        return self.acts[-1]
+
+    def head_grad(self, target):
+        """g[L] = fp16(2*S*(y - t)/numel): loss-scaled MSE gradient."""
+        y = self.acts[-1]
+        l2_head_grad(y, target, 2.0 * self.loss_scale / y.numel(), self.g[-1],
+                     stream=self.stream)
+
+    def set_output_grad(self, dy):
+        """Seed g[L] with a given gradient w.r.t. the chain output (after the
+        last ReLU, if any: it is applied here)."""
+        dy = torch.as_tensor(dy).to(self.dev).contiguous()
+        if self.layers[-1].relu:
+            relu_backward(dy, self.acts[-1], self.g[-1], stream=self.stream)
+        else:
+            self.g[-1].copy_(dy)
+
+    def backward(self, grad_path=False):
+        for i in reversed(range(len(self.layers))):
+            L = self.layers[i]
+            dy = self.g[i + 1]
+            gate = i > 0 and self.layers[i - 1].relu
+            epi = EPI_GATE if gate else EPI_NONE
+            gt = self.acts[i] if gate else None
+            if L.kind == "conv":
+                d = fwd_desc(L)
+                conv2d_bwd_weight(d, self.acts[i], dy, self.dw[i], self.ws,
+                                  stream=self.stream)
+                conv2d_bwd_data(d, dy, self.w[i], self.g[i], epi, gt,
+                                stream=self.stream)
+            else:
+                conv2d_bwd_weight(convt_dw_desc(L), dy, self.acts[i], self.dw[i],
+                                  self.ws, stream=self.stream)
+                conv2d_fwd(convt_dx_desc(L), dy, self.w[i], self.g[i], epi, gt,
+                           stream=self.stream)
+            if grad_path and self.groups is not None and i in self._group_done_at:
+                self.run_group(self._group_done_at[i])
+
+    def step(self, target):
+        """Forward, loss head, backward and the grouped gradient path."""
+        self.forward()
+        self.head_grad(target)
+        if self.groups is not None:
+            self.flags.zero_()
+        self.backward(grad_path=self.groups is not None)
+
+    # ---- accounting -------------------------------------------------------------
+    def conv_flops(self):
+        """Algorithmic flops of one forward + backward pass (3 passes/layer)."""
+        return sum(3 * L.flops for L in self.layers)

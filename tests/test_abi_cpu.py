@@ -1,0 +1,147 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+the header declares, validates arguments on the host (no device call is made
+on these paths) and plans the gradient groups."""
+import ctypes
+import json
+import os
+import re
+
+import pytest
+
+import paper_1909_11150_amd as fg
+import synth
+from oracle import grad as G
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fcngrad.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(fg.LIB_PATH):
+        from paper_1909_11150_amd import build
+        build.build()
+    return fg.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*([a-z_0-9]+)\s*\(",
+                                 text, flags=re.M)))
+
+
+def test_header_declares_the_seven_passes_and_helpers():
+    names = declared_functions()
+    for n in ("conv2d_fwd", "conv2d_bwd_data", "conv2d_bwd_weight",
+              "conv_transpose2d_fwd", "grad_group_pack", "grad_unscale_check",
+              "grad_group_unpack"):
+        assert n in names
+    assert set(names) == set(fg.ENTRY_POINTS)
+
+
+def test_library_exports_every_declared_symbol(L):
+    for n in declared_functions():
+        assert hasattr(L, n), n
+
+
+def _desc(**kw):
+    base = dict(n=2, h=8, w=8, c=16, k=16, r=3, s=3, stride=1, pad=1)
+    base.update(kw)
+    return fg.ConvDesc.make(**base)
+
+
+FAKE = 0x1000  # never dereferenced: every call below fails validation
+
+
+def test_invalid_arguments_return_einval(L):
+    d = _desc()
+    ref = ctypes.byref
+    assert L.conv2d_fwd(None, FAKE, FAKE + 4096, FAKE + 8192, 0, None, None, 0, None) == fg.FG_EINVAL
+    assert L.conv2d_fwd(ref(d), None, FAKE, FAKE + 8192, 0, None, None, 0, None) == fg.FG_EINVAL
+    # gate required for the gate epilogue
+    assert L.conv2d_fwd(ref(d), FAKE, FAKE + 1 << 20, FAKE + 1 << 22, fg.EPI_GATE,
+                        None, None, 0, None) == fg.FG_EINVAL
+    # unknown epilogue
+    assert L.conv2d_fwd(ref(d), FAKE, FAKE + (1 << 20), FAKE + (1 << 22), 7,
+                        None, None, 0, None) == fg.FG_EINVAL
+    # output aliasing the input
+    assert L.conv2d_fwd(ref(d), FAKE, FAKE + (1 << 20), FAKE, 0, None, None, 0,
+                        None) == fg.FG_EINVAL
+    # non-positive sizes and a kernel that does not fit
+    for bad in (_desc(n=0), _desc(c=-8), _desc(r=11, pad=0), _desc(stride=0)):
+        assert L.conv2d_fwd(ref(bad), FAKE, FAKE + (1 << 20), FAKE + (1 << 22), 0,
+                            None, None, 0, None) == fg.FG_EINVAL
+    # gradient path
+    seg = (fg.Segment * 1)(fg.Segment(FAKE, 10, 0))
+    assert L.grad_group_pack(seg, 0, FAKE + 4096, 10, None) == fg.FG_EINVAL
+    assert L.grad_group_pack(seg, 1, FAKE + 4096, 5, None) == fg.FG_EINVAL  # outside
+    two = (fg.Segment * 2)(fg.Segment(FAKE, 10, 0), fg.Segment(FAKE + 64, 10, 5))
+    assert L.grad_group_pack(two, 2, FAKE + 4096, 64, None) == fg.FG_EINVAL  # overlap
+    assert L.grad_unscale_check(FAKE, 0, 1.0, FAKE + 4096, FAKE + 8192, None) == fg.FG_EINVAL
+    assert L.grad_unscale_check(FAKE, 100, 1.0, FAKE + 100, FAKE + 8192, None) == fg.FG_EINVAL
+    assert L.grad_group_unpack(FAKE, 10, seg, 1, None) == fg.FG_EINVAL  # dst overlaps group
+    assert L.l2_head_grad(FAKE, FAKE + 4096, 10, 1.0, FAKE, None) == fg.FG_EINVAL
+    assert L.relu_backward(None, FAKE, 10, FAKE + 4096, None) == fg.FG_EINVAL
+
+
+def test_unsupported_shapes(L):
+    ref = ctypes.byref
+    for bad in (_desc(c=12), _desc(k=12), _desc(k=1, r=3), _desc(r=5, s=5, pad=2)):
+        assert L.conv2d_fwd(ref(bad), FAKE, FAKE + (1 << 20), FAKE + (1 << 22), 0,
+                            None, None, 0, None) == fg.FG_EUNSUPPORTED
+    # transposed conv is implemented for 4x4 stride 2 pad 1 only
+    t = fg.ConvDesc.make(1, 4, 4, 16, 16, 3, 3, 2, 1)
+    assert L.conv_transpose2d_fwd(ref(t), FAKE, FAKE + (1 << 20), FAKE + (1 << 22),
+                                  0, None, None, 0, None) == fg.FG_EUNSUPPORTED
+    segs = (fg.Segment * 65)(*[fg.Segment(FAKE + 64 * i, 1, i) for i in range(65)])
+    assert L.grad_group_pack(segs, 65, FAKE + (1 << 20), 65, None) == fg.FG_EUNSUPPORTED
+
+
+def test_workspace_query_and_shortfall(L):
+    ref = ctypes.byref
+    d = fg.ConvDesc.make(4, 64, 64, 512, 1024, 3, 3, 2, 1)
+    need = L.fg_conv_workspace_bytes(ref(d), fg.OP_BWD_WEIGHT)
+    assert need > 0 and need % 4 == 0
+    assert L.fg_conv_workspace_bytes(ref(d), fg.OP_FWD) == 0
+    assert L.conv2d_bwd_weight(ref(d), FAKE, FAKE + (1 << 28), FAKE + (1 << 30),
+                               None, 0, None) == fg.FG_EWORKSPACE
+    assert L.conv2d_bwd_weight(ref(d), FAKE, FAKE + (1 << 28), FAKE + (1 << 30),
+                               FAKE + (1 << 32), need - 4, None) == fg.FG_EWORKSPACE
+    head = fg.ConvDesc.make(4, 256, 256, 256, 1, 1, 1, 1, 0)
+    assert L.fg_conv_workspace_bytes(ref(head), fg.OP_BWD_WEIGHT) > 0
+
+
+def test_out_dims_match_layer_table():
+    for L_ in synth.fcn_layers():
+        n, h, w, c = L_.x_shape
+        d = fg.ConvDesc.make(n, h, w, c, L_.y_shape[3], L_.r, L_.s, L_.stride, L_.pad)
+        assert fg.out_dims(d, transpose=(L_.kind == "convT")) == L_.y_shape[1:3]
+
+
+def test_library_planner_matches_golden_and_oracle():
+    with open(os.path.join(ROOT, "tests", "golden", "fcn_groups.json")) as f:
+        gold = json.load(f)
+    gof, oof, gnum = fg.grad_group_plan(gold["numels"], gold["cap_bytes"],
+                                        gold["align_bytes"], 2)
+    assert gnum == [g["numel"] for g in gold["groups"]]
+    names = gold["completion_order"]
+    members = [[names[i] for i in range(len(names)) if gof[i] == g]
+               for g in range(len(gnum))]
+    assert members == [g["members"] for g in gold["groups"]]
+    # small cases against the oracle planner
+    import numpy as np
+    rng = np.random.default_rng(3)
+    for _ in range(50):
+        numels = [int(v) for v in rng.integers(1, 3000, size=rng.integers(1, 12))]
+        cap = int(rng.integers(512, 8192))
+        plan = G.plan_groups(numels, cap, 256)
+        gof, oof, gnum = fg.grad_group_plan(numels, cap, 256, 2)
+        assert gnum == [p["numel"] for p in plan]
+        for gi, p in enumerate(plan):
+            for m, off in zip(p["members"], p["offsets"]):
+                assert gof[m] == gi and oof[m] == off
+
+
+def test_status_strings(L):
+    assert fg.status_string(fg.FG_EWORKSPACE).startswith("FG_EWORKSPACE")

@@ -1,0 +1,212 @@
+"""GPU parity of whole workloads: the single conv, the encoder and decoder
+blocks, a reduced encoder-decoder step with the gradient path, and every
+layer of the full network at full size (sampled outputs).
+
+Chains: the oracle runs the same chain from the same seeded inputs, storing
+each activation and gradient in fp16 like the GPU (O16). Per-op differences
+(last bits of fp16 outputs, a ReLU decision on a value within an ulp of
+zero) propagate down a chain, so chained outputs cannot be held to the
+single-op rule. The bound is derived from the arithmetic instead: the GPU
+may differ from O16 by no more than fp16 storage itself moves the chain,
+measured as the distance between O16 and the same chain kept in fp64
+(O64), with the single-op bounds as a floor:
+    rel_L2(GPU, O16)      <= max(5e-3, rel_L2(O16, O64))
+    max_abs/RMS(GPU, O16) <= max(2e-2, max_abs/RMS(O16, O64)).
+Single ops (the first op of each chain, every full-size layer) keep the
+full single-op rule.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_1909_11150_amd as fg
+import synth
+from gpu_util import conv_parity, dev, host, sample_indices
+from oracle import chain as OC
+from oracle import grad as G
+from paper_1909_11150_amd.fcn import Chain
+
+pytestmark = pytest.mark.gpu
+
+
+def _dist(a, b):
+    a = np.asarray(a, np.float64).ravel()
+    b = np.asarray(b, np.float64).ravel()
+    d = a - b
+    rel = np.linalg.norm(d) / max(np.linalg.norm(b), 1e-30)
+    ratio = np.max(np.abs(d)) / max(np.sqrt(np.mean(b ** 2)), 1e-30)
+    return rel, ratio
+
+
+def chain_parity(g16, o16, o64, what):
+    assert np.all(np.isfinite(np.asarray(g16, np.float64))), what
+    rel, ratio = _dist(g16, o16)
+    rel_n, ratio_n = _dist(o16, o64)
+    assert rel <= max(5e-3, rel_n), f"{what}: rel_L2 {rel:.3e} (fp16 noise {rel_n:.3e})"
+    assert ratio <= max(2e-2, ratio_n), \
+        f"{what}: max_abs/RMS {ratio:.3e} (fp16 noise {ratio_n:.3e})"
+    return rel, ratio
+
+
+def test_single_conv_workload():
+    wl = synth.single_conv()
+    L = wl.layers[0]
+    ch = Chain(wl.layers, wl.weights, wl.x)
+    ch.forward()
+    ch.set_output_grad(wl.dy)
+    ch.backward()
+    conv_parity(host(ch.acts[1]), oracle.conv2d_fwd(wl.x, wl.weights[0], 1, 1), "fwd")
+    conv_parity(host(ch.g[0]),
+                oracle.conv2d_bwd_data(wl.dy, wl.weights[0], wl.x.shape, 1, 1), "dx")
+    conv_parity(host(ch.dw[0]), oracle.conv2d_bwd_weight(wl.x, wl.dy, 3, 3, 1, 1), "dW")
+    assert L.flops == 2 * 2 * 64 * 64 * 16 * 16 * 9
+
+
+def _check_block(wl, gate_top):
+    ch = Chain(wl.layers, wl.weights, wl.x)
+    ch.forward()
+    ch.set_output_grad(wl.dy)
+    ch.backward()
+    acts = OC.forward(wl.layers, wl.x, wl.weights)
+    dy = G.relu_backward(wl.dy, acts[-1]) if gate_top else wl.dy
+    dws, dxs = OC.backward(wl.layers, acts, wl.weights, dy)
+    a64 = OC.forward(wl.layers, wl.x, wl.weights, store_fp16=False)
+    dy64 = wl.dy.astype(np.float64)
+    if gate_top:
+        dy64 = np.where(a64[-1] > 0, dy64, 0.0)
+    dws64, dxs64 = OC.backward(wl.layers, a64, wl.weights, dy64, store_fp16=False)
+    for i in range(len(wl.layers)):
+        chain_parity(host(ch.acts[i + 1]), acts[i + 1], a64[i + 1], f"act{i}")
+        chain_parity(host(ch.dw[i]), dws[i], dws64[i], f"dW{i}")
+        chain_parity(host(ch.g[i]), dxs[i], dxs64[i], f"dx{i}")
+    # the first op of each chain sees identical inputs: full single-op rule
+    conv_parity(host(ch.acts[1]),
+                OC.layer_forward(wl.layers[0], wl.x, wl.weights[0]), "first fwd")
+
+
+def test_encoder_block_workload():
+    _check_block(synth.encoder_block(), gate_top=True)
+
+
+def test_decoder_block_workload():
+    _check_block(synth.decoder_block(), gate_top=False)
+
+
+def test_reduced_network_step_with_gradient_path():
+    """Same architecture at 1 x 64 x 64 x 32 with narrower layers; groups
+    capped at 64 KiB so that several groups form; loss scale 2^15."""
+    layers = synth.fcn_layers(n=1, h=64, c_in=32, widths=(32, 64, 64, 64),
+                              dec=(64, 64, 32, 32))
+    x = synth.diffraction_like(1, 64, 32, seed=0)
+    w = synth.he_weights(layers, seed=1)
+    t = synth.smooth_target(1, 64, seed=4)
+    S = 2.0 ** 15
+    ch = Chain(layers, w, x, loss_scale=S, group_cap_bytes=64 * 1024)
+    ch.step(dev(t))
+    acts = OC.forward(layers, x, w)
+    dy = OC.head_grad(acts[-1], t, S)
+    dws, _ = OC.backward(layers, acts, w, dy)
+    a64 = OC.forward(layers, x, w, store_fp16=False)
+    dws64, _ = OC.backward(layers, a64, w, OC.head_grad(a64[-1], t, S, store_fp16=False),
+                           store_fp16=False)
+    for i, L in enumerate(layers):
+        chain_parity(host(ch.acts[i + 1]), acts[i + 1], a64[i + 1], f"{L.name} act")
+        chain_parity(host(ch.dw[i]), dws[i], dws64[i], f"{L.name} dW")
+        # fp32 master gradient = fp16 dW / S, exactly, on the GPU's own dW
+        np.testing.assert_array_equal(
+            host(ch.master[i]),
+            host(ch.dw[i]).astype(np.float32) * np.float32(1.0 / S))
+    plan = G.plan_groups([layers[i].w_numel for i in reversed(range(len(layers)))],
+                         64 * 1024, 256)
+    assert len(ch.groups) == len(plan) > 1
+    flags = host(ch.flags)
+    ref_flags = [int(any(G.found_nonfinite(dws[len(layers) - 1 - m].view(np.uint16))
+                         for m in p["members"])) for p in plan]
+    np.testing.assert_array_equal(flags, ref_flags)
+
+
+LAYERS = synth.fcn_layers()
+
+
+def _layer_inputs(L, seed):
+    """Seeded full-size inputs of one layer: post-ReLU activations (or the
+    diffraction-like input for the first layer), He weights, and an output
+    gradient of the magnitude the loss-scaled network produces."""
+    rng = np.random.default_rng(seed)
+    if L.name == "E1a":
+        x = synth.diffraction_like(*L.x_shape[:2], L.x_shape[3], seed=0)
+    else:
+        x = np.maximum(synth.normal(rng, L.x_shape), np.float16(0))
+    w = synth.normal(rng, L.w_shape, synth.he_std(L))
+    dy = synth.normal(rng, L.y_shape, 1.0)
+    return x, w, dy
+
+
+@pytest.mark.parametrize("L", LAYERS, ids=[L.name for L in LAYERS])
+def test_full_size_layer_sampled(L):
+    x, w, dy = _layer_inputs(L, LAYERS.index(L) + 100)
+    rng = np.random.default_rng(7)
+    dx_, w_, dy_ = dev(x), dev(w), dev(dy)
+    y = torch.empty(L.y_shape, dtype=torch.float16, device="cuda")
+    dx = torch.empty(L.x_shape, dtype=torch.float16, device="cuda")
+    dw = torch.empty(L.w_shape, dtype=torch.float16, device="cuda")
+    from paper_1909_11150_amd import fcn
+    if L.kind == "conv":
+        d = fcn.fwd_desc(L)
+        ws = torch.empty(max(16, fg.workspace_bytes(d, fg.OP_BWD_WEIGHT)),
+                         dtype=torch.uint8, device="cuda")
+        fg.conv2d_fwd(d, dx_, w_, y, fg.EPI_RELU if L.relu else fg.EPI_NONE)
+        fg.conv2d_bwd_data(d, dy_, w_, dx, fg.EPI_GATE, dx_)
+        fg.conv2d_bwd_weight(d, dx_, dy_, dw, ws)
+        iy = sample_indices(L.y_shape, 3000, rng)
+        ref = oracle.conv2d_fwd_points(x, w, iy, L.stride, L.pad)
+        if L.relu:
+            ref = oracle.relu(ref)
+        conv_parity(host(y).ravel()[iy], ref, "fwd")
+        ix = sample_indices(L.x_shape, 3000, rng)
+        ref = oracle.conv2d_bwd_data_points(dy, w, x.shape, ix, L.stride, L.pad)
+        ref = np.where(x.ravel()[ix].astype(np.float64) > 0, ref, 0.0)
+        conv_parity(host(dx).ravel()[ix], ref, "dx")
+        iw = sample_indices(L.w_shape, 1500, rng)
+        ref = oracle.conv2d_bwd_weight_points(x, dy, L.r, L.s, iw, L.stride, L.pad)
+        conv_parity(host(dw).ravel()[iw], ref, "dW")
+    else:
+        d = fcn.fwd_desc(L)
+        dd = fcn.convt_dx_desc(L)
+        ws = torch.empty(max(16, fg.workspace_bytes(dd, fg.OP_BWD_WEIGHT)),
+                         dtype=torch.uint8, device="cuda")
+        fg.conv_transpose2d_fwd(d, dx_, w_, y, fg.EPI_RELU)
+        fg.conv2d_fwd(dd, dy_, w_, dx, fg.EPI_GATE, dx_)
+        fg.conv2d_bwd_weight(dd, dy_, dx_, dw, ws)
+        iy = sample_indices(L.y_shape, 3000, rng)
+        ref = oracle.relu(oracle.conv_transpose2d_fwd_points(x, w, iy, 2, 1))
+        conv_parity(host(y).ravel()[iy], ref, "convT fwd")
+        ix = sample_indices(L.x_shape, 3000, rng)
+        ref = oracle.conv2d_fwd_points(dy, w, ix, 2, 1)
+        ref = np.where(x.ravel()[ix].astype(np.float64) > 0, ref, 0.0)
+        conv_parity(host(dx).ravel()[ix], ref, "convT dx")
+        iw = sample_indices(L.w_shape, 1500, rng)
+        ref = oracle.conv2d_bwd_weight_points(dy, x, L.r, L.s, iw, 2, 1)
+        conv_parity(host(dw).ravel()[iw], ref, "convT dW")
+
+
+def test_full_network_step_is_deterministic_and_finite():
+    """The benchmarked step at full size: two steps give identical bits,
+    every activation is finite, and no group is flagged."""
+    wl = synth.fcn()
+    ch = Chain(wl.layers, wl.weights, wl.x, group_cap_bytes=synth.GROUP_CAP_BYTES)
+    t = dev(wl.target)
+    ch.step(t)
+    first = [host(a).view(np.uint16).copy() for a in ch.acts[1:]] + \
+            [host(m).view(np.uint32).copy() for m in ch.master]
+    f1 = host(ch.flags).copy()
+    ch.step(t)
+    second = [host(a).view(np.uint16) for a in ch.acts[1:]] + \
+             [host(m).view(np.uint32) for m in ch.master]
+    for a, b in zip(first, second):
+        assert np.array_equal(a, b)
+    np.testing.assert_array_equal(f1, host(ch.flags))
+    for a in ch.acts[1:]:
+        assert torch.isfinite(a).all()
+    assert len(ch.groups) == 9
