@@ -14,6 +14,10 @@ HIP events on its own stream inside the timed region), the gradient-path
 bandwidths and the CPU oracle timed on a bounded sample of the same work.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu]
+       python bench.py --op E2b.fwd|E2b.dx|E2b.dW|copy [--steps K]
+The --op form runs one pass of one layer (seeded full-size inputs) K times
+and prints its per-launch time; `copy` is a plain 256 MiB fp16 copy through
+grad_group_pack, the reference for scaling HBM byte counters.
 """
 import argparse
 import json
@@ -41,7 +45,70 @@ def parse():
                     help="approximate CPU work of the oracle sample")
     ap.add_argument("--detail", default=None,
                     help="write per-op timings (JSON) to this path")
+    ap.add_argument("--op", default=None,
+                    help="time one pass of one layer, e.g. E2b.fwd, or 'copy'")
     return ap.parse_args()
+
+
+def op_bench(label, steps, warmup):
+    """Time one library call in isolation on seeded full-size inputs."""
+    import torch
+
+    import paper_1909_11150_amd as fg
+    import synth
+    from paper_1909_11150_amd import fcn
+    rng = np.random.default_rng(5)
+    if label == "copy":
+        n = 128 * 1024 * 1024  # 256 MiB of fp16 in, 256 MiB out
+        src = torch.from_numpy(rng.integers(0, 0x7BFF, size=n, dtype=np.int16)).cuda()
+        dst = torch.empty(n, dtype=torch.int16, device="cuda")
+        fn = lambda: fg.grad_group_pack([src], [0], dst)
+        work, unit, kern = 4 * n, "GB/s", "copy_pieces_kernel<2>"
+    else:
+        name, pas = label.split(".")
+        L = {l.name: l for l in synth.fcn_layers()}[name]
+        x = torch.from_numpy(np.maximum(synth.normal(rng, L.x_shape), np.float16(0))).cuda()
+        w = torch.from_numpy(synth.normal(rng, L.w_shape, synth.he_std(L))).cuda()
+        dy = torch.from_numpy(synth.normal(rng, L.y_shape)).cuda()
+        y = torch.empty(L.y_shape, dtype=torch.float16, device="cuda")
+        dx = torch.empty(L.x_shape, dtype=torch.float16, device="cuda")
+        dw = torch.empty(L.w_shape, dtype=torch.float16, device="cuda")
+        ws = torch.empty(max(16, fcn.chain_workspace_bytes([L])), dtype=torch.uint8,
+                         device="cuda")
+        d, dd = fcn.fwd_desc(L), fcn.convt_dx_desc(L)
+        conv = L.kind == "conv"
+        calls = {
+            "fwd": (lambda: fg.conv2d_fwd(d, x, w, y, fg.EPI_RELU, None, ws),
+                    fg.kernel_name(d, fg.OP_FWD)) if conv else
+                   (lambda: fg.conv_transpose2d_fwd(d, x, w, y, fg.EPI_RELU, None, ws),
+                    fg.kernel_name(d, fg.OP_CONVT)),
+            "dx": (lambda: fg.conv2d_bwd_data(d, dy, w, dx, fg.EPI_GATE, x, ws),
+                   fg.kernel_name(d, fg.OP_BWD_DATA)) if conv else
+                  (lambda: fg.conv2d_fwd(dd, dy, w, dx, fg.EPI_GATE, x, ws),
+                   fg.kernel_name(dd, fg.OP_FWD)),
+            "dW": (lambda: fg.conv2d_bwd_weight(d, x, dy, dw, ws),
+                   fg.kernel_name(d, fg.OP_BWD_WEIGHT)) if conv else
+                  (lambda: fg.conv2d_bwd_weight(dd, dy, x, dw, ws),
+                   fg.kernel_name(dd, fg.OP_BWD_WEIGHT)),
+        }
+        fn, kern = calls[pas]
+        work, unit = L.flops, "TFLOP/s"
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    for e0, e1 in evs:
+        e0.record()
+        fn()
+        e1.record()
+    torch.cuda.synchronize()
+    ts = sorted(e0.elapsed_time(e1) for e0, e1 in evs)
+    med = ts[len(ts) // 2] * 1e-3
+    rate = work / med / (1e12 if unit == "TFLOP/s" else 1e9)
+    print(json.dumps({"op": label, "kernel": kern, "median_us": round(med * 1e6, 2),
+                      "min_us": round(ts[0] * 1e3, 2), "rate": round(rate, 1),
+                      "unit": unit, "launches": steps}), flush=True)
 
 
 class TimedChain:
@@ -73,11 +140,12 @@ class TimedChain:
             d = fcn.fwd_desc(L)
             if L.kind == "conv":
                 self.call(f"{L.name}.fwd", fg.kernel_name(d, fg.OP_FWD), L.flops,
-                          fg.conv2d_fwd, d, ch.acts[i], ch.w[i], ch.acts[i + 1], epi)
+                          fg.conv2d_fwd, d, ch.acts[i], ch.w[i], ch.acts[i + 1], epi,
+                          None, ch.ws)
             else:
                 self.call(f"{L.name}.fwd", fg.kernel_name(d, fg.OP_CONVT), L.flops,
                           fg.conv_transpose2d_fwd, d, ch.acts[i], ch.w[i],
-                          ch.acts[i + 1], epi)
+                          ch.acts[i + 1], epi, None, ch.ws)
         y = ch.acts[-1]
         self.call("head_grad", "head_grad_kernel", y.numel() * 6, fg.l2_head_grad,
                   y, target, 2.0 * ch.loss_scale / y.numel(), ch.g[-1])
@@ -93,13 +161,13 @@ class TimedChain:
                 self.call(f"{L.name}.dW", fg.kernel_name(d, fg.OP_BWD_WEIGHT), L.flops,
                           fg.conv2d_bwd_weight, d, ch.acts[i], dy, ch.dw[i], ch.ws)
                 self.call(f"{L.name}.dx", fg.kernel_name(d, fg.OP_BWD_DATA), L.flops,
-                          fg.conv2d_bwd_data, d, dy, ch.w[i], ch.g[i], epi, gt)
+                          fg.conv2d_bwd_data, d, dy, ch.w[i], ch.g[i], epi, gt, ch.ws)
             else:
                 dd = fcn.convt_dx_desc(L)
                 self.call(f"{L.name}.dW", fg.kernel_name(dd, fg.OP_BWD_WEIGHT), L.flops,
                           fg.conv2d_bwd_weight, dd, dy, ch.acts[i], ch.dw[i], ch.ws)
                 self.call(f"{L.name}.dx", fg.kernel_name(dd, fg.OP_FWD), L.flops,
-                          fg.conv2d_fwd, dd, dy, ch.w[i], ch.g[i], epi, gt)
+                          fg.conv2d_fwd, dd, dy, ch.w[i], ch.g[i], epi, gt, ch.ws)
             gi = ch._group_done_at.get(i)
             if gi is not None:
                 g = ch.groups[gi]
@@ -168,6 +236,9 @@ def cpu_baseline(layers, seconds):
 
 def main():
     args = parse()
+    if args.op:
+        op_bench(args.op, args.steps, args.warmup)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; "
                           "--gpus must be 1 (multi-GPU sharding is design-only)"}))

@@ -113,6 +113,101 @@ int make_phases(DataConvArgs &a, int32_t ho, int32_t wo, int32_t sh,
   return np;
 }
 
+// Argument builders shared by the launch, workspace and kernel-name paths.
+DataConvArgs fwd_args(const fg_conv_desc *d, int32_t P, int32_t Q) {
+  DataConvArgs a;
+  memset(&a, 0, sizeof(a));
+  a.n = d->n; a.hi = d->h; a.wi = d->w; a.cr = d->c;
+  a.ho = P; a.wo = Q; a.co = d->k;
+  a.istr = d->stride_h;
+  a.ostr = 1;
+  a.s = d->s;
+  a.ldw = d->r * d->s * d->c;
+  a.nphase = 1;
+  a.nsplit = 1;
+  Phase &ph = a.ph[0];
+  ph.mh = P; ph.mw = Q; ph.ooh = 0; ph.oow = 0;
+  ph.nr = d->r; ph.ns = d->s;
+  ph.dh0 = -d->pad_h; ph.dw0 = -d->pad_w; ph.dstep = 1;
+  ph.r0 = 0; ph.s0 = 0; ph.rstep = 1;
+  return a;
+}
+
+DataConvArgs bwd_data_args(const fg_conv_desc *d, int32_t P, int32_t Q) {
+  DataConvArgs a;
+  memset(&a, 0, sizeof(a));
+  a.n = d->n; a.hi = P; a.wi = Q; a.cr = d->k;
+  a.ho = d->h; a.wo = d->w; a.co = d->c;
+  a.istr = 1;
+  a.ostr = d->stride_h;
+  a.s = d->s;
+  a.w_red = d->r * d->s * d->c;  // W[k][r][s][c]: reduction index k
+  a.w_tap = d->c;
+  a.nsplit = 1;
+  a.nphase = make_phases(a, d->h, d->w, d->stride_h, d->stride_w, d->pad_h,
+                         d->pad_w, d->r, d->s);
+  return a;
+}
+
+DataConvArgs convt_args(const fg_conv_desc *d, int32_t HO, int32_t WO) {
+  DataConvArgs a;
+  memset(&a, 0, sizeof(a));
+  a.n = d->n; a.hi = d->h; a.wi = d->w; a.cr = d->c;
+  a.ho = HO; a.wo = WO; a.co = d->k;
+  a.istr = 1;
+  a.ostr = d->stride_h;
+  a.s = d->s;
+  a.w_red = d->r * d->s * d->k;  // Wt[c][r][s][k]: reduction index c
+  a.w_tap = d->k;
+  a.nsplit = 1;
+  a.nphase = make_phases(a, HO, WO, d->stride_h, d->stride_w, d->pad_h,
+                         d->pad_w, d->r, d->s);
+  return a;
+}
+
+bool convt_supported(const fg_conv_desc *d) {
+  return d->c % 8 == 0 && d->k % 8 == 0 && d->r == 4 && d->s == 4 &&
+         d->stride_h == 2 && d->stride_w == 2 && d->pad_h == 1 &&
+         d->pad_w == 1;
+}
+
+bool bwd_data_supported(const fg_conv_desc *d) {
+  return check_conv_support(d) == FG_OK && d->stride_h == d->stride_w &&
+         d->stride_h <= 2;
+}
+
+bool fwd_supported(const fg_conv_desc *d) {
+  return check_conv_support(d) == FG_OK && d->stride_h == d->stride_w;
+}
+
+// Workspace of a data convolution pass (0 when it does not split).
+size_t data_ws(const fg_conv_desc *d, int op) {
+  int32_t p, q;
+  if (op == FG_OP_CONVT) {
+    if (!convt_supported(d) || fg_conv_out_dims(d, 1, &p, &q) != FG_OK) return 0;
+    return plan_data_conv(convt_args(d, p, q)).ws_bytes;
+  }
+  if (fg_conv_out_dims(d, 0, &p, &q) != FG_OK || d->k == 1) return 0;
+  if (op == FG_OP_FWD)
+    return fwd_supported(d) ? plan_data_conv(fwd_args(d, p, q)).ws_bytes : 0;
+  return bwd_data_supported(d) ? plan_data_conv(bwd_data_args(d, p, q)).ws_bytes
+                               : 0;
+}
+
+// Workspace present and large enough, and not overlapping the tensors
+// (byte ranges (p_i, n_i)).
+fg_status check_ws(const fg_conv_desc *d, int op, void *ws, size_t ws_bytes,
+                   const void *p0, size_t n0, const void *p1, size_t n1,
+                   const void *p2, size_t n2, const void *p3, size_t n3) {
+  const size_t need = fg_conv_workspace_bytes(d, op);
+  if (need == 0) return FG_OK;
+  if (!ws || ws_bytes < need) return FG_EWORKSPACE;
+  if (overlap(ws, need, p0, n0) || overlap(ws, need, p1, n1) ||
+      (p2 && overlap(ws, need, p2, n2)) || (p3 && overlap(ws, need, p3, n3)))
+    return FG_EINVAL;
+  return FG_OK;
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
@@ -152,27 +247,34 @@ size_t fg_conv_workspace_bytes(const fg_conv_desc *d, int op) {
   if (op == FG_OP_BWD_WEIGHT) {
     int32_t p, q;
     if (fg_conv_out_dims(d, 0, &p, &q) != FG_OK) return 0;
+    if (check_conv_support(d) != FG_OK) return 0;
     if (is_head(d)) return head_wgrad_ws_bytes(*d);
     return plan_wgrad(*d, p, q).ws_bytes;
   }
+  if (op == FG_OP_FWD || op == FG_OP_BWD_DATA || op == FG_OP_CONVT)
+    return data_ws(d, op);
   return 0;
 }
 
 const char *fg_conv_kernel_name(const fg_conv_desc *d, int op) {
   if (check_desc(d) != FG_OK) return "";
+  int32_t p, q;
   switch (op) {
     case FG_OP_FWD:
-      if (check_conv_support(d) != FG_OK) return "";
-      return d->k == 1 ? "head_fwd_kernel" : data_conv_kernel_name(d->c, true);
+      if (!fwd_supported(d) || fg_conv_out_dims(d, 0, &p, &q) != FG_OK) return "";
+      return d->k == 1 ? "head_fwd_kernel"
+                       : data_conv_kernel_name(fwd_args(d, p, q), true);
     case FG_OP_BWD_DATA:
-      if (check_conv_support(d) != FG_OK) return "";
+      if (!bwd_data_supported(d) || fg_conv_out_dims(d, 0, &p, &q) != FG_OK)
+        return "";
       return d->k == 1 ? "head_bwd_data_kernel"
-                       : data_conv_kernel_name(d->k, false);
+                       : data_conv_kernel_name(bwd_data_args(d, p, q), false);
     case FG_OP_BWD_WEIGHT:
       if (check_conv_support(d) != FG_OK) return "";
-      return d->k == 1 ? "head_wgrad_kernel" : wgrad_kernel_name();
+      return d->k == 1 ? "head_wgrad_kernel" : wgrad_kernel_name(*d);
     case FG_OP_CONVT:
-      return data_conv_kernel_name(d->c, false);
+      if (!convt_supported(d) || fg_conv_out_dims(d, 1, &p, &q) != FG_OK) return "";
+      return data_conv_kernel_name(convt_args(d, p, q), false);
   }
   return "";
 }
@@ -181,8 +283,6 @@ fg_status conv2d_fwd(const fg_conv_desc *d, const uint16_t *x,
                      const uint16_t *w_krsc, uint16_t *y, fg_epilogue epi,
                      const uint16_t *gate, void *ws, size_t ws_bytes,
                      hipStream_t stream) {
-  (void)ws;
-  (void)ws_bytes;
   fg_status st = check_desc(d);
   if (st != FG_OK) return st;
   if (!x || !w_krsc || !y) return FG_EINVAL;
@@ -204,25 +304,16 @@ fg_status conv2d_fwd(const fg_conv_desc *d, const uint16_t *x,
   if (d->k == 1)
     return launch_status(launch_head_fwd(x, w_krsc, y, (int64_t)d->n * P * Q,
                                          d->c, epi, gate, stream));
-  DataConvArgs a;
-  memset(&a, 0, sizeof(a));
+  if ((st = check_ws(d, FG_OP_FWD, ws, ws_bytes, x, nx * 2, w_krsc, nw * 2, y,
+                     ny * 2, gate, ny * 2)) != FG_OK)
+    return st;
+  DataConvArgs a = fwd_args(d, P, Q);
   a.act = x;
   a.wgt = w_krsc;
   a.out = y;
   a.gate = gate;
-  a.n = d->n; a.hi = d->h; a.wi = d->w; a.cr = d->c;
-  a.ho = P; a.wo = Q; a.co = d->k;
-  a.istr = d->stride_h;
-  a.ostr = 1;
-  a.s = d->s;
-  a.ldw = d->r * d->s * d->c;
   a.epi = epi;
-  a.nphase = 1;
-  Phase &ph = a.ph[0];
-  ph.mh = P; ph.mw = Q; ph.ooh = 0; ph.oow = 0;
-  ph.nr = d->r; ph.ns = d->s;
-  ph.dh0 = -d->pad_h; ph.dw0 = -d->pad_w; ph.dstep = 1;
-  ph.r0 = 0; ph.s0 = 0; ph.rstep = 1;
+  a.part = (float *)ws;
   return launch_status(launch_data_conv(a, true, stream));
 }
 
@@ -230,8 +321,6 @@ fg_status conv2d_bwd_data(const fg_conv_desc *d, const uint16_t *dy,
                           const uint16_t *w_krsc, uint16_t *dx,
                           fg_epilogue epi, const uint16_t *gate, void *ws,
                           size_t ws_bytes, hipStream_t stream) {
-  (void)ws;
-  (void)ws_bytes;
   fg_status st = check_desc(d);
   if (st != FG_OK) return st;
   if (!dy || !w_krsc || !dx) return FG_EINVAL;
@@ -252,22 +341,16 @@ fg_status conv2d_bwd_data(const fg_conv_desc *d, const uint16_t *dy,
   if (d->k == 1)
     return launch_status(launch_head_bwd_data(
         dy, w_krsc, dx, (int64_t)d->n * d->h * d->w, d->c, epi, gate, stream));
-  DataConvArgs a;
-  memset(&a, 0, sizeof(a));
+  if ((st = check_ws(d, FG_OP_BWD_DATA, ws, ws_bytes, dy, ny * 2, w_krsc, nw * 2,
+                     dx, nx * 2, gate, nx * 2)) != FG_OK)
+    return st;
+  DataConvArgs a = bwd_data_args(d, P, Q);
   a.act = dy;
   a.wgt = w_krsc;
   a.out = dx;
   a.gate = gate;
-  a.n = d->n; a.hi = P; a.wi = Q; a.cr = d->k;
-  a.ho = d->h; a.wo = d->w; a.co = d->c;
-  a.istr = 1;
-  a.ostr = d->stride_h;
-  a.s = d->s;
-  a.w_red = d->r * d->s * d->c;  // W[k][r][s][c]: reduction index k
-  a.w_tap = d->c;
   a.epi = epi;
-  a.nphase = make_phases(a, d->h, d->w, d->stride_h, d->stride_w, d->pad_h,
-                         d->pad_w, d->r, d->s);
+  a.part = (float *)ws;
   return launch_status(launch_data_conv(a, false, stream));
 }
 
@@ -275,8 +358,6 @@ fg_status conv_transpose2d_fwd(const fg_conv_desc *d, const uint16_t *x,
                                const uint16_t *w_crsk, uint16_t *y,
                                fg_epilogue epi, const uint16_t *gate,
                                void *ws, size_t ws_bytes, hipStream_t stream) {
-  (void)ws;
-  (void)ws_bytes;
   fg_status st = check_desc(d);
   if (st != FG_OK) return st;
   if (!x || !w_crsk || !y) return FG_EINVAL;
@@ -291,26 +372,17 @@ fg_status conv_transpose2d_fwd(const fg_conv_desc *d, const uint16_t *x,
   if (!sizes_ok(nx, nw, ny)) return FG_EUNSUPPORTED;
   if (overlap(y, ny * 2, x, nx * 2) || overlap(y, ny * 2, w_crsk, nw * 2))
     return FG_EINVAL;
-  if (d->c % 8 != 0 || d->k % 8 != 0 || d->r != 4 || d->s != 4 ||
-      d->stride_h != 2 || d->stride_w != 2 || d->pad_h != 1 || d->pad_w != 1)
-    return FG_EUNSUPPORTED;
-
-  DataConvArgs a;
-  memset(&a, 0, sizeof(a));
+  if (!convt_supported(d)) return FG_EUNSUPPORTED;
+  if ((st = check_ws(d, FG_OP_CONVT, ws, ws_bytes, x, nx * 2, w_crsk, nw * 2, y,
+                     ny * 2, gate, ny * 2)) != FG_OK)
+    return st;
+  DataConvArgs a = convt_args(d, HO, WO);
   a.act = x;
   a.wgt = w_crsk;
   a.out = y;
   a.gate = gate;
-  a.n = d->n; a.hi = d->h; a.wi = d->w; a.cr = d->c;
-  a.ho = HO; a.wo = WO; a.co = d->k;
-  a.istr = 1;
-  a.ostr = d->stride_h;
-  a.s = d->s;
-  a.w_red = d->r * d->s * d->k;  // Wt[c][r][s][k]: reduction index c
-  a.w_tap = d->k;
   a.epi = epi;
-  a.nphase = make_phases(a, HO, WO, d->stride_h, d->stride_w, d->pad_h,
-                         d->pad_w, d->r, d->s);
+  a.part = (float *)ws;
   return launch_status(launch_data_conv(a, false, stream));
 }
 
@@ -330,11 +402,9 @@ fg_status conv2d_bwd_weight(const fg_conv_desc *d, const uint16_t *x,
       overlap(dw_krsc, nw * 2, dy, ny * 2))
     return FG_EINVAL;
   if ((st = check_conv_support(d)) != FG_OK) return st;
-  const size_t need = fg_conv_workspace_bytes(d, FG_OP_BWD_WEIGHT);
-  if (need > 0 && (!ws || ws_bytes < need)) return FG_EWORKSPACE;
-  if (need > 0 && (overlap(ws, need, dw_krsc, nw * 2) ||
-                   overlap(ws, need, x, nx * 2) || overlap(ws, need, dy, ny * 2)))
-    return FG_EINVAL;
+  if ((st = check_ws(d, FG_OP_BWD_WEIGHT, ws, ws_bytes, x, nx * 2, dy, ny * 2,
+                     dw_krsc, nw * 2, nullptr, 0)) != FG_OK)
+    return st;
 
   if (d->k == 1)
     return launch_status(launch_head_wgrad(x, dy, dw_krsc,

@@ -5,27 +5,36 @@
 // phase, and the reduction runs over (tap, input channel). The input image is
 // gathered straight from NHWC memory (zero outside the image); nothing is
 // materialised. Strided input gradients and transposed convolutions are split
-// into output phases so that no multiply touches an inserted zero.
+// into output phases so that no multiply touches an inserted zero. Shapes
+// that give too few output tiles to fill the GPU split the reduction across
+// workgroups; fp32 partials are then summed in split order by a second kernel
+// that also applies the epilogue.
 //
 // The kernel gradient is a second kernel: rows are (tap, input channel),
 // columns output channels, reduction over all output positions, split across
 // workgroups with fp32 partials summed afterwards in a fixed order.
 //
 // Both kernels stage 64-deep reduction slices of each operand in LDS (double
-// buffered, one barrier per slice) in a layout where every MFMA operand is a
-// single 16-byte read. Operands whose reduction dimension is strided in
-// memory are transposed in registers on their way to LDS.
+// buffered, one barrier per slice). LDS rows are 128 bytes with the eight
+// 16-byte chunks of a row permuted by an XOR of row bits, so the 16-byte MFMA
+// operand reads of 8 consecutive rows hit distinct banks. Operands whose
+// reduction dimension is strided in memory are transposed in registers on
+// their way to LDS. Each of the 4 waves owns a (BM/2) x (BN/2) block of the
+// tile and issues v_mfma_f32_32x32x16_f16 over it.
 #include "common.h"
 #include "internal.h"
 
 namespace fg {
 
-constexpr int BK = 64;        // reduction slice per LDS stage
-constexpr int LDK = BK + 8;   // LDS row pitch in halves (16-byte skew)
+constexpr int BK = 64;        // reduction slice per LDS stage (halves)
 constexpr int NT = 256;       // threads per workgroup (4 waves, 2 x 2)
 
+// Offset (in halves) of 16-byte chunk `chunk` (0..7) of LDS row `row`.
+__device__ __forceinline__ int lds_idx(int row, int chunk) {
+  return row * BK + ((chunk ^ ((row ^ (row >> 3)) & 7)) << 3);
+}
+
 // ---------------------------------------------------------------------------
-// MFMA core: each wave owns a (BM/2) x (BN/2) block of the tile.
 template <int BM, int BN>
 struct Core {
   static constexpr int WM = BM / 2, WN = BN / 2;
@@ -43,18 +52,18 @@ struct Core {
 
   __device__ void step(const uint16_t *sA, const uint16_t *sB, int wm0,
                        int wn0, int lane) {
-    const int r = lane & 31, kh = (lane >> 5) * 8;
+    const int r = lane & 31, kh = lane >> 5;
 #pragma unroll
-    for (int ks = 0; ks < BK; ks += 16) {
+    for (int ks = 0; ks < BK / 16; ++ks) {
       u32x4 a[FM], b[FN];
 #pragma unroll
       for (int i = 0; i < FM; ++i)
         a[i] = *reinterpret_cast<const u32x4 *>(
-            sA + (wm0 + i * 32 + r) * LDK + ks + kh);
+            sA + lds_idx(wm0 + i * 32 + r, 2 * ks + kh));
 #pragma unroll
       for (int j = 0; j < FN; ++j)
         b[j] = *reinterpret_cast<const u32x4 *>(
-            sB + (wn0 + j * 32 + r) * LDK + ks + kh);
+            sB + lds_idx(wn0 + j * 32 + r, 2 * ks + kh));
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -63,9 +72,10 @@ struct Core {
   }
 };
 
-// Transpose 4 rows of 8 halves (reduction index = row) into 8 columns of 4
-// halves and store column j at dst + j*LDK (8 bytes each).
-__device__ __forceinline__ void store_t4x8(uint16_t *dst, const u32x4 q[4]) {
+// Transpose 4 rows of 8 halves (row = reduction index) into 8 LDS rows
+// row0..row0+7 at 4-half unit kq (8 bytes each).
+__device__ __forceinline__ void store_t4x8(uint16_t *s, int row0, int kq,
+                                           const u32x4 q[4]) {
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     u32x2 lo, hi;
@@ -73,13 +83,37 @@ __device__ __forceinline__ void store_t4x8(uint16_t *dst, const u32x4 q[4]) {
     lo[1] = pack_lo(q[2][e], q[3][e]);
     hi[0] = pack_hi(q[0][e], q[1][e]);
     hi[1] = pack_hi(q[2][e], q[3][e]);
-    *reinterpret_cast<u32x2 *>(dst + (2 * e) * LDK) = lo;
-    *reinterpret_cast<u32x2 *>(dst + (2 * e + 1) * LDK) = hi;
+    const int r0 = row0 + 2 * e, r1 = r0 + 1;
+    *reinterpret_cast<u32x2 *>(s + lds_idx(r0, kq >> 1) + (kq & 1) * 4) = lo;
+    *reinterpret_cast<u32x2 *>(s + lds_idx(r1, kq >> 1) + (kq & 1) * 4) = hi;
   }
 }
 
 __device__ __forceinline__ u32x4 ldg16(const uint16_t *p) {
   return *reinterpret_cast<const u32x4 *>(p);
+}
+
+__device__ __forceinline__ u32x2 to_h4(float a, float b, float c, float d) {
+  u32x2 o;
+  o[0] = (uint32_t)f32_to_h(a) | ((uint32_t)f32_to_h(b) << 16);
+  o[1] = (uint32_t)f32_to_h(c) | ((uint32_t)f32_to_h(d) << 16);
+  return o;
+}
+
+// Apply the epilogue to 4 consecutive channels; gate word holds 4 halves.
+__device__ __forceinline__ void epilogue4(float v[4], int epi,
+                                          const uint16_t *gate) {
+  if (epi == FG_EPI_RELU) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = v[e] > 0.f ? v[e] : 0.f;
+  } else if (epi == FG_EPI_GATE) {
+    u32x2 gw = *reinterpret_cast<const u32x2 *>(gate);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      uint16_t gb = (uint16_t)(gw[e >> 1] >> (16 * (e & 1)));
+      v[e] = h_to_f32(gb) > 0.f ? v[e] : 0.f;
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -88,12 +122,14 @@ __device__ __forceinline__ u32x4 ldg16(const uint16_t *p) {
 //         channel) or mn-major (input gradient / transposed: output channel
 //         contiguous), the latter transposed in registers.
 //   FAST  reduction channels are a multiple of BK, so a slice is one tap.
+// blockIdx.z = phase * nsplit + split.
 template <int BM, int BN, bool WK, bool FAST>
 __global__ __launch_bounds__(NT) void data_conv_kernel(DataConvArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t sA[2][BM * LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t sB[2][BN * LDK];
+  __shared__ __attribute__((aligned(16))) uint16_t sA[2][BM * BK];
+  __shared__ __attribute__((aligned(16))) uint16_t sB[2][BN * BK];
 
-  const Phase P = a.ph[blockIdx.z];
+  const int phase = blockIdx.z / a.nsplit, split = blockIdx.z % a.nsplit;
+  const Phase P = a.ph[phase];
   const int npix = a.n * P.mh * P.mw;
   const int n0 = blockIdx.x * BN;
   const int m0 = blockIdx.y * BM;
@@ -101,41 +137,39 @@ __global__ __launch_bounds__(NT) void data_conv_kernel(DataConvArgs a) {
   const int ntap = P.nr * P.ns;
   const int ktot = ntap * a.cr;
   const int nk = (ktot + BK - 1) / BK;
+  const int kchunk = (nk + a.nsplit - 1) / a.nsplit;
+  const int kbeg = min(nk, split * kchunk), kend = min(nk, kbeg + kchunk);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm0 = (wave >> 1) * (BM / 2), wn0 = (wave & 1) * (BN / 2);
 
   // --- B (activation gather) loader state: BN/32 columns per thread.
   constexpr int BCOL = BN / 32;
   const int bc8 = tid & 7;
-  int bimg[BCOL], bh[BCOL], bw[BCOL];
+  int bbase[BCOL], bh[BCOL], bw[BCOL];
 #pragma unroll
   for (int i = 0; i < BCOL; ++i) {
     int col = n0 + (tid >> 3) + 32 * i;
     if (col < npix) {
       int b = col % P.mw, t = col / P.mw;
       int aa = t % P.mh, nn = t / P.mh;
-      bimg[i] = nn;
       bh[i] = aa * a.istr;
       bw[i] = b * a.istr;
+      bbase[i] = ((nn * a.hi + bh[i]) * a.wi + bw[i]) * a.cr;
     } else {
-      bimg[i] = -1;
-      bh[i] = 0;
+      bh[i] = -(1 << 29);  // fails every bounds check
       bw[i] = 0;
+      bbase[i] = 0;
     }
   }
 
-  // --- A (weight) loader: k-major uses BM/32 rows per thread; mn-major uses
-  // units of 4 reduction rows x 8 output channels.
   constexpr int AROW = BM / 32;
   constexpr int AUNITS = (BK / 4) * (BM / 8);
   constexpr int AUPT = (AUNITS + NT - 1) / NT;
-
   u32x4 ra[WK ? AROW : 4 * AUPT];
   u32x4 rb[BCOL];
 
-  auto tap_of = [&](int kk, int &dh, int &dw, int &woff, int &cr) {
-    int t = kk / a.cr;
-    cr = kk - t * a.cr;
+  // tap t -> input offset (dh, dw) and kernel element offset woff = r*S + s
+  auto tap_geom = [&](int t, int &dh, int &dw, int &woff) {
     int i = t / P.ns, j = t - (t / P.ns) * P.ns;
     dh = P.dh0 + P.dstep * i;
     dw = P.dw0 + P.dstep * j;
@@ -144,43 +178,48 @@ __global__ __launch_bounds__(NT) void data_conv_kernel(DataConvArgs a) {
 
   auto load = [&](int kt) {
     const int k0 = kt * BK;
+    int ft = 0, fcr = 0, fdh = 0, fdw = 0, fwoff = 0;
+    if (FAST) {  // the whole slice lies in one tap
+      ft = k0 / a.cr;
+      fcr = k0 - ft * a.cr;
+      tap_geom(ft, fdh, fdw, fwoff);
+    }
     // B: activations
     {
-      int kk = k0 + bc8 * 8;
-      int dh, dw, woff, cr;
+      int kk = k0 + bc8 * 8, dh, dw, woff, cr;
       bool kv = kk < ktot;
       if (FAST) {
-        tap_of(k0, dh, dw, woff, cr);
-        cr += bc8 * 8;
+        dh = fdh; dw = fdw; cr = fcr + bc8 * 8;
       } else {
-        tap_of(kv ? kk : 0, dh, dw, woff, cr);
+        int t = kv ? kk / a.cr : 0;
+        cr = kv ? kk - t * a.cr : 0;
+        tap_geom(t, dh, dw, woff);
       }
+      const int delta = (dh * a.wi + dw) * a.cr + cr;
 #pragma unroll
       for (int i = 0; i < BCOL; ++i) {
         int hh = bh[i] + dh, ww = bw[i] + dw;
-        bool v = kv && bimg[i] >= 0 && hh >= 0 && hh < a.hi && ww >= 0 &&
-                 ww < a.wi;
-        if (v)
-          rb[i] = ldg16(a.act +
-                        ((size_t)((bimg[i] * a.hi + hh) * a.wi + ww)) * a.cr +
-                        cr);
-        else
-          rb[i] = u32x4{0, 0, 0, 0};
+        bool v = kv && hh >= 0 && hh < a.hi && ww >= 0 && ww < a.wi;
+        rb[i] = v ? ldg16(a.act + (size_t)(bbase[i] + delta)) : u32x4{0, 0, 0, 0};
       }
     }
     // A: weights
     if (WK) {
-      int kk = k0 + bc8 * 8;
-      int dh, dw, woff, cr;
+      int kk = k0 + bc8 * 8, dh, dw, woff, cr;
       bool kv = kk < ktot;
-      tap_of(kv ? kk : 0, dh, dw, woff, cr);
+      if (FAST) {
+        woff = fwoff; cr = fcr + bc8 * 8;
+      } else {
+        int t = kv ? kk / a.cr : 0;
+        cr = kv ? kk - t * a.cr : 0;
+        tap_geom(t, dh, dw, woff);
+      }
+      const uint16_t *src = a.wgt + (size_t)woff * a.cr + cr;
 #pragma unroll
       for (int i = 0; i < AROW; ++i) {
         int row = m0 + (tid >> 3) + 32 * i;
-        if (kv && row < a.co)
-          ra[i] = ldg16(a.wgt + (size_t)row * a.ldw + (size_t)woff * a.cr + cr);
-        else
-          ra[i] = u32x4{0, 0, 0, 0};
+        ra[i] = (kv && row < a.co) ? ldg16(src + (size_t)row * a.ldw)
+                                   : u32x4{0, 0, 0, 0};
       }
     } else {
 #pragma unroll
@@ -191,17 +230,19 @@ __global__ __launch_bounds__(NT) void data_conv_kernel(DataConvArgs a) {
         int row = m0 + cg * 8;
         bool v = unit < AUNITS && kk < ktot && row < a.co;
         int dh, dw, woff, cr;
-        tap_of(v ? kk : 0, dh, dw, woff, cr);
+        if (FAST) {
+          woff = fwoff; cr = fcr + kq * 4;
+        } else {
+          int t = v ? kk / a.cr : 0;
+          cr = v ? kk - t * a.cr : 0;
+          tap_geom(t, dh, dw, woff);
+        }
+        // 4 consecutive reduction indices stay inside one tap (cr % 8 == 0)
         const uint16_t *src =
             a.wgt + (size_t)cr * a.w_red + (size_t)woff * a.w_tap + row;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          // 4 consecutive reduction indices stay inside one tap (cr % 8 == 0)
-          if (v)
-            ra[4 * u + e] = ldg16(src + (size_t)e * a.w_red);
-          else
-            ra[4 * u + e] = u32x4{0, 0, 0, 0};
-        }
+        for (int e = 0; e < 4; ++e)
+          ra[4 * u + e] = v ? ldg16(src + (size_t)e * a.w_red) : u32x4{0, 0, 0, 0};
       }
     }
   };
@@ -209,20 +250,20 @@ __global__ __launch_bounds__(NT) void data_conv_kernel(DataConvArgs a) {
   auto store = [&](int buf) {
 #pragma unroll
     for (int i = 0; i < BCOL; ++i)
-      *reinterpret_cast<u32x4 *>(&sB[buf][((tid >> 3) + 32 * i) * LDK +
-                                           bc8 * 8]) = rb[i];
+      *reinterpret_cast<u32x4 *>(&sB[buf][lds_idx((tid >> 3) + 32 * i, bc8)]) =
+          rb[i];
     if (WK) {
 #pragma unroll
       for (int i = 0; i < AROW; ++i)
-        *reinterpret_cast<u32x4 *>(&sA[buf][((tid >> 3) + 32 * i) * LDK +
-                                             bc8 * 8]) = ra[i];
+        *reinterpret_cast<u32x4 *>(
+            &sA[buf][lds_idx((tid >> 3) + 32 * i, bc8)]) = ra[i];
     } else {
 #pragma unroll
       for (int u = 0; u < AUPT; ++u) {
         int unit = tid + u * NT;
         if (unit < AUNITS) {
           int cg = unit % (BM / 8), kq = unit / (BM / 8);
-          store_t4x8(&sA[buf][(cg * 8) * LDK + kq * 4], &ra[4 * u]);
+          store_t4x8(sA[buf], cg * 8, kq, &ra[4 * u]);
         }
       }
     }
@@ -230,19 +271,22 @@ __global__ __launch_bounds__(NT) void data_conv_kernel(DataConvArgs a) {
 
   Core<BM, BN> core;
   core.zero();
-  load(0);
-  store(0);
+  if (kbeg < kend) {
+    load(kbeg);
+    store(0);
+  }
   __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) load(kt + 1);
+  for (int kt = kbeg; kt < kend; ++kt) {
+    const int cur = (kt - kbeg) & 1;
+    if (kt + 1 < kend) load(kt + 1);
     core.step(sA[cur], sB[cur], wm0, wn0, lane);
-    if (kt + 1 < nk) store(cur ^ 1);
+    if (kt + 1 < kend) store(cur ^ 1);
     __syncthreads();
   }
 
   // --- epilogue: lane holds 4 consecutive output channels of one position.
   constexpr int FM = Core<BM, BN>::FM, FN = Core<BM, BN>::FN;
+  const size_t out_total = (size_t)a.n * a.ho * a.wo * a.co;
 #pragma unroll
   for (int j = 0; j < FN; ++j) {
     int col = n0 + wn0 + j * 32 + (lane & 31);
@@ -261,31 +305,42 @@ __global__ __launch_bounds__(NT) void data_conv_kernel(DataConvArgs a) {
         float v[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[e] = core.acc[i][j][4 * g + e];
-        if (a.epi == FG_EPI_RELU) {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = v[e] > 0.f ? v[e] : 0.f;
-        } else if (a.epi == FG_EPI_GATE) {
-          u32x2 gw = *reinterpret_cast<const u32x2 *>(a.gate + obase + co);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            uint16_t gb = (uint16_t)(gw[e >> 1] >> (16 * (e & 1)));
-            v[e] = h_to_f32(gb) > 0.f ? v[e] : 0.f;
-          }
+        if (a.nsplit > 1) {
+          f32x4 o = {v[0], v[1], v[2], v[3]};
+          *reinterpret_cast<f32x4 *>(a.part + split * out_total + obase + co) = o;
+        } else {
+          epilogue4(v, a.epi, a.gate + obase + co);
+          *reinterpret_cast<u32x2 *>(a.out + obase + co) =
+              to_h4(v[0], v[1], v[2], v[3]);
         }
-        u32x2 o;
-        o[0] = (uint32_t)f32_to_h(v[0]) | ((uint32_t)f32_to_h(v[1]) << 16);
-        o[1] = (uint32_t)f32_to_h(v[2]) | ((uint32_t)f32_to_h(v[3]) << 16);
-        *reinterpret_cast<u32x2 *>(a.out + obase + co) = o;
       }
   }
+}
+
+// Sum nsplit fp32 partial arrays of len elements in split order, apply the
+// epilogue, round to fp16. len is a multiple of 4.
+__global__ __launch_bounds__(256) void split_epilogue_kernel(
+    const float *part, int nsplit, int64_t len, int epi, const uint16_t *gate,
+    uint16_t *out) {
+  int64_t i4 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (i4 >= len) return;
+  f32x4 s = *reinterpret_cast<const f32x4 *>(part + i4);
+  for (int k = 1; k < nsplit; ++k) {
+    f32x4 v = *reinterpret_cast<const f32x4 *>(part + (size_t)k * len + i4);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) s[e] += v[e];
+  }
+  float v[4] = {s[0], s[1], s[2], s[3]};
+  epilogue4(v, epi, gate + i4);
+  *reinterpret_cast<u32x2 *>(out + i4) = to_h4(v[0], v[1], v[2], v[3]);
 }
 
 // ---------------------------------------------------------------------------
 // Kernel-gradient kernel: rows rho = (tap, c) of the x patch, columns k.
 template <int BM, int BN>
 __global__ __launch_bounds__(NT) void wgrad_kernel(WgradArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t sA[2][BM * LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t sB[2][BN * LDK];
+  __shared__ __attribute__((aligned(16))) uint16_t sA[2][BM * BK];
+  __shared__ __attribute__((aligned(16))) uint16_t sB[2][BN * BK];
 
   const int rsc = a.r * a.s * a.c;
   const int m0 = blockIdx.x * BM;  // rho
@@ -293,7 +348,7 @@ __global__ __launch_bounds__(NT) void wgrad_kernel(WgradArgs a) {
   const int split = blockIdx.z;
   const int mbeg = split * a.mchunk;
   const int mend = min(a.mtot, mbeg + a.mchunk);
-  const int nk = (mend - mbeg + BK - 1) / BK;
+  const int nk = mend > mbeg ? (mend - mbeg + BK - 1) / BK : 0;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm0 = (wave >> 1) * (BM / 2), wn0 = (wave & 1) * (BN / 2);
   const int pq = a.p * a.q;
@@ -304,29 +359,37 @@ __global__ __launch_bounds__(NT) void wgrad_kernel(WgradArgs a) {
   constexpr int BUPT = (BUNITS + NT - 1) / NT;
   u32x4 ra[4 * AUPT], rb[4 * BUPT];
 
+  // per A unit: the tap and channel of its 8 rows are fixed for the block
+  int ar[AUPT], as_[AUPT], ac[AUPT];
+  bool arv[AUPT];
+#pragma unroll
+  for (int u = 0; u < AUPT; ++u) {
+    int unit = tid + u * NT;
+    int rho = m0 + (unit % (BM / 8)) * 8;
+    arv[u] = unit < AUNITS && rho < rsc;
+    int t = rho / a.c;
+    ac[u] = rho - t * a.c;
+    ar[u] = t / a.s;
+    as_[u] = t - ar[u] * a.s;
+  }
+
   auto load = [&](int kt) {
     const int k0 = mbeg + kt * BK;
 #pragma unroll
     for (int u = 0; u < AUPT; ++u) {
       int unit = tid + u * NT;
-      int rg = unit % (BM / 8), mq = unit / (BM / 8);
-      int rho = m0 + rg * 8;
-      bool uv = unit < AUNITS && rho < rsc;
-      int t = rho / a.c, c = rho - (rho / a.c) * a.c;
-      int r = t / a.s, s = t - (t / a.s) * a.s;
+      int mq = unit / (BM / 8);
       int m = k0 + mq * 4;
-      int nn = m / pq, rem = m - (m / pq) * pq;
-      int p = rem / a.q, q = rem - (rem / a.q) * a.q;
+      int nn = m / pq, rem = m - nn * pq;
+      int p = rem / a.q, q = rem - p * a.q;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        int hh = p * a.sh - a.ph + r, ww = q * a.sw - a.pw + s;
-        bool v = uv && (m + e) < mend && hh >= 0 && hh < a.h && ww >= 0 &&
+        int hh = p * a.sh - a.ph + ar[u], ww = q * a.sw - a.pw + as_[u];
+        bool v = arv[u] && (m + e) < mend && hh >= 0 && hh < a.h && ww >= 0 &&
                  ww < a.w;
-        if (v)
-          ra[4 * u + e] =
-              ldg16(a.x + ((size_t)((nn * a.h + hh) * a.w + ww)) * a.c + c);
-        else
-          ra[4 * u + e] = u32x4{0, 0, 0, 0};
+        ra[4 * u + e] =
+            v ? ldg16(a.x + ((size_t)((nn * a.h + hh) * a.w + ww)) * a.c + ac[u])
+              : u32x4{0, 0, 0, 0};
         // next reduction row: advance (n, p, q)
         if (++q == a.q) {
           q = 0;
@@ -344,13 +407,11 @@ __global__ __launch_bounds__(NT) void wgrad_kernel(WgradArgs a) {
       int k = n0 + kg * 8;
       int m = k0 + mq * 4;
       bool uv = unit < BUNITS && k < a.k;
+      const uint16_t *src = a.dy + (size_t)m * a.k + k;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        if (uv && (m + e) < mend)
-          rb[4 * u + e] = ldg16(a.dy + (size_t)(m + e) * a.k + k);
-        else
-          rb[4 * u + e] = u32x4{0, 0, 0, 0};
-      }
+      for (int e = 0; e < 4; ++e)
+        rb[4 * u + e] = (uv && (m + e) < mend) ? ldg16(src + (size_t)e * a.k)
+                                               : u32x4{0, 0, 0, 0};
     }
   };
 
@@ -358,18 +419,14 @@ __global__ __launch_bounds__(NT) void wgrad_kernel(WgradArgs a) {
 #pragma unroll
     for (int u = 0; u < AUPT; ++u) {
       int unit = tid + u * NT;
-      if (unit < AUNITS) {
-        int rg = unit % (BM / 8), mq = unit / (BM / 8);
-        store_t4x8(&sA[buf][(rg * 8) * LDK + mq * 4], &ra[4 * u]);
-      }
+      if (unit < AUNITS)
+        store_t4x8(sA[buf], (unit % (BM / 8)) * 8, unit / (BM / 8), &ra[4 * u]);
     }
 #pragma unroll
     for (int u = 0; u < BUPT; ++u) {
       int unit = tid + u * NT;
-      if (unit < BUNITS) {
-        int kg = unit % (BN / 8), mq = unit / (BN / 8);
-        store_t4x8(&sB[buf][(kg * 8) * LDK + mq * 4], &rb[4 * u]);
-      }
+      if (unit < BUNITS)
+        store_t4x8(sB[buf], (unit % (BN / 8)) * 8, unit / (BN / 8), &rb[4 * u]);
     }
   };
 
@@ -399,17 +456,12 @@ __global__ __launch_bounds__(NT) void wgrad_kernel(WgradArgs a) {
       for (int g = 0; g < 4; ++g) {
         int rho = m0 + wm0 + i * 32 + 8 * g + 4 * (lane >> 5);
         if (rho >= rsc) continue;
+        const f32x16 &c = core.acc[i][j];
         if (a.nsplit == 1) {
-          u32x2 o;
-          o[0] = (uint32_t)f32_to_h(core.acc[i][j][4 * g]) |
-                 ((uint32_t)f32_to_h(core.acc[i][j][4 * g + 1]) << 16);
-          o[1] = (uint32_t)f32_to_h(core.acc[i][j][4 * g + 2]) |
-                 ((uint32_t)f32_to_h(core.acc[i][j][4 * g + 3]) << 16);
-          *reinterpret_cast<u32x2 *>(a.dw + (size_t)k * rsc + rho) = o;
+          *reinterpret_cast<u32x2 *>(a.dw + (size_t)k * rsc + rho) =
+              to_h4(c[4 * g], c[4 * g + 1], c[4 * g + 2], c[4 * g + 3]);
         } else {
-          f32x4 o;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) o[e] = core.acc[i][j][4 * g + e];
+          f32x4 o = {c[4 * g], c[4 * g + 1], c[4 * g + 2], c[4 * g + 3]};
           *reinterpret_cast<f32x4 *>(
               a.part + ((size_t)split * a.k + k) * rsc + rho) = o;
         }
@@ -431,10 +483,37 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const float *part,
 #pragma unroll
     for (int e = 0; e < 4; ++e) s[e] += v[e];
   }
-  u32x2 o;
-  o[0] = (uint32_t)f32_to_h(s[0]) | ((uint32_t)f32_to_h(s[1]) << 16);
-  o[1] = (uint32_t)f32_to_h(s[2]) | ((uint32_t)f32_to_h(s[3]) << 16);
-  *reinterpret_cast<u32x2 *>(out + i4) = o;
+  *reinterpret_cast<u32x2 *>(out + i4) = to_h4(s[0], s[1], s[2], s[3]);
+}
+
+// Same sum when the partials are many and short (nsplit large, len small):
+// one workgroup per 4 outputs; thread t adds splits t, t+256, ... in order,
+// then a fixed-shape tree in LDS combines the 256 thread sums.
+__global__ __launch_bounds__(256) void split_reduce_wide_kernel(
+    const float *part, int nsplit, int64_t len, uint16_t *out) {
+  __shared__ f32x4 red[256];
+  const int64_t i4 = (int64_t)blockIdx.x * 4;
+  f32x4 s = {0.f, 0.f, 0.f, 0.f};
+  for (int k = threadIdx.x; k < nsplit; k += 256) {
+    f32x4 v = *reinterpret_cast<const f32x4 *>(part + (size_t)k * len + i4);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) s[e] += v[e];
+  }
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (threadIdx.x < w) {
+      f32x4 a = red[threadIdx.x], b = red[threadIdx.x + w];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) a[e] += b[e];
+      red[threadIdx.x] = a;
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    f32x4 t = red[0];
+    *reinterpret_cast<u32x2 *>(out + i4) = to_h4(t[0], t[1], t[2], t[3]);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -545,48 +624,120 @@ __global__ __launch_bounds__(kHeadWgradThreads) void head_wgrad_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Host launchers.
+// Host side: tile selection and launchers.
+namespace {
+
+int64_t data_tiles(const DataConvArgs &a, int bm, int bn) {
+  int64_t t = 0;
+  for (int i = 0; i < a.nphase; ++i) {
+    int64_t np = (int64_t)a.n * a.ph[i].mh * a.ph[i].mw;
+    t += ((np + bn - 1) / bn) * ((a.co + bm - 1) / bm);
+  }
+  return t;
+}
+
+int64_t data_nk_max(const DataConvArgs &a) {
+  int64_t nk = 0;
+  for (int i = 0; i < a.nphase; ++i) {
+    int64_t kt = (int64_t)a.ph[i].nr * a.ph[i].ns * a.cr;
+    nk = std::max<int64_t>(nk, (kt + BK - 1) / BK);
+  }
+  return nk;
+}
+
+constexpr int64_t kCUs = 256;
+
+}  // namespace
+
+DataPlan plan_data_conv(const DataConvArgs &a) {
+  DataPlan pl;
+  pl.big = data_tiles(a, 256, 256) >= kCUs && a.co >= 256;
+  const int64_t tiles = pl.big ? data_tiles(a, 256, 256) : data_tiles(a, 128, 128);
+  int64_t ns = 1;
+  if (!pl.big && tiles < kCUs) {
+    const int64_t nk = data_nk_max(a);
+    ns = (2 * kCUs + tiles - 1) / tiles;  // ~2 workgroups per CU
+    ns = std::min<int64_t>(ns, std::max<int64_t>(1, nk / 8));  // >= 8 slices each
+    ns = std::min<int64_t>(ns, 16);
+  }
+  pl.nsplit = (int32_t)std::max<int64_t>(ns, 1);
+  const int64_t out = (int64_t)a.n * a.ho * a.wo * a.co;
+  pl.ws_bytes = pl.nsplit > 1 ? (size_t)pl.nsplit * out * sizeof(float) : 0;
+  return pl;
+}
+
 template <int BM, int BN, bool WK, bool FAST>
 static hipError_t launch_dc(const DataConvArgs &a, hipStream_t st) {
   int maxpix = 0;
   for (int i = 0; i < a.nphase; ++i)
-    maxpix = max(maxpix, a.n * a.ph[i].mh * a.ph[i].mw);
-  dim3 grid((maxpix + BN - 1) / BN, (a.co + BM - 1) / BM, a.nphase);
+    maxpix = std::max(maxpix, a.n * a.ph[i].mh * a.ph[i].mw);
+  dim3 grid((maxpix + BN - 1) / BN, (a.co + BM - 1) / BM, a.nphase * a.nsplit);
   hipLaunchKernelGGL((data_conv_kernel<BM, BN, WK, FAST>), grid, dim3(NT), 0,
                      st, a);
   return hipGetLastError();
 }
 
-hipError_t launch_data_conv(const DataConvArgs &a, bool w_kmajor,
-                            hipStream_t st) {
+template <int BM, int BN>
+static hipError_t launch_dc_tile(const DataConvArgs &a, bool w_kmajor,
+                                 hipStream_t st) {
   const bool fast = (a.cr % BK) == 0;
   if (w_kmajor)
-    return fast ? launch_dc<128, 128, true, true>(a, st)
-                : launch_dc<128, 128, true, false>(a, st);
-  return fast ? launch_dc<128, 128, false, true>(a, st)
-              : launch_dc<128, 128, false, false>(a, st);
+    return fast ? launch_dc<BM, BN, true, true>(a, st)
+                : launch_dc<BM, BN, true, false>(a, st);
+  return fast ? launch_dc<BM, BN, false, true>(a, st)
+              : launch_dc<BM, BN, false, false>(a, st);
 }
 
-const char *data_conv_kernel_name(int32_t cr, bool w_kmajor) {
-  const bool fast = (cr % BK) == 0;
-  if (w_kmajor)
-    return fast ? "data_conv_kernel<128, 128, true, true>"
-                : "data_conv_kernel<128, 128, true, false>";
-  return fast ? "data_conv_kernel<128, 128, false, true>"
-              : "data_conv_kernel<128, 128, false, false>";
+hipError_t launch_data_conv(const DataConvArgs &a0, bool w_kmajor,
+                            hipStream_t st) {
+  DataConvArgs a = a0;
+  const DataPlan pl = plan_data_conv(a);
+  a.nsplit = pl.nsplit;
+  hipError_t e = pl.big ? launch_dc_tile<256, 256>(a, w_kmajor, st)
+                        : launch_dc_tile<128, 128>(a, w_kmajor, st);
+  if (e != hipSuccess || a.nsplit == 1) return e;
+  const int64_t len = (int64_t)a.n * a.ho * a.wo * a.co;
+  hipLaunchKernelGGL(split_epilogue_kernel,
+                     dim3((unsigned)((len / 4 + 255) / 256)), dim3(256), 0, st,
+                     a.part, a.nsplit, len, a.epi, a.gate, a.out);
+  return hipGetLastError();
 }
 
-const char *wgrad_kernel_name() { return "wgrad_kernel<128, 128>"; }
+const char *data_conv_kernel_name(const DataConvArgs &a, bool w_kmajor) {
+  static const char *names[2][2][2] = {
+      {{"data_conv_kernel<128, 128, false, false>",
+        "data_conv_kernel<128, 128, false, true>"},
+       {"data_conv_kernel<128, 128, true, false>",
+        "data_conv_kernel<128, 128, true, true>"}},
+      {{"data_conv_kernel<256, 256, false, false>",
+        "data_conv_kernel<256, 256, false, true>"},
+       {"data_conv_kernel<256, 256, true, false>",
+        "data_conv_kernel<256, 256, true, true>"}}};
+  const DataPlan pl = plan_data_conv(a);
+  return names[pl.big][w_kmajor][(a.cr % BK) == 0];
+}
+
+static bool wgrad_big(const fg_conv_desc &d) {
+  return (int64_t)d.r * d.s * d.c >= 256 && d.k >= 256;
+}
+
+const char *wgrad_kernel_name(const fg_conv_desc &d) {
+  return wgrad_big(d) ? "wgrad_kernel<256, 256>" : "wgrad_kernel<128, 128>";
+}
 
 WgradPlan plan_wgrad(const fg_conv_desc &d, int32_t p, int32_t q) {
   WgradPlan pl;
+  const int t = wgrad_big(d) ? 256 : 128;
   const int64_t rsc = (int64_t)d.r * d.s * d.c;
-  const int64_t tiles = ((rsc + 127) / 128) * ((d.k + 127) / 128);
+  const int64_t tiles = ((rsc + t - 1) / t) * ((d.k + t - 1) / t);
   const int64_t mtot = (int64_t)d.n * p * q;
-  int64_t want = (512 + tiles - 1) / tiles;             // ~2 waves of CUs
-  int64_t maxs = (mtot + 4 * BK - 1) / (4 * BK);         // >= 4 slices each
-  int64_t ns = want < maxs ? want : maxs;
-  if (ns < 1) ns = 1;
+  // resident workgroups: one per CU for 256 x 256 tiles, two for 128 x 128;
+  // take the largest split that keeps the grid within one such wave, so no
+  // partly filled second wave doubles the time
+  const int64_t slots = wgrad_big(d) ? kCUs : 2 * kCUs;
+  int64_t want = std::max<int64_t>(1, slots / tiles);
+  int64_t maxs = (mtot + 8 * BK - 1) / (8 * BK);  // >= 8 slices each
+  int64_t ns = std::max<int64_t>(1, std::min(want, maxs));
   int64_t chunk = (mtot + ns - 1) / ns;
   chunk = (chunk + BK - 1) / BK * BK;
   ns = (mtot + chunk - 1) / chunk;
@@ -598,8 +749,14 @@ WgradPlan plan_wgrad(const fg_conv_desc &d, int32_t p, int32_t q) {
 
 hipError_t launch_wgrad(const WgradArgs &a, hipStream_t st) {
   const int rsc = a.r * a.s * a.c;
-  dim3 grid((rsc + 127) / 128, (a.k + 127) / 128, a.nsplit);
-  hipLaunchKernelGGL((wgrad_kernel<128, 128>), grid, dim3(NT), 0, st, a);
+  const bool big = rsc >= 256 && a.k >= 256;
+  if (big) {
+    dim3 grid((rsc + 255) / 256, (a.k + 255) / 256, a.nsplit);
+    hipLaunchKernelGGL((wgrad_kernel<256, 256>), grid, dim3(NT), 0, st, a);
+  } else {
+    dim3 grid((rsc + 127) / 128, (a.k + 127) / 128, a.nsplit);
+    hipLaunchKernelGGL((wgrad_kernel<128, 128>), grid, dim3(NT), 0, st, a);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.nsplit == 1) return e;
   const int64_t len = (int64_t)a.k * rsc;
@@ -660,7 +817,7 @@ hipError_t launch_head_wgrad(const uint16_t *x, const uint16_t *dy,
                      ws);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(split_reduce_kernel, dim3((unsigned)((c / 4 + 255) / 256)),
+  hipLaunchKernelGGL(split_reduce_wide_kernel, dim3((unsigned)(c / 4)),
                      dim3(256), 0, st, ws, (int)nb, (int64_t)c, dw);
   return hipGetLastError();
 }

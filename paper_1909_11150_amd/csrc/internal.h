@@ -5,6 +5,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 #include "fcngrad.h"
 
 namespace fg {
@@ -38,8 +40,18 @@ struct DataConvArgs {
   int32_t ldw, w_red, w_tap;
   int32_t epi;
   int32_t nphase;
+  int32_t nsplit;        // reduction split (set by the launcher)
+  float *part;           // [nsplit][n*ho*wo*co] fp32 partials (nsplit > 1)
   Phase ph[4];
 };
+
+// Tile and split choice for a data convolution (pure host logic).
+struct DataPlan {
+  bool big;              // 256 x 256 tiles (else 128 x 128)
+  int32_t nsplit;
+  size_t ws_bytes;
+};
+DataPlan plan_data_conv(const DataConvArgs &a);
 
 struct WgradArgs {
   const uint16_t *x;     // [n][h][w][c]
@@ -64,8 +76,8 @@ size_t head_wgrad_ws_bytes(const fg_conv_desc &d);
 
 hipError_t launch_data_conv(const DataConvArgs &a, bool w_kmajor,
                             hipStream_t st);
-const char *data_conv_kernel_name(int32_t cr, bool w_kmajor);
-const char *wgrad_kernel_name();
+const char *data_conv_kernel_name(const DataConvArgs &a, bool w_kmajor);
+const char *wgrad_kernel_name(const fg_conv_desc &d);
 hipError_t launch_wgrad(const WgradArgs &a, hipStream_t st);
 hipError_t launch_head_fwd(const uint16_t *x, const uint16_t *w, uint16_t *y,
                            int64_t npix, int32_t c, int32_t epi,

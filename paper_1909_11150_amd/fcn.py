@@ -13,7 +13,8 @@ Layers are duck-typed: ``kind`` ("conv" | "convT"), ``x_shape``/``y_shape``
 """
 import torch
 
-from . import (EPI_GATE, EPI_NONE, EPI_RELU, OP_BWD_WEIGHT, ConvDesc,
+from . import (EPI_GATE, EPI_NONE, EPI_RELU, OP_BWD_DATA, OP_BWD_WEIGHT,
+               OP_CONVT, OP_FWD, ConvDesc,
                conv2d_bwd_data, conv2d_bwd_weight, conv2d_fwd,
                conv_transpose2d_fwd, grad_group_pack, grad_group_plan,
                grad_group_unpack, grad_unscale_check, l2_head_grad,
@@ -43,6 +44,23 @@ def convt_dw_desc(L):
     return convt_dx_desc(L)
 
 
+def chain_workspace_bytes(layers):
+    """Largest workspace any pass of any layer needs (one shared buffer:
+    the passes run in stream order)."""
+    ws = 0
+    for L in layers:
+        if L.kind == "conv":
+            d = fwd_desc(L)
+            for op in (OP_FWD, OP_BWD_DATA, OP_BWD_WEIGHT):
+                ws = max(ws, workspace_bytes(d, op))
+        else:
+            ws = max(ws, workspace_bytes(fwd_desc(L), OP_CONVT))
+            d = convt_dx_desc(L)
+            for op in (OP_FWD, OP_BWD_WEIGHT):
+                ws = max(ws, workspace_bytes(d, op))
+    return ws
+
+
 class Chain:
     def __init__(self, layers, weights, x, device="cuda", loss_scale=2.0 ** 15,
                  group_cap_bytes=None, group_align_bytes=256, stream=None):
@@ -62,11 +80,8 @@ class Chain:
                  [torch.empty(self.layers[-1].y_shape, dtype=F16, device=self.dev)]
         self.dw = [torch.empty(L.w_shape, dtype=F16, device=self.dev)
                    for L in self.layers]
-        ws = 0
-        for L in self.layers:
-            d = fwd_desc(L) if L.kind == "conv" else convt_dw_desc(L)
-            ws = max(ws, workspace_bytes(d, OP_BWD_WEIGHT))
-        self.ws = torch.empty(max(ws, 16), dtype=torch.uint8, device=self.dev)
+        self.ws = torch.empty(max(chain_workspace_bytes(self.layers), 16),
+                              dtype=torch.uint8, device=self.dev)
         self.groups = None
         if group_cap_bytes is not None:
             self._plan_groups(group_cap_bytes, group_align_bytes)
@@ -109,10 +124,11 @@ class Chain:
             epi = EPI_RELU if L.relu else EPI_NONE
             if L.kind == "conv":
                 conv2d_fwd(fwd_desc(L), self.acts[i], self.w[i], self.acts[i + 1],
-                           epi, stream=self.stream)
+                           epi, ws=self.ws, stream=self.stream)
             else:
                 conv_transpose2d_fwd(fwd_desc(L), self.acts[i], self.w[i],
-                                     self.acts[i + 1], epi, stream=self.stream)
+                                     self.acts[i + 1], epi, ws=self.ws,
+                                     stream=self.stream)
         return self.acts[-1]
 
     def head_grad(self, target):
@@ -142,12 +158,12 @@ class Chain:
                 conv2d_bwd_weight(d, self.acts[i], dy, self.dw[i], self.ws,
                                   stream=self.stream)
                 conv2d_bwd_data(d, dy, self.w[i], self.g[i], epi, gt,
-                                stream=self.stream)
+                                ws=self.ws, stream=self.stream)
             else:
                 conv2d_bwd_weight(convt_dw_desc(L), dy, self.acts[i], self.dw[i],
                                   self.ws, stream=self.stream)
                 conv2d_fwd(convt_dx_desc(L), dy, self.w[i], self.g[i], epi, gt,
-                           stream=self.stream)
+                           ws=self.ws, stream=self.stream)
             if grad_path and self.groups is not None and i in self._group_done_at:
                 self.run_group(self._group_done_at[i])
 

@@ -68,3 +68,10 @@ def sample_indices(shape, n, rng, extra=()):
                     idx.add(int(np.ravel_multi_index((a, b, c, d), dims)))
     idx.update(int(v) for v in extra)
     return np.array(sorted(idx), dtype=np.int64)
+
+
+def workspace(desc, op):
+    """Device workspace the library asks for (at least 16 bytes)."""
+    import paper_1909_11150_amd as fg
+    return torch.empty(max(16, fg.workspace_bytes(desc, op)), dtype=torch.uint8,
+                       device="cuda")

@@ -103,7 +103,14 @@ def test_workspace_query_and_shortfall(L):
     d = fg.ConvDesc.make(4, 64, 64, 512, 1024, 3, 3, 2, 1)
     need = L.fg_conv_workspace_bytes(ref(d), fg.OP_BWD_WEIGHT)
     assert need > 0 and need % 4 == 0
-    assert L.fg_conv_workspace_bytes(ref(d), fg.OP_FWD) == 0
+    # a shape with few output tiles splits its reduction and needs workspace
+    small = fg.ConvDesc.make(4, 32, 32, 1024, 1024, 3, 3, 2, 1)
+    assert L.fg_conv_workspace_bytes(ref(small), fg.OP_FWD) > 0
+    assert L.conv2d_fwd(ref(small), FAKE, FAKE + (1 << 28), FAKE + (1 << 30), 0, None,
+                        None, 0, None) == fg.FG_EWORKSPACE
+    # a large one does not
+    big = fg.ConvDesc.make(4, 128, 128, 512, 512, 3, 3, 1, 1)
+    assert L.fg_conv_workspace_bytes(ref(big), fg.OP_FWD) == 0
     assert L.conv2d_bwd_weight(ref(d), FAKE, FAKE + (1 << 28), FAKE + (1 << 30),
                                None, 0, None) == fg.FG_EWORKSPACE
     assert L.conv2d_bwd_weight(ref(d), FAKE, FAKE + (1 << 28), FAKE + (1 << 30),

@@ -13,7 +13,7 @@ import torch
 import oracle
 import paper_1909_11150_amd as fg
 import synth
-from gpu_util import conv_parity, dev, empty16, host
+from gpu_util import conv_parity, dev, empty16, host, workspace
 
 pytestmark = pytest.mark.gpu
 
@@ -53,7 +53,7 @@ def test_fwd(shape, epi):
     gate = synth.uniform(np.random.default_rng(9), dy.shape) if epi == "gate" else None
     y = empty16(dy.shape)
     fg.conv2d_fwd(d, dev(x), dev(W), y, {"none": 0, "relu": 1, "gate": 2}[epi],
-                  dev(gate) if gate is not None else None)
+                  dev(gate) if gate is not None else None, workspace(d, fg.OP_FWD))
     ref = oracle.conv2d_fwd(x, W, shape[6], shape[7],
                             epi=None if epi == "none" else epi, gate=gate)
     conv_parity(host(y), ref, f"fwd {shape} {epi}")
@@ -67,7 +67,8 @@ def test_bwd_data(shape, epi):
     gate = synth.uniform(np.random.default_rng(8), x.shape) if epi == "gate" else None
     dx = empty16(x.shape)
     fg.conv2d_bwd_data(d, dev(dy), dev(W), dx, 2 if epi == "gate" else 0,
-                       dev(gate) if gate is not None else None)
+                       dev(gate) if gate is not None else None,
+                       workspace(d, fg.OP_BWD_DATA))
     ref = oracle.conv2d_bwd_data(dy, W, x.shape, shape[6], shape[7],
                                  epi=None if epi == "none" else epi, gate=gate)
     conv_parity(host(dx), ref, f"bwd_data {shape} {epi}")
@@ -77,10 +78,8 @@ def test_bwd_data(shape, epi):
 def test_bwd_weight(shape):
     x, W, dy = _inputs(shape, 3)
     d = _desc(shape)
-    ws = torch.empty(max(16, fg.workspace_bytes(d, fg.OP_BWD_WEIGHT)),
-                     dtype=torch.uint8, device="cuda")
     dw = empty16(W.shape)
-    fg.conv2d_bwd_weight(d, dev(x), dev(dy), dw, ws)
+    fg.conv2d_bwd_weight(d, dev(x), dev(dy), dw, workspace(d, fg.OP_BWD_WEIGHT))
     ref = oracle.conv2d_bwd_weight(x, dy, shape[5], shape[5], shape[6], shape[7])
     conv_parity(host(dw), ref, f"bwd_weight {shape}")
 
@@ -99,10 +98,11 @@ def test_convt(shape, epi):
     oshape = (n, 2 * h, 2 * w, co)
     gate = synth.uniform(rng, oshape) if epi == "gate" else None
     y = empty16(oshape)
-    fg.conv_transpose2d_fwd(fg.ConvDesc.make(n, h, w, ci, co, 4, 4, 2, 1),
-                            dev(x), dev(Wt), y,
+    d = fg.ConvDesc.make(n, h, w, ci, co, 4, 4, 2, 1)
+    fg.conv_transpose2d_fwd(d, dev(x), dev(Wt), y,
                             {"none": 0, "relu": 1, "gate": 2}[epi],
-                            dev(gate) if gate is not None else None)
+                            dev(gate) if gate is not None else None,
+                            workspace(d, fg.OP_CONVT))
     ref = oracle.conv_transpose2d_fwd(x, Wt, 2, 1,
                                       epi=None if epi == "none" else epi, gate=gate)
     conv_parity(host(y), ref, f"convT {shape} {epi}")
@@ -115,10 +115,10 @@ def test_convt_matches_bwd_data_with_roles_exchanged():
     x = synth.uniform(rng, (2, 8, 8, 64))
     Wt = synth.normal(rng, (64, 4, 4, 32), 0.05)
     y1, y2 = empty16((2, 16, 16, 32)), empty16((2, 16, 16, 32))
-    fg.conv_transpose2d_fwd(fg.ConvDesc.make(2, 8, 8, 64, 32, 4, 4, 2, 1),
-                            dev(x), dev(Wt), y1)
-    fg.conv2d_bwd_data(fg.ConvDesc.make(2, 16, 16, 32, 64, 4, 4, 2, 1),
-                       dev(x), dev(Wt), y2)
+    dt = fg.ConvDesc.make(2, 8, 8, 64, 32, 4, 4, 2, 1)
+    db = fg.ConvDesc.make(2, 16, 16, 32, 64, 4, 4, 2, 1)
+    fg.conv_transpose2d_fwd(dt, dev(x), dev(Wt), y1, ws=workspace(dt, fg.OP_CONVT))
+    fg.conv2d_bwd_data(db, dev(x), dev(Wt), y2, ws=workspace(db, fg.OP_BWD_DATA))
     np.testing.assert_array_equal(host(y1), host(y2))
 
 
@@ -153,7 +153,8 @@ def test_identity_weight_is_bit_exact():
     x = synth.uniform(rng, (2, 10, 11, 64))
     eye = np.eye(64, dtype=np.float16).reshape(64, 1, 1, 64)
     y = empty16(x.shape)
-    fg.conv2d_fwd(fg.ConvDesc.make(2, 10, 11, 64, 64, 1, 1, 1, 0), dev(x), dev(eye), y)
+    d = fg.ConvDesc.make(2, 10, 11, 64, 64, 1, 1, 1, 0)
+    fg.conv2d_fwd(d, dev(x), dev(eye), y, ws=workspace(d, fg.OP_FWD))
     np.testing.assert_array_equal(host(y), x)
 
 
@@ -163,10 +164,8 @@ def test_all_ones_weight_gradient_rounds_to_even():
     x = np.ones((2, 64, 64, 16), np.float16)
     dy = np.ones((2, 64, 64, 16), np.float16)
     d = fg.ConvDesc.make(2, 64, 64, 16, 16, 3, 3, 1, 1)
-    ws = torch.empty(max(16, fg.workspace_bytes(d, fg.OP_BWD_WEIGHT)),
-                     dtype=torch.uint8, device="cuda")
     dw = empty16((16, 3, 3, 16))
-    fg.conv2d_bwd_weight(d, dev(x), dev(dy), dw, ws)
+    fg.conv2d_bwd_weight(d, dev(x), dev(dy), dw, workspace(d, fg.OP_BWD_WEIGHT))
     got = host(dw)
     cnt = np.array([63, 64, 63])
     ref = (2 * np.outer(cnt, cnt)).astype(np.float16)
@@ -182,7 +181,8 @@ def test_fp16_overflow_gives_infinity():
     W = np.full((8, 1, 1, 64), 30.0, np.float16)
     W[1::2] *= -1
     y = empty16((1, 4, 4, 8))
-    fg.conv2d_fwd(fg.ConvDesc.make(1, 4, 4, 64, 8, 1, 1, 1, 0), dev(x), dev(W), y)
+    d = fg.ConvDesc.make(1, 4, 4, 64, 8, 1, 1, 1, 0)
+    fg.conv2d_fwd(d, dev(x), dev(W), y, ws=workspace(d, fg.OP_FWD))
     got = host(y)
     assert np.all(np.isposinf(got[..., 0::2])) and np.all(np.isneginf(got[..., 1::2]))
 
@@ -193,8 +193,8 @@ def test_adjoint_identity_on_gpu_outputs():
     x, W, dy = _inputs(shape, 10)
     d = _desc(shape)
     y, dx = empty16(dy.shape), empty16(x.shape)
-    fg.conv2d_fwd(d, dev(x), dev(W), y)
-    fg.conv2d_bwd_data(d, dev(dy), dev(W), dx)
+    fg.conv2d_fwd(d, dev(x), dev(W), y, ws=workspace(d, fg.OP_FWD))
+    fg.conv2d_bwd_data(d, dev(dy), dev(W), dx, ws=workspace(d, fg.OP_BWD_DATA))
     lhs = float(np.sum(host(y).astype(np.float64) * dy))
     rhs = float(np.sum(x.astype(np.float64) * host(dx)))
     assert abs(lhs - rhs) <= 1e-3 * np.sqrt(np.sum(host(y).astype(np.float64) ** 2) *
@@ -206,14 +206,13 @@ def test_deterministic_repeats():
     x, W, dy = _inputs(shape, 11)
     d = _desc(shape)
     xs, Ws, dys = dev(x), dev(W), dev(dy)
-    ws = torch.empty(fg.workspace_bytes(d, fg.OP_BWD_WEIGHT) + 16, dtype=torch.uint8,
-                     device="cuda")
+    ws = [workspace(d, op) for op in (fg.OP_FWD, fg.OP_BWD_DATA, fg.OP_BWD_WEIGHT)]
     outs = []
     for _ in range(2):
         y, dx, dw = empty16(dy.shape), empty16(x.shape), empty16(W.shape)
-        fg.conv2d_fwd(d, xs, Ws, y)
-        fg.conv2d_bwd_data(d, dys, Ws, dx)
-        fg.conv2d_bwd_weight(d, xs, dys, dw, ws)
+        fg.conv2d_fwd(d, xs, Ws, y, ws=ws[0])
+        fg.conv2d_bwd_data(d, dys, Ws, dx, ws=ws[1])
+        fg.conv2d_bwd_weight(d, xs, dys, dw, ws[2])
         outs.append([host(t) for t in (y, dx, dw)])
     for a, b in zip(*outs):
         assert np.array_equal(a.view(np.uint16), b.view(np.uint16))
