@@ -27,7 +27,21 @@
 namespace fg {
 
 constexpr int BK = 64;        // reduction slice per LDS stage (halves)
-constexpr int NT = 256;       // threads per workgroup (4 waves, 2 x 2)
+
+// Tile configuration: BM x BN output tile, WGM x WGN waves, each owning a
+// (BM/WGM) x (BN/WGN) block of 32x32 MFMA fragments.
+template <int BM_, int BN_, int WGM_, int WGN_>
+struct Cfg {
+  static constexpr int BM = BM_, BN = BN_, WGM = WGM_, WGN = WGN_;
+  static constexpr int NT = 64 * WGM * WGN;
+  static constexpr int WM = BM / WGM, WN = BN / WGN;
+  static constexpr int FM = WM / 32, FN = WN / 32;
+};
+// 256x256 tile, 8 waves (two per SIMD) of 128x64: one wave's MFMAs overlap
+// the other's address, load and LDS instructions.
+using BigCfg = Cfg<256, 256, 2, 4>;
+// 128x128 tile, 4 waves of 64x64; two workgroups fit on a CU.
+using SmallCfg = Cfg<128, 128, 2, 2>;
 
 // Offset (in halves) of 16-byte chunk `chunk` (0..7) of LDS row `row`.
 __device__ __forceinline__ int lds_idx(int row, int chunk) {
@@ -35,10 +49,9 @@ __device__ __forceinline__ int lds_idx(int row, int chunk) {
 }
 
 // ---------------------------------------------------------------------------
-template <int BM, int BN>
+template <class C>
 struct Core {
-  static constexpr int WM = BM / 2, WN = BN / 2;
-  static constexpr int FM = WM / 32, FN = WN / 32;
+  static constexpr int FM = C::FM, FN = C::FN;
   f32x16 acc[FM][FN];
 
   __device__ void zero() {
@@ -123,8 +136,9 @@ __device__ __forceinline__ void epilogue4(float v[4], int epi,
 //         contiguous), the latter transposed in registers.
 //   FAST  reduction channels are a multiple of BK, so a slice is one tap.
 // blockIdx.z = phase * nsplit + split.
-template <int BM, int BN, bool WK, bool FAST>
-__global__ __launch_bounds__(NT) void data_conv_kernel(DataConvArgs a) {
+template <class C, bool WK, bool FAST>
+__global__ __launch_bounds__(C::NT) void data_conv_kernel(DataConvArgs a) {
+  constexpr int BM = C::BM, BN = C::BN, NT = C::NT;
   __shared__ __attribute__((aligned(16))) uint16_t sA[2][BM * BK];
   __shared__ __attribute__((aligned(16))) uint16_t sB[2][BN * BK];
 
@@ -140,15 +154,17 @@ __global__ __launch_bounds__(NT) void data_conv_kernel(DataConvArgs a) {
   const int kchunk = (nk + a.nsplit - 1) / a.nsplit;
   const int kbeg = min(nk, split * kchunk), kend = min(nk, kbeg + kchunk);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm0 = (wave >> 1) * (BM / 2), wn0 = (wave & 1) * (BN / 2);
+  const int wm0 = (wave / C::WGN) * C::WM, wn0 = (wave % C::WGN) * C::WN;
 
-  // --- B (activation gather) loader state: BN/32 columns per thread.
-  constexpr int BCOL = BN / 32;
+  // --- B (activation gather) loader state: 8 threads per column (one
+  // 16-byte chunk each), NT/8 columns per pass, BCOL passes.
+  constexpr int RPP = NT / 8;  // rows per pass
+  constexpr int BCOL = BN / RPP;
   const int bc8 = tid & 7;
   int bbase[BCOL], bh[BCOL], bw[BCOL];
 #pragma unroll
   for (int i = 0; i < BCOL; ++i) {
-    int col = n0 + (tid >> 3) + 32 * i;
+    int col = n0 + (tid >> 3) + RPP * i;
     if (col < npix) {
       int b = col % P.mw, t = col / P.mw;
       int aa = t % P.mh, nn = t / P.mh;
@@ -162,7 +178,7 @@ __global__ __launch_bounds__(NT) void data_conv_kernel(DataConvArgs a) {
     }
   }
 
-  constexpr int AROW = BM / 32;
+  constexpr int AROW = BM / RPP;
   constexpr int AUNITS = (BK / 4) * (BM / 8);
   constexpr int AUPT = (AUNITS + NT - 1) / NT;
   u32x4 ra[WK ? AROW : 4 * AUPT];
@@ -217,7 +233,7 @@ __global__ __launch_bounds__(NT) void data_conv_kernel(DataConvArgs a) {
       const uint16_t *src = a.wgt + (size_t)woff * a.cr + cr;
 #pragma unroll
       for (int i = 0; i < AROW; ++i) {
-        int row = m0 + (tid >> 3) + 32 * i;
+        int row = m0 + (tid >> 3) + RPP * i;
         ra[i] = (kv && row < a.co) ? ldg16(src + (size_t)row * a.ldw)
                                    : u32x4{0, 0, 0, 0};
       }
@@ -250,13 +266,13 @@ __global__ __launch_bounds__(NT) void data_conv_kernel(DataConvArgs a) {
   auto store = [&](int buf) {
 #pragma unroll
     for (int i = 0; i < BCOL; ++i)
-      *reinterpret_cast<u32x4 *>(&sB[buf][lds_idx((tid >> 3) + 32 * i, bc8)]) =
+      *reinterpret_cast<u32x4 *>(&sB[buf][lds_idx((tid >> 3) + RPP * i, bc8)]) =
           rb[i];
     if (WK) {
 #pragma unroll
       for (int i = 0; i < AROW; ++i)
         *reinterpret_cast<u32x4 *>(
-            &sA[buf][lds_idx((tid >> 3) + 32 * i, bc8)]) = ra[i];
+            &sA[buf][lds_idx((tid >> 3) + RPP * i, bc8)]) = ra[i];
     } else {
 #pragma unroll
       for (int u = 0; u < AUPT; ++u) {
@@ -269,7 +285,7 @@ __global__ __launch_bounds__(NT) void data_conv_kernel(DataConvArgs a) {
     }
   };
 
-  Core<BM, BN> core;
+  Core<C> core;
   core.zero();
   if (kbeg < kend) {
     load(kbeg);
@@ -285,7 +301,7 @@ __global__ __launch_bounds__(NT) void data_conv_kernel(DataConvArgs a) {
   }
 
   // --- epilogue: lane holds 4 consecutive output channels of one position.
-  constexpr int FM = Core<BM, BN>::FM, FN = Core<BM, BN>::FN;
+  constexpr int FM = C::FM, FN = C::FN;
   const size_t out_total = (size_t)a.n * a.ho * a.wo * a.co;
 #pragma unroll
   for (int j = 0; j < FN; ++j) {
@@ -337,8 +353,9 @@ __global__ __launch_bounds__(256) void split_epilogue_kernel(
 
 // ---------------------------------------------------------------------------
 // Kernel-gradient kernel: rows rho = (tap, c) of the x patch, columns k.
-template <int BM, int BN>
-__global__ __launch_bounds__(NT) void wgrad_kernel(WgradArgs a) {
+template <class C>
+__global__ __launch_bounds__(C::NT) void wgrad_kernel(WgradArgs a) {
+  constexpr int BM = C::BM, BN = C::BN, NT = C::NT;
   __shared__ __attribute__((aligned(16))) uint16_t sA[2][BM * BK];
   __shared__ __attribute__((aligned(16))) uint16_t sB[2][BN * BK];
 
@@ -350,7 +367,7 @@ __global__ __launch_bounds__(NT) void wgrad_kernel(WgradArgs a) {
   const int mend = min(a.mtot, mbeg + a.mchunk);
   const int nk = mend > mbeg ? (mend - mbeg + BK - 1) / BK : 0;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm0 = (wave >> 1) * (BM / 2), wn0 = (wave & 1) * (BN / 2);
+  const int wm0 = (wave / C::WGN) * C::WM, wn0 = (wave % C::WGN) * C::WN;
   const int pq = a.p * a.q;
 
   constexpr int AUNITS = (BK / 4) * (BM / 8);
@@ -430,7 +447,7 @@ __global__ __launch_bounds__(NT) void wgrad_kernel(WgradArgs a) {
     }
   };
 
-  Core<BM, BN> core;
+  Core<C> core;
   core.zero();
   if (nk > 0) {
     load(0);
@@ -445,7 +462,7 @@ __global__ __launch_bounds__(NT) void wgrad_kernel(WgradArgs a) {
     __syncthreads();
   }
 
-  constexpr int FM = Core<BM, BN>::FM, FN = Core<BM, BN>::FN;
+  constexpr int FM = C::FM, FN = C::FN;
 #pragma unroll
   for (int j = 0; j < FN; ++j) {
     int k = n0 + wn0 + j * 32 + (lane & 31);
@@ -666,26 +683,27 @@ DataPlan plan_data_conv(const DataConvArgs &a) {
   return pl;
 }
 
-template <int BM, int BN, bool WK, bool FAST>
+template <class C, bool WK, bool FAST>
 static hipError_t launch_dc(const DataConvArgs &a, hipStream_t st) {
   int maxpix = 0;
   for (int i = 0; i < a.nphase; ++i)
     maxpix = std::max(maxpix, a.n * a.ph[i].mh * a.ph[i].mw);
-  dim3 grid((maxpix + BN - 1) / BN, (a.co + BM - 1) / BM, a.nphase * a.nsplit);
-  hipLaunchKernelGGL((data_conv_kernel<BM, BN, WK, FAST>), grid, dim3(NT), 0,
+  dim3 grid((maxpix + C::BN - 1) / C::BN, (a.co + C::BM - 1) / C::BM,
+            a.nphase * a.nsplit);
+  hipLaunchKernelGGL((data_conv_kernel<C, WK, FAST>), grid, dim3(C::NT), 0,
                      st, a);
   return hipGetLastError();
 }
 
-template <int BM, int BN>
+template <class C>
 static hipError_t launch_dc_tile(const DataConvArgs &a, bool w_kmajor,
                                  hipStream_t st) {
   const bool fast = (a.cr % BK) == 0;
   if (w_kmajor)
-    return fast ? launch_dc<BM, BN, true, true>(a, st)
-                : launch_dc<BM, BN, true, false>(a, st);
-  return fast ? launch_dc<BM, BN, false, true>(a, st)
-              : launch_dc<BM, BN, false, false>(a, st);
+    return fast ? launch_dc<C, true, true>(a, st)
+                : launch_dc<C, true, false>(a, st);
+  return fast ? launch_dc<C, false, true>(a, st)
+              : launch_dc<C, false, false>(a, st);
 }
 
 hipError_t launch_data_conv(const DataConvArgs &a0, bool w_kmajor,
@@ -693,8 +711,8 @@ hipError_t launch_data_conv(const DataConvArgs &a0, bool w_kmajor,
   DataConvArgs a = a0;
   const DataPlan pl = plan_data_conv(a);
   a.nsplit = pl.nsplit;
-  hipError_t e = pl.big ? launch_dc_tile<256, 256>(a, w_kmajor, st)
-                        : launch_dc_tile<128, 128>(a, w_kmajor, st);
+  hipError_t e = pl.big ? launch_dc_tile<BigCfg>(a, w_kmajor, st)
+                        : launch_dc_tile<SmallCfg>(a, w_kmajor, st);
   if (e != hipSuccess || a.nsplit == 1) return e;
   const int64_t len = (int64_t)a.n * a.ho * a.wo * a.co;
   hipLaunchKernelGGL(split_epilogue_kernel,
@@ -705,14 +723,14 @@ hipError_t launch_data_conv(const DataConvArgs &a0, bool w_kmajor,
 
 const char *data_conv_kernel_name(const DataConvArgs &a, bool w_kmajor) {
   static const char *names[2][2][2] = {
-      {{"data_conv_kernel<128, 128, false, false>",
-        "data_conv_kernel<128, 128, false, true>"},
-       {"data_conv_kernel<128, 128, true, false>",
-        "data_conv_kernel<128, 128, true, true>"}},
-      {{"data_conv_kernel<256, 256, false, false>",
-        "data_conv_kernel<256, 256, false, true>"},
-       {"data_conv_kernel<256, 256, true, false>",
-        "data_conv_kernel<256, 256, true, true>"}}};
+      {{"data_conv_kernel<Cfg<128, 128, 2, 2>, false, false>",
+        "data_conv_kernel<Cfg<128, 128, 2, 2>, false, true>"},
+       {"data_conv_kernel<Cfg<128, 128, 2, 2>, true, false>",
+        "data_conv_kernel<Cfg<128, 128, 2, 2>, true, true>"}},
+      {{"data_conv_kernel<Cfg<256, 256, 2, 4>, false, false>",
+        "data_conv_kernel<Cfg<256, 256, 2, 4>, false, true>"},
+       {"data_conv_kernel<Cfg<256, 256, 2, 4>, true, false>",
+        "data_conv_kernel<Cfg<256, 256, 2, 4>, true, true>"}}};
   const DataPlan pl = plan_data_conv(a);
   return names[pl.big][w_kmajor][(a.cr % BK) == 0];
 }
@@ -722,7 +740,8 @@ static bool wgrad_big(const fg_conv_desc &d) {
 }
 
 const char *wgrad_kernel_name(const fg_conv_desc &d) {
-  return wgrad_big(d) ? "wgrad_kernel<256, 256>" : "wgrad_kernel<128, 128>";
+  return wgrad_big(d) ? "wgrad_kernel<Cfg<256, 256, 2, 4>>"
+                      : "wgrad_kernel<Cfg<128, 128, 2, 2>>";
 }
 
 WgradPlan plan_wgrad(const fg_conv_desc &d, int32_t p, int32_t q) {
@@ -752,10 +771,11 @@ hipError_t launch_wgrad(const WgradArgs &a, hipStream_t st) {
   const bool big = rsc >= 256 && a.k >= 256;
   if (big) {
     dim3 grid((rsc + 255) / 256, (a.k + 255) / 256, a.nsplit);
-    hipLaunchKernelGGL((wgrad_kernel<256, 256>), grid, dim3(NT), 0, st, a);
+    hipLaunchKernelGGL((wgrad_kernel<BigCfg>), grid, dim3(BigCfg::NT), 0, st, a);
   } else {
     dim3 grid((rsc + 127) / 128, (a.k + 127) / 128, a.nsplit);
-    hipLaunchKernelGGL((wgrad_kernel<128, 128>), grid, dim3(NT), 0, st, a);
+    hipLaunchKernelGGL((wgrad_kernel<SmallCfg>), grid, dim3(SmallCfg::NT), 0, st,
+                       a);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.nsplit == 1) return e;
