@@ -111,76 +111,28 @@ def op_bench(label, steps, warmup):
                       "unit": unit, "launches": steps}), flush=True)
 
 
-class TimedChain:
-    """Wraps Chain so every library call in a step records HIP events on the
-    stream it is launched on (the current stream)."""
-
-    def __init__(self, chain):
-        self.ch = chain
-        self.records = []   # (label, kernel, flops_or_bytes, ev0, ev1)
-
-    def _ev(self):
-        import torch
-        return torch.cuda.Event(enable_timing=True)
-
-    def call(self, label, kernel, work, fn, *a, **k):
-        e0, e1 = self._ev(), self._ev()
-        e0.record()
-        fn(*a, **k)
-        e1.record()
-        self.records.append((label, kernel, work, e0, e1))
-
-    def step(self, target):
-        import paper_1909_11150_amd as fg
-        from paper_1909_11150_amd import fcn
-        ch = self.ch
-        # forward
-        for i, L in enumerate(ch.layers):
-            epi = fg.EPI_RELU if L.relu else fg.EPI_NONE
-            d = fcn.fwd_desc(L)
-            if L.kind == "conv":
-                self.call(f"{L.name}.fwd", fg.kernel_name(d, fg.OP_FWD), L.flops,
-                          fg.conv2d_fwd, d, ch.acts[i], ch.w[i], ch.acts[i + 1], epi,
-                          None, ch.ws)
-            else:
-                self.call(f"{L.name}.fwd", fg.kernel_name(d, fg.OP_CONVT), L.flops,
-                          fg.conv_transpose2d_fwd, d, ch.acts[i], ch.w[i],
-                          ch.acts[i + 1], epi, None, ch.ws)
-        y = ch.acts[-1]
-        self.call("head_grad", "head_grad_kernel", y.numel() * 6, fg.l2_head_grad,
-                  y, target, 2.0 * ch.loss_scale / y.numel(), ch.g[-1])
-        ch.flags.zero_()
-        for i in reversed(range(len(ch.layers))):
-            L = ch.layers[i]
-            dy = ch.g[i + 1]
-            gate = i > 0 and ch.layers[i - 1].relu
-            epi = fg.EPI_GATE if gate else fg.EPI_NONE
-            gt = ch.acts[i] if gate else None
-            if L.kind == "conv":
-                d = fcn.fwd_desc(L)
-                self.call(f"{L.name}.dW", fg.kernel_name(d, fg.OP_BWD_WEIGHT), L.flops,
-                          fg.conv2d_bwd_weight, d, ch.acts[i], dy, ch.dw[i], ch.ws)
-                self.call(f"{L.name}.dx", fg.kernel_name(d, fg.OP_BWD_DATA), L.flops,
-                          fg.conv2d_bwd_data, d, dy, ch.w[i], ch.g[i], epi, gt, ch.ws)
-            else:
-                dd = fcn.convt_dx_desc(L)
-                self.call(f"{L.name}.dW", fg.kernel_name(dd, fg.OP_BWD_WEIGHT), L.flops,
-                          fg.conv2d_bwd_weight, dd, dy, ch.acts[i], ch.dw[i], ch.ws)
-                self.call(f"{L.name}.dx", fg.kernel_name(dd, fg.OP_FWD), L.flops,
-                          fg.conv2d_fwd, dd, dy, ch.w[i], ch.g[i], epi, gt, ch.ws)
-            gi = ch._group_done_at.get(i)
-            if gi is not None:
-                g = ch.groups[gi]
-                n = g["numel"]
-                self.call(f"G{gi}.pack", "copy_pieces_kernel<2>", 4 * n,
-                          fg.grad_group_pack, [ch.dw[m] for m in g["members"]],
-                          g["offsets"], ch.gbuf16[gi])
-                self.call(f"G{gi}.unscale", "unscale_vec_kernel", 6 * n,
-                          fg.grad_unscale_check, ch.gbuf16[gi], 1.0 / ch.loss_scale,
-                          ch.gbuf32[gi], ch.flags[gi:gi + 1])
-                self.call(f"G{gi}.unpack", "copy_pieces_kernel<4>", 8 * n,
-                          fg.grad_group_unpack, ch.gbuf32[gi],
-                          [ch.master[m] for m in g["members"]], g["offsets"])
+def recorded_traffic(kernel):
+    """HBM bytes per launch of `kernel` from profiles/fcn_step_hbm_traffic.md
+    (rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled by a plain copy's reading),
+    or None when no record exists for it or the kernel source has changed
+    since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "fcn_step_hbm_traffic.md")
+    src = os.path.join(ROOT, "paper_1909_11150_amd", "csrc", "conv_igemm.hip")
+    try:
+        lines = open(path).read().splitlines()
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    except OSError:
+        return None
+    for ln in lines:
+        if not ln.startswith("traffic: kernel="):
+            continue
+        body = ln[len("traffic: kernel="):]
+        name, rest = body.split(" src_sha256_16=")
+        h, b = rest.split(" bytes_per_launch=")
+        if name == kernel and h == sha:
+            return int(b)
+    return None
 
 
 def cpu_baseline(layers, seconds):
@@ -216,15 +168,18 @@ def cpu_baseline(layers, seconds):
                                                                2, 1))]
         for total, fn in tasks:
             fpe = L.flops / total   # algorithmic flops per output element
-            probe = rng.choice(total, size=min(total, 16), replace=False)
-            t0 = time.perf_counter()
-            fn(probe)
-            dt = max(time.perf_counter() - t0, 1e-6)
-            k = int(min(total, max(16, 16 * per_task / dt)))
-            idx = rng.choice(total, size=k, replace=False)
-            t0 = time.perf_counter()
-            fn(idx)
-            t_total += time.perf_counter() - t0
+            # grow the sample until one evaluation takes a quarter of the
+            # per-task budget or more (the last, largest one is the timed one)
+            k = min(total, 64)
+            while True:
+                idx = rng.choice(total, size=k, replace=False)
+                t0 = time.perf_counter()
+                fn(idx)
+                dt = time.perf_counter() - t0
+                if k >= total or dt >= per_task / 4:
+                    break
+                k = min(total, k * 4)
+            t_total += dt
             flops_done += fpe * k
         del xs, ws, dys
     return {"value": flops_done / t_total / 1e12, "unit": "TFLOP/s",
@@ -253,50 +208,70 @@ def main():
     ch = Chain(layers, wl.weights, wl.x, loss_scale=synth.LOSS_SCALE,
                group_cap_bytes=synth.GROUP_CAP_BYTES)
     target = torch.from_numpy(wl.target).cuda()
+    prog = ch.program(target)
+    calls = prog.calls
     torch.cuda.synchronize()
-    tc = TimedChain(ch)
+
+    def ev():
+        return torch.cuda.Event(enable_timing=True)
+
     for _ in range(args.warmup):
-        tc.step(target)
+        prog.run()
     torch.cuda.synchronize()
-    tc.records.clear()
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
+
+    # detail pass (untimed for `value`): events around every call
+    det_steps = 2
+    det = [{i: (ev(), ev()) for i, c in enumerate(calls) if c.fn is not None}
+           for _ in range(det_steps)]
+    for s_ev in det:
+        prog.run(s_ev)
+    torch.cuda.synchronize()
+    per_kernel, per_op = {}, {}
+    for s_ev in det:
+        for i, (e0, e1) in s_ev.items():
+            c = calls[i]
+            t = e0.elapsed_time(e1) / det_steps
+            k = per_kernel.setdefault(c.kernel, [0, 0.0, 0.0, c.single])
+            k[0] += 1.0 / det_steps
+            k[1] += t
+            k[2] += c.work / det_steps
+            k[3] = k[3] and c.single
+            o = per_op.setdefault(c.label, [0.0, c.work, c.kernel])
+            o[0] += t
+    # dominant kernel: the single-launch MFMA conv kernel with the most time
+    dom = max((k for k, v in per_kernel.items()
+               if v[3] and k.startswith(("data_conv", "wgrad"))),
+              key=lambda k: per_kernel[k][1])
+    dom_idx = [i for i, c in enumerate(calls) if c.kernel == dom]
+
+    # timed pass: K whole steps; events only around the dominant kernel
+    dom_ev = [{i: (ev(), ev()) for i in dom_idx} for _ in range(args.steps)]
+    e_start, e_end = ev(), ev()
+    torch.cuda.synchronize()
     t0 = time.perf_counter()
-    ev0.record()
-    for _ in range(args.steps):
-        tc.step(target)
-    ev1.record()
+    e_start.record()
+    for s_ev in dom_ev:
+        prog.run(s_ev)
+    e_end.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    ms_step = ev0.elapsed_time(ev1) / args.steps
+    ms_step = e_start.elapsed_time(e_end) / args.steps
     flops_step = sum(3 * L.flops for L in layers)
     value = flops_step / (ms_step * 1e-3) / 1e12
 
-    # per-kernel aggregation of the event timings
-    per_kernel, per_op = {}, {}
-    for label, kern, work, e0, e1 in tc.records:
-        t = e0.elapsed_time(e1)
-        k = per_kernel.setdefault(kern, [0, 0.0, 0.0])
-        k[0] += 1
-        k[1] += t
-        k[2] += work
-        o = per_op.setdefault(label, [0, 0.0, work])
-        o[0] += 1
-        o[1] += t
-    conv_kernels = {k: v for k, v in per_kernel.items()
-                    if k.startswith(("data_conv", "wgrad", "head_fwd", "head_bwd",
-                                     "head_wgrad"))}
-    conv_ms = sum(v[1] for v in conv_kernels.values()) / args.steps
-    dom = max((k for k in conv_kernels if k.startswith("data_conv")),
-              key=lambda k: conv_kernels[k][1])
-    n, tsum, fsum = conv_kernels[dom]
-    avg_s = tsum / n * 1e-3
-    achieved = fsum / n / avg_s / 1e12
+    n_dom = len(dom_idx) * args.steps
+    t_dom = sum(e0.elapsed_time(e1) for s_ev in dom_ev for e0, e1 in s_ev.values())
+    f_dom = sum(calls[i].work for i in dom_idx) * args.steps
+    avg_s = t_dom / n_dom * 1e-3
+    achieved = f_dom / n_dom / avg_s / 1e12
     roof = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),
             "peak": MFMA_F16_PEAK_TFLOPS, "unit": "TFLOP/s",
             "frac": round(achieved / MFMA_F16_PEAK_TFLOPS, 4),
-            "avg_launch_us": round(avg_s * 1e6, 2), "launches_per_step": n // args.steps,
-            "traffic": None}
+            "avg_launch_us": round(avg_s * 1e6, 2), "launches_per_step": len(dom_idx),
+            "traffic": recorded_traffic(dom)}
+    conv_ms = sum(v[1] for k, v in per_kernel.items()
+                  if k.startswith(("data_conv", "wgrad", "head_fwd", "head_bwd",
+                                   "head_wgrad")))
 
     def bw(name):
         v = per_kernel.get(name)
@@ -328,11 +303,11 @@ def main():
         "roofline": roof,
     }
     if args.detail:
-        det = {"per_kernel": {k: {"launches": v[0], "ms_total": v[1], "work": v[2]}
+        det = {"per_kernel": {k: {"launches_per_step": v[0], "ms_per_step": v[1],
+                                  "work_per_step": v[2], "single_launch": v[3]}
                               for k, v in per_kernel.items()},
-               "per_op_ms": {k: v[1] / v[0] for k, v in per_op.items()},
-               "per_op_tflops_or_gbps": {k: v[2] / (v[1] / v[0] * 1e-3) / 1e12
-                                         for k, v in per_op.items()}}
+               "per_op": {k: {"ms": v[0], "rate": v[1] / (v[0] * 1e-3) / 1e12,
+                              "kernel": v[2]} for k, v in per_op.items()}}
         with open(args.detail, "w") as f:
             json.dump(det, f, indent=1)
     if not args.no_cpu:

@@ -423,7 +423,7 @@ fg_status conv2d_bwd_weight(const fg_conv_desc *d, const uint16_t *x,
   a.mtot = d->n * P * Q;
   a.mchunk = pl.mchunk;
   a.nsplit = pl.nsplit;
-  return launch_status(launch_wgrad(a, stream));
+  return launch_status(launch_wgrad(a, pl.big, stream));
 }
 
 // ---------------------------------------------------------------------------

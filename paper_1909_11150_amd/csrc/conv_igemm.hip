@@ -135,8 +135,10 @@ __device__ __forceinline__ void epilogue4(float v[4], int epi,
 //         channel) or mn-major (input gradient / transposed: output channel
 //         contiguous), the latter transposed in registers.
 //   FAST  reduction channels are a multiple of BK, so a slice is one tap.
+//   SPLIT the reduction is split across workgroups: write fp32 partials
+//         (a.nsplit > 1) instead of the fp16 output.
 // blockIdx.z = phase * nsplit + split.
-template <class C, bool WK, bool FAST>
+template <class C, bool WK, bool FAST, bool SPLIT>
 __global__ __launch_bounds__(C::NT) void data_conv_kernel(DataConvArgs a) {
   constexpr int BM = C::BM, BN = C::BN, NT = C::NT;
   __shared__ __attribute__((aligned(16))) uint16_t sA[2][BM * BK];
@@ -321,7 +323,7 @@ __global__ __launch_bounds__(C::NT) void data_conv_kernel(DataConvArgs a) {
         float v[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[e] = core.acc[i][j][4 * g + e];
-        if (a.nsplit > 1) {
+        if (SPLIT) {
           f32x4 o = {v[0], v[1], v[2], v[3]};
           *reinterpret_cast<f32x4 *>(a.part + split * out_total + obase + co) = o;
         } else {
@@ -353,7 +355,7 @@ __global__ __launch_bounds__(256) void split_epilogue_kernel(
 
 // ---------------------------------------------------------------------------
 // Kernel-gradient kernel: rows rho = (tap, c) of the x patch, columns k.
-template <class C>
+template <class C, bool SPLIT>
 __global__ __launch_bounds__(C::NT) void wgrad_kernel(WgradArgs a) {
   constexpr int BM = C::BM, BN = C::BN, NT = C::NT;
   __shared__ __attribute__((aligned(16))) uint16_t sA[2][BM * BK];
@@ -474,7 +476,7 @@ __global__ __launch_bounds__(C::NT) void wgrad_kernel(WgradArgs a) {
         int rho = m0 + wm0 + i * 32 + 8 * g + 4 * (lane >> 5);
         if (rho >= rsc) continue;
         const f32x16 &c = core.acc[i][j];
-        if (a.nsplit == 1) {
+        if (!SPLIT) {
           *reinterpret_cast<u32x2 *>(a.dw + (size_t)k * rsc + rho) =
               to_h4(c[4 * g], c[4 * g + 1], c[4 * g + 2], c[4 * g + 3]);
         } else {
@@ -666,19 +668,53 @@ constexpr int64_t kCUs = 256;
 
 }  // namespace
 
+// Split/tile choice by an estimate of the run time: resident workgroup
+// slots per GPU (one 256x256 workgroup or two 128x128 ones per CU), the
+// per-workgroup MFMA rate each reaches (measured on MI355X), waves of
+// workgroups, and the fp32 partials a split writes and re-reads.
+struct TileChoice {
+  bool big;
+  int32_t nsplit;
+};
+
+TileChoice choose_tiles(int64_t tiles_big, int64_t tiles_small, int64_t nk,
+                        int64_t out_elems, bool allow_big) {
+  constexpr double kRateBig = 3.0e12;    // flop/s of one 256x256 workgroup
+  constexpr double kRateSmall = 1.3e12;  // flop/s of one 128x128 workgroup
+  constexpr double kPartialBw = 6.0e12;  // B/s for fp32 partial traffic
+  constexpr double kReduceLaunch = 4e-6;
+  TileChoice best{false, 1};
+  double best_t = 1e30;
+  for (int big = 0; big < 2; ++big) {
+    if (big && !allow_big) continue;
+    const int64_t tiles = big ? tiles_big : tiles_small;
+    const int64_t slots = big ? kCUs : 2 * kCUs;
+    const int t = big ? 256 : 128;
+    const double rate = big ? kRateBig : kRateSmall;
+    for (int ns = 1; ns <= 16; ++ns) {
+      if (ns > 1 && (nk + ns - 1) / ns < 4) break;  // >= 4 slices per split
+      const int64_t waves = (tiles * ns + slots - 1) / slots;
+      const int64_t nk_split = (nk + ns - 1) / ns;
+      const double t_block = 2.0 * t * t * BK * (double)nk_split / rate;
+      double tt = waves * t_block;
+      if (ns > 1) tt += ns * (double)out_elems * 8.0 / kPartialBw + kReduceLaunch;
+      if (tt < best_t * 0.98) {  // prefer fewer splits on near ties
+        best_t = tt;
+        best = TileChoice{big != 0, ns};
+      }
+    }
+  }
+  return best;
+}
+
 DataPlan plan_data_conv(const DataConvArgs &a) {
   DataPlan pl;
-  pl.big = data_tiles(a, 256, 256) >= kCUs && a.co >= 256;
-  const int64_t tiles = pl.big ? data_tiles(a, 256, 256) : data_tiles(a, 128, 128);
-  int64_t ns = 1;
-  if (!pl.big && tiles < kCUs) {
-    const int64_t nk = data_nk_max(a);
-    ns = (2 * kCUs + tiles - 1) / tiles;  // ~2 workgroups per CU
-    ns = std::min<int64_t>(ns, std::max<int64_t>(1, nk / 8));  // >= 8 slices each
-    ns = std::min<int64_t>(ns, 16);
-  }
-  pl.nsplit = (int32_t)std::max<int64_t>(ns, 1);
   const int64_t out = (int64_t)a.n * a.ho * a.wo * a.co;
+  const TileChoice c = choose_tiles(data_tiles(a, 256, 256),
+                                    data_tiles(a, 128, 128), data_nk_max(a), out,
+                                    a.co >= 256);
+  pl.big = c.big;
+  pl.nsplit = c.nsplit;
   pl.ws_bytes = pl.nsplit > 1 ? (size_t)pl.nsplit * out * sizeof(float) : 0;
   return pl;
 }
@@ -690,8 +726,12 @@ static hipError_t launch_dc(const DataConvArgs &a, hipStream_t st) {
     maxpix = std::max(maxpix, a.n * a.ph[i].mh * a.ph[i].mw);
   dim3 grid((maxpix + C::BN - 1) / C::BN, (a.co + C::BM - 1) / C::BM,
             a.nphase * a.nsplit);
-  hipLaunchKernelGGL((data_conv_kernel<C, WK, FAST>), grid, dim3(C::NT), 0,
-                     st, a);
+  if (a.nsplit > 1)
+    hipLaunchKernelGGL((data_conv_kernel<C, WK, FAST, true>), grid, dim3(C::NT),
+                       0, st, a);
+  else
+    hipLaunchKernelGGL((data_conv_kernel<C, WK, FAST, false>), grid,
+                       dim3(C::NT), 0, st, a);
   return hipGetLastError();
 }
 
@@ -722,60 +762,86 @@ hipError_t launch_data_conv(const DataConvArgs &a0, bool w_kmajor,
 }
 
 const char *data_conv_kernel_name(const DataConvArgs &a, bool w_kmajor) {
-  static const char *names[2][2][2] = {
-      {{"data_conv_kernel<Cfg<128, 128, 2, 2>, false, false>",
-        "data_conv_kernel<Cfg<128, 128, 2, 2>, false, true>"},
-       {"data_conv_kernel<Cfg<128, 128, 2, 2>, true, false>",
-        "data_conv_kernel<Cfg<128, 128, 2, 2>, true, true>"}},
-      {{"data_conv_kernel<Cfg<256, 256, 2, 4>, false, false>",
-        "data_conv_kernel<Cfg<256, 256, 2, 4>, false, true>"},
-       {"data_conv_kernel<Cfg<256, 256, 2, 4>, true, false>",
-        "data_conv_kernel<Cfg<256, 256, 2, 4>, true, true>"}}};
+  // [big][w_kmajor][fast][split], as a kernel trace prints them
+  static const char *names[2][2][2][2] = {
+      {{{"data_conv_kernel<Cfg<128, 128, 2, 2>, false, false, false>",
+         "data_conv_kernel<Cfg<128, 128, 2, 2>, false, false, true>"},
+        {"data_conv_kernel<Cfg<128, 128, 2, 2>, false, true, false>",
+         "data_conv_kernel<Cfg<128, 128, 2, 2>, false, true, true>"}},
+       {{"data_conv_kernel<Cfg<128, 128, 2, 2>, true, false, false>",
+         "data_conv_kernel<Cfg<128, 128, 2, 2>, true, false, true>"},
+        {"data_conv_kernel<Cfg<128, 128, 2, 2>, true, true, false>",
+         "data_conv_kernel<Cfg<128, 128, 2, 2>, true, true, true>"}}},
+      {{{"data_conv_kernel<Cfg<256, 256, 2, 4>, false, false, false>",
+         "data_conv_kernel<Cfg<256, 256, 2, 4>, false, false, true>"},
+        {"data_conv_kernel<Cfg<256, 256, 2, 4>, false, true, false>",
+         "data_conv_kernel<Cfg<256, 256, 2, 4>, false, true, true>"}},
+       {{"data_conv_kernel<Cfg<256, 256, 2, 4>, true, false, false>",
+         "data_conv_kernel<Cfg<256, 256, 2, 4>, true, false, true>"},
+        {"data_conv_kernel<Cfg<256, 256, 2, 4>, true, true, false>",
+         "data_conv_kernel<Cfg<256, 256, 2, 4>, true, true, true>"}}}};
   const DataPlan pl = plan_data_conv(a);
-  return names[pl.big][w_kmajor][(a.cr % BK) == 0];
+  return names[pl.big][w_kmajor][(a.cr % BK) == 0][pl.nsplit > 1];
 }
 
-static bool wgrad_big(const fg_conv_desc &d) {
-  return (int64_t)d.r * d.s * d.c >= 256 && d.k >= 256;
+static TileChoice wgrad_choice(const fg_conv_desc &d, int32_t p, int32_t q) {
+  const int64_t rsc = (int64_t)d.r * d.s * d.c;
+  const int64_t mtot = (int64_t)d.n * p * q;
+  const int64_t tb = ((rsc + 255) / 256) * ((d.k + 255) / 256);
+  const int64_t ts = ((rsc + 127) / 128) * ((d.k + 127) / 128);
+  return choose_tiles(tb, ts, (mtot + BK - 1) / BK, (int64_t)d.k * rsc,
+                      rsc >= 256 && d.k >= 256);
 }
+
+WgradPlan plan_wgrad(const fg_conv_desc &d, int32_t p, int32_t q);
 
 const char *wgrad_kernel_name(const fg_conv_desc &d) {
-  return wgrad_big(d) ? "wgrad_kernel<Cfg<256, 256, 2, 4>>"
-                      : "wgrad_kernel<Cfg<128, 128, 2, 2>>";
+  int32_t p = (d.h + 2 * d.pad_h - d.r) / d.stride_h + 1;
+  int32_t q = (d.w + 2 * d.pad_w - d.s) / d.stride_w + 1;
+  const WgradPlan pl = plan_wgrad(d, p, q);
+  static const char *names[2][2] = {
+      {"wgrad_kernel<Cfg<128, 128, 2, 2>, false>",
+       "wgrad_kernel<Cfg<128, 128, 2, 2>, true>"},
+      {"wgrad_kernel<Cfg<256, 256, 2, 4>, false>",
+       "wgrad_kernel<Cfg<256, 256, 2, 4>, true>"}};
+  return names[pl.big][pl.nsplit > 1];
 }
 
 WgradPlan plan_wgrad(const fg_conv_desc &d, int32_t p, int32_t q) {
   WgradPlan pl;
-  const int t = wgrad_big(d) ? 256 : 128;
+  const TileChoice c = wgrad_choice(d, p, q);
   const int64_t rsc = (int64_t)d.r * d.s * d.c;
-  const int64_t tiles = ((rsc + t - 1) / t) * ((d.k + t - 1) / t);
   const int64_t mtot = (int64_t)d.n * p * q;
-  // resident workgroups: one per CU for 256 x 256 tiles, two for 128 x 128;
-  // take the largest split that keeps the grid within one such wave, so no
-  // partly filled second wave doubles the time
-  const int64_t slots = wgrad_big(d) ? kCUs : 2 * kCUs;
-  int64_t want = std::max<int64_t>(1, slots / tiles);
-  int64_t maxs = (mtot + 8 * BK - 1) / (8 * BK);  // >= 8 slices each
-  int64_t ns = std::max<int64_t>(1, std::min(want, maxs));
+  int64_t ns = c.nsplit;
   int64_t chunk = (mtot + ns - 1) / ns;
   chunk = (chunk + BK - 1) / BK * BK;
   ns = (mtot + chunk - 1) / chunk;
+  pl.big = c.big;
   pl.nsplit = (int32_t)ns;
   pl.mchunk = (int32_t)chunk;
   pl.ws_bytes = ns > 1 ? (size_t)ns * d.k * rsc * sizeof(float) : 0;
   return pl;
 }
 
-hipError_t launch_wgrad(const WgradArgs &a, hipStream_t st) {
+hipError_t launch_wgrad(const WgradArgs &a, bool big, hipStream_t st) {
   const int rsc = a.r * a.s * a.c;
-  const bool big = rsc >= 256 && a.k >= 256;
+  const bool split = a.nsplit > 1;
   if (big) {
     dim3 grid((rsc + 255) / 256, (a.k + 255) / 256, a.nsplit);
-    hipLaunchKernelGGL((wgrad_kernel<BigCfg>), grid, dim3(BigCfg::NT), 0, st, a);
+    if (split)
+      hipLaunchKernelGGL((wgrad_kernel<BigCfg, true>), grid, dim3(BigCfg::NT), 0,
+                         st, a);
+    else
+      hipLaunchKernelGGL((wgrad_kernel<BigCfg, false>), grid, dim3(BigCfg::NT), 0,
+                         st, a);
   } else {
     dim3 grid((rsc + 127) / 128, (a.k + 127) / 128, a.nsplit);
-    hipLaunchKernelGGL((wgrad_kernel<SmallCfg>), grid, dim3(SmallCfg::NT), 0, st,
-                       a);
+    if (split)
+      hipLaunchKernelGGL((wgrad_kernel<SmallCfg, true>), grid, dim3(SmallCfg::NT),
+                         0, st, a);
+    else
+      hipLaunchKernelGGL((wgrad_kernel<SmallCfg, false>), grid,
+                         dim3(SmallCfg::NT), 0, st, a);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.nsplit == 1) return e;

@@ -68,6 +68,7 @@ struct WgradArgs {
 // Kernel selection for a shape; pure host logic, shared by the workspace
 // query and the launchers so both always agree.
 struct WgradPlan {
+  bool big;              // 256 x 256 tiles (else 128 x 128)
   int32_t nsplit, mchunk;
   size_t ws_bytes;
 };
@@ -78,7 +79,7 @@ hipError_t launch_data_conv(const DataConvArgs &a, bool w_kmajor,
                             hipStream_t st);
 const char *data_conv_kernel_name(const DataConvArgs &a, bool w_kmajor);
 const char *wgrad_kernel_name(const fg_conv_desc &d);
-hipError_t launch_wgrad(const WgradArgs &a, hipStream_t st);
+hipError_t launch_wgrad(const WgradArgs &a, bool big, hipStream_t st);
 hipError_t launch_head_fwd(const uint16_t *x, const uint16_t *w, uint16_t *y,
                            int64_t npix, int32_t c, int32_t epi,
                            const uint16_t *gate, hipStream_t st);

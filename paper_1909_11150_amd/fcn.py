@@ -11,10 +11,13 @@ scaling). Device memory comes from torch; every step is a libfcngrad call.
 Layers are duck-typed: ``kind`` ("conv" | "convT"), ``x_shape``/``y_shape``
 (NHWC), ``r``, ``s``, ``stride``, ``pad``, ``relu`` and ``w_shape``.
 """
+import ctypes
+from collections import namedtuple
+
 import torch
 
 from . import (EPI_GATE, EPI_NONE, EPI_RELU, OP_BWD_DATA, OP_BWD_WEIGHT,
-               OP_CONVT, OP_FWD, ConvDesc,
+               OP_CONVT, OP_FWD, ConvDesc, FgError, Segment, kernel_name, lib,
                conv2d_bwd_data, conv2d_bwd_weight, conv2d_fwd,
                conv_transpose2d_fwd, grad_group_pack, grad_group_plan,
                grad_group_unpack, grad_unscale_check, l2_head_grad,
@@ -169,13 +172,145 @@ class Chain:
 
     def step(self, target):
         """Forward, loss head, backward and the grouped gradient path."""
+        if self.groups is not None:
+            key = target.data_ptr()
+            if getattr(self, "_prog_key", None) != key:
+                self._prog = self.program(target)
+                self._prog_key = key
+            self._prog.run()
+            return
         self.forward()
         self.head_grad(target)
-        if self.groups is not None:
-            self.flags.zero_()
-        self.backward(grad_path=self.groups is not None)
+        self.backward()
 
     # ---- accounting -------------------------------------------------------------
     def conv_flops(self):
         """Algorithmic flops of one forward + backward pass (3 passes/layer)."""
         return sum(3 * L.flops for L in self.layers)
+
+    # ---- prepared step -----------------------------------------------------------
+    def program(self, target):
+        """The step as a list of library calls with every argument marshalled
+        once (descriptors, pointers, segment tables); running it costs one
+        foreign call per launch. Same calls, same order as ``step``."""
+        return StepProgram(self, target)
+
+
+# label, main kernel, algorithmic work (flops, or bytes for the gradient
+# path), C function (None: a Python callable), argument tuple, and whether
+# the call is exactly one launch of that kernel
+Call = namedtuple("Call", "label kernel work fn args single", defaults=(True,))
+
+
+class StepProgram:
+    def __init__(self, ch, target):
+        if ch.groups is None:
+            raise ValueError("the step program needs gradient groups")
+        L_ = lib()
+        st = ch.stream if ch.stream is not None else \
+            torch.cuda.current_stream(ch.dev).cuda_stream
+        st = ctypes.c_void_p(st)
+        self._keep = [target]
+        calls = []
+        ws, wsb = ch.ws.data_ptr(), ch.ws.numel()
+
+        def ptr(t):
+            return None if t is None else t.data_ptr()
+
+        def desc(d):
+            self._keep.append(d)
+            return ctypes.byref(d)
+
+        def one(d, op):  # no workspace: no split, one kernel launch
+            return workspace_bytes(d, op) == 0
+
+        for i, L in enumerate(ch.layers):
+            epi = EPI_RELU if L.relu else EPI_NONE
+            d = fwd_desc(L)
+            if L.kind == "conv":
+                calls.append(Call(f"{L.name}.fwd", kernel_name(d, OP_FWD), L.flops,
+                                  L_.conv2d_fwd,
+                                  (desc(d), ptr(ch.acts[i]), ptr(ch.w[i]),
+                                   ptr(ch.acts[i + 1]), epi, None, ws, wsb, st),
+                                  one(d, OP_FWD)))
+            else:
+                calls.append(Call(f"{L.name}.fwd", kernel_name(d, OP_CONVT), L.flops,
+                                  L_.conv_transpose2d_fwd,
+                                  (desc(d), ptr(ch.acts[i]), ptr(ch.w[i]),
+                                   ptr(ch.acts[i + 1]), epi, None, ws, wsb, st),
+                                  one(d, OP_CONVT)))
+        y = ch.acts[-1]
+        calls.append(Call("head_grad", "head_grad_kernel", 6 * y.numel(),
+                          L_.l2_head_grad,
+                          (ptr(y), ptr(target), y.numel(),
+                           2.0 * ch.loss_scale / y.numel(), ptr(ch.g[-1]), st)))
+        calls.append(Call("flags.zero", "", 0, None, (ch.flags.zero_,), False))
+        for i in reversed(range(len(ch.layers))):
+            L = ch.layers[i]
+            dy = ch.g[i + 1]
+            gate = i > 0 and ch.layers[i - 1].relu
+            epi = EPI_GATE if gate else EPI_NONE
+            gt = ptr(ch.acts[i]) if gate else None
+            if L.kind == "conv":
+                d = fwd_desc(L)
+                calls.append(Call(f"{L.name}.dW", kernel_name(d, OP_BWD_WEIGHT),
+                                  L.flops, L_.conv2d_bwd_weight,
+                                  (desc(d), ptr(ch.acts[i]), ptr(dy), ptr(ch.dw[i]),
+                                   ws, wsb, st), one(d, OP_BWD_WEIGHT)))
+                calls.append(Call(f"{L.name}.dx", kernel_name(d, OP_BWD_DATA),
+                                  L.flops, L_.conv2d_bwd_data,
+                                  (desc(d), ptr(dy), ptr(ch.w[i]), ptr(ch.g[i]), epi,
+                                   gt, ws, wsb, st), one(d, OP_BWD_DATA)))
+            else:
+                d = convt_dx_desc(L)
+                calls.append(Call(f"{L.name}.dW", kernel_name(d, OP_BWD_WEIGHT),
+                                  L.flops, L_.conv2d_bwd_weight,
+                                  (desc(d), ptr(dy), ptr(ch.acts[i]), ptr(ch.dw[i]),
+                                   ws, wsb, st), one(d, OP_BWD_WEIGHT)))
+                calls.append(Call(f"{L.name}.dx", kernel_name(d, OP_FWD), L.flops,
+                                  L_.conv2d_fwd,
+                                  (desc(d), ptr(dy), ptr(ch.w[i]), ptr(ch.g[i]), epi,
+                                   gt, ws, wsb, st), one(d, OP_FWD)))
+            gi = ch._group_done_at.get(i)
+            if gi is not None:
+                calls += self._group_calls(ch, gi, L_, st)
+        self.calls = calls
+
+    def _group_calls(self, ch, gi, L_, st):
+        g = ch.groups[gi]
+        n = g["numel"]
+        src = (Segment * len(g["members"]))(
+            *[Segment(ch.dw[m].data_ptr(), ch.dw[m].numel(), off)
+              for m, off in zip(g["members"], g["offsets"])])
+        dst = (Segment * len(g["members"]))(
+            *[Segment(ch.master[m].data_ptr(), ch.master[m].numel(), off)
+              for m, off in zip(g["members"], g["offsets"])])
+        self._keep += [src, dst]
+        g16, g32 = ch.gbuf16[gi], ch.gbuf32[gi]
+        flag = ch.flags[gi:gi + 1]
+        self._keep.append(flag)
+        return [
+            Call(f"G{gi}.pack", "copy_pieces_kernel<2>", 4 * n, L_.grad_group_pack,
+                 (src, len(g["members"]), g16.data_ptr(), n, st)),
+            Call(f"G{gi}.unscale", "unscale_vec_kernel", 6 * n, L_.grad_unscale_check,
+                 (g16.data_ptr(), n, 1.0 / ch.loss_scale, g32.data_ptr(),
+                  flag.data_ptr(), st)),
+            Call(f"G{gi}.unpack", "copy_pieces_kernel<4>", 8 * n, L_.grad_group_unpack,
+                 (g32.data_ptr(), n, dst, len(g["members"]), st)),
+        ]
+
+    def run(self, events=None):
+        """Run the step once. events: {call index: (start, end)} HIP events
+        recorded around those calls on the launch stream."""
+        for i, c in enumerate(self.calls):
+            ev = events.get(i) if events else None
+            if ev:
+                ev[0].record()
+            if c.fn is None:
+                c.args[0]()
+            else:
+                st = c.fn(*c.args)
+                if st:
+                    raise FgError(c.label, st)
+            if ev:
+                ev[1].record()

@@ -6,12 +6,13 @@ Chains: the oracle runs the same chain from the same seeded inputs, storing
 each activation and gradient in fp16 like the GPU (O16). Per-op differences
 (last bits of fp16 outputs, a ReLU decision on a value within an ulp of
 zero) propagate down a chain, so chained outputs cannot be held to the
-single-op rule. The bound is derived from the arithmetic instead: fp16
-storage moves the chain away from the same chain kept in fp64 (O64) by a
-measurable distance; the GPU chain and O16 are two such fp16 realisations
-with independent rounding, so their distance is expected near sqrt(2) times
-that, and is allowed 2 times, with the single-op bound as a floor:
-    rel_L2(GPU, O16) <= max(5e-3, 2 * rel_L2(O16, O64)).
+single-op rule. The bound is calibrated instead by two measured drifts of
+the same chain: O16 against the chain kept entirely in fp64 (O64, what fp16
+storage costs), and an independent fp32-accumulating implementation with
+fp16 storage (PyTorch CPU float32, tests/fp32_chain.py) against O16 (what
+any correct fp32 accumulation order costs). The GPU is allowed twice the
+larger, with the single-op bound as a floor:
+    rel_L2(GPU, O16) <= max(5e-3, 2 * rel_L2(O16, O64), 2 * rel_L2(T32, O16)).
 The largest single difference of a chain is set by the few positions where
 a ReLU decision flipped on either side and is heavy-tailed, so for chains it
 is printed, not gated. Single ops (the first op of each chain, every
@@ -25,6 +26,7 @@ import torch
 import oracle
 import paper_1909_11150_amd as fg
 import synth
+import fp32_chain as T32
 from gpu_util import conv_parity, dev, host, sample_indices
 from oracle import chain as OC
 from oracle import grad as G
@@ -42,10 +44,11 @@ def _dist(a, b):
     return rel, ratio
 
 
-def chain_parity(g16, o16, o64, what):
+def chain_parity(g16, o16, o64, t32, what):
     assert np.all(np.isfinite(np.asarray(g16, np.float64))), what
     rel, ratio = _dist(g16, o16)
     rel_n, ratio_n = _dist(o16, o64)
+    rel_n = max(rel_n, _dist(t32, o16)[0])
     print(f"{what}: rel_L2 {rel:.3e} (fp16 noise {rel_n:.3e}), "
           f"max_abs/RMS {ratio:.3e} (fp16 noise {ratio_n:.3e})")
     assert rel <= max(5e-3, 2 * rel_n), \
@@ -80,10 +83,13 @@ def _check_block(wl, gate_top):
     if gate_top:
         dy64 = np.where(a64[-1] > 0, dy64, 0.0)
     dws64, dxs64 = OC.backward(wl.layers, a64, wl.weights, dy64, store_fp16=False)
+    at = T32.forward(wl.layers, wl.x, wl.weights)
+    dyt = G.relu_backward(wl.dy, at[-1]) if gate_top else wl.dy
+    dwt, dxt = T32.backward(wl.layers, at, wl.weights, dyt)
     for i in range(len(wl.layers)):
-        chain_parity(host(ch.acts[i + 1]), acts[i + 1], a64[i + 1], f"act{i}")
-        chain_parity(host(ch.dw[i]), dws[i], dws64[i], f"dW{i}")
-        chain_parity(host(ch.g[i]), dxs[i], dxs64[i], f"dx{i}")
+        chain_parity(host(ch.acts[i + 1]), acts[i + 1], a64[i + 1], at[i + 1], f"act{i}")
+        chain_parity(host(ch.dw[i]), dws[i], dws64[i], dwt[i], f"dW{i}")
+        chain_parity(host(ch.g[i]), dxs[i], dxs64[i], dxt[i], f"dx{i}")
     # the first op of each chain sees identical inputs: full single-op rule
     conv_parity(host(ch.acts[1]),
                 OC.layer_forward(wl.layers[0], wl.x, wl.weights[0]), "first fwd")
@@ -114,9 +120,12 @@ def test_reduced_network_step_with_gradient_path():
     a64 = OC.forward(layers, x, w, store_fp16=False)
     dws64, _ = OC.backward(layers, a64, w, OC.head_grad(a64[-1], t, S, store_fp16=False),
                            store_fp16=False)
+    at = T32.forward(layers, x, w)
+    dwt, _ = T32.backward(layers, at, w, G.head_grad(at[-1], t, S))
     for i, L in enumerate(layers):
-        chain_parity(host(ch.acts[i + 1]), acts[i + 1], a64[i + 1], f"{L.name} act")
-        chain_parity(host(ch.dw[i]), dws[i], dws64[i], f"{L.name} dW")
+        chain_parity(host(ch.acts[i + 1]), acts[i + 1], a64[i + 1], at[i + 1],
+                     f"{L.name} act")
+        chain_parity(host(ch.dw[i]), dws[i], dws64[i], dwt[i], f"{L.name} dW")
         # fp32 master gradient = fp16 dW / S, exactly, on the GPU's own dW
         np.testing.assert_array_equal(
             host(ch.master[i]),
