@@ -123,6 +123,8 @@ DataConvArgs fwd_args(const fg_conv_desc *d, int32_t P, int32_t Q) {
   a.ostr = 1;
   a.s = d->s;
   a.ldw = d->r * d->s * d->c;
+  a.wbytes = (int32_t)std::min<int64_t>(elems4(d->k, d->r, d->s, d->c) * 2,
+                                        0x7FFFFFFF);
   a.nphase = 1;
   a.nsplit = 1;
   Phase &ph = a.ph[0];
@@ -143,6 +145,8 @@ DataConvArgs bwd_data_args(const fg_conv_desc *d, int32_t P, int32_t Q) {
   a.s = d->s;
   a.w_red = d->r * d->s * d->c;  // W[k][r][s][c]: reduction index k
   a.w_tap = d->c;
+  a.wbytes = (int32_t)std::min<int64_t>(elems4(d->k, d->r, d->s, d->c) * 2,
+                                        0x7FFFFFFF);
   a.nsplit = 1;
   a.nphase = make_phases(a, d->h, d->w, d->stride_h, d->stride_w, d->pad_h,
                          d->pad_w, d->r, d->s);
@@ -159,6 +163,8 @@ DataConvArgs convt_args(const fg_conv_desc *d, int32_t HO, int32_t WO) {
   a.s = d->s;
   a.w_red = d->r * d->s * d->k;  // Wt[c][r][s][k]: reduction index c
   a.w_tap = d->k;
+  a.wbytes = (int32_t)std::min<int64_t>(elems4(d->c, d->r, d->s, d->k) * 2,
+                                        0x7FFFFFFF);
   a.nsplit = 1;
   a.nphase = make_phases(a, HO, WO, d->stride_h, d->stride_w, d->pad_h,
                          d->pad_w, d->r, d->s);

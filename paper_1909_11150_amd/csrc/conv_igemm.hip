@@ -751,7 +751,8 @@ hipError_t launch_data_conv(const DataConvArgs &a0, bool w_kmajor,
   DataConvArgs a = a0;
   const DataPlan pl = plan_data_conv(a);
   a.nsplit = pl.nsplit;
-  hipError_t e = pl.big ? launch_dc_tile<BigCfg>(a, w_kmajor, st)
+  hipError_t e = pl.big ? (data_dma_ok(a) ? launch_data_conv_dma(a, w_kmajor, st)
+                                          : launch_dc_tile<BigCfg>(a, w_kmajor, st))
                         : launch_dc_tile<SmallCfg>(a, w_kmajor, st);
   if (e != hipSuccess || a.nsplit == 1) return e;
   const int64_t len = (int64_t)a.n * a.ho * a.wo * a.co;
@@ -781,6 +782,12 @@ const char *data_conv_kernel_name(const DataConvArgs &a, bool w_kmajor) {
         {"data_conv_kernel<Cfg<256, 256, 2, 4>, true, true, false>",
          "data_conv_kernel<Cfg<256, 256, 2, 4>, true, true, true>"}}}};
   const DataPlan pl = plan_data_conv(a);
+  if (pl.big && data_dma_ok(a)) {
+    static const char *dn[2][2] = {
+        {"data_conv_dma_kernel<false, false>", "data_conv_dma_kernel<false, true>"},
+        {"data_conv_dma_kernel<true, false>", "data_conv_dma_kernel<true, true>"}};
+    return dn[w_kmajor][pl.nsplit > 1];
+  }
   return names[pl.big][w_kmajor][(a.cr % BK) == 0][pl.nsplit > 1];
 }
 
@@ -799,6 +806,11 @@ const char *wgrad_kernel_name(const fg_conv_desc &d) {
   int32_t p = (d.h + 2 * d.pad_h - d.r) / d.stride_h + 1;
   int32_t q = (d.w + 2 * d.pad_w - d.s) / d.stride_w + 1;
   const WgradPlan pl = plan_wgrad(d, p, q);
+  WgradArgs wa;
+  wa.n = d.n; wa.h = d.h; wa.w = d.w; wa.c = d.c; wa.k = d.k;
+  wa.mtot = d.n * p * q;
+  if (pl.big && wgrad_dma_ok(wa))
+    return pl.nsplit > 1 ? "wgrad_dma_kernel<true>" : "wgrad_dma_kernel<false>";
   static const char *names[2][2] = {
       {"wgrad_kernel<Cfg<128, 128, 2, 2>, false>",
        "wgrad_kernel<Cfg<128, 128, 2, 2>, true>"},
@@ -826,7 +838,10 @@ WgradPlan plan_wgrad(const fg_conv_desc &d, int32_t p, int32_t q) {
 hipError_t launch_wgrad(const WgradArgs &a, bool big, hipStream_t st) {
   const int rsc = a.r * a.s * a.c;
   const bool split = a.nsplit > 1;
-  if (big) {
+  if (big && wgrad_dma_ok(a)) {
+    hipError_t e = launch_wgrad_dma(a, st);
+    if (e != hipSuccess || !split) return e;
+  } else if (big) {
     dim3 grid((rsc + 255) / 256, (a.k + 255) / 256, a.nsplit);
     if (split)
       hipLaunchKernelGGL((wgrad_kernel<BigCfg, true>), grid, dim3(BigCfg::NT), 0,

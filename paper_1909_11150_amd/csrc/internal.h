@@ -38,6 +38,7 @@ struct DataConvArgs {
   //   k-major:  wgt[co*ldw + (r*S + s)*cr_stride + cr]
   //   mn-major: wgt[cr*w_red + (r*S + s)*w_tap + co]
   int32_t ldw, w_red, w_tap;
+  int32_t wbytes;        // size of the weight tensor in bytes
   int32_t epi;
   int32_t nphase;
   int32_t nsplit;        // reduction split (set by the launcher)
@@ -80,6 +81,13 @@ hipError_t launch_data_conv(const DataConvArgs &a, bool w_kmajor,
 const char *data_conv_kernel_name(const DataConvArgs &a, bool w_kmajor);
 const char *wgrad_kernel_name(const fg_conv_desc &d);
 hipError_t launch_wgrad(const WgradArgs &a, bool big, hipStream_t st);
+
+// LDS-DMA kernels (256 x 256 tiles): applicability and launchers.
+bool data_dma_ok(const DataConvArgs &a);
+bool wgrad_dma_ok(const WgradArgs &a);
+hipError_t launch_data_conv_dma(const DataConvArgs &a, bool w_kmajor,
+                                hipStream_t st);
+hipError_t launch_wgrad_dma(const WgradArgs &a, hipStream_t st);
 hipError_t launch_head_fwd(const uint16_t *x, const uint16_t *w, uint16_t *y,
                            int64_t npix, int32_t c, int32_t epi,
                            const uint16_t *gate, hipStream_t st);
