@@ -3,17 +3,18 @@
 // Same GEMM formulation as the register-staged kernels in conv_igemm.hip
 // (data convolutions: rows = output channels, columns = output positions of
 // one phase; kernel gradient: rows = (tap, input channel), columns = output
-// channels), for 256 x 256 tiles with 8 waves of 128 x 64. Operands go from
-// global memory straight into LDS: no register staging, no LDS store
-// instructions, and a ring of four 32-deep reduction stages (128 KiB), so
-// each stage's loads are issued three stages before they are consumed.
-// Padding and ragged tails cost nothing: an out-of-range buffer offset
-// returns zeros.
+// channels), for 256 x 256 tiles. Operands go from global memory straight
+// into LDS: no register staging and no LDS store instructions. A ring of NS
+// reduction stages, each BK deep, holds 128 KiB, so a stage's loads are
+// issued NS - 1 stages before they are consumed. Padding and ragged tails
+// cost nothing: an out-of-range buffer offset returns zeros. The tile is
+// split among WGM x WGN waves; stage depth, ring length and wave grid are
+// template parameters (the configurations in use are named below).
 //
 // Two LDS tile layouts:
-//   k-major  (row = GEMM row/column, 32 reduction halves = 64 bytes per row;
-//            16-byte chunk c stored at c ^ g(row)); MFMA operands are single
-//            16-byte reads, conflict-free for 8 or 16 consecutive rows.
+//   k-major  (row = GEMM row/column, BK reduction halves per row; 16-byte
+//            chunk c stored at c ^ g(row)); MFMA operands are single 16-byte
+//            reads, conflict-free for 8 or 16 consecutive rows.
 //   mn-major (row = reduction index, 256 halves = 512 bytes per row; 32-byte
 //            block b stored at b ^ s(row)); MFMA operands are two transposing
 //            8-byte reads (ds_read_b64_tr_b16), each 64-lane read touching
@@ -27,22 +28,51 @@
 namespace fg {
 namespace dma {
 
-constexpr int BK = 32;        // reduction per stage
-constexpr int NS = 4;         // stages in the ring
-constexpr int TM = 256, TN = 256;
-constexpr int NT = 512;       // 8 waves: 2 (rows) x 4 (columns)
-constexpr int WM = 128, WN = 64;
-constexpr int FM = WM / 32, FN = WN / 32;
-constexpr int TILE_BYTES = TM * BK * 2;  // 16 KiB per operand per stage
+constexpr int TM = 256, TN = 256;       // output tile
 constexpr unsigned kOOB = 0x80000000u;   // beyond any tensor: loads zero
+
+// Pipeline configuration: BK-deep reduction stages, NS of them in the LDS
+// ring, WGM x WGN waves each owning (TM/WGM) x (TN/WGN) of the tile.
+template <int BK_, int NS_, int WGM_, int WGN_>
+struct K {
+  static constexpr int BK = BK_, NS = NS_, WGM = WGM_, WGN = WGN_;
+  static constexpr int NW = WGM * WGN, NT = 64 * NW;
+  static constexpr int WM = TM / WGM, WN = TN / WGN;
+  static constexpr int FM = WM / 32, FN = WN / 32;
+  static constexpr int KS = BK / 16;                 // MFMA steps per stage
+  static constexpr int TILE_BYTES = TM * BK * 2;     // per operand per stage
+  static constexpr int NI = TILE_BYTES / 1024;       // DMA instrs per operand
+  static constexpr int PW = NI / NW;                 // ... per wave
+  static constexpr int CPR = BK / 8;                 // 16-byte chunks per row
+  static_assert(NI % NW == 0, "DMA instructions must divide among waves");
+};
+// The configurations the library runs, chosen by timing the network's layers:
+// data convolutions take 64-deep stages in a 2-stage ring with 16 waves of
+// 64 x 64; the kernel gradient (whose operand decode needs more registers)
+// 32-deep stages in a 4-stage ring with 16 waves of 64 x 64.
+#ifndef FG_DMA_DATA_CFG
+#define FG_DMA_DATA_CFG 64, 2, 4, 4
+#endif
+#ifndef FG_DMA_WGRAD_CFG
+#define FG_DMA_WGRAD_CFG 32, 4, 4, 4
+#endif
+using DataRun = K<FG_DMA_DATA_CFG>;
+using WgradRun = K<FG_DMA_WGRAD_CFG>;
 constexpr int kRsrcFlags = 0x00020000;   // raw buffer, 32-bit data format
 
 typedef short v4s __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4s lds_v4s;
 typedef __attribute__((address_space(3))) void lds_void;
 
-__device__ __forceinline__ int kmaj_off(int row, int c) {  // bytes
-  return row * 64 + ((c ^ (((row >> 1) ^ (row >> 3)) & 3)) << 4);
+// k-major: 16-byte chunk c of tile row `row` (bytes). 64-byte rows (BK 32)
+// permute the 4 chunks by g(row); 128-byte rows (BK 64) the 8 chunks.
+template <int BK>
+__device__ __forceinline__ int kmaj_swz(int row) {
+  return BK == 32 ? (((row >> 1) ^ (row >> 3)) & 3) : ((row ^ (row >> 3)) & 7);
+}
+template <int BK>
+__device__ __forceinline__ int kmaj_off(int row, int c) {
+  return row * (2 * BK) + ((c ^ kmaj_swz<BK>(row)) << 4);
 }
 __device__ __forceinline__ int mn_swz(int k) {
   return (k & 3) | (((k >> 3) & 1) << 2);
@@ -74,12 +104,12 @@ __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, uint8_t *lds,
 }
 
 // MFMA operand of a 32-row block starting at `base` for reduction step ks.
-template <bool KMAJOR>
+template <int BK, bool KMAJOR>
 __device__ __forceinline__ u32x4 frag(const uint8_t *tile, int base, int ks,
                                       int lane) {
   if (KMAJOR) {
     return *reinterpret_cast<const u32x4 *>(
-        tile + kmaj_off(base + (lane & 31), 2 * ks + (lane >> 5)));
+        tile + kmaj_off<BK>(base + (lane & 31), 2 * ks + (lane >> 5)));
   } else {
     const int g = lane >> 4, m = lane & 15;
     const int k = 8 * (g >> 1) + (m >> 2) + 16 * ks;
@@ -93,50 +123,70 @@ __device__ __forceinline__ u32x4 frag(const uint8_t *tile, int base, int ks,
   }
 }
 
-template <bool AK, bool BKM>
-__device__ __forceinline__ void mma_stage(f32x16 (&acc)[FM][FN],
-                                          const uint8_t *ta, const uint8_t *tb,
-                                          int wm0, int wn0, int lane) {
+// Fragments of one 16-deep reduction step for this wave.
+template <class C>
+struct Frags {
+  u32x4 a[C::FM], b[C::FN];
+};
+
+template <class C, bool AK, bool BKM>
+__device__ __forceinline__ void load_frags(Frags<C> &f, const uint8_t *ta,
+                                           const uint8_t *tb, int ks, int wm0,
+                                           int wn0, int lane) {
 #pragma unroll
-  for (int ks = 0; ks < BK / 16; ++ks) {
-    u32x4 a[FM], b[FN];
+  for (int i = 0; i < C::FM; ++i)
+    f.a[i] = frag<C::BK, AK>(ta, wm0 + 32 * i, ks, lane);
 #pragma unroll
-    for (int i = 0; i < FM; ++i) a[i] = frag<AK>(ta, wm0 + 32 * i, ks, lane);
-#pragma unroll
-    for (int j = 0; j < FN; ++j) b[j] = frag<BKM>(tb, wn0 + 32 * j, ks, lane);
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int j = 0; j < FN; ++j) acc[i][j] = mfma32(a[i], b[j], acc[i][j]);
-  }
+  for (int j = 0; j < C::FN; ++j)
+    f.b[j] = frag<C::BK, BKM>(tb, wn0 + 32 * j, ks, lane);
 }
 
-// Position of this lane's two DMA slots in a k-major tile (rows) and in an
-// mn-major tile (reduction rows, column offsets), per wave instruction jj.
+template <class C>
+__device__ __forceinline__ void mma(f32x16 (&acc)[C::FM][C::FN],
+                                    const Frags<C> &f) {
+#pragma unroll
+  for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+    for (int j = 0; j < C::FN; ++j) acc[i][j] = mfma32(f.a[i], f.b[j], acc[i][j]);
+}
+
+// s_waitcnt with only lgkmcnt (LDS) constrained to 0.
+__device__ __forceinline__ void wait_lds() {
+  __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));
+}
+
+// Position of this lane's DMA slots (one per wave instruction jj) in a
+// k-major tile (row, reduction offset of the chunk) and in an mn-major tile
+// (reduction row within the stage, tile column). Each instruction fills 1 KiB
+// of LDS: 512/BK k-major rows or 2 mn-major rows.
+template <class C>
 struct KmSlot {
-  int row[2], coff[2];  // tile row, reduction offset (halves) of the chunk
+  int row[C::PW], coff[C::PW];
 };
+template <class C>
 struct MnSlot {
-  int krow[2], ncol[2];  // reduction row within the stage, tile column
+  int krow[C::PW], ncol[C::PW];
 };
 
-__device__ __forceinline__ KmSlot km_slots(int wave, int lane) {
-  KmSlot s;
+template <class C>
+__device__ __forceinline__ KmSlot<C> km_slots(int wave, int lane) {
+  KmSlot<C> s;
 #pragma unroll
-  for (int jj = 0; jj < 2; ++jj) {
-    int row = 16 * (2 * wave + jj) + (lane >> 2);
-    int pc = lane & 3;
+  for (int jj = 0; jj < C::PW; ++jj) {
+    int row = (512 / C::BK) * (C::PW * wave + jj) + lane / C::CPR;
+    int pc = lane % C::CPR;
     s.row[jj] = row;
-    s.coff[jj] = 8 * (pc ^ (((row >> 1) ^ (row >> 3)) & 3));
+    s.coff[jj] = 8 * (pc ^ kmaj_swz<C::BK>(row));
   }
   return s;
 }
 
-__device__ __forceinline__ MnSlot mn_slots(int wave, int lane) {
-  MnSlot s;
+template <class C>
+__device__ __forceinline__ MnSlot<C> mn_slots(int wave, int lane) {
+  MnSlot<C> s;
 #pragma unroll
-  for (int jj = 0; jj < 2; ++jj) {
-    int k = 2 * (2 * wave + jj) + (lane >> 5);
+  for (int jj = 0; jj < C::PW; ++jj) {
+    int k = 2 * (C::PW * wave + jj) + (lane >> 5);
     int p = lane & 31;
     s.krow[jj] = k;
     s.ncol[jj] = ((p >> 1) ^ mn_swz(k)) * 16 + (p & 1) * 8;
@@ -144,12 +194,10 @@ __device__ __forceinline__ MnSlot mn_slots(int wave, int lane) {
   return s;
 }
 
-// LDS destination of wave instruction jj of a stage (wave-uniform).
-__device__ __forceinline__ int km_dst(int wave, int jj) {
-  return 16 * (2 * wave + jj) * 64;
-}
-__device__ __forceinline__ int mn_dst(int wave, int jj) {
-  return 2 * (2 * wave + jj) * 512;
+// LDS destination (bytes, wave-uniform) of wave instruction jj of a stage.
+template <class C>
+__device__ __forceinline__ int dma_dst(int wave, int jj) {
+  return 1024 * (C::PW * wave + jj);
 }
 
 __device__ __forceinline__ u32x2 to_h4(float a, float b, float c, float d) {
@@ -175,49 +223,99 @@ __device__ __forceinline__ void epilogue4(float v[4], int epi,
 }
 
 // The ring: stage s of operand X lives in its own LDS array so that the
-// compiler can tell the stages apart when it places waits.
+// compiler can tell the stages apart when it places waits. Unused slots of a
+// ring shorter than four stages are token-sized.
 struct Ring {
-  uint8_t *a[NS];
-  uint8_t *b[NS];
+  uint8_t *a[4];
+  uint8_t *b[4];
 };
+#define FG_DMA_RING(C, R)                                                     \
+  constexpr int T0_ = C::TILE_BYTES, T2_ = C::NS > 2 ? T0_ : 16,              \
+                T3_ = C::NS > 3 ? T0_ : 16;                                   \
+  __shared__ __attribute__((aligned(1024))) uint8_t sA0[T0_], sA1[T0_],       \
+      sA2[T2_], sA3[T3_];                                                     \
+  __shared__ __attribute__((aligned(1024))) uint8_t sB0[T0_], sB1[T0_],       \
+      sB2[T2_], sB3[T3_];                                                     \
+  const Ring R{{sA0, sA1, sA2, sA3}, {sB0, sB1, sB2, sB3}}
+
+// Wait until at most n stages of this wave's DMA loads remain outstanding
+// (n <= 2; each stage is 2 * PW load instructions).
+template <class C>
+__device__ __forceinline__ void wait_stages(int n) {
+  constexpr int PS = 2 * C::PW;
+  if (n >= 2) wait_vm<2 * PS>();
+  else if (n == 1) wait_vm<PS>();
+  else wait_vm<0>();
+}
 
 // Runs the pipelined main loop over stages [0, nst): issue(st, slot) issues
-// this wave's 4 DMA loads of stage st into ring slot `slot`.
-template <bool AK, bool BKM, class Issue>
-__device__ __forceinline__ void pipeline(f32x16 (&acc)[FM][FN], const Ring &R,
-                                         int nst, int wm0, int wn0, int lane,
-                                         Issue &&issue) {
+// this wave's DMA loads of stage st into ring slot `slot`. A stage is KS
+// 16-deep steps; the fragments of step k+1 are read from LDS while the MFMAs
+// of step k run. The barrier that publishes stage s+1 sits before the last
+// step of stage s, so the first fragments of s+1 are read while that last
+// step's MFMAs run:
+//   ... read (s,KS-1) | mma (s,KS-2) | wait own DMA of s+1, own LDS reads |
+//   barrier | DMA s+NS -> slot of s | read (s+1,0) | mma (s,KS-1)
+// A slot is refilled only after every wave's reads of it have completed
+// (each wave waits on its own LDS reads before the barrier).
+template <class C, bool AK, bool BKM, class Issue>
+__device__ __forceinline__ void pipeline(f32x16 (&acc)[C::FM][C::FN],
+                                         const Ring &R, int nst, int wm0,
+                                         int wn0, int lane, Issue &&issue) {
+  constexpr int NS = C::NS, KS = C::KS;
+  static_assert(NS >= 2 && NS <= 4 && KS >= 2 && KS % 2 == 0, "pipeline shape");
+  if (nst <= 0) return;
 #pragma unroll
   for (int s = 0; s < NS - 1; ++s)
     if (s < nst) issue(s, s);
+  wait_stages<C>(min(NS - 2, nst - 1));  // publish stage 0
+  barrier_nofence();
+  if (NS - 1 < nst) issue(NS - 1, NS - 1);
+  Frags<C> f[2];
+  load_frags<C, AK, BKM>(f[0], R.a[0], R.b[0], 0, wm0, wn0, lane);
   for (int it0 = 0; it0 < nst; it0 += NS) {
 #pragma unroll
     for (int u = 0; u < NS; ++u) {
       const int it = it0 + u;
       if (it < nst) {
-        // own loads of stage `it` done: only later stages may remain
-        const int after = min(NS - 2, nst - 1 - it);
-        if (after >= 2) wait_vm<8>();
-        else if (after == 1) wait_vm<4>();
-        else wait_vm<0>();
-        barrier_nofence();  // every wave's stage `it` landed; slot of it-1 free
-        if (it + NS - 1 < nst) issue(it + NS - 1, (u + NS - 1) % NS);
-        mma_stage<AK, BKM>(acc, R.a[u], R.b[u], wm0, wn0, lane);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          if (ks + 1 < KS)
+            load_frags<C, AK, BKM>(f[(ks + 1) & 1], R.a[u], R.b[u], ks + 1, wm0,
+                                   wn0, lane);
+          mma<C>(acc, f[ks & 1]);
+          if (ks == KS - 2 && it + 1 < nst) {
+            // own DMA of stage it+1 done: later stages may remain in flight
+            wait_stages<C>(min(NS - 2, nst - 2 - it));
+            wait_lds();  // this wave's reads of slot u are complete
+            barrier_nofence();
+            if (it + NS < nst) issue(it + NS, u);
+            load_frags<C, AK, BKM>(f[0], R.a[(u + 1) % NS], R.b[(u + 1) % NS], 0,
+                                   wm0, wn0, lane);
+          }
+        }
       }
     }
   }
 }
 
+template <class C>
+__device__ __forceinline__ void zero(f32x16 (&acc)[C::FM][C::FN]) {
+#pragma unroll
+  for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+    for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+}
+
 // ---------------------------------------------------------------------------
 // Data convolution (forward / input gradient / transposed forward).
-// Requires reduction channels cr % 32 == 0 (a stage lies in one tap).
-template <bool WK, bool SPLIT>
-__global__ __launch_bounds__(NT) void data_conv_dma_kernel(DataConvArgs a) {
-  __shared__ __attribute__((aligned(1024))) uint8_t sA0[TILE_BYTES], sA1[TILE_BYTES],
-      sA2[TILE_BYTES], sA3[TILE_BYTES];
-  __shared__ __attribute__((aligned(1024))) uint8_t sB0[TILE_BYTES], sB1[TILE_BYTES],
-      sB2[TILE_BYTES], sB3[TILE_BYTES];
-  const Ring R{{sA0, sA1, sA2, sA3}, {sB0, sB1, sB2, sB3}};
+// Requires reduction channels cr % BK == 0 (a stage lies in one tap).
+template <class C, bool WK, bool SPLIT>
+__global__ __launch_bounds__(C::NT) void data_conv_dma_kernel(DataConvArgs a) {
+  FG_DMA_RING(C, R);
+  constexpr int PW = C::PW;
 
   const int phase = blockIdx.z / a.nsplit, split = blockIdx.z % a.nsplit;
   const Phase P = a.ph[phase];
@@ -226,22 +324,22 @@ __global__ __launch_bounds__(NT) void data_conv_dma_kernel(DataConvArgs a) {
   const int m0 = blockIdx.y * TM;
   if (n0 >= npix) return;
   const int ktot = P.nr * P.ns * a.cr;
-  const int nk = ktot / BK;
+  const int nk = ktot / C::BK;
   const int kchunk = (nk + a.nsplit - 1) / a.nsplit;
   const int kbeg = min(nk, split * kchunk), kend = min(nk, kbeg + kchunk);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm0 = (wave >> 2) * WM, wn0 = (wave & 3) * WN;
+  const int wm0 = (wave / C::WGN) * C::WM, wn0 = (wave % C::WGN) * C::WN;
 
   const __amdgpu_buffer_rsrc_t rs_act = __builtin_amdgcn_make_buffer_rsrc(
       (void *)a.act, 0, (int)((size_t)a.n * a.hi * a.wi * a.cr * 2), kRsrcFlags);
   const __amdgpu_buffer_rsrc_t rs_w = __builtin_amdgcn_make_buffer_rsrc(
       (void *)a.wgt, 0, a.wbytes, kRsrcFlags);
 
-  // B: this lane's two output positions and chunk offsets
-  const KmSlot bs = km_slots(wave, lane);
-  int bh[2], bw[2], bbase[2];
+  // B: this lane's output positions and chunk offsets
+  const KmSlot<C> bs = km_slots<C>(wave, lane);
+  int bh[PW], bw[PW], bbase[PW];
 #pragma unroll
-  for (int jj = 0; jj < 2; ++jj) {
+  for (int jj = 0; jj < PW; ++jj) {
     int col = n0 + bs.row[jj];
     if (col < npix) {
       int b = col % P.mw, t = col / P.mw;
@@ -255,11 +353,11 @@ __global__ __launch_bounds__(NT) void data_conv_dma_kernel(DataConvArgs a) {
       bbase[jj] = 0;
     }
   }
-  const KmSlot as_k = km_slots(wave, lane);
-  const MnSlot as_m = mn_slots(wave, lane);
+  const KmSlot<C> as_k = km_slots<C>(wave, lane);
+  const MnSlot<C> as_m = mn_slots<C>(wave, lane);
 
   auto issue = [&](int st, int slot) {
-    const int k0 = (kbeg + st) * BK;
+    const int k0 = (kbeg + st) * C::BK;
     const int t = k0 / a.cr, cr0 = k0 - t * a.cr;
     const int ti = t / P.ns, tj = t - ti * P.ns;
     const int dh = P.dh0 + P.dstep * ti, dw = P.dw0 + P.dstep * tj;
@@ -267,46 +365,40 @@ __global__ __launch_bounds__(NT) void data_conv_dma_kernel(DataConvArgs a) {
     const int delta = (dh * a.wi + dw) * a.cr + cr0;
     uint8_t *ta = R.a[slot], *tb = R.b[slot];
 #pragma unroll
-    for (int jj = 0; jj < 2; ++jj) {
+    for (int jj = 0; jj < PW; ++jj) {
       int hh = bh[jj] + dh, ww = bw[jj] + dw;
       bool v = hh >= 0 && hh < a.hi && ww >= 0 && ww < a.wi;
       unsigned off = v ? (unsigned)(bbase[jj] + delta) * 2u : kOOB;
-      dma16(rs_act, tb + km_dst(wave, jj), off);
+      dma16(rs_act, tb + dma_dst<C>(wave, jj), off);
     }
     if (WK) {
 #pragma unroll
-      for (int jj = 0; jj < 2; ++jj) {
+      for (int jj = 0; jj < PW; ++jj) {
         int co = m0 + as_k.row[jj];
         unsigned off =
             co < a.co ? (unsigned)(co * a.ldw + woff * a.cr + cr0 + as_k.coff[jj]) * 2u
                       : kOOB;
-        dma16(rs_w, ta + km_dst(wave, jj), off);
+        dma16(rs_w, ta + dma_dst<C>(wave, jj), off);
       }
     } else {
 #pragma unroll
-      for (int jj = 0; jj < 2; ++jj) {
+      for (int jj = 0; jj < PW; ++jj) {
         int kred = cr0 + as_m.krow[jj];
         int co = m0 + as_m.ncol[jj];
         unsigned off =
             co < a.co ? (unsigned)(kred * a.w_red + woff * a.w_tap + co) * 2u : kOOB;
-        dma16(rs_w, ta + mn_dst(wave, jj), off);
+        dma16(rs_w, ta + dma_dst<C>(wave, jj), off);
       }
     }
   };
 
-  f32x16 acc[FM][FN];
-#pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int j = 0; j < FN; ++j)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
-
-  pipeline<WK, true>(acc, R, kend - kbeg, wm0, wn0, lane, issue);
+  f32x16 acc[C::FM][C::FN];
+  zero<C>(acc);
+  pipeline<C, WK, true>(acc, R, kend - kbeg, wm0, wn0, lane, issue);
 
   const size_t out_total = (size_t)a.n * a.ho * a.wo * a.co;
 #pragma unroll
-  for (int j = 0; j < FN; ++j) {
+  for (int j = 0; j < C::FN; ++j) {
     int col = n0 + wn0 + j * 32 + (lane & 31);
     if (col >= npix) continue;
     int b = col % P.mw, t = col / P.mw;
@@ -315,7 +407,7 @@ __global__ __launch_bounds__(NT) void data_conv_dma_kernel(DataConvArgs a) {
                     b * a.ostr + P.oow) *
                    a.co;
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
+    for (int i = 0; i < C::FM; ++i)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         int co = m0 + wm0 + i * 32 + 8 * g + 4 * (lane >> 5);
@@ -338,13 +430,10 @@ __global__ __launch_bounds__(NT) void data_conv_dma_kernel(DataConvArgs a) {
 // ---------------------------------------------------------------------------
 // Kernel gradient: rows rho = (tap, c) of one tap (c % 256 == 0 tiles),
 // columns k (K % 256 == 0), reduction over output positions m.
-template <bool SPLIT>
-__global__ __launch_bounds__(NT) void wgrad_dma_kernel(WgradArgs a) {
-  __shared__ __attribute__((aligned(1024))) uint8_t sA0[TILE_BYTES], sA1[TILE_BYTES],
-      sA2[TILE_BYTES], sA3[TILE_BYTES];
-  __shared__ __attribute__((aligned(1024))) uint8_t sB0[TILE_BYTES], sB1[TILE_BYTES],
-      sB2[TILE_BYTES], sB3[TILE_BYTES];
-  const Ring R{{sA0, sA1, sA2, sA3}, {sB0, sB1, sB2, sB3}};
+template <class C, bool SPLIT>
+__global__ __launch_bounds__(C::NT) void wgrad_dma_kernel(WgradArgs a) {
+  FG_DMA_RING(C, R);
+  constexpr int PW = C::PW;
 
   const int rsc = a.r * a.s * a.c;
   const int m0 = blockIdx.x * TM;  // rho
@@ -352,9 +441,9 @@ __global__ __launch_bounds__(NT) void wgrad_dma_kernel(WgradArgs a) {
   const int split = blockIdx.z;
   const int mbeg = split * a.mchunk;
   const int mend = min(a.mtot, mbeg + a.mchunk);
-  const int nst = mend > mbeg ? (mend - mbeg + BK - 1) / BK : 0;
+  const int nst = mend > mbeg ? (mend - mbeg + C::BK - 1) / C::BK : 0;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm0 = (wave >> 2) * WM, wn0 = (wave & 3) * WN;
+  const int wm0 = (wave / C::WGN) * C::WM, wn0 = (wave % C::WGN) * C::WN;
 
   const int tap = m0 / a.c, c0 = m0 - tap * a.c;
   const int tr = tap / a.s, ts = tap - tr * a.s;
@@ -364,11 +453,11 @@ __global__ __launch_bounds__(NT) void wgrad_dma_kernel(WgradArgs a) {
   const __amdgpu_buffer_rsrc_t rs_dy = __builtin_amdgcn_make_buffer_rsrc(
       (void *)a.dy, 0, (int)((size_t)a.mtot * a.k * 2), kRsrcFlags);
 
-  // this lane's two reduction rows per stage: m = mbeg + 32*st + krow
-  const MnSlot sl = mn_slots(wave, lane);
-  int qn[2], qp[2], qq[2];  // (n, p, q) of the row at the current stage
+  // this lane's reduction rows per stage: m = mbeg + BK*st + krow
+  const MnSlot<C> sl = mn_slots<C>(wave, lane);
+  int qn[PW], qp[PW], qq[PW];  // (n, p, q) of the row at the current stage
 #pragma unroll
-  for (int jj = 0; jj < 2; ++jj) {
+  for (int jj = 0; jj < PW; ++jj) {
     int m = mbeg + sl.krow[jj];
     qn[jj] = m / (a.p * a.q);
     int rem = m - qn[jj] * a.p * a.q;
@@ -381,8 +470,8 @@ __global__ __launch_bounds__(NT) void wgrad_dma_kernel(WgradArgs a) {
     // advance the row decode to stage st (stages are issued in order)
     while (next_st < st) {
 #pragma unroll
-      for (int jj = 0; jj < 2; ++jj) {
-        qq[jj] += BK;
+      for (int jj = 0; jj < PW; ++jj) {
+        qq[jj] += C::BK;
         while (qq[jj] >= a.q) {
           qq[jj] -= a.q;
           if (++qp[jj] == a.p) {
@@ -395,35 +484,29 @@ __global__ __launch_bounds__(NT) void wgrad_dma_kernel(WgradArgs a) {
     }
     uint8_t *ta = R.a[slot], *tb = R.b[slot];
 #pragma unroll
-    for (int jj = 0; jj < 2; ++jj) {
-      const int m = mbeg + st * BK + sl.krow[jj];
+    for (int jj = 0; jj < PW; ++jj) {
+      const int m = mbeg + st * C::BK + sl.krow[jj];
       const bool mv = m < mend;
       const int hh = qp[jj] * a.sh - a.ph + tr, ww = qq[jj] * a.sw - a.pw + ts;
       const bool v = mv && hh >= 0 && hh < a.h && ww >= 0 && ww < a.w;
       unsigned ox = v ? (unsigned)((((qn[jj] * a.h + hh) * a.w + ww) * a.c) + c0 +
                                    sl.ncol[jj]) * 2u
                       : kOOB;
-      dma16(rs_x, ta + mn_dst(wave, jj), ox);
+      dma16(rs_x, ta + dma_dst<C>(wave, jj), ox);
       unsigned od = mv ? (unsigned)(m * a.k + n0 + sl.ncol[jj]) * 2u : kOOB;
-      dma16(rs_dy, tb + mn_dst(wave, jj), od);
+      dma16(rs_dy, tb + dma_dst<C>(wave, jj), od);
     }
   };
 
-  f32x16 acc[FM][FN];
-#pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int j = 0; j < FN; ++j)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
-
-  pipeline<false, false>(acc, R, nst, wm0, wn0, lane, issue);
+  f32x16 acc[C::FM][C::FN];
+  zero<C>(acc);
+  pipeline<C, false, false>(acc, R, nst, wm0, wn0, lane, issue);
 
 #pragma unroll
-  for (int j = 0; j < FN; ++j) {
+  for (int j = 0; j < C::FN; ++j) {
     int k = n0 + wn0 + j * 32 + (lane & 31);
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
+    for (int i = 0; i < C::FM; ++i)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         int rho = m0 + wm0 + i * 32 + 8 * g + 4 * (lane >> 5);
@@ -444,7 +527,7 @@ __global__ __launch_bounds__(NT) void wgrad_dma_kernel(WgradArgs a) {
 
 // ---------------------------------------------------------------------------
 bool data_dma_ok(const DataConvArgs &a) {
-  return a.cr % dma::BK == 0 &&
+  return a.cr % dma::DataRun::BK == 0 &&
          (size_t)a.n * a.hi * a.wi * a.cr * 2 < 0x7FFFFFFFull &&
          (size_t)a.wbytes < 0x7FFFFFFFull;
 }
@@ -465,18 +548,18 @@ hipError_t launch_data_conv_dma(const DataConvArgs &a, bool w_kmajor,
   const bool split = a.nsplit > 1;
   if (w_kmajor) {
     if (split)
-      hipLaunchKernelGGL((dma::data_conv_dma_kernel<true, true>), grid,
-                         dim3(dma::NT), 0, st, a);
+      hipLaunchKernelGGL((dma::data_conv_dma_kernel<dma::DataRun, true, true>), grid,
+                         dim3(dma::DataRun::NT), 0, st, a);
     else
-      hipLaunchKernelGGL((dma::data_conv_dma_kernel<true, false>), grid,
-                         dim3(dma::NT), 0, st, a);
+      hipLaunchKernelGGL((dma::data_conv_dma_kernel<dma::DataRun, true, false>), grid,
+                         dim3(dma::DataRun::NT), 0, st, a);
   } else {
     if (split)
-      hipLaunchKernelGGL((dma::data_conv_dma_kernel<false, true>), grid,
-                         dim3(dma::NT), 0, st, a);
+      hipLaunchKernelGGL((dma::data_conv_dma_kernel<dma::DataRun, false, true>), grid,
+                         dim3(dma::DataRun::NT), 0, st, a);
     else
-      hipLaunchKernelGGL((dma::data_conv_dma_kernel<false, false>), grid,
-                         dim3(dma::NT), 0, st, a);
+      hipLaunchKernelGGL((dma::data_conv_dma_kernel<dma::DataRun, false, false>), grid,
+                         dim3(dma::DataRun::NT), 0, st, a);
   }
   return hipGetLastError();
 }
@@ -485,10 +568,10 @@ hipError_t launch_wgrad_dma(const WgradArgs &a, hipStream_t st) {
   const int rsc = a.r * a.s * a.c;
   dim3 grid(rsc / dma::TM, a.k / dma::TN, a.nsplit);
   if (a.nsplit > 1)
-    hipLaunchKernelGGL((dma::wgrad_dma_kernel<true>), grid, dim3(dma::NT), 0, st,
+    hipLaunchKernelGGL((dma::wgrad_dma_kernel<dma::WgradRun, true>), grid, dim3(dma::WgradRun::NT), 0, st,
                        a);
   else
-    hipLaunchKernelGGL((dma::wgrad_dma_kernel<false>), grid, dim3(dma::NT), 0, st,
+    hipLaunchKernelGGL((dma::wgrad_dma_kernel<dma::WgradRun, false>), grid, dim3(dma::WgradRun::NT), 0, st,
                        a);
   return hipGetLastError();
 }
