@@ -103,6 +103,21 @@ __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, uint8_t *lds,
   __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void *)lds, 16, voff, 0, 0, 0);
 }
 
+// Unsigned division by a divisor fixed per launch, as a multiply-high and two
+// shifts (Granlund and Montgomery, "Division by invariant integers using
+// multiplication", 1994): exact for every 32-bit dividend.
+struct FastDiv {
+  uint32_t magic;
+  int32_t s1, s2;
+  __device__ __forceinline__ unsigned div(unsigned n) const {
+    const unsigned t = __umulhi(magic, n);
+    return (t + ((n - t) >> s1)) >> s2;
+  }
+};
+struct WgradDiv {
+  FastDiv pq, q;  // by p * q and by q
+};
+
 // MFMA operand of a 32-row block starting at `base` for reduction step ks.
 template <int BK, bool KMAJOR>
 __device__ __forceinline__ u32x4 frag(const uint8_t *tile, int base, int ks,
@@ -258,6 +273,55 @@ __device__ __forceinline__ void wait_stages(int n) {
 //   barrier | DMA s+NS -> slot of s | read (s+1,0) | mma (s,KS-1)
 // A slot is refilled only after every wave's reads of it have completed
 // (each wave waits on its own LDS reads before the barrier).
+// One stage (ring slot U) of the main loop. With `next`, the stage has a
+// successor: the barrier that publishes it is crossed before the last step
+// and the successor's first fragments are read into f[0].
+template <class C, bool AK, bool BKM, int U, class Issue>
+__device__ __forceinline__ void stage(f32x16 (&acc)[C::FM][C::FN],
+                                      Frags<C> (&f)[2], const Ring &R, int it,
+                                      int nst, bool next, int wm0, int wn0,
+                                      int lane, Issue &issue) {
+  constexpr int NS = C::NS, KS = C::KS;
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    if (ks + 1 < KS)
+      load_frags<C, AK, BKM>(f[(ks + 1) & 1], R.a[U], R.b[U], ks + 1, wm0, wn0,
+                             lane);
+    mma<C>(acc, f[ks & 1]);
+    if (ks == KS - 2 && next) {
+      // own DMA of stage it+1 done: later stages may remain in flight
+      wait_stages<C>(min(NS - 2, nst - 2 - it));
+      wait_lds();  // this wave's reads of slot U are complete
+      barrier_nofence();
+      if (it + NS < nst) issue(it + NS, U);
+      load_frags<C, AK, BKM>(f[0], R.a[(U + 1) % NS], R.b[(U + 1) % NS], 0, wm0,
+                             wn0, lane);
+    }
+  }
+}
+
+template <class C, bool AK, bool BKM, int U, class Issue>
+__device__ __forceinline__ void group(f32x16 (&acc)[C::FM][C::FN],
+                                      Frags<C> (&f)[2], const Ring &R, int it0,
+                                      int nst, bool tail, int wm0, int wn0,
+                                      int lane, Issue &issue) {
+  if constexpr (U < C::NS) {
+    const int it = it0 + U;
+    if (!tail) {
+      stage<C, AK, BKM, U>(acc, f, R, it, nst, true, wm0, wn0, lane, issue);
+    } else if (it < nst) {
+      stage<C, AK, BKM, U>(acc, f, R, it, nst, it + 1 < nst, wm0, wn0, lane,
+                           issue);
+    }
+    group<C, AK, BKM, U + 1>(acc, f, R, it0, nst, tail, wm0, wn0, lane, issue);
+  }
+}
+
+// Runs the pipelined main loop over stages [0, nst): issue(st, slot) issues
+// this wave's DMA loads of stage st into ring slot `slot`; stages are issued
+// strictly in order. Full groups of NS stages that all have a successor run
+// in a loop whose body has no data-dependent control flow around the MFMAs
+// (so the compiler's own LDS waits stay exact); the last group is peeled.
 template <class C, bool AK, bool BKM, class Issue>
 __device__ __forceinline__ void pipeline(f32x16 (&acc)[C::FM][C::FN],
                                          const Ring &R, int nst, int wm0,
@@ -273,30 +337,10 @@ __device__ __forceinline__ void pipeline(f32x16 (&acc)[C::FM][C::FN],
   if (NS - 1 < nst) issue(NS - 1, NS - 1);
   Frags<C> f[2];
   load_frags<C, AK, BKM>(f[0], R.a[0], R.b[0], 0, wm0, wn0, lane);
-  for (int it0 = 0; it0 < nst; it0 += NS) {
-#pragma unroll
-    for (int u = 0; u < NS; ++u) {
-      const int it = it0 + u;
-      if (it < nst) {
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          if (ks + 1 < KS)
-            load_frags<C, AK, BKM>(f[(ks + 1) & 1], R.a[u], R.b[u], ks + 1, wm0,
-                                   wn0, lane);
-          mma<C>(acc, f[ks & 1]);
-          if (ks == KS - 2 && it + 1 < nst) {
-            // own DMA of stage it+1 done: later stages may remain in flight
-            wait_stages<C>(min(NS - 2, nst - 2 - it));
-            wait_lds();  // this wave's reads of slot u are complete
-            barrier_nofence();
-            if (it + NS < nst) issue(it + NS, u);
-            load_frags<C, AK, BKM>(f[0], R.a[(u + 1) % NS], R.b[(u + 1) % NS], 0,
-                                   wm0, wn0, lane);
-          }
-        }
-      }
-    }
-  }
+  int it0 = 0;
+  for (; it0 + NS < nst; it0 += NS)
+    group<C, AK, BKM, 0>(acc, f, R, it0, nst, false, wm0, wn0, lane, issue);
+  group<C, AK, BKM, 0>(acc, f, R, it0, nst, true, wm0, wn0, lane, issue);
 }
 
 template <class C>
@@ -327,7 +371,8 @@ __global__ __launch_bounds__(C::NT) void data_conv_dma_kernel(DataConvArgs a) {
   const int nk = ktot / C::BK;
   const int kchunk = (nk + a.nsplit - 1) / a.nsplit;
   const int kbeg = min(nk, split * kchunk), kend = min(nk, kbeg + kchunk);
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm0 = (wave / C::WGN) * C::WM, wn0 = (wave % C::WGN) * C::WN;
 
   const __amdgpu_buffer_rsrc_t rs_act = __builtin_amdgcn_make_buffer_rsrc(
@@ -335,7 +380,8 @@ __global__ __launch_bounds__(C::NT) void data_conv_dma_kernel(DataConvArgs a) {
   const __amdgpu_buffer_rsrc_t rs_w = __builtin_amdgcn_make_buffer_rsrc(
       (void *)a.wgt, 0, a.wbytes, kRsrcFlags);
 
-  // B: this lane's output positions and chunk offsets
+  // B: this lane's output positions (image row/column of tap (0, 0) of the
+  // phase) and element offsets
   const KmSlot<C> bs = km_slots<C>(wave, lane);
   int bh[PW], bw[PW], bbase[PW];
 #pragma unroll
@@ -348,46 +394,64 @@ __global__ __launch_bounds__(C::NT) void data_conv_dma_kernel(DataConvArgs a) {
       bw[jj] = b * a.istr;
       bbase[jj] = ((nn * a.hi + bh[jj]) * a.wi + bw[jj]) * a.cr + bs.coff[jj];
     } else {
-      bh[jj] = -(1 << 29);
+      bh[jj] = -(1 << 29);  // never inside the image
       bw[jj] = 0;
       bbase[jj] = 0;
     }
   }
-  const KmSlot<C> as_k = km_slots<C>(wave, lane);
-  const MnSlot<C> as_m = mn_slots<C>(wave, lane);
+  // A: this lane's weight offsets without the stage part, and whether its
+  // output channel exists
+  int wbase[PW];
+  bool wok[PW];
+#pragma unroll
+  for (int jj = 0; jj < PW; ++jj) {
+    if (WK) {
+      const KmSlot<C> as = km_slots<C>(wave, lane);
+      const int co = m0 + as.row[jj];
+      wok[jj] = co < a.co;
+      wbase[jj] = co * a.ldw + as.coff[jj];
+    } else {
+      const MnSlot<C> as = mn_slots<C>(wave, lane);
+      const int co = m0 + as.ncol[jj];
+      wok[jj] = co < a.co;
+      wbase[jj] = as.krow[jj] * a.w_red + co;
+    }
+  }
 
-  auto issue = [&](int st, int slot) {
-    const int k0 = (kbeg + st) * C::BK;
-    const int t = k0 / a.cr, cr0 = k0 - t * a.cr;
-    const int ti = t / P.ns, tj = t - ti * P.ns;
+  // Stage decode (uniform), advanced by one stage per issue() call: the
+  // pipeline issues stages strictly in order. Stage st covers reduction
+  // offsets [k0, k0 + BK) of tap t = k0 / cr, t = ti * ns + tj.
+  int cr0, ti, tj;
+  {
+    const int k0 = kbeg * C::BK, t = k0 / a.cr;
+    cr0 = k0 - t * a.cr;
+    ti = t / P.ns;
+    tj = t - ti * P.ns;
+  }
+  auto issue = [&](int, int slot) {
     const int dh = P.dh0 + P.dstep * ti, dw = P.dw0 + P.dstep * tj;
     const int woff = (P.r0 + P.rstep * ti) * a.s + (P.s0 + P.rstep * tj);
     const int delta = (dh * a.wi + dw) * a.cr + cr0;
+    const int wst = WK ? woff * a.cr + cr0 : cr0 * a.w_red + woff * a.w_tap;
     uint8_t *ta = R.a[slot], *tb = R.b[slot];
 #pragma unroll
     for (int jj = 0; jj < PW; ++jj) {
-      int hh = bh[jj] + dh, ww = bw[jj] + dw;
-      bool v = hh >= 0 && hh < a.hi && ww >= 0 && ww < a.wi;
-      unsigned off = v ? (unsigned)(bbase[jj] + delta) * 2u : kOOB;
-      dma16(rs_act, tb + dma_dst<C>(wave, jj), off);
+      const bool v = (unsigned)(bh[jj] + dh) < (unsigned)a.hi &&
+                     (unsigned)(bw[jj] + dw) < (unsigned)a.wi;
+      const unsigned o = (unsigned)(bbase[jj] + delta) * 2u;
+      dma16(rs_act, tb + dma_dst<C>(wave, jj), v ? o : kOOB);
     }
-    if (WK) {
 #pragma unroll
-      for (int jj = 0; jj < PW; ++jj) {
-        int co = m0 + as_k.row[jj];
-        unsigned off =
-            co < a.co ? (unsigned)(co * a.ldw + woff * a.cr + cr0 + as_k.coff[jj]) * 2u
-                      : kOOB;
-        dma16(rs_w, ta + dma_dst<C>(wave, jj), off);
-      }
-    } else {
-#pragma unroll
-      for (int jj = 0; jj < PW; ++jj) {
-        int kred = cr0 + as_m.krow[jj];
-        int co = m0 + as_m.ncol[jj];
-        unsigned off =
-            co < a.co ? (unsigned)(kred * a.w_red + woff * a.w_tap + co) * 2u : kOOB;
-        dma16(rs_w, ta + dma_dst<C>(wave, jj), off);
+    for (int jj = 0; jj < PW; ++jj) {
+      const unsigned o = (unsigned)(wbase[jj] + wst) * 2u;
+      dma16(rs_w, ta + dma_dst<C>(wave, jj), wok[jj] ? o : kOOB);
+    }
+    cr0 += C::BK;
+    if (cr0 == a.cr) {
+      cr0 = 0;
+      if (++tj == P.ns) {
+        tj = 0;
+        ++ti;
       }
     }
   };
@@ -431,7 +495,7 @@ __global__ __launch_bounds__(C::NT) void data_conv_dma_kernel(DataConvArgs a) {
 // Kernel gradient: rows rho = (tap, c) of one tap (c % 256 == 0 tiles),
 // columns k (K % 256 == 0), reduction over output positions m.
 template <class C, bool SPLIT>
-__global__ __launch_bounds__(C::NT) void wgrad_dma_kernel(WgradArgs a) {
+__global__ __launch_bounds__(C::NT) void wgrad_dma_kernel(WgradArgs a, WgradDiv fd) {
   FG_DMA_RING(C, R);
   constexpr int PW = C::PW;
 
@@ -442,7 +506,8 @@ __global__ __launch_bounds__(C::NT) void wgrad_dma_kernel(WgradArgs a) {
   const int mbeg = split * a.mchunk;
   const int mend = min(a.mtot, mbeg + a.mchunk);
   const int nst = mend > mbeg ? (mend - mbeg + C::BK - 1) / C::BK : 0;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm0 = (wave / C::WGN) * C::WM, wn0 = (wave % C::WGN) * C::WN;
 
   const int tap = m0 / a.c, c0 = m0 - tap * a.c;
@@ -453,48 +518,35 @@ __global__ __launch_bounds__(C::NT) void wgrad_dma_kernel(WgradArgs a) {
   const __amdgpu_buffer_rsrc_t rs_dy = __builtin_amdgcn_make_buffer_rsrc(
       (void *)a.dy, 0, (int)((size_t)a.mtot * a.k * 2), kRsrcFlags);
 
-  // this lane's reduction rows per stage: m = mbeg + BK*st + krow
+  // this lane's reduction rows: m = mbeg + BK * st + krow, decoded into
+  // (n, p, q) with multiply-shift division (no loops, no branches)
   const MnSlot<C> sl = mn_slots<C>(wave, lane);
-  int qn[PW], qp[PW], qq[PW];  // (n, p, q) of the row at the current stage
+  int mrow[PW], xcol[PW], dcol[PW];
 #pragma unroll
   for (int jj = 0; jj < PW; ++jj) {
-    int m = mbeg + sl.krow[jj];
-    qn[jj] = m / (a.p * a.q);
-    int rem = m - qn[jj] * a.p * a.q;
-    qp[jj] = rem / a.q;
-    qq[jj] = rem - qp[jj] * a.q;
+    mrow[jj] = mbeg + sl.krow[jj];
+    xcol[jj] = c0 + sl.ncol[jj];
+    dcol[jj] = n0 + sl.ncol[jj];
   }
-  int next_st = 0;  // stage the (n, p, q) above belong to
+  const int h0 = tr - a.ph, w0 = ts - a.pw;
 
-  auto issue = [&](int st, int slot) {
-    // advance the row decode to stage st (stages are issued in order)
-    while (next_st < st) {
-#pragma unroll
-      for (int jj = 0; jj < PW; ++jj) {
-        qq[jj] += C::BK;
-        while (qq[jj] >= a.q) {
-          qq[jj] -= a.q;
-          if (++qp[jj] == a.p) {
-            qp[jj] = 0;
-            ++qn[jj];
-          }
-        }
-      }
-      ++next_st;
-    }
+  auto issue = [&](int, int slot) {
     uint8_t *ta = R.a[slot], *tb = R.b[slot];
 #pragma unroll
     for (int jj = 0; jj < PW; ++jj) {
-      const int m = mbeg + st * C::BK + sl.krow[jj];
+      const int m = mrow[jj];
+      const unsigned nn = fd.pq.div((unsigned)m);
+      const unsigned rem = (unsigned)m - nn * (unsigned)(a.p * a.q);
+      const unsigned pp = fd.q.div(rem);
+      const int qq = (int)(rem - pp * (unsigned)a.q);
+      const int hh = (int)pp * a.sh + h0, ww = qq * a.sw + w0;
       const bool mv = m < mend;
-      const int hh = qp[jj] * a.sh - a.ph + tr, ww = qq[jj] * a.sw - a.pw + ts;
-      const bool v = mv && hh >= 0 && hh < a.h && ww >= 0 && ww < a.w;
-      unsigned ox = v ? (unsigned)((((qn[jj] * a.h + hh) * a.w + ww) * a.c) + c0 +
-                                   sl.ncol[jj]) * 2u
-                      : kOOB;
-      dma16(rs_x, ta + dma_dst<C>(wave, jj), ox);
-      unsigned od = mv ? (unsigned)(m * a.k + n0 + sl.ncol[jj]) * 2u : kOOB;
-      dma16(rs_dy, tb + dma_dst<C>(wave, jj), od);
+      const bool v = mv && (unsigned)hh < (unsigned)a.h && (unsigned)ww < (unsigned)a.w;
+      const unsigned ox = (unsigned)((((int)nn * a.h + hh) * a.w + ww) * a.c + xcol[jj]) * 2u;
+      dma16(rs_x, ta + dma_dst<C>(wave, jj), v ? ox : kOOB);
+      const unsigned od = (unsigned)(m * a.k + dcol[jj]) * 2u;
+      dma16(rs_dy, tb + dma_dst<C>(wave, jj), mv ? od : kOOB);
+      mrow[jj] = m + C::BK;
     }
   };
 
@@ -564,15 +616,23 @@ hipError_t launch_data_conv_dma(const DataConvArgs &a, bool w_kmajor,
   return hipGetLastError();
 }
 
+static dma::FastDiv make_fastdiv(uint32_t d) {
+  int l = 0;
+  while ((1ull << l) < d) ++l;
+  const uint64_t m = ((1ull << 32) * ((1ull << l) - d)) / d + 1;
+  return {(uint32_t)m, l ? 1 : 0, l ? l - 1 : 0};
+}
+
 hipError_t launch_wgrad_dma(const WgradArgs &a, hipStream_t st) {
   const int rsc = a.r * a.s * a.c;
+  const dma::WgradDiv fd{make_fastdiv((uint32_t)(a.p * a.q)), make_fastdiv((uint32_t)a.q)};
   dim3 grid(rsc / dma::TM, a.k / dma::TN, a.nsplit);
   if (a.nsplit > 1)
     hipLaunchKernelGGL((dma::wgrad_dma_kernel<dma::WgradRun, true>), grid, dim3(dma::WgradRun::NT), 0, st,
-                       a);
+                       a, fd);
   else
     hipLaunchKernelGGL((dma::wgrad_dma_kernel<dma::WgradRun, false>), grid, dim3(dma::WgradRun::NT), 0, st,
-                       a);
+                       a, fd);
   return hipGetLastError();
 }
 
