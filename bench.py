@@ -15,9 +15,16 @@ bandwidths and the CPU oracle timed on a bounded sample of the same work.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu]
        python bench.py --op E2b.fwd|E2b.dx|E2b.dW|copy [--steps K]
+       python bench.py --summarize-stats CSV
+       python bench.py --summarize-pmc DIR
 The --op form runs one pass of one layer (seeded full-size inputs) K times
 and prints its per-launch time; `copy` is a plain 256 MiB fp16 copy through
 grad_group_pack, the reference for scaling HBM byte counters.
+--summarize-stats turns a rocprofv3 --stats kernel_stats.csv into a markdown
+table; --summarize-pmc turns four rocprofv3 --pmc runs (DIR/step_FETCH_SIZE,
+DIR/step_WRITE_SIZE, DIR/copy_FETCH_SIZE, DIR/copy_WRITE_SIZE, each holding
+run_counter_collection.csv) into a per-kernel HBM traffic table plus the
+machine-readable lines recorded_traffic() reads.
 """
 import argparse
 import json
@@ -47,7 +54,90 @@ def parse():
                     help="write per-op timings (JSON) to this path")
     ap.add_argument("--op", default=None,
                     help="time one pass of one layer, e.g. E2b.fwd, or 'copy'")
+    ap.add_argument("--summarize-stats", default=None, metavar="CSV")
+    ap.add_argument("--summarize-pmc", default=None, metavar="DIR")
     return ap.parse_args()
+
+
+COPY_KIB = 256 * 1024  # bytes read (and written) by `--op copy`, in KiB
+
+
+def short_kernel_name(name):
+    """rocprofv3 kernel name -> the name fg.kernel_name() reports."""
+    import re
+    name = name.split("(")[0].replace("void ", "")
+    name = name.replace("fg::dma::", "").replace("fg::", "")
+    return re.sub(r"K<\d+, \d+, \d+, \d+>, ", "", name)
+
+
+def kernel_source(kernel):
+    """Source file (under paper_1909_11150_amd/csrc) that defines `kernel`."""
+    if "_dma_kernel" in kernel:
+        return "conv_dma.hip"
+    if kernel.startswith(("copy_pieces", "unscale", "head_grad", "relu_backward")):
+        return "grad_path.hip"
+    return "conv_igemm.hip"
+
+
+def source_hash(kernel):
+    import hashlib
+    src = os.path.join(ROOT, "paper_1909_11150_amd", "csrc", kernel_source(kernel))
+    return hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+
+
+def summarize_stats(path):
+    import csv
+    print("| kernel | calls | total ms | avg us | % | min us | max us |")
+    print("|---|---:|---:|---:|---:|---:|---:|")
+    for r in csv.DictReader(open(path)):
+        print(f"| `{short_kernel_name(r['Name'])}` | {r['Calls']} | "
+              f"{float(r['TotalDurationNs']) / 1e6:.3f} | {float(r['AverageNs']) / 1e3:.2f} | "
+              f"{float(r['Percentage']):.2f} | {float(r['MinNs']) / 1e3:.2f} | "
+              f"{float(r['MaxNs']) / 1e3:.2f} |")
+
+
+def summarize_pmc(d):
+    import csv
+
+    def per_kernel(run):
+        out = {}
+        for r in csv.DictReader(open(os.path.join(d, run, "run_counter_collection.csv"))):
+            k = short_kernel_name(r["Kernel_Name"])
+            v = out.setdefault(k, [0, 0.0])
+            v[0] += 1
+            v[1] += float(r["Counter_Value"])
+        return {k: (n, tot / n) for k, (n, tot) in out.items()}
+
+    cf, cw = per_kernel("copy_FETCH_SIZE"), per_kernel("copy_WRITE_SIZE")
+    cname = "copy_pieces_kernel<2>"
+    fscale = COPY_KIB / cf[cname][1]
+    wscale = COPY_KIB / cw[cname][1]
+    print(f"Calibration: a plain copy of {COPY_KIB} KiB (read, and the same written) "
+          f"reads FETCH_SIZE {cf[cname][1]:.0f} KiB and WRITE_SIZE {cw[cname][1]:.0f} KiB "
+          f"per dispatch, so the scale factors are fetch x{fscale:.3f}, write x{wscale:.3f}.")
+    print()
+    sf, sw = per_kernel("step_FETCH_SIZE"), per_kernel("step_WRITE_SIZE")
+    rows = []
+    for k in sf:
+        if k not in sw:
+            continue
+        mb = (sf[k][1] * fscale + sw[k][1] * wscale) * 1024 / 1e6
+        rows.append((mb * sf[k][0], k, sf[k][0], sf[k][1], sw[k][1], mb))
+    rows.sort(reverse=True)
+    print("| kernel | dispatches | FETCH_SIZE KiB per dispatch (raw) | "
+          "WRITE_SIZE KiB per dispatch (raw) | scaled MB per dispatch |")
+    print("|---|---:|---:|---:|---:|")
+    for _, k, n, f, w, mb in rows[:16]:
+        print(f"| `{k}` | {n} | {f:.0f} | {w:.0f} | {mb:.1f} |")
+    print()
+    print("Machine-readable lines for bench.py (kernel, hash of the source file "
+          "that defines it when measured, scaled HBM bytes per dispatch averaged "
+          "over the kernel's dispatches in the step):")
+    print()
+    for _, k, n, f, w, mb in rows:
+        if k.startswith(("data_conv", "wgrad")):
+            print(f"traffic: kernel={k} src_sha256_16={source_hash(k)} "
+                  f"bytes_per_launch={int(round(mb * 1e6))}")
 
 
 def op_bench(label, steps, warmup):
@@ -114,14 +204,12 @@ def op_bench(label, steps, warmup):
 def recorded_traffic(kernel):
     """HBM bytes per launch of `kernel` from profiles/fcn_step_hbm_traffic.md
     (rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled by a plain copy's reading),
-    or None when no record exists for it or the kernel source has changed
-    since the counters were taken."""
-    import hashlib
+    or None when no record exists for it or the kernel's source file has
+    changed since the counters were taken."""
     path = os.path.join(ROOT, "profiles", "fcn_step_hbm_traffic.md")
-    src = os.path.join(ROOT, "paper_1909_11150_amd", "csrc", "conv_igemm.hip")
     try:
         lines = open(path).read().splitlines()
-        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+        sha = source_hash(kernel)
     except OSError:
         return None
     for ln in lines:
@@ -191,6 +279,12 @@ def cpu_baseline(layers, seconds):
 
 def main():
     args = parse()
+    if args.summarize_stats:
+        summarize_stats(args.summarize_stats)
+        return
+    if args.summarize_pmc:
+        summarize_pmc(args.summarize_pmc)
+        return
     if args.op:
         op_bench(args.op, args.steps, args.warmup)
         return

@@ -47,11 +47,11 @@ struct K {
   static_assert(NI % NW == 0, "DMA instructions must divide among waves");
 };
 // The configurations the library runs, chosen by timing the network's layers:
-// data convolutions take 64-deep stages in a 2-stage ring with 16 waves of
-// 64 x 64; the kernel gradient (whose operand decode needs more registers)
-// 32-deep stages in a 4-stage ring with 16 waves of 64 x 64.
+// data convolutions take 32-deep stages in a 5-stage ring (160 KiB) with 8
+// waves of 128 x 64; the kernel gradient (whose operand decode needs more
+// registers) 32-deep stages in a 4-stage ring with 16 waves of 64 x 64.
 #ifndef FG_DMA_DATA_CFG
-#define FG_DMA_DATA_CFG 64, 2, 4, 4
+#define FG_DMA_DATA_CFG 32, 5, 2, 4
 #endif
 #ifndef FG_DMA_WGRAD_CFG
 #define FG_DMA_WGRAD_CFG 32, 4, 4, 4
@@ -100,8 +100,41 @@ __device__ __forceinline__ void wait_vm() {
 
 __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, uint8_t *lds,
                                       unsigned voff) {
+#if defined(FG_DMA_EXP_L2)
+  voff = voff < 0x80000000u ? (voff & 0xFFFF0u) : voff;
+#endif
+#if defined(FG_DMA_EXP_L1)
+  voff = voff < 0x80000000u ? (voff & 0x3FF0u) : voff;
+#endif
+#ifndef FG_DMA_EXP_NO_DMA
   __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void *)lds, 16, voff, 0, 0, 0);
+#endif
 }
+
+// Tile order across the chip. Workgroups are handed to the 8 XCDs (each with
+// its own L2) round-robin by launch index L; tile v = (L % 8) * per + L / 8
+// gives each XCD a contiguous run of the tile sequence, in which neighbours
+// share operands (the output channels of one column tile, the halo rows of
+// adjacent column tiles, one reduction chunk), so they are fetched into that
+// XCD's L2 once. The grid is 8 * per one-dimensional; indices past the tile
+// count exit.
+struct TileMap {
+  int32_t n0, n1, n2;  // tile counts, fastest first
+  int32_t per;         // ceil(n0 * n1 * n2 / 8)
+  __device__ __forceinline__ bool decode(int L, int &i0, int &i1, int &i2) const {
+#ifdef FG_DMA_LINEAR_TILES
+    const int v = L;
+#else
+    const int v = (L & 7) * per + (L >> 3);
+#endif
+    if (v >= n0 * n1 * n2) return false;
+    i0 = v % n0;
+    const int r = v / n0;
+    i1 = r % n1;
+    i2 = r / n1;
+    return true;
+  }
+};
 
 // Unsigned division by a divisor fixed per launch, as a multiply-high and two
 // shifts (Granlund and Montgomery, "Division by invariant integers using
@@ -239,65 +272,101 @@ __device__ __forceinline__ void epilogue4(float v[4], int epi,
 
 // The ring: stage s of operand X lives in its own LDS array so that the
 // compiler can tell the stages apart when it places waits. Unused slots of a
-// ring shorter than four stages are token-sized.
+// ring shorter than five stages are token-sized.
 struct Ring {
-  uint8_t *a[4];
-  uint8_t *b[4];
+  uint8_t *a[5];
+  uint8_t *b[5];
 };
 #define FG_DMA_RING(C, R)                                                     \
   constexpr int T0_ = C::TILE_BYTES, T2_ = C::NS > 2 ? T0_ : 16,              \
-                T3_ = C::NS > 3 ? T0_ : 16;                                   \
+                T3_ = C::NS > 3 ? T0_ : 16, T4_ = C::NS > 4 ? T0_ : 16;       \
   __shared__ __attribute__((aligned(1024))) uint8_t sA0[T0_], sA1[T0_],       \
-      sA2[T2_], sA3[T3_];                                                     \
+      sA2[T2_], sA3[T3_], sA4[T4_];                                           \
   __shared__ __attribute__((aligned(1024))) uint8_t sB0[T0_], sB1[T0_],       \
-      sB2[T2_], sB3[T3_];                                                     \
-  const Ring R{{sA0, sA1, sA2, sA3}, {sB0, sB1, sB2, sB3}}
+      sB2[T2_], sB3[T3_], sB4[T4_];                                           \
+  const Ring R{{sA0, sA1, sA2, sA3, sA4}, {sB0, sB1, sB2, sB3, sB4}}
 
 // Wait until at most n stages of this wave's DMA loads remain outstanding
-// (n <= 2; each stage is 2 * PW load instructions).
+// (n <= 3; each stage is 2 * PW load instructions).
 template <class C>
 __device__ __forceinline__ void wait_stages(int n) {
   constexpr int PS = 2 * C::PW;
-  if (n >= 2) wait_vm<2 * PS>();
+  static_assert(3 * PS < 64, "vmcnt range");
+  if (n >= 3) wait_vm<3 * PS>();
+  else if (n == 2) wait_vm<2 * PS>();
   else if (n == 1) wait_vm<PS>();
   else wait_vm<0>();
 }
 
-// Runs the pipelined main loop over stages [0, nst): issue(st, slot) issues
-// this wave's DMA loads of stage st into ring slot `slot`. A stage is KS
-// 16-deep steps; the fragments of step k+1 are read from LDS while the MFMAs
-// of step k run. The barrier that publishes stage s+1 sits before the last
-// step of stage s, so the first fragments of s+1 are read while that last
-// step's MFMAs run:
-//   ... read (s,KS-1) | mma (s,KS-2) | wait own DMA of s+1, own LDS reads |
-//   barrier | DMA s+NS -> slot of s | read (s+1,0) | mma (s,KS-1)
-// A slot is refilled only after every wave's reads of it have completed
-// (each wave waits on its own LDS reads before the barrier).
+// Instruction-scheduling hints (LLVM AMDGPU IGroupLP): within the current
+// scheduling region, place the MFMAs one by one and put `per` LDS reads
+// after each of the first ones, so the reads of the next step issue among
+// the MFMAs of this one instead of in a block.
+template <int NMF, int NRD>
+__device__ __forceinline__ void sched_mfma_reads() {
+#ifndef FG_DMA_NO_SCHED
+  constexpr int per = (NRD + NMF - 1) / NMF;
+#pragma unroll
+  for (int i = 0; i < NMF; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+    if (i * per < NRD) __builtin_amdgcn_sched_group_barrier(0x100, per, 0);  // DS read
+  }
+#endif
+}
+// After the barrier: reads first (they gate the next step), then the DMA
+// loads of the refilled slot with their address arithmetic.
+template <int NMF, int NRD, int NVM>
+__device__ __forceinline__ void sched_mfma_reads_dma() {
+#ifndef FG_DMA_NO_SCHED
+  constexpr int per = (NRD + NMF / 2 - 1) / (NMF / 2);
+#pragma unroll
+  for (int i = 0; i < NMF / 2; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    if (i * per < NRD) __builtin_amdgcn_sched_group_barrier(0x100, per, 0);
+  }
+  constexpr int pv = (NVM + NMF / 2 - 1) / (NMF / 2);
+#pragma unroll
+  for (int i = 0; i < NMF / 2; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    if (i * pv < NVM) {
+      __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);  // VALU
+      __builtin_amdgcn_sched_group_barrier(0x020, pv, 0);  // VMEM read
+    }
+  }
+#endif
+}
+
 // One stage (ring slot U) of the main loop. With `next`, the stage has a
 // successor: the barrier that publishes it is crossed before the last step
-// and the successor's first fragments are read into f[0].
+// and the successor's first fragments are read into f[0]. `full` asserts
+// that NS - 2 stages after the successor have been issued and that stage
+// it + NS exists.
 template <class C, bool AK, bool BKM, int U, class Issue>
 __device__ __forceinline__ void stage(f32x16 (&acc)[C::FM][C::FN],
                                       Frags<C> (&f)[2], const Ring &R, int it,
-                                      int nst, bool next, int wm0, int wn0,
-                                      int lane, Issue &issue) {
+                                      int nst, bool next, bool full, int wm0,
+                                      int wn0, int lane, Issue &issue) {
   constexpr int NS = C::NS, KS = C::KS;
+  constexpr int NMF = C::FM * C::FN;
+  constexpr int NRD = C::FM * (AK ? 1 : 2) + C::FN * (BKM ? 1 : 2);
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
     if (ks + 1 < KS)
       load_frags<C, AK, BKM>(f[(ks + 1) & 1], R.a[U], R.b[U], ks + 1, wm0, wn0,
                              lane);
     mma<C>(acc, f[ks & 1]);
+    if (ks + 1 < KS) sched_mfma_reads<NMF, NRD>();
     if (ks == KS - 2 && next) {
       // own DMA of stage it+1 done: later stages may remain in flight
-      wait_stages<C>(min(NS - 2, nst - 2 - it));
+      wait_stages<C>(full ? NS - 2 : min(NS - 2, nst - 2 - it));
       wait_lds();  // this wave's reads of slot U are complete
       barrier_nofence();
-      if (it + NS < nst) issue(it + NS, U);
+      if (full || it + NS < nst) issue(it + NS, U);
       load_frags<C, AK, BKM>(f[0], R.a[(U + 1) % NS], R.b[(U + 1) % NS], 0, wm0,
                              wn0, lane);
     }
   }
+  if (next) sched_mfma_reads_dma<NMF, NRD, 2 * C::PW>();
 }
 
 template <class C, bool AK, bool BKM, int U, class Issue>
@@ -308,10 +377,10 @@ __device__ __forceinline__ void group(f32x16 (&acc)[C::FM][C::FN],
   if constexpr (U < C::NS) {
     const int it = it0 + U;
     if (!tail) {
-      stage<C, AK, BKM, U>(acc, f, R, it, nst, true, wm0, wn0, lane, issue);
+      stage<C, AK, BKM, U>(acc, f, R, it, nst, true, true, wm0, wn0, lane, issue);
     } else if (it < nst) {
-      stage<C, AK, BKM, U>(acc, f, R, it, nst, it + 1 < nst, wm0, wn0, lane,
-                           issue);
+      stage<C, AK, BKM, U>(acc, f, R, it, nst, it + 1 < nst, false, wm0, wn0,
+                           lane, issue);
     }
     group<C, AK, BKM, U + 1>(acc, f, R, it0, nst, tail, wm0, wn0, lane, issue);
   }
@@ -319,15 +388,16 @@ __device__ __forceinline__ void group(f32x16 (&acc)[C::FM][C::FN],
 
 // Runs the pipelined main loop over stages [0, nst): issue(st, slot) issues
 // this wave's DMA loads of stage st into ring slot `slot`; stages are issued
-// strictly in order. Full groups of NS stages that all have a successor run
-// in a loop whose body has no data-dependent control flow around the MFMAs
-// (so the compiler's own LDS waits stay exact); the last group is peeled.
+// strictly in order. Full groups of NS stages run in a loop whose body has no
+// data-dependent control flow around the MFMAs (so the compiler's own LDS
+// waits stay exact and its scheduling regions span whole steps); the last
+// groups run with per-stage checks.
 template <class C, bool AK, bool BKM, class Issue>
 __device__ __forceinline__ void pipeline(f32x16 (&acc)[C::FM][C::FN],
                                          const Ring &R, int nst, int wm0,
                                          int wn0, int lane, Issue &&issue) {
   constexpr int NS = C::NS, KS = C::KS;
-  static_assert(NS >= 2 && NS <= 4 && KS >= 2 && KS % 2 == 0, "pipeline shape");
+  static_assert(NS >= 2 && NS <= 5 && KS >= 2 && KS % 2 == 0, "pipeline shape");
   if (nst <= 0) return;
 #pragma unroll
   for (int s = 0; s < NS - 1; ++s)
@@ -337,10 +407,14 @@ __device__ __forceinline__ void pipeline(f32x16 (&acc)[C::FM][C::FN],
   if (NS - 1 < nst) issue(NS - 1, NS - 1);
   Frags<C> f[2];
   load_frags<C, AK, BKM>(f[0], R.a[0], R.b[0], 0, wm0, wn0, lane);
+  // In a full group every stage has a successor, NS - 2 stages issued after
+  // it, and a stage NS ahead to issue, so its waits and issues need no
+  // checks: it0 + 2 NS - 1 < nst.
   int it0 = 0;
-  for (; it0 + NS < nst; it0 += NS)
+  for (; it0 + 2 * NS - 1 < nst; it0 += NS)
     group<C, AK, BKM, 0>(acc, f, R, it0, nst, false, wm0, wn0, lane, issue);
-  group<C, AK, BKM, 0>(acc, f, R, it0, nst, true, wm0, wn0, lane, issue);
+  for (; it0 < nst; it0 += NS)
+    group<C, AK, BKM, 0>(acc, f, R, it0, nst, true, wm0, wn0, lane, issue);
 }
 
 template <class C>
@@ -357,15 +431,18 @@ __device__ __forceinline__ void zero(f32x16 (&acc)[C::FM][C::FN]) {
 // Data convolution (forward / input gradient / transposed forward).
 // Requires reduction channels cr % BK == 0 (a stage lies in one tap).
 template <class C, bool WK, bool SPLIT>
-__global__ __launch_bounds__(C::NT) void data_conv_dma_kernel(DataConvArgs a) {
+__global__ __launch_bounds__(C::NT) void data_conv_dma_kernel(DataConvArgs a,
+                                                              TileMap tm) {
   FG_DMA_RING(C, R);
   constexpr int PW = C::PW;
 
-  const int phase = blockIdx.z / a.nsplit, split = blockIdx.z % a.nsplit;
+  int tz, ty, tx;  // phase x split, output-channel tile, position tile
+  if (!tm.decode(blockIdx.x, tz, ty, tx)) return;
+  const int phase = tz / a.nsplit, split = tz % a.nsplit;
   const Phase P = a.ph[phase];
   const int npix = a.n * P.mh * P.mw;
-  const int n0 = blockIdx.x * TN;
-  const int m0 = blockIdx.y * TM;
+  const int n0 = tx * TN;
+  const int m0 = ty * TM;
   if (n0 >= npix) return;
   const int ktot = P.nr * P.ns * a.cr;
   const int nk = ktot / C::BK;
@@ -446,14 +523,14 @@ __global__ __launch_bounds__(C::NT) void data_conv_dma_kernel(DataConvArgs a) {
       const unsigned o = (unsigned)(wbase[jj] + wst) * 2u;
       dma16(rs_w, ta + dma_dst<C>(wave, jj), wok[jj] ? o : kOOB);
     }
+    // next stage, without branches (keeps the scheduling region whole)
     cr0 += C::BK;
-    if (cr0 == a.cr) {
-      cr0 = 0;
-      if (++tj == P.ns) {
-        tj = 0;
-        ++ti;
-      }
-    }
+    const bool wrap = cr0 == a.cr;
+    cr0 = wrap ? 0 : cr0;
+    tj += wrap;
+    const bool wrap2 = tj == P.ns;
+    tj = wrap2 ? 0 : tj;
+    ti += wrap2;
   };
 
   f32x16 acc[C::FM][C::FN];
@@ -495,14 +572,16 @@ __global__ __launch_bounds__(C::NT) void data_conv_dma_kernel(DataConvArgs a) {
 // Kernel gradient: rows rho = (tap, c) of one tap (c % 256 == 0 tiles),
 // columns k (K % 256 == 0), reduction over output positions m.
 template <class C, bool SPLIT>
-__global__ __launch_bounds__(C::NT) void wgrad_dma_kernel(WgradArgs a, WgradDiv fd) {
+__global__ __launch_bounds__(C::NT) void wgrad_dma_kernel(WgradArgs a, WgradDiv fd,
+                                                          TileMap tm) {
   FG_DMA_RING(C, R);
   constexpr int PW = C::PW;
 
   const int rsc = a.r * a.s * a.c;
-  const int m0 = blockIdx.x * TM;  // rho
-  const int n0 = blockIdx.y * TN;  // k
-  const int split = blockIdx.z;
+  int tx, ty, split;  // rho tile, k tile, reduction split
+  if (!tm.decode(blockIdx.x, tx, ty, split)) return;
+  const int m0 = tx * TM;  // rho
+  const int n0 = ty * TN;  // k
   const int mbeg = split * a.mchunk;
   const int mend = min(a.mtot, mbeg + a.mchunk);
   const int nst = mend > mbeg ? (mend - mbeg + C::BK - 1) / C::BK : 0;
@@ -595,23 +674,27 @@ hipError_t launch_data_conv_dma(const DataConvArgs &a, bool w_kmajor,
   int maxpix = 0;
   for (int i = 0; i < a.nphase; ++i)
     maxpix = std::max(maxpix, a.n * a.ph[i].mh * a.ph[i].mw);
-  dim3 grid((maxpix + dma::TN - 1) / dma::TN, (a.co + dma::TM - 1) / dma::TM,
-            a.nphase * a.nsplit);
+  // phases (whose tap counts differ) and splits fastest, so every XCD gets
+  // an even share of each and the phases of one position tile share input
+  dma::TileMap tm{a.nphase * a.nsplit, (a.co + dma::TM - 1) / dma::TM,
+                  (maxpix + dma::TN - 1) / dma::TN, 0};
+  tm.per = (tm.n0 * tm.n1 * tm.n2 + 7) / 8;
+  dim3 grid(8 * tm.per);
   const bool split = a.nsplit > 1;
   if (w_kmajor) {
     if (split)
       hipLaunchKernelGGL((dma::data_conv_dma_kernel<dma::DataRun, true, true>), grid,
-                         dim3(dma::DataRun::NT), 0, st, a);
+                         dim3(dma::DataRun::NT), 0, st, a, tm);
     else
       hipLaunchKernelGGL((dma::data_conv_dma_kernel<dma::DataRun, true, false>), grid,
-                         dim3(dma::DataRun::NT), 0, st, a);
+                         dim3(dma::DataRun::NT), 0, st, a, tm);
   } else {
     if (split)
       hipLaunchKernelGGL((dma::data_conv_dma_kernel<dma::DataRun, false, true>), grid,
-                         dim3(dma::DataRun::NT), 0, st, a);
+                         dim3(dma::DataRun::NT), 0, st, a, tm);
     else
       hipLaunchKernelGGL((dma::data_conv_dma_kernel<dma::DataRun, false, false>), grid,
-                         dim3(dma::DataRun::NT), 0, st, a);
+                         dim3(dma::DataRun::NT), 0, st, a, tm);
   }
   return hipGetLastError();
 }
@@ -626,13 +709,15 @@ static dma::FastDiv make_fastdiv(uint32_t d) {
 hipError_t launch_wgrad_dma(const WgradArgs &a, hipStream_t st) {
   const int rsc = a.r * a.s * a.c;
   const dma::WgradDiv fd{make_fastdiv((uint32_t)(a.p * a.q)), make_fastdiv((uint32_t)a.q)};
-  dim3 grid(rsc / dma::TM, a.k / dma::TN, a.nsplit);
+  dma::TileMap tm{rsc / dma::TM, a.k / dma::TN, a.nsplit, 0};
+  tm.per = (tm.n0 * tm.n1 * tm.n2 + 7) / 8;
+  dim3 grid(8 * tm.per);
   if (a.nsplit > 1)
     hipLaunchKernelGGL((dma::wgrad_dma_kernel<dma::WgradRun, true>), grid, dim3(dma::WgradRun::NT), 0, st,
-                       a, fd);
+                       a, fd, tm);
   else
     hipLaunchKernelGGL((dma::wgrad_dma_kernel<dma::WgradRun, false>), grid, dim3(dma::WgradRun::NT), 0, st,
-                       a, fd);
+                       a, fd, tm);
   return hipGetLastError();
 }
 
