@@ -100,15 +100,7 @@ __device__ __forceinline__ void wait_vm() {
 
 __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, uint8_t *lds,
                                       unsigned voff) {
-#if defined(FG_DMA_EXP_L2)
-  voff = voff < 0x80000000u ? (voff & 0xFFFF0u) : voff;
-#endif
-#if defined(FG_DMA_EXP_L1)
-  voff = voff < 0x80000000u ? (voff & 0x3FF0u) : voff;
-#endif
-#ifndef FG_DMA_EXP_NO_DMA
   __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void *)lds, 16, voff, 0, 0, 0);
-#endif
 }
 
 // Tile order across the chip. Workgroups are handed to the 8 XCDs (each with
@@ -122,11 +114,7 @@ struct TileMap {
   int32_t n0, n1, n2;  // tile counts, fastest first
   int32_t per;         // ceil(n0 * n1 * n2 / 8)
   __device__ __forceinline__ bool decode(int L, int &i0, int &i1, int &i2) const {
-#ifdef FG_DMA_LINEAR_TILES
-    const int v = L;
-#else
     const int v = (L & 7) * per + (L >> 3);
-#endif
     if (v >= n0 * n1 * n2) return false;
     i0 = v % n0;
     const int r = v / n0;
@@ -304,20 +292,17 @@ __device__ __forceinline__ void wait_stages(int n) {
 // the MFMAs of this one instead of in a block.
 template <int NMF, int NRD>
 __device__ __forceinline__ void sched_mfma_reads() {
-#ifndef FG_DMA_NO_SCHED
   constexpr int per = (NRD + NMF - 1) / NMF;
 #pragma unroll
   for (int i = 0; i < NMF; ++i) {
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
     if (i * per < NRD) __builtin_amdgcn_sched_group_barrier(0x100, per, 0);  // DS read
   }
-#endif
 }
 // After the barrier: reads first (they gate the next step), then the DMA
 // loads of the refilled slot with their address arithmetic.
 template <int NMF, int NRD, int NVM>
 __device__ __forceinline__ void sched_mfma_reads_dma() {
-#ifndef FG_DMA_NO_SCHED
   constexpr int per = (NRD + NMF / 2 - 1) / (NMF / 2);
 #pragma unroll
   for (int i = 0; i < NMF / 2; ++i) {
@@ -333,7 +318,6 @@ __device__ __forceinline__ void sched_mfma_reads_dma() {
       __builtin_amdgcn_sched_group_barrier(0x020, pv, 0);  // VMEM read
     }
   }
-#endif
 }
 
 // One stage (ring slot U) of the main loop. With `next`, the stage has a
