@@ -272,7 +272,9 @@ struct Ring {
       sA2[T2_], sA3[T3_], sA4[T4_];                                           \
   __shared__ __attribute__((aligned(1024))) uint8_t sB0[T0_], sB1[T0_],       \
       sB2[T2_], sB3[T3_], sB4[T4_];                                           \
-  const Ring R{{sA0, sA1, sA2, sA3, sA4}, {sB0, sB1, sB2, sB3, sB4}}
+  Ring R;                                                                     \
+  R.a[0] = sA0, R.a[1] = sA1, R.a[2] = sA2, R.a[3] = sA3, R.a[4] = sA4;        \
+  R.b[0] = sB0, R.b[1] = sB1, R.b[2] = sB2, R.b[3] = sB3, R.b[4] = sB4
 
 // Wait until at most n stages of this wave's DMA loads remain outstanding
 // (n <= 3; each stage is 2 * PW load instructions).
@@ -412,6 +414,129 @@ __device__ __forceinline__ void zero(f32x16 (&acc)[C::FM][C::FN]) {
 }
 
 // ---------------------------------------------------------------------------
+// Output tile store of the data convolutions. The accumulator layout gives
+// each lane 4 consecutive channels of one output position per register
+// group, so storing it directly would scatter 8-byte pieces over 32
+// positions per instruction. Instead each wave stages its 128-channel x
+// 64-position block in LDS (the ring is free once the last stage is read),
+// position-major with 16-byte chunks permuted by the position, and reads it
+// back so that 16 lanes cover one position's 256 contiguous bytes: stores
+// (and, for the gate epilogue, the gate loads) are whole 128-byte lines.
+// fp32 partials (SPLIT) go in two passes of 64 channels.
+template <class C, bool SPLIT>
+__device__ __forceinline__ void store_tile(f32x16 (&acc)[C::FM][C::FN],
+                                           const Ring &R, const DataConvArgs &a,
+                                           const Phase &P, int npix, int n0,
+                                           int m0, int wm0, int wn0, int lane,
+                                           int wave, int split) {
+  static_assert(C::WM == 128 && C::WN == 64, "store_tile expects 128 x 64 waves");
+  static_assert(2 * C::NS >= C::NW + 1 && C::TILE_BYTES >= 16384,
+                "store_tile needs one 16 KiB ring array per wave plus one");
+  // every wave is done reading the ring, and no DMA is in flight
+  __syncthreads();
+  // ring array `wave` (a-side arrays first), by constant indices only
+  uint8_t *buf = R.a[0];
+#pragma unroll
+  for (int k = 1; k < C::NW; ++k)
+    if (wave == k) buf = k < C::NS ? R.a[k] : R.b[k - C::NS];
+  int32_t *pos = reinterpret_cast<int32_t *>(R.b[C::NW - C::NS]) + 64 * wave;
+  if (lane < 32) {
+#pragma unroll
+    for (int j = 0; j < C::FN; ++j) {
+      const int col = n0 + wn0 + j * 32 + lane;
+      int32_t ob = -1;
+      if (col < npix) {
+        const int b = col % P.mw, t = col / P.mw;
+        const int aa = t % P.mh, nn = t / P.mh;
+        ob = ((nn * a.ho + aa * a.ostr + P.ooh) * a.wo + b * a.ostr + P.oow) * a.co;
+      }
+      pos[j * 32 + lane] = ob;
+    }
+  }
+  const size_t out_total = (size_t)a.n * a.ho * a.wo * a.co;
+  const int cw = m0 + wm0;  // first channel of this wave's block
+  constexpr int PASSES = SPLIT ? 2 : 1;
+#pragma unroll
+  for (int pass = 0; pass < PASSES; ++pass) {
+    // acc -> LDS: position p = j*32 + lane%32, 4 channels per register group
+#pragma unroll
+    for (int j = 0; j < C::FN; ++j) {
+      const int p = j * 32 + (lane & 31);
+      uint8_t *row = buf + p * 256;
+#pragma unroll
+      for (int ii = 0; ii < C::FM / PASSES; ++ii) {
+        const int i = pass * (C::FM / PASSES) + ii;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          float v[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * g + e];
+          if (SPLIT) {
+            const int chunk = 8 * ii + 2 * g + (lane >> 5);
+            *reinterpret_cast<f32x4 *>(row + ((chunk ^ (p & 15)) << 4)) =
+                f32x4{v[0], v[1], v[2], v[3]};
+          } else {
+            if (a.epi == FG_EPI_RELU) {
+#pragma unroll
+              for (int e = 0; e < 4; ++e) v[e] = v[e] > 0.f ? v[e] : 0.f;
+            }
+            const int chunk = 4 * i + g;
+            *reinterpret_cast<u32x2 *>(row + ((chunk ^ (p & 15)) << 4) +
+                                       8 * (lane >> 5)) =
+                to_h4(v[0], v[1], v[2], v[3]);
+          }
+        }
+      }
+    }
+    wait_lds();
+    __builtin_amdgcn_wave_barrier();
+    // LDS -> global: 16 lanes per position, 16-byte chunk q of its row.
+    // All reads (and gate loads) are issued before any use, so their
+    // latencies overlap; gate loads of absent positions read element 0.
+    const int q = lane & 15;
+    const int ch = SPLIT ? pass * 64 + 4 * q : 8 * q;  // channel within block
+    const bool chok = cw + ch < a.co;
+    u32x4 d[16];
+    int32_t ob[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const int p = 4 * k + (lane >> 4);
+      d[k] = *reinterpret_cast<const u32x4 *>(buf + p * 256 + ((q ^ (p & 15)) << 4));
+      ob[k] = chok ? pos[p] : -1;
+    }
+    if (!SPLIT && a.epi == FG_EPI_GATE) {
+      u32x4 gw[16];
+#pragma unroll
+      for (int k = 0; k < 16; ++k)
+        gw[k] = *reinterpret_cast<const u32x4 *>(a.gate + (ob[k] < 0 ? 0 : ob[k] + cw + ch));
+#pragma unroll
+      for (int k = 0; k < 16; ++k)
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const uint32_t lo = h_to_f32((uint16_t)(gw[k][w] & 0xFFFFu)) > 0.f
+                                  ? 0x0000FFFFu : 0u;
+          const uint32_t hi = h_to_f32((uint16_t)(gw[k][w] >> 16)) > 0.f
+                                  ? 0xFFFF0000u : 0u;
+          d[k][w] &= lo | hi;
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      if (ob[k] < 0) continue;
+      if (SPLIT)
+        *reinterpret_cast<u32x4 *>(a.part + (size_t)split * out_total + ob[k] + cw +
+                                   ch) = d[k];
+      else
+        *reinterpret_cast<u32x4 *>(a.out + ob[k] + cw + ch) = d[k];
+    }
+    if (pass + 1 < PASSES) {
+      wait_lds();
+      __builtin_amdgcn_wave_barrier();
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Data convolution (forward / input gradient / transposed forward).
 // Requires reduction channels cr % BK == 0 (a stage lies in one tap).
 template <class C, bool WK, bool SPLIT>
@@ -521,34 +646,79 @@ __global__ __launch_bounds__(C::NT) void data_conv_dma_kernel(DataConvArgs a,
   zero<C>(acc);
   pipeline<C, WK, true>(acc, R, kend - kbeg, wm0, wn0, lane, issue);
 
-  const size_t out_total = (size_t)a.n * a.ho * a.wo * a.co;
+  store_tile<C, SPLIT>(acc, R, a, P, npix, n0, m0, wm0, wn0, lane, wave, split);
+}
+
+// ---------------------------------------------------------------------------
+// Output tile store of the kernel gradient: rows rho (contiguous in memory
+// for a fixed output channel k), columns k. As for the data convolutions, a
+// wave's 64 x 64 block is staged in LDS k-major (128-byte rows: 64 fp16 or,
+// per pass, 32 fp32 values; 16-byte chunks permuted by the row) and read
+// back so that 8 lanes write one row's contiguous 128 bytes.
+template <class C, bool SPLIT>
+__device__ __forceinline__ void store_tile_w(f32x16 (&acc)[C::FM][C::FN],
+                                             const Ring &R, const WgradArgs &a,
+                                             int rsc, int rho0, int k0, int lane,
+                                             int wave, int split) {
+  static_assert(C::WM == 64 && C::WN == 64, "store_tile_w expects 64 x 64 waves");
+  static_assert(2 * C::NS * C::TILE_BYTES >= C::NW * 8192, "LDS for staging");
+  __syncthreads();  // every wave is done reading the ring
+  // 8 KiB per wave: two waves per 16 KiB ring array, by constant indices
+  uint8_t *buf = R.a[0];
 #pragma unroll
-  for (int j = 0; j < C::FN; ++j) {
-    int col = n0 + wn0 + j * 32 + (lane & 31);
-    if (col >= npix) continue;
-    int b = col % P.mw, t = col / P.mw;
-    int aa = t % P.mh, nn = t / P.mh;
-    size_t obase = ((size_t)(nn * a.ho + aa * a.ostr + P.ooh) * a.wo +
-                    b * a.ostr + P.oow) *
-                   a.co;
+  for (int k = 1; k < C::NW / 2; ++k)
+    if ((wave >> 1) == k) buf = k < C::NS ? R.a[k] : R.b[k - C::NS];
+  buf += (wave & 1) * 8192;
+  constexpr int PASSES = SPLIT ? 2 : 1;
 #pragma unroll
-    for (int i = 0; i < C::FM; ++i)
+  for (int pass = 0; pass < PASSES; ++pass) {
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        int co = m0 + wm0 + i * 32 + 8 * g + 4 * (lane >> 5);
-        if (co >= a.co) continue;
-        float v[4];
+    for (int j = 0; j < C::FN; ++j) {
+      const int kr = j * 32 + (lane & 31);  // row within the block
+      uint8_t *row = buf + kr * 128;
+      const int sw = (kr >> 1) & 7;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * g + e];
-        if (SPLIT) {
-          f32x4 o = {v[0], v[1], v[2], v[3]};
-          *reinterpret_cast<f32x4 *>(a.part + split * out_total + obase + co) = o;
-        } else {
-          epilogue4(v, a.epi, a.gate + obase + co);
-          *reinterpret_cast<u32x2 *>(a.out + obase + co) =
-              to_h4(v[0], v[1], v[2], v[3]);
+      for (int ii = 0; ii < C::FM / PASSES; ++ii) {
+        const int i = pass * (C::FM / PASSES) + ii;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const f32x16 &c = acc[i][j];
+          if (SPLIT) {
+            const int chunk = 2 * g + (lane >> 5);
+            *reinterpret_cast<f32x4 *>(row + ((chunk ^ sw) << 4)) =
+                f32x4{c[4 * g], c[4 * g + 1], c[4 * g + 2], c[4 * g + 3]};
+          } else {
+            const int chunk = 4 * i + g;
+            *reinterpret_cast<u32x2 *>(row + ((chunk ^ sw) << 4) + 8 * (lane >> 5)) =
+                to_h4(c[4 * g], c[4 * g + 1], c[4 * g + 2], c[4 * g + 3]);
+          }
         }
       }
+    }
+    wait_lds();
+    __builtin_amdgcn_wave_barrier();
+    // 8 lanes per row, 16-byte chunk q
+    const int q = lane & 7;
+    u32x4 d[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const int kr = 8 * t + (lane >> 3);
+      d[t] = *reinterpret_cast<const u32x4 *>(buf + kr * 128 +
+                                              ((q ^ ((kr >> 1) & 7)) << 4));
+    }
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const int k = k0 + 8 * t + (lane >> 3);
+      if (SPLIT)
+        *reinterpret_cast<u32x4 *>(a.part + ((size_t)split * a.k + k) * rsc + rho0 +
+                                   pass * 32 + 4 * q) = d[t];
+      else
+        *reinterpret_cast<u32x4 *>(a.dw + (size_t)k * rsc + rho0 + 8 * q) = d[t];
+    }
+    if (pass + 1 < PASSES) {
+      wait_lds();
+      __builtin_amdgcn_wave_barrier();
+    }
   }
 }
 
@@ -616,26 +786,7 @@ __global__ __launch_bounds__(C::NT) void wgrad_dma_kernel(WgradArgs a, WgradDiv 
   f32x16 acc[C::FM][C::FN];
   zero<C>(acc);
   pipeline<C, false, false>(acc, R, nst, wm0, wn0, lane, issue);
-
-#pragma unroll
-  for (int j = 0; j < C::FN; ++j) {
-    int k = n0 + wn0 + j * 32 + (lane & 31);
-#pragma unroll
-    for (int i = 0; i < C::FM; ++i)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        int rho = m0 + wm0 + i * 32 + 8 * g + 4 * (lane >> 5);
-        const f32x16 &c = acc[i][j];
-        if (!SPLIT) {
-          *reinterpret_cast<u32x2 *>(a.dw + (size_t)k * rsc + rho) =
-              to_h4(c[4 * g], c[4 * g + 1], c[4 * g + 2], c[4 * g + 3]);
-        } else {
-          f32x4 o = {c[4 * g], c[4 * g + 1], c[4 * g + 2], c[4 * g + 3]};
-          *reinterpret_cast<f32x4 *>(
-              a.part + ((size_t)split * a.k + k) * rsc + rho) = o;
-        }
-      }
-  }
+  store_tile_w<C, SPLIT>(acc, R, a, rsc, m0 + wm0, n0 + wn0, lane, wave, split);
 }
 
 }  // namespace dma
