@@ -72,7 +72,7 @@ def short_kernel_name(name):
 
 def kernel_source(kernel):
     """Source file (under paper_1909_11150_amd/csrc) that defines `kernel`."""
-    if "_dma_kernel" in kernel:
+    if "_dma_kernel" in kernel or "_halo_kernel" in kernel:
         return "conv_dma.hip"
     if kernel.startswith(("copy_pieces", "unscale", "head_grad", "relu_backward")):
         return "grad_path.hip"

@@ -22,6 +22,8 @@
 // The mn-major layout lets operands whose reduction index is strided in
 // memory (input-gradient and transposed-conv weights, both kernel-gradient
 // operands) be copied row by row as they lie in memory.
+#include <type_traits>
+
 #include "common.h"
 #include "internal.h"
 
@@ -58,6 +60,10 @@ struct K {
 #endif
 using DataRun = K<FG_DMA_DATA_CFG>;
 using WgradRun = K<FG_DMA_WGRAD_CFG>;
+#ifndef FG_DMA_HALO_NS
+#define FG_DMA_HALO_NS 3
+#endif
+using HaloRun = K<32, FG_DMA_HALO_NS, 2, 4>;  // weights ring; the rest is patches
 constexpr int kRsrcFlags = 0x00020000;   // raw buffer, 32-bit data format
 
 typedef short v4s __attribute__((ext_vector_type(4)));
@@ -423,23 +429,18 @@ __device__ __forceinline__ void zero(f32x16 (&acc)[C::FM][C::FN]) {
 // back so that 16 lanes cover one position's 256 contiguous bytes: stores
 // (and, for the gate epilogue, the gate loads) are whole 128-byte lines.
 // fp32 partials (SPLIT) go in two passes of 64 channels.
+// `buf` is this wave's 16 KiB of staging LDS and `pos` its 64-entry table;
+// the caller guarantees that no wave still reads, and no DMA still writes,
+// the LDS they alias (the store begins with a workgroup barrier).
 template <class C, bool SPLIT>
 __device__ __forceinline__ void store_tile(f32x16 (&acc)[C::FM][C::FN],
-                                           const Ring &R, const DataConvArgs &a,
+                                           uint8_t *buf, int32_t *pos,
+                                           const DataConvArgs &a,
                                            const Phase &P, int npix, int n0,
                                            int m0, int wm0, int wn0, int lane,
-                                           int wave, int split) {
+                                           int split) {
   static_assert(C::WM == 128 && C::WN == 64, "store_tile expects 128 x 64 waves");
-  static_assert(2 * C::NS >= C::NW + 1 && C::TILE_BYTES >= 16384,
-                "store_tile needs one 16 KiB ring array per wave plus one");
-  // every wave is done reading the ring, and no DMA is in flight
   __syncthreads();
-  // ring array `wave` (a-side arrays first), by constant indices only
-  uint8_t *buf = R.a[0];
-#pragma unroll
-  for (int k = 1; k < C::NW; ++k)
-    if (wave == k) buf = k < C::NS ? R.a[k] : R.b[k - C::NS];
-  int32_t *pos = reinterpret_cast<int32_t *>(R.b[C::NW - C::NS]) + 64 * wave;
   if (lane < 32) {
 #pragma unroll
     for (int j = 0; j < C::FN; ++j) {
@@ -646,7 +647,246 @@ __global__ __launch_bounds__(C::NT) void data_conv_dma_kernel(DataConvArgs a,
   zero<C>(acc);
   pipeline<C, WK, true>(acc, R, kend - kbeg, wm0, wn0, lane, issue);
 
-  store_tile<C, SPLIT>(acc, R, a, P, npix, n0, m0, wm0, wn0, lane, wave, split);
+  // staging: ring array `wave` (a-side arrays first, constant indices only)
+  // and the position tables in the next one
+  static_assert(2 * C::NS >= C::NW + 1 && C::TILE_BYTES >= 16384,
+                "the store needs one 16 KiB ring array per wave plus one");
+  uint8_t *sbuf = R.a[0];
+#pragma unroll
+  for (int k = 1; k < C::NW; ++k)
+    if (wave == k) sbuf = k < C::NS ? R.a[k] : R.b[k - C::NS];
+  int32_t *spos = reinterpret_cast<int32_t *>(R.b[C::NW - C::NS]) + 64 * wave;
+  store_tile<C, SPLIT>(acc, sbuf, spos, a, P, npix, n0, m0, wm0, wn0, lane, split);
+}
+
+// ---------------------------------------------------------------------------
+// Data convolution with input reuse ("halo" tiles): stride-1 3x3 convolutions
+// (forward, and input gradient, which is one phase whose taps walk the input
+// backward) whose 256-position
+// tile is a block of whole output rows of one image. Instead of gathering the
+// activation operand once per tap (9 times), the tile's input window, with a
+// one-pixel halo, is loaded into LDS once per 32-channel chunk as a "patch"
+// of (rows + 2) x (width + 2) positions; the 9 taps read shifted views of it.
+// The reduction runs channel chunk by chunk, taps inside: stage s = 9 c + t.
+// Weights take a 3-stage ring of 32-deep stages; the patch two slots, the
+// next chunk's patch being loaded during the current chunk. Every stage
+// issues the same number of loads (stages and patches past the end load
+// nothing, through the out-of-range offset), so all waits are constants. The
+// next chunk's patch is loaded a block per stage, spread over the chunk.
+constexpr int kHaloTaps = 9;
+
+// f(integral_constant<int, U>) for U = B .. E-1, unrolled at compile time.
+template <int B, int E, class F>
+__device__ __forceinline__ void unroll(F &f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    unroll<B + 1, E>(f);
+  }
+}
+constexpr int kPatchRows = 768;                  // capacity, rows of 64 bytes
+constexpr int kPatchBytes = kPatchRows * 64;
+
+template <class C>
+__device__ __forceinline__ u32x4 frag_row(const uint8_t *tile, int row, int ks,
+                                          int lane) {
+  return *reinterpret_cast<const u32x4 *>(
+      tile + kmaj_off<32>(row, 2 * ks + (lane >> 5)));
+}
+
+// Loads in flight after stage s+1's loads, at the barrier inside stage s
+// (position u of the unrolled group). The barrier of stage b issues weight
+// stage b + NS and then, when its tap t(b) < NPW, this wave's patch block
+// t(b) of the next chunk; stage s+1's weights were issued at the barrier of
+// stage s+1-NS. (Stages before the first have taps 9-NS+1 .. 8 >= NPW, so
+// the prologue needs no stand-ins.)
+template <class C, int NPW>
+__device__ __forceinline__ constexpr int halo_flight(int u) {
+  int f = (C::NS - 2) * C::PW;
+  for (int b = 1; b <= C::NS - 1; ++b)
+    f += ((u - b) % kHaloTaps + kHaloTaps) % kHaloTaps < NPW ? 1 : 0;
+  return f;
+}
+
+template <class C, bool WK, bool SPLIT>
+__global__ __launch_bounds__(C::NT) void data_conv_halo_kernel(DataConvArgs a,
+                                                               TileMap tm) {
+  static_assert(C::BK == 32 && (C::NS == 3 || C::NS == 4) && C::KS == 2,
+                "halo pipeline shape");
+  static_assert(C::WM == 128 && C::WN == 64 && C::NW == 8, "halo wave layout");
+  constexpr int NS = C::NS, PW = C::PW;
+  constexpr int NPW = kPatchRows / 16 / C::NW;  // patch loads per wave
+  // stages per unrolled group: whole pairs of chunks (both patch slots) and
+  // whole turns of the weight ring
+  constexpr int UNR = NS == 3 ? 2 * kHaloTaps : 4 * kHaloTaps;
+  constexpr int TA3 = NS > 3 ? C::TILE_BYTES : 16;
+  __shared__ __attribute__((aligned(1024))) uint8_t sA0[C::TILE_BYTES],
+      sA1[C::TILE_BYTES], sA2[C::TILE_BYTES], sA3[TA3];
+  __shared__ __attribute__((aligned(1024))) uint8_t sP0[kPatchBytes],
+      sP1[kPatchBytes];
+  uint8_t *ringA[4];
+  ringA[0] = sA0, ringA[1] = sA1, ringA[2] = sA2, ringA[3] = sA3;
+  uint8_t *patch[2];
+  patch[0] = sP0, patch[1] = sP1;
+
+  int split, ty, tx;  // reduction split, output-channel tile, position tile
+  if (!tm.decode(blockIdx.x, split, ty, tx)) return;
+  const Phase P = a.ph[0];
+  const int n0 = tx * TN, m0 = ty * TM;
+  const int nchunk = a.cr / 32;
+  const int cps = (nchunk + a.nsplit - 1) / a.nsplit;
+  const int cbeg = min(nchunk, split * cps), cend = min(nchunk, cbeg + cps);
+  const int nst = kHaloTaps * (cend - cbeg);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm0 = (wave / C::WGN) * C::WM, wn0 = (wave % C::WGN) * C::WN;
+
+  const __amdgpu_buffer_rsrc_t rs_act = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)a.act, 0, (int)((size_t)a.n * a.hi * a.wi * a.cr * 2), kRsrcFlags);
+  const __amdgpu_buffer_rsrc_t rs_w = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)a.wgt, 0, a.wbytes, kRsrcFlags);
+
+  // tile geometry: rows [aa0, aa0 + 256 / mw) of image img
+  const int mw = P.mw, pwid = mw + 2;
+  const int img = n0 / (P.mh * mw), aa0 = (n0 / mw) % P.mh;
+  const int prows = (TN / mw + 2) * pwid;
+  // window origin: the taps walk the input forward (dstep 1, forward pass)
+  // or backward (dstep -1, input gradient)
+  const int dsg = P.dstep, back = dsg < 0 ? 2 : 0;
+  const int h0 = aa0 + P.dh0 - back, w0 = P.dw0 - back;
+  // patch loads of this lane: row r, 16-byte chunk (lane & 3) ^ g(r); byte
+  // offset of channel 0 of its input position, or -1 outside the image
+  int pbase[NPW];
+#pragma unroll
+  for (int jj = 0; jj < NPW; ++jj) {
+    const int r = 16 * (NPW * wave + jj) + (lane >> 2);
+    const int h = h0 + r / pwid, w = w0 + r % pwid;
+    const bool v = r < prows && (unsigned)h < (unsigned)a.hi &&
+                   (unsigned)w < (unsigned)a.wi;
+    pbase[jj] = v ? (((img * a.hi + h) * a.wi + w) * a.cr +
+                     8 * ((lane & 3) ^ kmaj_swz<32>(r))) * 2
+                  : -1;
+  }
+  // B fragment rows (patch row of tap (0, 0)) of this lane's positions
+  int brow[C::FN];
+#pragma unroll
+  for (int j = 0; j < C::FN; ++j) {
+    const int i = wn0 + 32 * j + (lane & 31);
+    brow[j] = (i / mw) * pwid + i % mw;
+  }
+  // A: weight offsets without the stage part
+  int wbase[PW];
+  bool wok[PW];
+#pragma unroll
+  for (int jj = 0; jj < PW; ++jj) {
+    if (WK) {
+      const KmSlot<C> as = km_slots<C>(wave, lane);
+      const int co = m0 + as.row[jj];
+      wok[jj] = co < a.co;
+      wbase[jj] = co * a.ldw + as.coff[jj];
+    } else {
+      const MnSlot<C> as = mn_slots<C>(wave, lane);
+      const int co = m0 + as.ncol[jj];
+      wok[jj] = co < a.co;
+      wbase[jj] = as.krow[jj] * a.w_red + co;
+    }
+  }
+  // weight stage decode, advanced by one stage per issue (in order)
+  int ic = cbeg, it_ = 0;
+  auto issue_w = [&](int slot) {
+    const int ti = it_ / 3, tj = it_ - 3 * ti;
+    const int woff = (P.r0 + P.rstep * ti) * a.s + (P.s0 + P.rstep * tj);
+    const int cr0 = 32 * ic;
+    const int wst = WK ? woff * a.cr + cr0 : cr0 * a.w_red + woff * a.w_tap;
+    const bool live = ic < cend;
+#pragma unroll
+    for (int jj = 0; jj < PW; ++jj) {
+      const unsigned o = (unsigned)(wbase[jj] + wst) * 2u;
+      dma16(rs_w, ringA[slot] + dma_dst<C>(wave, jj), live && wok[jj] ? o : kOOB);
+    }
+    const bool wrap = ++it_ == kHaloTaps;
+    it_ = wrap ? 0 : it_;
+    ic += wrap;
+  };
+  // block jj of this wave's share of chunk c's patch
+  auto issue_pb = [&](int pslot, int c, int jj) {
+    const unsigned o = (unsigned)(pbase[jj] + 64 * c);
+    dma16(rs_act, patch[pslot] + 1024 * (NPW * wave + jj),
+          c < cend && pbase[jj] >= 0 ? o : kOOB);
+  };
+
+  f32x16 acc[C::FM][C::FN];
+  zero<C>(acc);
+  Frags<C> f[2];
+  auto load = [&](Frags<C> &fr, int slot, int pslot, int t, int ks) {
+    const int toff = back * (pwid + 1) + dsg * ((t / 3) * pwid + t % 3);
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i)
+      fr.a[i] = frag<32, WK>(ringA[slot], wm0 + 32 * i, ks, lane);
+#pragma unroll
+    for (int j = 0; j < C::FN; ++j)
+      fr.b[j] = frag_row<C>(patch[pslot], brow[j] + toff, ks, lane);
+  };
+  constexpr int NMF = C::FM * C::FN;
+  constexpr int NRD = C::FM * (WK ? 1 : 2) + C::FN;
+
+  // One stage at position U of the unrolled pair of chunks: A slot U % 3,
+  // patch slot U / 9, tap U % 9.
+  auto stage = [&](auto Uc, int it) {
+    constexpr int U = decltype(Uc)::value;
+    constexpr int T = U % kHaloTaps, SLOT = U % NS, PS = (U / kHaloTaps) & 1;
+    constexpr int U1 = (U + 1) % UNR;
+    // The patch row of a fragment depends on the tap; keep the compiler
+    // from precomputing all taps' addresses across the unrolled stages.
+#pragma unroll
+    for (int j = 0; j < C::FN; ++j) asm volatile("" : "+v"(brow[j]));
+    load(f[1], SLOT, PS, T, 1);
+    mma<C>(acc, f[0]);
+    sched_mfma_reads<NMF, NRD>();
+    wait_vm<halo_flight<C, NPW>(U)>();
+    wait_lds();
+    barrier_nofence();
+    issue_w(SLOT);  // stage it + NS
+    // the next chunk's patch, one block per stage over its first NPW taps
+    // (its slot's previous chunk is done: every wave is past this barrier)
+    if (T < NPW) issue_pb(PS ^ 1, cbeg + it / kHaloTaps + 1, T);
+    load(f[0], U1 % NS, (U1 / kHaloTaps) & 1, U1 % kHaloTaps, 0);
+    mma<C>(acc, f[1]);
+    sched_mfma_reads_dma<NMF, NRD, (T < NPW ? PW + 1 : PW)>();
+  };
+
+  static_assert(NPW <= kHaloTaps - (NS - 1), "patch blocks fit the taps");
+  // prologue: patch of the first chunk, weight stages 0 .. NS-2; publish
+  // stage 0; weight stage NS-1
+#pragma unroll
+  for (int jj = 0; jj < NPW; ++jj) issue_pb(0, cbeg, jj);
+#pragma unroll
+  for (int st = 0; st < NS - 1; ++st) issue_w(st);
+  wait_vm<(NS - 2) * PW>();
+  barrier_nofence();
+  issue_w(NS - 1);
+  load(f[0], 0, 0, 0, 0);
+  int it0 = 0;
+  auto step = [&](auto Uc) { stage(Uc, it0 + decltype(Uc)::value); };
+  for (; it0 + UNR <= nst; it0 += UNR) unroll<0, UNR>(step);
+  // the rest, a whole number of chunks, as a prefix of a group
+  constexpr int G9 = kHaloTaps;
+  if (it0 + G9 <= nst) unroll<0, G9>(step);
+  if constexpr (UNR > 2 * G9) {
+    if (it0 + 2 * G9 <= nst) unroll<G9, 2 * G9>(step);
+    if (it0 + 3 * G9 <= nst) unroll<2 * G9, 3 * G9>(step);
+  }
+  wait_vm<0>();  // loads issued past the end have landed
+
+  // staging for the store: A slots, then 16 KiB pieces of the patch slots;
+  // position tables after them
+  uint8_t *sbuf = sA0;
+  if (wave == 1) sbuf = sA1;
+  if (wave == 2) sbuf = sA2;
+  if (wave >= 3 && wave < 6) sbuf = sP0 + 16384 * (wave - 3);  // (sA3 unused)
+  if (wave >= 6) sbuf = sP1 + 16384 * (wave - 6);
+  int32_t *spos = reinterpret_cast<int32_t *>(sP1 + 32768) + 64 * wave;
+  const int npix = a.n * P.mh * P.mw;
+  store_tile<C, SPLIT>(acc, sbuf, spos, a, P, npix, n0, m0, wm0, wn0, lane, split);
 }
 
 // ---------------------------------------------------------------------------
@@ -802,6 +1042,44 @@ bool wgrad_dma_ok(const WgradArgs &a) {
   return a.c % dma::TM == 0 && a.k % dma::TN == 0 &&
          (size_t)a.n * a.h * a.w * a.c * 2 < 0x7FFFFFFFull &&
          (size_t)a.mtot * a.k * 2 < 0x7FFFFFFFull;
+}
+
+bool data_halo_ok(const DataConvArgs &a) {
+  if (a.nphase != 1 || a.istr != 1 || a.cr % 32 != 0) return false;
+  const Phase &P = a.ph[0];
+  if ((P.dstep != 1 && P.dstep != -1) || P.nr != 3 || P.ns != 3 || P.mw <= 0 ||
+      dma::TN % P.mw != 0)
+    return false;
+  const int rt = dma::TN / P.mw;  // output rows per tile
+  if (P.mh % rt != 0 || (rt + 2) * (P.mw + 2) > dma::kPatchRows) return false;
+  return (size_t)a.n * a.hi * a.wi * a.cr * 2 < 0x7FFFFFFFull &&
+         (size_t)a.wbytes < 0x7FFFFFFFull;
+}
+
+hipError_t launch_data_conv_halo(const DataConvArgs &a, bool w_kmajor,
+                                 hipStream_t st) {
+  const int npix = a.n * a.ph[0].mh * a.ph[0].mw;
+  dma::TileMap tm{a.nsplit, (a.co + dma::TM - 1) / dma::TM,
+                  (npix + dma::TN - 1) / dma::TN, 0};
+  tm.per = (tm.n0 * tm.n1 * tm.n2 + 7) / 8;
+  dim3 grid(8 * tm.per), block(dma::HaloRun::NT);
+  const bool split = a.nsplit > 1;
+  if (w_kmajor) {
+    if (split)
+      hipLaunchKernelGGL((dma::data_conv_halo_kernel<dma::HaloRun, true, true>),
+                         grid, block, 0, st, a, tm);
+    else
+      hipLaunchKernelGGL((dma::data_conv_halo_kernel<dma::HaloRun, true, false>),
+                         grid, block, 0, st, a, tm);
+  } else {
+    if (split)
+      hipLaunchKernelGGL((dma::data_conv_halo_kernel<dma::HaloRun, false, true>),
+                         grid, block, 0, st, a, tm);
+    else
+      hipLaunchKernelGGL((dma::data_conv_halo_kernel<dma::HaloRun, false, false>),
+                         grid, block, 0, st, a, tm);
+  }
+  return hipGetLastError();
 }
 
 hipError_t launch_data_conv_dma(const DataConvArgs &a, bool w_kmajor,

@@ -751,9 +751,11 @@ hipError_t launch_data_conv(const DataConvArgs &a0, bool w_kmajor,
   DataConvArgs a = a0;
   const DataPlan pl = plan_data_conv(a);
   a.nsplit = pl.nsplit;
-  hipError_t e = pl.big ? (data_dma_ok(a) ? launch_data_conv_dma(a, w_kmajor, st)
-                                          : launch_dc_tile<BigCfg>(a, w_kmajor, st))
-                        : launch_dc_tile<SmallCfg>(a, w_kmajor, st);
+  hipError_t e =
+      !pl.big ? launch_dc_tile<SmallCfg>(a, w_kmajor, st)
+      : data_halo_ok(a) ? launch_data_conv_halo(a, w_kmajor, st)
+      : data_dma_ok(a)  ? launch_data_conv_dma(a, w_kmajor, st)
+                        : launch_dc_tile<BigCfg>(a, w_kmajor, st);
   if (e != hipSuccess || a.nsplit == 1) return e;
   const int64_t len = (int64_t)a.n * a.ho * a.wo * a.co;
   hipLaunchKernelGGL(split_epilogue_kernel,
@@ -782,6 +784,12 @@ const char *data_conv_kernel_name(const DataConvArgs &a, bool w_kmajor) {
         {"data_conv_kernel<Cfg<256, 256, 2, 4>, true, true, false>",
          "data_conv_kernel<Cfg<256, 256, 2, 4>, true, true, true>"}}}};
   const DataPlan pl = plan_data_conv(a);
+  if (pl.big && data_halo_ok(a)) {
+    static const char *hn[2][2] = {
+        {"data_conv_halo_kernel<false, false>", "data_conv_halo_kernel<false, true>"},
+        {"data_conv_halo_kernel<true, false>", "data_conv_halo_kernel<true, true>"}};
+    return hn[w_kmajor][pl.nsplit > 1];
+  }
   if (pl.big && data_dma_ok(a)) {
     static const char *dn[2][2] = {
         {"data_conv_dma_kernel<false, false>", "data_conv_dma_kernel<false, true>"},

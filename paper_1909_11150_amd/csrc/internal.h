@@ -84,6 +84,11 @@ hipError_t launch_wgrad(const WgradArgs &a, bool big, hipStream_t st);
 
 // LDS-DMA kernels (256 x 256 tiles): applicability and launchers.
 bool data_dma_ok(const DataConvArgs &a);
+// Stride-1 3x3 data convolution whose tile is whole output rows: the
+// input-reuse kernel (conv_dma.hip) applies.
+bool data_halo_ok(const DataConvArgs &a);
+hipError_t launch_data_conv_halo(const DataConvArgs &a, bool w_kmajor,
+                                 hipStream_t st);
 bool wgrad_dma_ok(const WgradArgs &a);
 hipError_t launch_data_conv_dma(const DataConvArgs &a, bool w_kmajor,
                                 hipStream_t st);
