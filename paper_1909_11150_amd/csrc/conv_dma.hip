@@ -22,6 +22,7 @@
 // The mn-major layout lets operands whose reduction index is strided in
 // memory (input-gradient and transposed-conv weights, both kernel-gradient
 // operands) be copied row by row as they lie in memory.
+#include <algorithm>
 #include <type_traits>
 
 #include "common.h"
@@ -116,11 +117,14 @@ __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, uint8_t *lds,
 // adjacent column tiles, one reduction chunk), so they are fetched into that
 // XCD's L2 once. The grid is 8 * per one-dimensional; indices past the tile
 // count exit.
+// With `linear`, tile v = L instead: launch order is tile order, for launches
+// whose tiles differ in cost and are listed costliest first.
 struct TileMap {
   int32_t n0, n1, n2;  // tile counts, fastest first
   int32_t per;         // ceil(n0 * n1 * n2 / 8)
+  int32_t linear;
   __device__ __forceinline__ bool decode(int L, int &i0, int &i1, int &i2) const {
-    const int v = (L & 7) * per + (L >> 3);
+    const int v = linear ? L : (L & 7) * per + (L >> 3);
     if (v >= n0 * n1 * n2) return false;
     i0 = v % n0;
     const int r = v / n0;
@@ -547,7 +551,9 @@ __global__ __launch_bounds__(C::NT) void data_conv_dma_kernel(DataConvArgs a,
   constexpr int PW = C::PW;
 
   int tz, ty, tx;  // phase x split, output-channel tile, position tile
-  if (!tm.decode(blockIdx.x, tz, ty, tx)) return;
+  if (tm.linear ? !tm.decode(blockIdx.x, tx, ty, tz)
+                : !tm.decode(blockIdx.x, tz, ty, tx))
+    return;
   const int phase = tz / a.nsplit, split = tz % a.nsplit;
   const Phase P = a.ph[phase];
   const int npix = a.n * P.mh * P.mw;
@@ -1060,7 +1066,7 @@ hipError_t launch_data_conv_halo(const DataConvArgs &a, bool w_kmajor,
                                  hipStream_t st) {
   const int npix = a.n * a.ph[0].mh * a.ph[0].mw;
   dma::TileMap tm{a.nsplit, (a.co + dma::TM - 1) / dma::TM,
-                  (npix + dma::TN - 1) / dma::TN, 0};
+                  (npix + dma::TN - 1) / dma::TN, 0, 0};
   tm.per = (tm.n0 * tm.n1 * tm.n2 + 7) / 8;
   dim3 grid(8 * tm.per), block(dma::HaloRun::NT);
   const bool split = a.nsplit > 1;
@@ -1082,15 +1088,29 @@ hipError_t launch_data_conv_halo(const DataConvArgs &a, bool w_kmajor,
   return hipGetLastError();
 }
 
-hipError_t launch_data_conv_dma(const DataConvArgs &a, bool w_kmajor,
+hipError_t launch_data_conv_dma(const DataConvArgs &a0, bool w_kmajor,
                                 hipStream_t st) {
+  DataConvArgs a = a0;
   int maxpix = 0;
-  for (int i = 0; i < a.nphase; ++i)
+  bool uneven = false;
+  for (int i = 0; i < a.nphase; ++i) {
     maxpix = std::max(maxpix, a.n * a.ph[i].mh * a.ph[i].mw);
-  // phases (whose tap counts differ) and splits fastest, so every XCD gets
-  // an even share of each and the phases of one position tile share input
-  dma::TileMap tm{a.nphase * a.nsplit, (a.co + dma::TM - 1) / dma::TM,
-                  (maxpix + dma::TN - 1) / dma::TN, 0};
+    uneven |= a.ph[i].nr * a.ph[i].ns != a.ph[0].nr * a.ph[0].ns;
+  }
+  const int tco = (a.co + dma::TM - 1) / dma::TM, tpix = (maxpix + dma::TN - 1) / dma::TN;
+  dma::TileMap tm;
+  if (uneven) {
+    // phases with different tap counts (strided input gradients): costliest
+    // phase first, in launch order, so the cheap tiles fill the tail
+    std::stable_sort(a.ph, a.ph + a.nphase, [](const Phase &x, const Phase &y) {
+      return x.nr * x.ns > y.nr * y.ns;
+    });
+    tm = dma::TileMap{tpix, tco, a.nphase * a.nsplit, 0, 1};
+  } else {
+    // phases and splits fastest, so every XCD gets an even share of each
+    // and the phases of one position tile share input
+    tm = dma::TileMap{a.nphase * a.nsplit, tco, tpix, 0, 0};
+  }
   tm.per = (tm.n0 * tm.n1 * tm.n2 + 7) / 8;
   dim3 grid(8 * tm.per);
   const bool split = a.nsplit > 1;
@@ -1122,7 +1142,7 @@ static dma::FastDiv make_fastdiv(uint32_t d) {
 hipError_t launch_wgrad_dma(const WgradArgs &a, hipStream_t st) {
   const int rsc = a.r * a.s * a.c;
   const dma::WgradDiv fd{make_fastdiv((uint32_t)(a.p * a.q)), make_fastdiv((uint32_t)a.q)};
-  dma::TileMap tm{rsc / dma::TM, a.k / dma::TN, a.nsplit, 0};
+  dma::TileMap tm{rsc / dma::TM, a.k / dma::TN, a.nsplit, 0, 0};
   tm.per = (tm.n0 * tm.n1 * tm.n2 + 7) / 8;
   dim3 grid(8 * tm.per);
   if (a.nsplit > 1)
