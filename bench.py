@@ -67,7 +67,9 @@ def short_kernel_name(name):
     import re
     name = name.split("(")[0].replace("void ", "")
     name = name.replace("fg::dma::", "").replace("fg::", "")
-    return re.sub(r"K<\d+, \d+, \d+, \d+>, ", "", name)
+    # the pipeline configuration: dropped, except a tile size other than 256
+    name = re.sub(r"K<\d+, \d+, \d+, \d+(, 256)?>, ", "", name)
+    return re.sub(r"K<\d+, \d+, \d+, \d+, (\d+)>, ", r"\1, ", name)
 
 
 def kernel_source(kernel):

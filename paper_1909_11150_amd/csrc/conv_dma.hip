@@ -31,22 +31,26 @@
 namespace fg {
 namespace dma {
 
-constexpr int TM = 256, TN = 256;       // output tile
+constexpr int TM = 256, TN = 256;       // output tile of the large kernels
 constexpr unsigned kOOB = 0x80000000u;   // beyond any tensor: loads zero
 
-// Pipeline configuration: BK-deep reduction stages, NS of them in the LDS
-// ring, WGM x WGN waves each owning (TM/WGM) x (TN/WGN) of the tile.
-template <int BK_, int NS_, int WGM_, int WGN_>
+// Pipeline configuration: T x T output tile, BK-deep reduction stages, NS of
+// them in the LDS ring, WGM x WGN waves each owning (T/WGM) x (T/WGN).
+template <int BK_, int NS_, int WGM_, int WGN_, int T_ = 256>
 struct K {
-  static constexpr int BK = BK_, NS = NS_, WGM = WGM_, WGN = WGN_;
+  static constexpr int BK = BK_, NS = NS_, WGM = WGM_, WGN = WGN_, T = T_;
   static constexpr int NW = WGM * WGN, NT = 64 * NW;
-  static constexpr int WM = TM / WGM, WN = TN / WGN;
+  static constexpr int WM = T / WGM, WN = T / WGN;
   static constexpr int FM = WM / 32, FN = WN / 32;
   static constexpr int KS = BK / 16;                 // MFMA steps per stage
-  static constexpr int TILE_BYTES = TM * BK * 2;     // per operand per stage
+  static constexpr int TILE_BYTES = T * BK * 2;      // per operand per stage
   static constexpr int NI = TILE_BYTES / 1024;       // DMA instrs per operand
   static constexpr int PW = NI / NW;                 // ... per wave
   static constexpr int CPR = BK / 8;                 // 16-byte chunks per row
+  static constexpr int RB = 2 * T;                   // mn-major row bytes
+  static constexpr int RPI = 1024 / RB;              // mn-major rows per DMA
+  // waves per SIMD the kernel must fit (small tiles run two per CU)
+  static constexpr int WPE = T == 128 ? 2 * NW / 4 : (NW + 3) / 4;
   static_assert(NI % NW == 0, "DMA instructions must divide among waves");
 };
 // The configurations the library runs, chosen by timing the network's layers:
@@ -65,6 +69,9 @@ using WgradRun = K<FG_DMA_WGRAD_CFG>;
 #define FG_DMA_HALO_NS 3
 #endif
 using HaloRun = K<32, FG_DMA_HALO_NS, 2, 4>;  // weights ring; the rest is patches
+// 128 x 128 tiles for layers with few output positions: 4 waves of 64 x 64,
+// 80 KiB of ring, two workgroups per CU
+using SmallRun = K<32, 5, 2, 2, 128>;
 constexpr int kRsrcFlags = 0x00020000;   // raw buffer, 32-bit data format
 
 typedef short v4s __attribute__((ext_vector_type(4)));
@@ -84,8 +91,9 @@ __device__ __forceinline__ int kmaj_off(int row, int c) {
 __device__ __forceinline__ int mn_swz(int k) {
   return (k & 3) | (((k >> 3) & 1) << 2);
 }
+template <int RB>
 __device__ __forceinline__ int mnmaj_off(int k, int n) {  // bytes, n % 4 == 0
-  return k * 512 + ((2 * n) ^ (mn_swz(k) << 5));
+  return k * RB + ((2 * n) ^ (mn_swz(k) << 5));
 }
 
 // Workgroup barrier without a memory fence. __syncthreads() would add a
@@ -150,7 +158,7 @@ struct WgradDiv {
 };
 
 // MFMA operand of a 32-row block starting at `base` for reduction step ks.
-template <int BK, bool KMAJOR>
+template <int BK, bool KMAJOR, int RB = 512>
 __device__ __forceinline__ u32x4 frag(const uint8_t *tile, int base, int ks,
                                       int lane) {
   if (KMAJOR) {
@@ -161,9 +169,9 @@ __device__ __forceinline__ u32x4 frag(const uint8_t *tile, int base, int ks,
     const int k = 8 * (g >> 1) + (m >> 2) + 16 * ks;
     const int n = base + 16 * (g & 1) + 4 * (m & 3);
     v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-        (lds_v4s *)(tile + mnmaj_off(k, n)));
+        (lds_v4s *)(tile + mnmaj_off<RB>(k, n)));
     v4s hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-        (lds_v4s *)(tile + mnmaj_off(k + 4, n)));
+        (lds_v4s *)(tile + mnmaj_off<RB>(k + 4, n)));
     u32x2 a = __builtin_bit_cast(u32x2, lo), b = __builtin_bit_cast(u32x2, hi);
     return u32x4{a[0], a[1], b[0], b[1]};
   }
@@ -181,10 +189,10 @@ __device__ __forceinline__ void load_frags(Frags<C> &f, const uint8_t *ta,
                                            int wn0, int lane) {
 #pragma unroll
   for (int i = 0; i < C::FM; ++i)
-    f.a[i] = frag<C::BK, AK>(ta, wm0 + 32 * i, ks, lane);
+    f.a[i] = frag<C::BK, AK, C::RB>(ta, wm0 + 32 * i, ks, lane);
 #pragma unroll
   for (int j = 0; j < C::FN; ++j)
-    f.b[j] = frag<C::BK, BKM>(tb, wn0 + 32 * j, ks, lane);
+    f.b[j] = frag<C::BK, BKM, C::RB>(tb, wn0 + 32 * j, ks, lane);
 }
 
 template <class C>
@@ -204,7 +212,7 @@ __device__ __forceinline__ void wait_lds() {
 // Position of this lane's DMA slots (one per wave instruction jj) in a
 // k-major tile (row, reduction offset of the chunk) and in an mn-major tile
 // (reduction row within the stage, tile column). Each instruction fills 1 KiB
-// of LDS: 512/BK k-major rows or 2 mn-major rows.
+// of LDS: 512/BK k-major rows or 1024/RB mn-major rows.
 template <class C>
 struct KmSlot {
   int row[C::PW], coff[C::PW];
@@ -232,8 +240,9 @@ __device__ __forceinline__ MnSlot<C> mn_slots(int wave, int lane) {
   MnSlot<C> s;
 #pragma unroll
   for (int jj = 0; jj < C::PW; ++jj) {
-    int k = 2 * (C::PW * wave + jj) + (lane >> 5);
-    int p = lane & 31;
+    constexpr int CPM = C::RB / 16;  // 16-byte chunks per mn-major row
+    int k = C::RPI * (C::PW * wave + jj) + lane / CPM;
+    int p = lane % CPM;
     s.krow[jj] = k;
     s.ncol[jj] = ((p >> 1) ^ mn_swz(k)) * 16 + (p & 1) * 8;
   }
@@ -541,11 +550,48 @@ __device__ __forceinline__ void store_tile(f32x16 (&acc)[C::FM][C::FN],
   }
 }
 
+// Direct store of the accumulators (small tiles, whose ring has no room to
+// stage a wave's block): 8-byte pieces of 4 channels per lane.
+template <class C, bool SPLIT>
+__device__ __forceinline__ void store_direct(f32x16 (&acc)[C::FM][C::FN],
+                                             const DataConvArgs &a, const Phase &P,
+                                             int npix, int n0, int m0, int wm0,
+                                             int wn0, int lane, int split) {
+  const size_t out_total = (size_t)a.n * a.ho * a.wo * a.co;
+#pragma unroll
+  for (int j = 0; j < C::FN; ++j) {
+    const int col = n0 + wn0 + j * 32 + (lane & 31);
+    if (col >= npix) continue;
+    const int b = col % P.mw, t = col / P.mw;
+    const int aa = t % P.mh, nn = t / P.mh;
+    const size_t obase =
+        ((size_t)(nn * a.ho + aa * a.ostr + P.ooh) * a.wo + b * a.ostr + P.oow) * a.co;
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int co = m0 + wm0 + i * 32 + 8 * g + 4 * (lane >> 5);
+        if (co >= a.co) continue;
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * g + e];
+        if (SPLIT) {
+          *reinterpret_cast<f32x4 *>(a.part + split * out_total + obase + co) =
+              f32x4{v[0], v[1], v[2], v[3]};
+        } else {
+          epilogue4(v, a.epi, a.gate + obase + co);
+          *reinterpret_cast<u32x2 *>(a.out + obase + co) =
+              to_h4(v[0], v[1], v[2], v[3]);
+        }
+      }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Data convolution (forward / input gradient / transposed forward).
 // Requires reduction channels cr % BK == 0 (a stage lies in one tap).
 template <class C, bool WK, bool SPLIT>
-__global__ __launch_bounds__(C::NT) void data_conv_dma_kernel(DataConvArgs a,
+__global__ __launch_bounds__(C::NT, C::WPE) void data_conv_dma_kernel(DataConvArgs a,
                                                               TileMap tm) {
   FG_DMA_RING(C, R);
   constexpr int PW = C::PW;
@@ -557,8 +603,8 @@ __global__ __launch_bounds__(C::NT) void data_conv_dma_kernel(DataConvArgs a,
   const int phase = tz / a.nsplit, split = tz % a.nsplit;
   const Phase P = a.ph[phase];
   const int npix = a.n * P.mh * P.mw;
-  const int n0 = tx * TN;
-  const int m0 = ty * TM;
+  const int n0 = tx * C::T;
+  const int m0 = ty * C::T;
   if (n0 >= npix) return;
   const int ktot = P.nr * P.ns * a.cr;
   const int nk = ktot / C::BK;
@@ -653,16 +699,20 @@ __global__ __launch_bounds__(C::NT) void data_conv_dma_kernel(DataConvArgs a,
   zero<C>(acc);
   pipeline<C, WK, true>(acc, R, kend - kbeg, wm0, wn0, lane, issue);
 
-  // staging: ring array `wave` (a-side arrays first, constant indices only)
-  // and the position tables in the next one
-  static_assert(2 * C::NS >= C::NW + 1 && C::TILE_BYTES >= 16384,
-                "the store needs one 16 KiB ring array per wave plus one");
-  uint8_t *sbuf = R.a[0];
+  if constexpr (C::WM == 128 && C::WN == 64) {
+    // staging: ring array `wave` (a-side arrays first, constant indices
+    // only) and the position tables in the next one
+    static_assert(2 * C::NS >= C::NW + 1 && C::TILE_BYTES >= 16384,
+                  "the store needs one 16 KiB ring array per wave plus one");
+    uint8_t *sbuf = R.a[0];
 #pragma unroll
-  for (int k = 1; k < C::NW; ++k)
-    if (wave == k) sbuf = k < C::NS ? R.a[k] : R.b[k - C::NS];
-  int32_t *spos = reinterpret_cast<int32_t *>(R.b[C::NW - C::NS]) + 64 * wave;
-  store_tile<C, SPLIT>(acc, sbuf, spos, a, P, npix, n0, m0, wm0, wn0, lane, split);
+    for (int k = 1; k < C::NW; ++k)
+      if (wave == k) sbuf = k < C::NS ? R.a[k] : R.b[k - C::NS];
+    int32_t *spos = reinterpret_cast<int32_t *>(R.b[C::NW - C::NS]) + 64 * wave;
+    store_tile<C, SPLIT>(acc, sbuf, spos, a, P, npix, n0, m0, wm0, wn0, lane, split);
+  } else {
+    store_direct<C, SPLIT>(acc, a, P, npix, n0, m0, wm0, wn0, lane, split);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -980,8 +1030,8 @@ __global__ __launch_bounds__(C::NT) void wgrad_dma_kernel(WgradArgs a, WgradDiv 
   const int rsc = a.r * a.s * a.c;
   int tx, ty, split;  // rho tile, k tile, reduction split
   if (!tm.decode(blockIdx.x, tx, ty, split)) return;
-  const int m0 = tx * TM;  // rho
-  const int n0 = ty * TN;  // k
+  const int m0 = tx * C::T;  // rho
+  const int n0 = ty * C::T;  // k
   const int mbeg = split * a.mchunk;
   const int mend = min(a.mtot, mbeg + a.mchunk);
   const int nst = mend > mbeg ? (mend - mbeg + C::BK - 1) / C::BK : 0;
@@ -1088,8 +1138,9 @@ hipError_t launch_data_conv_halo(const DataConvArgs &a, bool w_kmajor,
   return hipGetLastError();
 }
 
-hipError_t launch_data_conv_dma(const DataConvArgs &a0, bool w_kmajor,
-                                hipStream_t st) {
+template <class C>
+static hipError_t launch_dma_cfg(const DataConvArgs &a0, bool w_kmajor,
+                                 hipStream_t st) {
   DataConvArgs a = a0;
   int maxpix = 0;
   bool uneven = false;
@@ -1097,7 +1148,7 @@ hipError_t launch_data_conv_dma(const DataConvArgs &a0, bool w_kmajor,
     maxpix = std::max(maxpix, a.n * a.ph[i].mh * a.ph[i].mw);
     uneven |= a.ph[i].nr * a.ph[i].ns != a.ph[0].nr * a.ph[0].ns;
   }
-  const int tco = (a.co + dma::TM - 1) / dma::TM, tpix = (maxpix + dma::TN - 1) / dma::TN;
+  const int tco = (a.co + C::T - 1) / C::T, tpix = (maxpix + C::T - 1) / C::T;
   dma::TileMap tm;
   if (uneven) {
     // phases with different tap counts (strided input gradients): costliest
@@ -1112,24 +1163,34 @@ hipError_t launch_data_conv_dma(const DataConvArgs &a0, bool w_kmajor,
     tm = dma::TileMap{a.nphase * a.nsplit, tco, tpix, 0, 0};
   }
   tm.per = (tm.n0 * tm.n1 * tm.n2 + 7) / 8;
-  dim3 grid(8 * tm.per);
+  dim3 grid(8 * tm.per), block(C::NT);
   const bool split = a.nsplit > 1;
   if (w_kmajor) {
     if (split)
-      hipLaunchKernelGGL((dma::data_conv_dma_kernel<dma::DataRun, true, true>), grid,
-                         dim3(dma::DataRun::NT), 0, st, a, tm);
+      hipLaunchKernelGGL((dma::data_conv_dma_kernel<C, true, true>), grid, block, 0,
+                         st, a, tm);
     else
-      hipLaunchKernelGGL((dma::data_conv_dma_kernel<dma::DataRun, true, false>), grid,
-                         dim3(dma::DataRun::NT), 0, st, a, tm);
+      hipLaunchKernelGGL((dma::data_conv_dma_kernel<C, true, false>), grid, block, 0,
+                         st, a, tm);
   } else {
     if (split)
-      hipLaunchKernelGGL((dma::data_conv_dma_kernel<dma::DataRun, false, true>), grid,
-                         dim3(dma::DataRun::NT), 0, st, a, tm);
+      hipLaunchKernelGGL((dma::data_conv_dma_kernel<C, false, true>), grid, block, 0,
+                         st, a, tm);
     else
-      hipLaunchKernelGGL((dma::data_conv_dma_kernel<dma::DataRun, false, false>), grid,
-                         dim3(dma::DataRun::NT), 0, st, a, tm);
+      hipLaunchKernelGGL((dma::data_conv_dma_kernel<C, false, false>), grid, block,
+                         0, st, a, tm);
   }
   return hipGetLastError();
+}
+
+hipError_t launch_data_conv_dma(const DataConvArgs &a, bool w_kmajor,
+                                hipStream_t st) {
+  return launch_dma_cfg<dma::DataRun>(a, w_kmajor, st);
+}
+
+hipError_t launch_data_conv_dma_small(const DataConvArgs &a, bool w_kmajor,
+                                      hipStream_t st) {
+  return launch_dma_cfg<dma::SmallRun>(a, w_kmajor, st);
 }
 
 static dma::FastDiv make_fastdiv(uint32_t d) {

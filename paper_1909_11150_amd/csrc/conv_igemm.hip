@@ -665,6 +665,13 @@ int64_t data_nk_max(const DataConvArgs &a) {
 }
 
 constexpr int64_t kCUs = 256;
+// flop/s of one 128x128 workgroup (two share a CU): LDS-DMA kernel and
+// register-staged kernel
+#ifndef FG_RATE_SMALL_DMA
+#define FG_RATE_SMALL_DMA 1.3e12
+#endif
+constexpr double kRateSmallDma = FG_RATE_SMALL_DMA;
+constexpr double kRateSmallRegs = 1.3e12;
 
 }  // namespace
 
@@ -678,9 +685,8 @@ struct TileChoice {
 };
 
 TileChoice choose_tiles(int64_t tiles_big, int64_t tiles_small, int64_t nk,
-                        int64_t out_elems, bool allow_big) {
+                        int64_t out_elems, bool allow_big, double rate_small) {
   constexpr double kRateBig = 3.0e12;    // flop/s of one 256x256 workgroup
-  constexpr double kRateSmall = 1.3e12;  // flop/s of one 128x128 workgroup
   constexpr double kPartialBw = 6.0e12;  // B/s for fp32 partial traffic
   constexpr double kReduceLaunch = 4e-6;
   TileChoice best{false, 1};
@@ -690,7 +696,7 @@ TileChoice choose_tiles(int64_t tiles_big, int64_t tiles_small, int64_t nk,
     const int64_t tiles = big ? tiles_big : tiles_small;
     const int64_t slots = big ? kCUs : 2 * kCUs;
     const int t = big ? 256 : 128;
-    const double rate = big ? kRateBig : kRateSmall;
+    const double rate = big ? kRateBig : rate_small;
     for (int ns = 1; ns <= 16; ++ns) {
       if (ns > 1 && (nk + ns - 1) / ns < 4) break;  // >= 4 slices per split
       const int64_t waves = (tiles * ns + slots - 1) / slots;
@@ -712,7 +718,8 @@ DataPlan plan_data_conv(const DataConvArgs &a) {
   const int64_t out = (int64_t)a.n * a.ho * a.wo * a.co;
   const TileChoice c = choose_tiles(data_tiles(a, 256, 256),
                                     data_tiles(a, 128, 128), data_nk_max(a), out,
-                                    a.co >= 256);
+                                    a.co >= 256,
+                                    data_dma_ok(a) ? kRateSmallDma : kRateSmallRegs);
   pl.big = c.big;
   pl.nsplit = c.nsplit;
   pl.ws_bytes = pl.nsplit > 1 ? (size_t)pl.nsplit * out * sizeof(float) : 0;
@@ -752,7 +759,8 @@ hipError_t launch_data_conv(const DataConvArgs &a0, bool w_kmajor,
   const DataPlan pl = plan_data_conv(a);
   a.nsplit = pl.nsplit;
   hipError_t e =
-      !pl.big ? launch_dc_tile<SmallCfg>(a, w_kmajor, st)
+      !pl.big ? (data_dma_ok(a) ? launch_data_conv_dma_small(a, w_kmajor, st)
+                                : launch_dc_tile<SmallCfg>(a, w_kmajor, st))
       : data_halo_ok(a) ? launch_data_conv_halo(a, w_kmajor, st)
       : data_dma_ok(a)  ? launch_data_conv_dma(a, w_kmajor, st)
                         : launch_dc_tile<BigCfg>(a, w_kmajor, st);
@@ -790,6 +798,12 @@ const char *data_conv_kernel_name(const DataConvArgs &a, bool w_kmajor) {
         {"data_conv_halo_kernel<true, false>", "data_conv_halo_kernel<true, true>"}};
     return hn[w_kmajor][pl.nsplit > 1];
   }
+  if (!pl.big && data_dma_ok(a)) {
+    static const char *sn[2][2] = {
+        {"data_conv_dma_kernel<128, false, false>", "data_conv_dma_kernel<128, false, true>"},
+        {"data_conv_dma_kernel<128, true, false>", "data_conv_dma_kernel<128, true, true>"}};
+    return sn[w_kmajor][pl.nsplit > 1];
+  }
   if (pl.big && data_dma_ok(a)) {
     static const char *dn[2][2] = {
         {"data_conv_dma_kernel<false, false>", "data_conv_dma_kernel<false, true>"},
@@ -805,7 +819,7 @@ static TileChoice wgrad_choice(const fg_conv_desc &d, int32_t p, int32_t q) {
   const int64_t tb = ((rsc + 255) / 256) * ((d.k + 255) / 256);
   const int64_t ts = ((rsc + 127) / 128) * ((d.k + 127) / 128);
   return choose_tiles(tb, ts, (mtot + BK - 1) / BK, (int64_t)d.k * rsc,
-                      rsc >= 256 && d.k >= 256);
+                      rsc >= 256 && d.k >= 256, kRateSmallRegs);
 }
 
 WgradPlan plan_wgrad(const fg_conv_desc &d, int32_t p, int32_t q);

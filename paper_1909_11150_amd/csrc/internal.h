@@ -90,6 +90,9 @@ bool data_halo_ok(const DataConvArgs &a);
 hipError_t launch_data_conv_halo(const DataConvArgs &a, bool w_kmajor,
                                  hipStream_t st);
 bool wgrad_dma_ok(const WgradArgs &a);
+// The same with 128 x 128 tiles (two workgroups per CU).
+hipError_t launch_data_conv_dma_small(const DataConvArgs &a, bool w_kmajor,
+                                      hipStream_t st);
 hipError_t launch_data_conv_dma(const DataConvArgs &a, bool w_kmajor,
                                 hipStream_t st);
 hipError_t launch_wgrad_dma(const WgradArgs &a, hipStream_t st);

@@ -1,7 +1,8 @@
 """GPU parity of the LDS-DMA kernels on ragged shapes.
 
 The tile planner sends large shapes to the LDS-DMA kernels (256 x 256
-tiles fed by buffer loads straight into LDS). These cases are chosen so that
+tiles fed by buffer loads straight into LDS) and shapes with few output
+positions to their 128 x 128 version. These cases are chosen so that
 each of those kernels is reached with ragged edges: output positions and
 channels that do not fill the last tile, odd image sizes with padding at the
 borders, stride-2 phases, reduction splits and partial last stages. Outputs
@@ -26,6 +27,12 @@ CASES = [
     ((1, 77, 79, 512, 512, 3, 1, 1), fg.OP_BWD_DATA, "data_conv_dma_kernel<false, true>"),
     ((1, 127, 129, 512, 256, 3, 2, 1), fg.OP_BWD_DATA, "data_conv_dma_kernel<false, false>"),
     ((1, 93, 95, 512, 512, 3, 1, 1), fg.OP_BWD_WEIGHT, "wgrad_dma_kernel<true>"),
+    # 128 x 128 tiles
+    ((2, 15, 17, 1024, 1024, 3, 1, 1), fg.OP_FWD, "data_conv_dma_kernel<128, true, true>"),
+    ((8, 64, 64, 64, 128, 3, 1, 1), fg.OP_FWD, "data_conv_dma_kernel<128, true, false>"),
+    ((1, 31, 33, 512, 768, 3, 2, 1), fg.OP_FWD, "data_conv_dma_kernel<128, true, true>"),
+    ((4, 64, 64, 256, 128, 3, 1, 1), fg.OP_BWD_DATA, "data_conv_dma_kernel<128, false, false>"),
+    ((1, 33, 31, 1024, 512, 3, 2, 1), fg.OP_BWD_DATA, "data_conv_dma_kernel<128, false, true>"),
 ]
 
 
@@ -83,6 +90,21 @@ def test_dma_convt_ragged():
     idx = sample_indices(y.shape, 3000, rng)
     ref = oracle.conv_transpose2d_fwd_points(x, Wt, idx, 2, 1)
     conv_parity(host(y).ravel()[idx], ref, "convT")
+
+
+def test_dma_small_convt_ragged():
+    n, h, w, ci, co = 1, 15, 16, 1024, 1024
+    d = fg.ConvDesc.make(n, h, w, ci, co, 4, 4, 2, 1)
+    assert fg.kernel_name(d, fg.OP_CONVT) == "data_conv_dma_kernel<128, false, true>"
+    rng = np.random.default_rng(25)
+    x = synth.uniform(rng, (n, h, w, ci))
+    Wt = synth.normal(rng, (ci, 4, 4, co), np.sqrt(2.0 / (4 * ci)))
+    y = empty16((n, 2 * h, 2 * w, co))
+    fg.conv_transpose2d_fwd(d, dev(x), dev(Wt), y, fg.EPI_RELU, None,
+                            workspace(d, fg.OP_CONVT))
+    idx = sample_indices(y.shape, 3000, rng)
+    ref = oracle.relu(oracle.conv_transpose2d_fwd_points(x, Wt, idx, 2, 1))
+    conv_parity(host(y).ravel()[idx], ref, "convT small")
 
 
 def test_dma_deterministic():
