@@ -48,7 +48,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu", action="store_true",
                     help="skip the CPU oracle baseline leg")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+    ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="approximate CPU work of the oracle sample")
     ap.add_argument("--detail", default=None,
                     help="write per-op timings (JSON) to this path")
@@ -258,17 +258,17 @@ def cpu_baseline(layers, seconds):
                                                                2, 1))]
         for total, fn in tasks:
             fpe = L.flops / total   # algorithmic flops per output element
-            # grow the sample until one evaluation takes a quarter of the
-            # per-task budget or more (the last, largest one is the timed one)
+            # grow the sample until one evaluation takes half the per-task
+            # budget or more (the last, largest one is the timed one)
             k = min(total, 64)
             while True:
                 idx = rng.choice(total, size=k, replace=False)
                 t0 = time.perf_counter()
                 fn(idx)
                 dt = time.perf_counter() - t0
-                if k >= total or dt >= per_task / 4:
+                if k >= total or dt >= per_task / 2:
                     break
-                k = min(total, k * 4)
+                k = min(total, k * 2)
             t_total += dt
             flops_done += fpe * k
         del xs, ws, dys
