@@ -1082,7 +1082,29 @@ __global__ __launch_bounds__(C::NT) void wgrad_dma_kernel(WgradArgs a, WgradDiv 
   f32x16 acc[C::FM][C::FN];
   zero<C>(acc);
   pipeline<C, false, false>(acc, R, nst, wm0, wn0, lane, issue);
-  store_tile_w<C, SPLIT>(acc, R, a, rsc, m0 + wm0, n0 + wn0, lane, wave, split);
+  if constexpr (C::WM == 64 && C::WN == 64) {
+    store_tile_w<C, SPLIT>(acc, R, a, rsc, m0 + wm0, n0 + wn0, lane, wave, split);
+  } else {
+    // direct: each lane writes 4 consecutive rho of one output channel k
+#pragma unroll
+    for (int j = 0; j < C::FN; ++j) {
+      const int k = n0 + wn0 + j * 32 + (lane & 31);
+#pragma unroll
+      for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int rho = m0 + wm0 + i * 32 + 8 * g + 4 * (lane >> 5);
+          const f32x16 &c = acc[i][j];
+          if (!SPLIT)
+            *reinterpret_cast<u32x2 *>(a.dw + (size_t)k * rsc + rho) =
+                to_h4(c[4 * g], c[4 * g + 1], c[4 * g + 2], c[4 * g + 3]);
+          else
+            *reinterpret_cast<f32x4 *>(a.part + ((size_t)split * a.k + k) * rsc +
+                                       rho) =
+                f32x4{c[4 * g], c[4 * g + 1], c[4 * g + 2], c[4 * g + 3]};
+        }
+    }
+  }
 }
 
 }  // namespace dma
