@@ -667,7 +667,7 @@ __global__ __launch_bounds__(C::NT, C::WPE) void data_conv_dma_kernel(DataConvAr
     ti = t / P.ns;
     tj = t - ti * P.ns;
   }
-  auto issue = [&](int, int slot) {
+  auto issue = [&](int, int slot) __attribute__((always_inline)) {
     const int dh = P.dh0 + P.dstep * ti, dw = P.dw0 + P.dstep * tj;
     const int woff = (P.r0 + P.rstep * ti) * a.s + (P.s0 + P.rstep * tj);
     const int delta = (dh * a.wi + dw) * a.cr + cr0;
@@ -848,7 +848,7 @@ __global__ __launch_bounds__(C::NT) void data_conv_halo_kernel(DataConvArgs a,
   }
   // weight stage decode, advanced by one stage per issue (in order)
   int ic = cbeg, it_ = 0;
-  auto issue_w = [&](int slot) {
+  auto issue_w = [&](int slot) __attribute__((always_inline)) {
     const int ti = it_ / 3, tj = it_ - 3 * ti;
     const int woff = (P.r0 + P.rstep * ti) * a.s + (P.s0 + P.rstep * tj);
     const int cr0 = 32 * ic;
@@ -864,7 +864,7 @@ __global__ __launch_bounds__(C::NT) void data_conv_halo_kernel(DataConvArgs a,
     ic += wrap;
   };
   // block jj of this wave's share of chunk c's patch
-  auto issue_pb = [&](int pslot, int c, int jj) {
+  auto issue_pb = [&](int pslot, int c, int jj) __attribute__((always_inline)) {
     const unsigned o = (unsigned)(pbase[jj] + 64 * c);
     dma16(rs_act, patch[pslot] + 1024 * (NPW * wave + jj),
           c < cend && pbase[jj] >= 0 ? o : kOOB);
@@ -873,7 +873,7 @@ __global__ __launch_bounds__(C::NT) void data_conv_halo_kernel(DataConvArgs a,
   f32x16 acc[C::FM][C::FN];
   zero<C>(acc);
   Frags<C> f[2];
-  auto load = [&](Frags<C> &fr, int slot, int pslot, int t, int ks) {
+  auto load = [&](Frags<C> &fr, int slot, int pslot, int t, int ks) __attribute__((always_inline)) {
     const int toff = back * (pwid + 1) + dsg * ((t / 3) * pwid + t % 3);
 #pragma unroll
     for (int i = 0; i < C::FM; ++i)
@@ -887,7 +887,7 @@ __global__ __launch_bounds__(C::NT) void data_conv_halo_kernel(DataConvArgs a,
 
   // One stage at position U of the unrolled pair of chunks: A slot U % 3,
   // patch slot U / 9, tap U % 9.
-  auto stage = [&](auto Uc, int it) {
+  auto stage = [&](auto Uc, int it) __attribute__((always_inline)) {
     constexpr int U = decltype(Uc)::value;
     constexpr int T = U % kHaloTaps, SLOT = U % NS, PS = (U / kHaloTaps) & 1;
     constexpr int U1 = (U + 1) % UNR;
@@ -922,7 +922,7 @@ __global__ __launch_bounds__(C::NT) void data_conv_halo_kernel(DataConvArgs a,
   issue_w(NS - 1);
   load(f[0], 0, 0, 0, 0);
   int it0 = 0;
-  auto step = [&](auto Uc) { stage(Uc, it0 + decltype(Uc)::value); };
+  auto step = [&](auto Uc) __attribute__((always_inline)) { stage(Uc, it0 + decltype(Uc)::value); };
   for (; it0 + UNR <= nst; it0 += UNR) unroll<0, UNR>(step);
   // the rest, a whole number of chunks, as a prefix of a group
   constexpr int G9 = kHaloTaps;
@@ -1059,7 +1059,7 @@ __global__ __launch_bounds__(C::NT) void wgrad_dma_kernel(WgradArgs a, WgradDiv 
   }
   const int h0 = tr - a.ph, w0 = ts - a.pw;
 
-  auto issue = [&](int, int slot) {
+  auto issue = [&](int, int slot) __attribute__((always_inline)) {
     uint8_t *ta = R.a[slot], *tb = R.b[slot];
 #pragma unroll
     for (int jj = 0; jj < PW; ++jj) {
