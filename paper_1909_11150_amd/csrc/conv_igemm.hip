@@ -617,7 +617,25 @@ __global__ __launch_bounds__(kHeadWgradThreads) void head_wgrad_kernel(
   int64_t beg = (int64_t)blockIdx.x * chunk;
   int64_t end = beg + chunk < npix ? beg + chunk : npix;
   if (row < rows) {
-    for (int64_t pix = beg + row; pix < end; pix += rows) {
+    // four positions per iteration, their loads issued together
+    int64_t pix = beg + row;
+    for (; pix + 3 * rows < end; pix += 4 * rows) {
+      float d[4];
+      u32x4 xv[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        d[u] = h_to_f32(dy[pix + u * rows]);
+        xv[u] = ldg16(x + (pix + u * rows) * c + ch * 8);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          acc[2 * e] += d[u] * h_to_f32((uint16_t)xv[u][e]);
+          acc[2 * e + 1] += d[u] * h_to_f32((uint16_t)(xv[u][e] >> 16));
+        }
+    }
+    for (; pix < end; pix += rows) {
       float d = h_to_f32(dy[pix]);
       u32x4 xv = ldg16(x + pix * c + ch * 8);
 #pragma unroll
@@ -921,8 +939,10 @@ hipError_t launch_head_bwd_data(const uint16_t *dy, const uint16_t *w,
 }
 
 static int64_t head_wgrad_blocks(int64_t npix) {
-  int64_t b = (npix + 1023) / 1024;
-  return b < 1 ? 1 : (b > 1024 ? 1024 : b);
+  // about 256 positions per workgroup, four workgroups per CU on the
+  // full-size head
+  int64_t b = (npix + 255) / 256;
+  return b < 1 ? 1 : (b > 2048 ? 2048 : b);
 }
 
 size_t head_wgrad_ws_bytes(const fg_conv_desc &d) {
