@@ -14,11 +14,16 @@
 // Two LDS tile layouts:
 //   k-major  (row = GEMM row/column, BK reduction halves per row; 16-byte
 //            chunk c stored at c ^ g(row)); MFMA operands are single 16-byte
-//            reads, conflict-free for 8 or 16 consecutive rows.
-//   mn-major (row = reduction index, 256 halves = 512 bytes per row; 32-byte
-//            block b stored at b ^ s(row)); MFMA operands are two transposing
-//            8-byte reads (ds_read_b64_tr_b16), each 64-lane read touching
-//            every bank pair at most twice.
+//            reads of 32 consecutive rows.
+//   mn-major (row = reduction index, 256 halves = 512 bytes per row; 64-byte
+//            block b stored at b ^ (row & 3)); MFMA operands are two
+//            transposing 8-byte reads (ds_read_b64_tr_b16).
+// The permutations are chosen by measurement on gfx950, whose LDS has 64
+// banks of 4 bytes: g(row) = (row >> 2) & 3 reads 32 consecutive 64-byte rows
+// at full rate from any starting row (the previous ((row >> 1) ^ (row >> 3))
+// & 3 ran at half rate), and the mn-major xor of (row & 3) * 64 bytes serves
+// each half-wave of a transposing read without conflicts (xor of 32-byte
+// blocks: two-way conflicts).
 // The mn-major layout lets operands whose reduction index is strided in
 // memory (input-gradient and transposed-conv weights, both kernel-gradient
 // operands) be copied row by row as they lie in memory.
@@ -80,20 +85,22 @@ typedef __attribute__((address_space(3))) void lds_void;
 
 // k-major: 16-byte chunk c of tile row `row` (bytes). 64-byte rows (BK 32)
 // permute the 4 chunks by g(row); 128-byte rows (BK 64) the 8 chunks.
+// mn-major: byte xor of reduction row k (a multiple of 64, below 256, so rows
+// of 256 bytes take it too).
 template <int BK>
 __device__ __forceinline__ int kmaj_swz(int row) {
-  return BK == 32 ? (((row >> 1) ^ (row >> 3)) & 3) : ((row ^ (row >> 3)) & 7);
+  return BK == 32 ? ((row >> 2) & 3) : ((row ^ (row >> 3)) & 7);
 }
 template <int BK>
 __device__ __forceinline__ int kmaj_off(int row, int c) {
   return row * (2 * BK) + ((c ^ kmaj_swz<BK>(row)) << 4);
 }
-__device__ __forceinline__ int mn_swz(int k) {
-  return (k & 3) | (((k >> 3) & 1) << 2);
+__device__ __forceinline__ int mn_xor(int k) {
+  return (k & 3) << 6;
 }
 template <int RB>
 __device__ __forceinline__ int mnmaj_off(int k, int n) {  // bytes, n % 4 == 0
-  return k * RB + ((2 * n) ^ (mn_swz(k) << 5));
+  return k * RB + ((2 * n) ^ mn_xor(k));
 }
 
 // Workgroup barrier without a memory fence. __syncthreads() would add a
@@ -244,7 +251,7 @@ __device__ __forceinline__ MnSlot<C> mn_slots(int wave, int lane) {
     int k = C::RPI * (C::PW * wave + jj) + lane / CPM;
     int p = lane % CPM;
     s.krow[jj] = k;
-    s.ncol[jj] = ((p >> 1) ^ mn_swz(k)) * 16 + (p & 1) * 8;
+    s.ncol[jj] = ((16 * p) ^ mn_xor(k)) / 2;
   }
   return s;
 }
