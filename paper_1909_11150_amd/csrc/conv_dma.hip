@@ -16,8 +16,9 @@
 //            chunk c stored at c ^ g(row)); MFMA operands are single 16-byte
 //            reads of 32 consecutive rows.
 //   mn-major (row = reduction index, 256 halves = 512 bytes per row; 64-byte
-//            block b stored at b ^ (row & 3)); MFMA operands are two
-//            transposing 8-byte reads (ds_read_b64_tr_b16).
+//            block b stored at b ^ (row & 3), or for the halo kernel's
+//            weights 32-byte blocks as described at mn_xor); MFMA operands
+//            are two transposing 8-byte reads (ds_read_b64_tr_b16).
 // The permutations are chosen by measurement on gfx950, whose LDS has 64
 // banks of 4 bytes: g(row) = (row >> 2) & 3 reads 32 consecutive 64-byte rows
 // at full rate from any starting row (the previous ((row >> 1) ^ (row >> 3))
@@ -85,8 +86,11 @@ typedef __attribute__((address_space(3))) void lds_void;
 
 // k-major: 16-byte chunk c of tile row `row` (bytes). 64-byte rows (BK 32)
 // permute the 4 chunks by g(row); 128-byte rows (BK 64) the 8 chunks.
-// mn-major: byte xor of reduction row k (a multiple of 64, below 256, so rows
-// of 256 bytes take it too).
+// mn-major: byte xor of reduction row k, below 256 so that rows of 256 bytes
+// take it too. MX = 1: 64-byte blocks permuted by k & 3 (conflict-free
+// transposing reads); MX = 0: 32-byte blocks permuted by (k & 3) | bit 3 of k
+// (two-way conflicts), kept for the halo kernel's weights, whose register
+// allocation spills into its main loop with the other permutation.
 template <int BK>
 __device__ __forceinline__ int kmaj_swz(int row) {
   return BK == 32 ? ((row >> 2) & 3) : ((row ^ (row >> 3)) & 7);
@@ -95,12 +99,13 @@ template <int BK>
 __device__ __forceinline__ int kmaj_off(int row, int c) {
   return row * (2 * BK) + ((c ^ kmaj_swz<BK>(row)) << 4);
 }
+template <int MX>
 __device__ __forceinline__ int mn_xor(int k) {
-  return (k & 3) << 6;
+  return MX ? (k & 3) << 6 : ((k & 3) | (((k >> 3) & 1) << 2)) << 5;
 }
-template <int RB>
+template <int RB, int MX = 1>
 __device__ __forceinline__ int mnmaj_off(int k, int n) {  // bytes, n % 4 == 0
-  return k * RB + ((2 * n) ^ mn_xor(k));
+  return k * RB + ((2 * n) ^ mn_xor<MX>(k));
 }
 
 // Workgroup barrier without a memory fence. __syncthreads() would add a
@@ -165,7 +170,7 @@ struct WgradDiv {
 };
 
 // MFMA operand of a 32-row block starting at `base` for reduction step ks.
-template <int BK, bool KMAJOR, int RB = 512>
+template <int BK, bool KMAJOR, int RB = 512, int MX = 1>
 __device__ __forceinline__ u32x4 frag(const uint8_t *tile, int base, int ks,
                                       int lane) {
   if (KMAJOR) {
@@ -176,9 +181,9 @@ __device__ __forceinline__ u32x4 frag(const uint8_t *tile, int base, int ks,
     const int k = 8 * (g >> 1) + (m >> 2) + 16 * ks;
     const int n = base + 16 * (g & 1) + 4 * (m & 3);
     v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-        (lds_v4s *)(tile + mnmaj_off<RB>(k, n)));
+        (lds_v4s *)(tile + mnmaj_off<RB, MX>(k, n)));
     v4s hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-        (lds_v4s *)(tile + mnmaj_off<RB>(k + 4, n)));
+        (lds_v4s *)(tile + mnmaj_off<RB, MX>(k + 4, n)));
     u32x2 a = __builtin_bit_cast(u32x2, lo), b = __builtin_bit_cast(u32x2, hi);
     return u32x4{a[0], a[1], b[0], b[1]};
   }
@@ -242,7 +247,7 @@ __device__ __forceinline__ KmSlot<C> km_slots(int wave, int lane) {
   return s;
 }
 
-template <class C>
+template <class C, int MX = 1>
 __device__ __forceinline__ MnSlot<C> mn_slots(int wave, int lane) {
   MnSlot<C> s;
 #pragma unroll
@@ -251,7 +256,7 @@ __device__ __forceinline__ MnSlot<C> mn_slots(int wave, int lane) {
     int k = C::RPI * (C::PW * wave + jj) + lane / CPM;
     int p = lane % CPM;
     s.krow[jj] = k;
-    s.ncol[jj] = ((16 * p) ^ mn_xor(k)) / 2;
+    s.ncol[jj] = ((16 * p) ^ mn_xor<MX>(k)) / 2;
   }
   return s;
 }
@@ -847,7 +852,7 @@ __global__ __launch_bounds__(C::NT) void data_conv_halo_kernel(DataConvArgs a,
       wok[jj] = co < a.co;
       wbase[jj] = co * a.ldw + as.coff[jj];
     } else {
-      const MnSlot<C> as = mn_slots<C>(wave, lane);
+      const MnSlot<C> as = mn_slots<C, 0>(wave, lane);
       const int co = m0 + as.ncol[jj];
       wok[jj] = co < a.co;
       wbase[jj] = as.krow[jj] * a.w_red + co;
@@ -884,7 +889,7 @@ __global__ __launch_bounds__(C::NT) void data_conv_halo_kernel(DataConvArgs a,
     const int toff = back * (pwid + 1) + dsg * ((t / 3) * pwid + t % 3);
 #pragma unroll
     for (int i = 0; i < C::FM; ++i)
-      fr.a[i] = frag<32, WK>(ringA[slot], wm0 + 32 * i, ks, lane);
+      fr.a[i] = frag<32, WK, 512, 0>(ringA[slot], wm0 + 32 * i, ks, lane);
 #pragma unroll
     for (int j = 0; j < C::FN; ++j)
       fr.b[j] = frag_row<C>(patch[pslot], brow[j] + toff, ks, lane);
