@@ -696,17 +696,33 @@ constexpr double kRateSmallRegs = 1.3e12;
 // Split/tile choice by an estimate of the run time: resident workgroup
 // slots per GPU (one 256x256 workgroup or two 128x128 ones per CU), the
 // per-workgroup MFMA rate each reaches (measured on MI355X), waves of
-// workgroups, and the fp32 partials a split writes and re-reads.
+// workgroups with a fixed cost per wave (prologue and tile store, which one
+// workgroup per CU cannot overlap with its MFMA work), and the fp32
+// partials a split writes and re-reads.
 struct TileChoice {
   bool big;
   int32_t nsplit;
 };
+struct TileCost {
+  double rate_big, rate_small;  // flop/s of one 256x256 / 128x128 workgroup
+  double partial_bw;            // B/s for fp32 partial traffic (8 B/element)
+  double split_const;           // s, the reduction launch of a split
+  double wave_const;            // s per wave of workgroups
+};
+// Data convolutions: rates chosen by timing the network's layers.
+static TileCost data_cost(bool dma_small) {
+  return TileCost{3.0e12, dma_small ? kRateSmallDma : kRateSmallRegs, 6.0e12, 4e-6, 0.0};
+}
+// Kernel gradient: a least-squares fit of this model to the DMA kernel's
+// times on the network's twelve kernel-gradient shapes at 1-8 splits
+// (per 256x256x32 stage 0.66 us, 4.2 us per wave, partials at 4.05 TB/s,
+// 6.3 us per split launch; mean error 9%). The 128x128 rate is the
+// register-staged kernel's, which only shapes too small for 256x256 tiles
+// take.
+constexpr TileCost kWgradCost{6.35e12, 1.3e12, 4.05e12, 6.3e-6, 4.2e-6};
 
 TileChoice choose_tiles(int64_t tiles_big, int64_t tiles_small, int64_t nk,
-                        int64_t out_elems, bool allow_big, double rate_small) {
-  constexpr double kRateBig = 3.0e12;    // flop/s of one 256x256 workgroup
-  constexpr double kPartialBw = 6.0e12;  // B/s for fp32 partial traffic
-  constexpr double kReduceLaunch = 4e-6;
+                        int64_t out_elems, bool allow_big, const TileCost &cost) {
   TileChoice best{false, 1};
   double best_t = 1e30;
   for (int big = 0; big < 2; ++big) {
@@ -714,14 +730,14 @@ TileChoice choose_tiles(int64_t tiles_big, int64_t tiles_small, int64_t nk,
     const int64_t tiles = big ? tiles_big : tiles_small;
     const int64_t slots = big ? kCUs : 2 * kCUs;
     const int t = big ? 256 : 128;
-    const double rate = big ? kRateBig : rate_small;
+    const double rate = big ? cost.rate_big : cost.rate_small;
     for (int ns = 1; ns <= 16; ++ns) {
       if (ns > 1 && (nk + ns - 1) / ns < 4) break;  // >= 4 slices per split
       const int64_t waves = (tiles * ns + slots - 1) / slots;
       const int64_t nk_split = (nk + ns - 1) / ns;
       const double t_block = 2.0 * t * t * BK * (double)nk_split / rate;
-      double tt = waves * t_block;
-      if (ns > 1) tt += ns * (double)out_elems * 8.0 / kPartialBw + kReduceLaunch;
+      double tt = waves * (t_block + cost.wave_const);
+      if (ns > 1) tt += ns * (double)out_elems * 8.0 / cost.partial_bw + cost.split_const;
       if (tt < best_t * 0.98) {  // prefer fewer splits on near ties
         best_t = tt;
         best = TileChoice{big != 0, ns};
@@ -736,8 +752,7 @@ DataPlan plan_data_conv(const DataConvArgs &a) {
   const int64_t out = (int64_t)a.n * a.ho * a.wo * a.co;
   const TileChoice c = choose_tiles(data_tiles(a, 256, 256),
                                     data_tiles(a, 128, 128), data_nk_max(a), out,
-                                    a.co >= 256,
-                                    data_dma_ok(a) ? kRateSmallDma : kRateSmallRegs);
+                                    a.co >= 256, data_cost(data_dma_ok(a)));
   pl.big = c.big;
   pl.nsplit = c.nsplit;
   pl.ws_bytes = pl.nsplit > 1 ? (size_t)pl.nsplit * out * sizeof(float) : 0;
@@ -837,7 +852,7 @@ static TileChoice wgrad_choice(const fg_conv_desc &d, int32_t p, int32_t q) {
   const int64_t tb = ((rsc + 255) / 256) * ((d.k + 255) / 256);
   const int64_t ts = ((rsc + 127) / 128) * ((d.k + 127) / 128);
   return choose_tiles(tb, ts, (mtot + BK - 1) / BK, (int64_t)d.k * rsc,
-                      rsc >= 256 && d.k >= 256, kRateSmallRegs);
+                      rsc >= 256 && d.k >= 256, kWgradCost);
 }
 
 WgradPlan plan_wgrad(const fg_conv_desc &d, int32_t p, int32_t q);
