@@ -969,7 +969,10 @@ __device__ __forceinline__ void store_tile_w(f32x16 (&acc)[C::FM][C::FN],
                                              int rsc, int rho0, int k0, int lane,
                                              int wave, int split) {
   static_assert(C::WM == 64 && C::WN == 64, "store_tile_w expects 64 x 64 waves");
-  static_assert(2 * C::NS * C::TILE_BYTES >= C::NW * 8192, "LDS for staging");
+  // every pair of waves stages in one 16 KiB ring array: arrays 1..NW/2-1
+  // must exist (a.k.a. a[1..NS-1], then b[0..]) and be 16 KiB each
+  static_assert(C::TILE_BYTES == 16384 && C::NW / 2 <= 2 * C::NS,
+                "store_tile_w stages in 16 KiB ring arrays, one per two waves");
   __syncthreads();  // every wave is done reading the ring
   // 8 KiB per wave: two waves per 16 KiB ring array, by constant indices
   uint8_t *buf = R.a[0];
