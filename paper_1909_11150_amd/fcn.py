@@ -189,30 +189,73 @@ class Chain:
         return sum(3 * L.flops for L in self.layers)
 
     # ---- prepared step -----------------------------------------------------------
-    def program(self, target):
+    def program(self, target, streams=3):
         """The step as a list of library calls with every argument marshalled
         once (descriptors, pointers, segment tables); running it costs one
-        foreign call per launch. Same calls, same order as ``step``."""
-        return StepProgram(self, target)
+        foreign call per launch. Same calls as ``step``; see StepProgram for
+        the streams."""
+        return StepProgram(self, target, streams)
 
 
 # label, main kernel, algorithmic work (flops, or bytes for the gradient
-# path), C function (None: a Python callable), argument tuple, and whether
-# the call is exactly one launch of that kernel
-Call = namedtuple("Call", "label kernel work fn args single", defaults=(True,))
+# path), C function (None: a Python callable), argument tuple (the stream
+# last), whether the call is exactly one launch of that kernel, its stream
+# (0: main, 1: kernel gradients, 2: gradient path) and the calls (indices)
+# that must finish before it starts
+Call = namedtuple("Call", "label kernel work fn args single sid deps",
+                  defaults=(True, 0, ()))
+
+
+def kernel_gradient_workspace_bytes(layers):
+    """Largest workspace of the chain's kernel-gradient passes."""
+    ws = 0
+    for L in layers:
+        d = fwd_desc(L) if L.kind == "conv" else convt_dx_desc(L)
+        ws = max(ws, workspace_bytes(d, OP_BWD_WEIGHT))
+    return ws
 
 
 class StepProgram:
-    def __init__(self, ch, target):
+    """The step as prepared library calls on up to three streams.
+
+    The main stream runs the forward pass, the loss head and the
+    input-gradient chain; stream 1 runs every kernel gradient as soon as its
+    output gradient exists (an event recorded after the pass that wrote it);
+    stream 2 runs each group's pack, unscale and unpack once the group's last
+    kernel gradient is written. Kernel gradients and the gradient path thus
+    fill the CUs that the input-gradient kernels leave idle (partial waves,
+    tails) and the other way round. Stream 1 has its own workspace. The main
+    stream waits for the other streams' last calls at the end of the step, so
+    the next step's forward pass cannot overwrite activations a kernel
+    gradient still reads, nor its kernel gradients a buffer a pack still
+    reads. Every kernel is deterministic and reads only finished inputs, so
+    the results are identical to the one-stream order (``streams=1``)."""
+
+    def __init__(self, ch, target, streams=3):
         if ch.groups is None:
             raise ValueError("the step program needs gradient groups")
+        if streams not in (1, 3):
+            raise ValueError("streams must be 1 or 3")
         L_ = lib()
-        st = ch.stream if ch.stream is not None else \
-            torch.cuda.current_stream(ch.dev).cuda_stream
-        st = ctypes.c_void_p(st)
+        if ch.stream is not None:
+            main = torch.cuda.ExternalStream(ch.stream, device=ch.dev)
+        else:
+            main = torch.cuda.current_stream(ch.dev)
+        if streams == 3:  # default priorities
+            self.streams = (main, torch.cuda.Stream(device=ch.dev),
+                            torch.cuda.Stream(device=ch.dev))
+        else:
+            self.streams = (main,)
+        sptr = [ctypes.c_void_p(x.cuda_stream) for x in self.streams]
         self._keep = [target]
         calls = []
         ws, wsb = ch.ws.data_ptr(), ch.ws.numel()
+        ws_side = torch.empty(max(kernel_gradient_workspace_bytes(ch.layers), 16),
+                              dtype=torch.uint8, device=ch.dev)
+        self._keep.append(ws_side)
+        ws2, wsb2 = ws_side.data_ptr(), ws_side.numel()
+        nl = len(ch.layers)
+        st = None  # placeholder: each call's stream is filled in below
 
         def ptr(t):
             return None if t is None else t.data_ptr()
@@ -244,8 +287,10 @@ class StepProgram:
                           L_.l2_head_grad,
                           (ptr(y), ptr(target), y.numel(),
                            2.0 * ch.loss_scale / y.numel(), ptr(ch.g[-1]), st)))
-        calls.append(Call("flags.zero", "", 0, None, (ch.flags.zero_,), False))
-        for i in reversed(range(len(ch.layers))):
+        writer = {nl: len(calls) - 1}  # call that writes g[i]
+        calls.append(Call("flags.zero", "", 0, None, (ch.flags.zero_,), False, sid=2))
+        last_dw = {}
+        for i in reversed(range(nl)):
             L = ch.layers[i]
             dy = ch.g[i + 1]
             gate = i > 0 and ch.layers[i - 1].relu
@@ -256,7 +301,9 @@ class StepProgram:
                 calls.append(Call(f"{L.name}.dW", kernel_name(d, OP_BWD_WEIGHT),
                                   L.flops, L_.conv2d_bwd_weight,
                                   (desc(d), ptr(ch.acts[i]), ptr(dy), ptr(ch.dw[i]),
-                                   ws, wsb, st), one(d, OP_BWD_WEIGHT)))
+                                   ws2, wsb2, st), one(d, OP_BWD_WEIGHT),
+                                  sid=1, deps=(writer[i + 1],)))
+                last_dw[i] = len(calls) - 1
                 calls.append(Call(f"{L.name}.dx", kernel_name(d, OP_BWD_DATA),
                                   L.flops, L_.conv2d_bwd_data,
                                   (desc(d), ptr(dy), ptr(ch.w[i]), ptr(ch.g[i]), epi,
@@ -266,14 +313,28 @@ class StepProgram:
                 calls.append(Call(f"{L.name}.dW", kernel_name(d, OP_BWD_WEIGHT),
                                   L.flops, L_.conv2d_bwd_weight,
                                   (desc(d), ptr(dy), ptr(ch.acts[i]), ptr(ch.dw[i]),
-                                   ws, wsb, st), one(d, OP_BWD_WEIGHT)))
+                                   ws2, wsb2, st), one(d, OP_BWD_WEIGHT),
+                                  sid=1, deps=(writer[i + 1],)))
+                last_dw[i] = len(calls) - 1
                 calls.append(Call(f"{L.name}.dx", kernel_name(d, OP_FWD), L.flops,
                                   L_.conv2d_fwd,
                                   (desc(d), ptr(dy), ptr(ch.w[i]), ptr(ch.g[i]), epi,
                                    gt, ws, wsb, st), one(d, OP_FWD)))
+            writer[i] = len(calls) - 1
             gi = ch._group_done_at.get(i)
             if gi is not None:
-                calls += self._group_calls(ch, gi, L_, st)
+                gc = self._group_calls(ch, gi, L_, st)
+                gc[0] = gc[0]._replace(deps=(last_dw[i],))
+                calls += gc
+        if streams == 1:  # program order already respects every dependency
+            calls = [c._replace(sid=0, deps=()) for c in calls]
+        # the stream argument of each library call
+        calls = [c if c.fn is None else
+                 c._replace(args=c.args[:-1] + (sptr[c.sid],)) for c in calls]
+        self.final = tuple(max(j for j, c in enumerate(calls) if c.sid == sid)
+                           for sid in range(1, len(self.streams)))
+        needed = {d for c in calls for d in c.deps} | set(self.final)
+        self.events = {j: torch.cuda.Event() for j in sorted(needed)}
         self.calls = calls
 
     def _group_calls(self, ch, gi, L_, st):
@@ -291,26 +352,35 @@ class StepProgram:
         self._keep.append(flag)
         return [
             Call(f"G{gi}.pack", "copy_pieces_kernel<2>", 4 * n, L_.grad_group_pack,
-                 (src, len(g["members"]), g16.data_ptr(), n, st)),
+                 (src, len(g["members"]), g16.data_ptr(), n, st), sid=2),
             Call(f"G{gi}.unscale", "unscale_vec_kernel", 6 * n, L_.grad_unscale_check,
                  (g16.data_ptr(), n, 1.0 / ch.loss_scale, g32.data_ptr(),
-                  flag.data_ptr(), st)),
+                  flag.data_ptr(), st), sid=2),
             Call(f"G{gi}.unpack", "copy_pieces_kernel<4>", 8 * n, L_.grad_group_unpack,
-                 (g32.data_ptr(), n, dst, len(g["members"]), st)),
+                 (g32.data_ptr(), n, dst, len(g["members"]), st), sid=2),
         ]
 
     def run(self, events=None):
         """Run the step once. events: {call index: (start, end)} HIP events
-        recorded around those calls on the launch stream."""
+        recorded around those calls on the call's stream."""
+        streams, evs = self.streams, self.events
         for i, c in enumerate(self.calls):
+            s = streams[c.sid]
+            for d in c.deps:
+                s.wait_event(evs[d])
             ev = events.get(i) if events else None
             if ev:
-                ev[0].record()
+                ev[0].record(s)
             if c.fn is None:
-                c.args[0]()
+                with torch.cuda.stream(s):
+                    c.args[0]()
             else:
                 st = c.fn(*c.args)
                 if st:
                     raise FgError(c.label, st)
             if ev:
-                ev[1].record()
+                ev[1].record(s)
+            if i in evs:
+                evs[i].record(s)
+        for j in self.final:
+            streams[0].wait_event(evs[j])
