@@ -59,6 +59,9 @@ def parse():
                     help="time one pass of one layer, e.g. E2b.fwd, or 'copy'")
     ap.add_argument("--summarize-stats", default=None, metavar="CSV")
     ap.add_argument("--summarize-pmc", default=None, metavar="DIR")
+    ap.add_argument("--summarize-trace", nargs=2, default=None, metavar=("CSV", "KERNEL"),
+                    help="durations of KERNEL in a kernel trace of the default bench "
+                         "(6 launches per step; pass the traced run's --steps and --warmup)")
     return ap.parse_args()
 
 
@@ -99,6 +102,24 @@ def summarize_stats(path):
               f"{float(r['TotalDurationNs']) / 1e6:.3f} | {float(r['AverageNs']) / 1e3:.2f} | "
               f"{float(r['Percentage']):.2f} | {float(r['MinNs']) / 1e3:.2f} | "
               f"{float(r['MaxNs']) / 1e3:.2f} |")
+
+
+def summarize_trace(path, kernel, per_step, timed_steps, one_stream_steps):
+    """Launch durations of one kernel from a rocprofv3 kernel trace of the
+    default bench command: all launches, the first per_step *
+    one_stream_steps (warm-up and detail pass, one stream) and the last
+    per_step * timed_steps (the timed region, three streams)."""
+    import csv
+    rows = [r for r in csv.DictReader(open(path))
+            if short_kernel_name(r["Kernel_Name"]) == kernel]
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    dur = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in rows]
+    timed = dur[-per_step * timed_steps:]
+    alone = dur[:per_step * one_stream_steps]
+    print(f"`{kernel}`: {len(dur)} launches, average {sum(dur) / len(dur):.2f} us; "
+          f"one-stream steps (first {one_stream_steps}): {len(alone)} launches, average "
+          f"{sum(alone) / len(alone):.2f} us; timed region (last {timed_steps} steps): "
+          f"{len(timed)} launches, average {sum(timed) / len(timed):.2f} us")
 
 
 def summarize_pmc(d):
@@ -289,6 +310,10 @@ def main():
         return
     if args.summarize_pmc:
         summarize_pmc(args.summarize_pmc)
+        return
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace[0], args.summarize_trace[1], 6, args.steps,
+                        args.warmup + 2)
         return
     if args.op:
         op_bench(args.op, args.steps, args.warmup)
