@@ -61,13 +61,13 @@ struct K {
 };
 // The configurations the library runs, chosen by timing the network's layers:
 // data convolutions take 32-deep stages in a 5-stage ring (160 KiB) with 8
-// waves of 128 x 64; the kernel gradient (whose operand decode needs more
-// registers) 32-deep stages in a 4-stage ring with 16 waves of 64 x 64.
+// waves of 128 x 64; the kernel gradient 32-deep stages in a 4-stage ring
+// (128 KiB) with 8 waves of 128 x 64.
 #ifndef FG_DMA_DATA_CFG
 #define FG_DMA_DATA_CFG 32, 5, 2, 4
 #endif
 #ifndef FG_DMA_WGRAD_CFG
-#define FG_DMA_WGRAD_CFG 32, 4, 4, 4
+#define FG_DMA_WGRAD_CFG 32, 4, 2, 4
 #endif
 using DataRun = K<FG_DMA_DATA_CFG>;
 using WgradRun = K<FG_DMA_WGRAD_CFG>;
@@ -970,75 +970,84 @@ __global__ __launch_bounds__(C::NT) void data_conv_halo_kernel(DataConvArgs a,
 // ---------------------------------------------------------------------------
 // Output tile store of the kernel gradient: rows rho (contiguous in memory
 // for a fixed output channel k), columns k. As for the data convolutions, a
-// wave's 64 x 64 block is staged in LDS k-major (128-byte rows: 64 fp16 or,
-// per pass, 32 fp32 values; 16-byte chunks permuted by the row) and read
-// back so that 8 lanes write one row's contiguous 128 bytes.
+// wave's block is staged in LDS k-major, 64 rows of rho at a time (128-byte
+// rows: 64 fp16 or, per pass, 32 fp32 values; 16-byte chunks permuted by the
+// row), and read back so that 8 lanes write one row's contiguous 128 bytes.
+// Waves 64 rows high stage 8 KiB (two per 16 KiB ring array), waves 128 rows
+// high two halves of 8 KiB in a ring array of their own.
 template <class C, bool SPLIT>
 __device__ __forceinline__ void store_tile_w(f32x16 (&acc)[C::FM][C::FN],
                                              const Ring &R, const WgradArgs &a,
                                              int rsc, int rho0, int k0, int lane,
                                              int wave, int split) {
-  static_assert(C::WM == 64 && C::WN == 64, "store_tile_w expects 64 x 64 waves");
-  // every pair of waves stages in one 16 KiB ring array: arrays 1..NW/2-1
-  // must exist (a.k.a. a[1..NS-1], then b[0..]) and be 16 KiB each
-  static_assert(C::TILE_BYTES == 16384 && C::NW / 2 <= 2 * C::NS,
-                "store_tile_w stages in 16 KiB ring arrays, one per two waves");
+  static_assert((C::WM == 64 || C::WM == 128) && C::WN == 64,
+                "store_tile_w expects waves 64 wide and 64 or 128 high");
+  constexpr int HM = C::WM / 64;   // 64-row halves of the wave's block
+  constexpr int WPA = 2 / HM;      // waves per 16 KiB ring array
+  // the ring arrays 0..NW/WPA-1 (a[0..NS-1], then b[0..]) must exist and be
+  // 16 KiB each
+  static_assert(C::TILE_BYTES == 16384 && C::NW / WPA <= 2 * C::NS,
+                "store_tile_w stages in 16 KiB ring arrays");
   __syncthreads();  // every wave is done reading the ring
-  // 8 KiB per wave: two waves per 16 KiB ring array, by constant indices
   uint8_t *buf = R.a[0];
 #pragma unroll
-  for (int k = 1; k < C::NW / 2; ++k)
-    if ((wave >> 1) == k) buf = k < C::NS ? R.a[k] : R.b[k - C::NS];
-  buf += (wave & 1) * 8192;
+  for (int k = 1; k < C::NW / WPA; ++k)
+    if (wave / WPA == k) buf = k < C::NS ? R.a[k] : R.b[k - C::NS];
+  if (HM == 1) buf += (wave & 1) * 8192;
   constexpr int PASSES = SPLIT ? 2 : 1;
 #pragma unroll
-  for (int pass = 0; pass < PASSES; ++pass) {
+  for (int h = 0; h < HM; ++h) {
+    uint8_t *hb = buf + h * 8192;
 #pragma unroll
-    for (int j = 0; j < C::FN; ++j) {
-      const int kr = j * 32 + (lane & 31);  // row within the block
-      uint8_t *row = buf + kr * 128;
-      const int sw = (kr >> 1) & 7;
+    for (int pass = 0; pass < PASSES; ++pass) {
 #pragma unroll
-      for (int ii = 0; ii < C::FM / PASSES; ++ii) {
-        const int i = pass * (C::FM / PASSES) + ii;
+      for (int j = 0; j < C::FN; ++j) {
+        const int kr = j * 32 + (lane & 31);  // row within the block
+        uint8_t *row = hb + kr * 128;
+        const int sw = (kr >> 1) & 7;
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const f32x16 &c = acc[i][j];
-          if (SPLIT) {
-            const int chunk = 2 * g + (lane >> 5);
-            *reinterpret_cast<f32x4 *>(row + ((chunk ^ sw) << 4)) =
-                f32x4{c[4 * g], c[4 * g + 1], c[4 * g + 2], c[4 * g + 3]};
-          } else {
-            const int chunk = 4 * i + g;
-            *reinterpret_cast<u32x2 *>(row + ((chunk ^ sw) << 4) + 8 * (lane >> 5)) =
-                to_h4(c[4 * g], c[4 * g + 1], c[4 * g + 2], c[4 * g + 3]);
+        for (int ii = 0; ii < 2 / PASSES; ++ii) {
+          const int il = pass * (2 / PASSES) + ii;  // fragment within the half
+          const f32x16 &c = acc[2 * h + il][j];
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            if (SPLIT) {
+              const int chunk = 2 * g + (lane >> 5);
+              *reinterpret_cast<f32x4 *>(row + ((chunk ^ sw) << 4)) =
+                  f32x4{c[4 * g], c[4 * g + 1], c[4 * g + 2], c[4 * g + 3]};
+            } else {
+              const int chunk = 4 * il + g;
+              *reinterpret_cast<u32x2 *>(row + ((chunk ^ sw) << 4) + 8 * (lane >> 5)) =
+                  to_h4(c[4 * g], c[4 * g + 1], c[4 * g + 2], c[4 * g + 3]);
+            }
           }
         }
       }
-    }
-    wait_lds();
-    __builtin_amdgcn_wave_barrier();
-    // 8 lanes per row, 16-byte chunk q
-    const int q = lane & 7;
-    u32x4 d[8];
-#pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      const int kr = 8 * t + (lane >> 3);
-      d[t] = *reinterpret_cast<const u32x4 *>(buf + kr * 128 +
-                                              ((q ^ ((kr >> 1) & 7)) << 4));
-    }
-#pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      const int k = k0 + 8 * t + (lane >> 3);
-      if (SPLIT)
-        *reinterpret_cast<u32x4 *>(a.part + ((size_t)split * a.k + k) * rsc + rho0 +
-                                   pass * 32 + 4 * q) = d[t];
-      else
-        *reinterpret_cast<u32x4 *>(a.dw + (size_t)k * rsc + rho0 + 8 * q) = d[t];
-    }
-    if (pass + 1 < PASSES) {
       wait_lds();
       __builtin_amdgcn_wave_barrier();
+      // 8 lanes per row, 16-byte chunk q
+      const int q = lane & 7;
+      u32x4 d[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const int kr = 8 * t + (lane >> 3);
+        d[t] = *reinterpret_cast<const u32x4 *>(hb + kr * 128 +
+                                                ((q ^ ((kr >> 1) & 7)) << 4));
+      }
+      const int rho = rho0 + 64 * h;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const int k = k0 + 8 * t + (lane >> 3);
+        if (SPLIT)
+          *reinterpret_cast<u32x4 *>(a.part + ((size_t)split * a.k + k) * rsc + rho +
+                                     pass * 32 + 4 * q) = d[t];
+        else
+          *reinterpret_cast<u32x4 *>(a.dw + (size_t)k * rsc + rho + 8 * q) = d[t];
+      }
+      if (pass + 1 < PASSES || h + 1 < HM) {
+        wait_lds();
+        __builtin_amdgcn_wave_barrier();
+      }
     }
   }
 }
@@ -1072,42 +1081,69 @@ __global__ __launch_bounds__(C::NT) void wgrad_dma_kernel(WgradArgs a, WgradDiv 
   const __amdgpu_buffer_rsrc_t rs_dy = __builtin_amdgcn_make_buffer_rsrc(
       (void *)a.dy, 0, (int)((size_t)a.mtot * a.k * 2), kRsrcFlags);
 
-  // this lane's reduction rows: m = mbeg + BK * st + krow, decoded into
-  // (n, p, q) with multiply-shift division (no loops, no branches)
+  // This lane's reduction row m = mbeg + BK * st + krow is decoded into
+  // (n, p, q) once, with multiply-shift division; each stage then advances
+  // it by BK rows with adds and at most one carry into p and one into n
+  // (BK = dq + Q * (dp + P * dn) with dq < Q, dp < P), tracking the input
+  // position (hh, ww) and the byte offsets of both operands directly.
+  // Integer multiplies run at a quarter of the VALU rate: a division per
+  // stage cost more VALU time than the stage's MFMAs leave free.
   const MnSlot<C> sl = mn_slots<C>(wave, lane);
-  int mrow[PW], xcol[PW], dcol[PW];
+  const int h0 = tr - a.ph, w0 = ts - a.pw;
+  const int pixb = a.c * 2, rowb = a.w * pixb, imgb = a.h * rowb;
+  int hh[PW], ww[PW], ox[PW], od[PW];
 #pragma unroll
   for (int jj = 0; jj < PW; ++jj) {
-    mrow[jj] = mbeg + sl.krow[jj];
-    xcol[jj] = c0 + sl.ncol[jj];
-    dcol[jj] = n0 + sl.ncol[jj];
+    const int m = mbeg + sl.krow[jj];
+    const unsigned nn = fd.pq.div((unsigned)m);
+    const unsigned rem = (unsigned)m - nn * (unsigned)(a.p * a.q);
+    const unsigned pp = fd.q.div(rem);
+    const int qq = (int)(rem - pp * (unsigned)a.q);
+    hh[jj] = (int)pp * a.sh + h0;
+    ww[jj] = qq * a.sw + w0;
+    ox[jj] = (int)nn * imgb + hh[jj] * rowb + ww[jj] * pixb + (c0 + sl.ncol[jj]) * 2;
+    od[jj] = (m * a.k + n0 + sl.ncol[jj]) * 2;
   }
-  const int h0 = tr - a.ph, w0 = ts - a.pw;
+  const int dq = C::BK % a.q, dpt = C::BK / a.q, dp = dpt % a.p, dn = dpt / a.p;
+  const int inc_w = dq * a.sw, inc_h = dp * a.sh;
+  const int inc_o = inc_w * pixb + inc_h * rowb + dn * imgb;
+  const int wlim = a.q * a.sw + w0, hlim = a.p * a.sh + h0;
+  const int wrap_o = a.sh * rowb - a.q * a.sw * pixb;  // q wraps into p
+  const int hwrap_o = imgb - a.p * a.sh * rowb;         // p wraps into n
+  const int inc_d = C::BK * a.k * 2;
+  const int mleft = mend - mbeg;
 
-  auto issue = [&](int, int slot) __attribute__((always_inline)) {
+  auto issue = [&](int st, int slot) __attribute__((always_inline)) {
     uint8_t *ta = R.a[slot], *tb = R.b[slot];
 #pragma unroll
     for (int jj = 0; jj < PW; ++jj) {
-      const int m = mrow[jj];
-      const unsigned nn = fd.pq.div((unsigned)m);
-      const unsigned rem = (unsigned)m - nn * (unsigned)(a.p * a.q);
-      const unsigned pp = fd.q.div(rem);
-      const int qq = (int)(rem - pp * (unsigned)a.q);
-      const int hh = (int)pp * a.sh + h0, ww = qq * a.sw + w0;
-      const bool mv = m < mend;
-      const bool v = mv && (unsigned)hh < (unsigned)a.h && (unsigned)ww < (unsigned)a.w;
-      const unsigned ox = (unsigned)((((int)nn * a.h + hh) * a.w + ww) * a.c + xcol[jj]) * 2u;
-      dma16(rs_x, ta + dma_dst<C>(wave, jj), v ? ox : kOOB);
-      const unsigned od = (unsigned)(m * a.k + dcol[jj]) * 2u;
-      dma16(rs_dy, tb + dma_dst<C>(wave, jj), mv ? od : kOOB);
-      mrow[jj] = m + C::BK;
+      // row krow = RPI (PW wave + jj) + lane / (RB / 16) of stage st exists
+      const bool mv = (int)(lane / (C::RB / 16)) <
+                      mleft - C::BK * st - C::RPI * (C::PW * wave + jj);
+      const bool v = mv && (unsigned)hh[jj] < (unsigned)a.h &&
+                     (unsigned)ww[jj] < (unsigned)a.w;
+      dma16(rs_x, ta + dma_dst<C>(wave, jj), v ? (unsigned)ox[jj] : kOOB);
+      dma16(rs_dy, tb + dma_dst<C>(wave, jj), mv ? (unsigned)od[jj] : kOOB);
+      od[jj] += inc_d;
+      ww[jj] += inc_w;
+      hh[jj] += inc_h;
+      ox[jj] += inc_o;
+      if (ww[jj] >= wlim) {
+        ww[jj] -= a.q * a.sw;
+        hh[jj] += a.sh;
+        ox[jj] += wrap_o;
+      }
+      if (hh[jj] >= hlim) {
+        hh[jj] -= a.p * a.sh;
+        ox[jj] += hwrap_o;
+      }
     }
   };
 
   f32x16 acc[C::FM][C::FN];
   zero<C>(acc);
   pipeline<C, false, false>(acc, R, nst, wm0, wn0, lane, issue);
-  if constexpr (C::WM == 64 && C::WN == 64) {
+  if constexpr ((C::WM == 64 || C::WM == 128) && C::WN == 64) {
     store_tile_w<C, SPLIT>(acc, R, a, rsc, m0 + wm0, n0 + wn0, lane, wave, split);
   } else {
     // direct: each lane writes 4 consecutive rho of one output channel k
