@@ -55,6 +55,9 @@ def parse():
     ap.add_argument("--streams", type=int, default=3, choices=(1, 3),
                     help="streams of the timed step (3: kernel gradients and the "
                          "gradient path beside the input-gradient chain)")
+    ap.add_argument("--zero-copy", action="store_true",
+                    help="kernel gradients write into their group slots (no pack; "
+                         "the non-finite check fused into their store)")
     ap.add_argument("--op", default=None,
                     help="time one pass of one layer, e.g. E2b.fwd, or 'copy'")
     ap.add_argument("--summarize-stats", default=None, metavar="CSV")
@@ -330,7 +333,7 @@ def main():
     wl = synth.fcn()
     layers = wl.layers
     ch = Chain(layers, wl.weights, wl.x, loss_scale=synth.LOSS_SCALE,
-               group_cap_bytes=synth.GROUP_CAP_BYTES)
+               group_cap_bytes=synth.GROUP_CAP_BYTES, zero_copy=args.zero_copy)
     target = torch.from_numpy(wl.target).cuda()
     # per-call accounting on one stream, where a call's duration is its own
     prog = ch.program(target, streams=1)
@@ -438,7 +441,7 @@ def main():
                                "13 layers (99,483,904 weights), L2 head, loss scale 2^15, "
                                "25 MiB gradient groups (9)",
                    "global_batch": 4, "conv_tflop_per_step": round(flops_step / 1e12, 4),
-                   "streams": args.streams},
+                   "streams": args.streams, "zero_copy_groups": args.zero_copy},
         "mfma_peak_frac": round(value / MFMA_F16_PEAK_TFLOPS, 4),
         "conv_kernels_tflops": round(flops_step / (conv_ms * 1e-3) / 1e12, 2),
         "grad_pack_GBps": bw("copy_pieces_kernel<2>"),

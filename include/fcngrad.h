@@ -142,6 +142,21 @@ fg_status conv2d_bwd_weight(const fg_conv_desc *d, const uint16_t *x,
                             const uint16_t *dy, uint16_t *dw_krsc, void *ws,
                             size_t ws_bytes, hipStream_t stream);
 
+/* Kernel gradient straight into a gradient group (zero-copy fusion buffer,
+ * Section 4.2 Grouping, with the non-finite check of Section 6.2 loss
+ * scaling fused into its store). Computes exactly what conv2d_bwd_weight
+ * computes, same arguments and errors, and in addition sets
+ * *found_nonfinite (device int32) to 1 if any fp16 element written to
+ * dw_krsc is +-inf or NaN; it never clears it. dw_krsc may point into a
+ * group buffer at a member's element offset (16-byte aligned, as
+ * grad_group_plan's 256-byte alignment guarantees), which makes that
+ * member's grad_group_pack unnecessary. found_nonfinite must not be null
+ * (FG_EINVAL) and must not overlap x, dy, dw_krsc or ws. */
+fg_status conv2d_bwd_weight_checked(const fg_conv_desc *d, const uint16_t *x,
+                                    const uint16_t *dy, uint16_t *dw_krsc,
+                                    int32_t *found_nonfinite, void *ws,
+                                    size_t ws_bytes, hipStream_t stream);
+
 /* Transposed convolution (decoder upsampling):
  * y[n,o,u,k] = epi(sum over c and the taps (r,s) with o + ph - r = i*sh and
  * u + pw - s = j*sw for an input position (i,j), of x[n,i,j,c] *

@@ -20,7 +20,7 @@ MAX_SEGMENTS = 64
 
 ENTRY_POINTS = (
     "conv2d_fwd", "conv2d_bwd_data", "conv2d_bwd_weight",
-    "conv_transpose2d_fwd", "grad_group_pack", "grad_unscale_check",
+    "conv2d_bwd_weight_checked", "conv_transpose2d_fwd", "grad_group_pack", "grad_unscale_check",
     "grad_group_unpack", "l2_head_grad", "relu_backward",
     "fg_conv_workspace_bytes", "fg_conv_out_dims", "grad_group_plan",
     "fg_conv_kernel_name", "fg_status_string",
@@ -72,6 +72,7 @@ def lib():
         "conv2d_fwd": [pdesc, vp, vp, vp, i32, vp, vp, sz, vp],
         "conv2d_bwd_data": [pdesc, vp, vp, vp, i32, vp, vp, sz, vp],
         "conv2d_bwd_weight": [pdesc, vp, vp, vp, vp, sz, vp],
+        "conv2d_bwd_weight_checked": [pdesc, vp, vp, vp, vp, vp, sz, vp],
         "conv_transpose2d_fwd": [pdesc, vp, vp, vp, i32, vp, vp, sz, vp],
         "grad_group_pack": [pseg, i32, vp, u64, vp],
         "grad_unscale_check": [vp, u64, ctypes.c_float, vp, vp, vp],
@@ -163,6 +164,17 @@ def conv2d_bwd_weight(desc, x, dy, dw, ws=None, stream=None):
     wp, wb = _ws(ws)
     _check("conv2d_bwd_weight", lib().conv2d_bwd_weight(
         ctypes.byref(desc), _p(x), _p(dy), _p(dw), wp, wb, _s(stream)))
+
+
+def conv2d_bwd_weight_checked(desc, x, dy, dw, found_nonfinite, ws=None,
+                              stream=None):
+    """conv2d_bwd_weight that also sets the device int32 found_nonfinite to 1
+    if a written dW element is +-inf or NaN; dw may be a view into a group
+    buffer (zero-copy pack)."""
+    wp, wb = _ws(ws)
+    _check("conv2d_bwd_weight_checked", lib().conv2d_bwd_weight_checked(
+        ctypes.byref(desc), _p(x), _p(dy), _p(dw), _p(found_nonfinite), wp, wb,
+        _s(stream)))
 
 
 def conv_transpose2d_fwd(desc, x, w, y, epi=EPI_NONE, gate=None, ws=None,

@@ -392,9 +392,10 @@ fg_status conv_transpose2d_fwd(const fg_conv_desc *d, const uint16_t *x,
   return launch_status(launch_data_conv(a, false, stream));
 }
 
-fg_status conv2d_bwd_weight(const fg_conv_desc *d, const uint16_t *x,
-                            const uint16_t *dy, uint16_t *dw_krsc, void *ws,
-                            size_t ws_bytes, hipStream_t stream) {
+static fg_status bwd_weight(const fg_conv_desc *d, const uint16_t *x,
+                            const uint16_t *dy, uint16_t *dw_krsc,
+                            int32_t *found_nonfinite, void *ws, size_t ws_bytes,
+                            hipStream_t stream) {
   fg_status st = check_desc(d);
   if (st != FG_OK) return st;
   if (!x || !dy || !dw_krsc) return FG_EINVAL;
@@ -407,6 +408,12 @@ fg_status conv2d_bwd_weight(const fg_conv_desc *d, const uint16_t *x,
   if (overlap(dw_krsc, nw * 2, x, nx * 2) ||
       overlap(dw_krsc, nw * 2, dy, ny * 2))
     return FG_EINVAL;
+  if (found_nonfinite &&
+      (overlap(found_nonfinite, 4, dw_krsc, nw * 2) ||
+       overlap(found_nonfinite, 4, x, nx * 2) ||
+       overlap(found_nonfinite, 4, dy, ny * 2) ||
+       overlap(found_nonfinite, 4, ws, ws_bytes)))
+    return FG_EINVAL;
   if ((st = check_conv_support(d)) != FG_OK) return st;
   if ((st = check_ws(d, FG_OP_BWD_WEIGHT, ws, ws_bytes, x, nx * 2, dy, ny * 2,
                      dw_krsc, nw * 2, nullptr, 0)) != FG_OK)
@@ -415,7 +422,7 @@ fg_status conv2d_bwd_weight(const fg_conv_desc *d, const uint16_t *x,
   if (d->k == 1)
     return launch_status(launch_head_wgrad(x, dy, dw_krsc,
                                            (int64_t)d->n * d->h * d->w, d->c,
-                                           (float *)ws, stream));
+                                           (float *)ws, found_nonfinite, stream));
   WgradPlan pl = plan_wgrad(*d, P, Q);
   WgradArgs a;
   memset(&a, 0, sizeof(a));
@@ -429,7 +436,22 @@ fg_status conv2d_bwd_weight(const fg_conv_desc *d, const uint16_t *x,
   a.mtot = d->n * P * Q;
   a.mchunk = pl.mchunk;
   a.nsplit = pl.nsplit;
+  a.flag = found_nonfinite;
   return launch_status(launch_wgrad(a, pl.big, stream));
+}
+
+fg_status conv2d_bwd_weight(const fg_conv_desc *d, const uint16_t *x,
+                            const uint16_t *dy, uint16_t *dw_krsc, void *ws,
+                            size_t ws_bytes, hipStream_t stream) {
+  return bwd_weight(d, x, dy, dw_krsc, nullptr, ws, ws_bytes, stream);
+}
+
+fg_status conv2d_bwd_weight_checked(const fg_conv_desc *d, const uint16_t *x,
+                                    const uint16_t *dy, uint16_t *dw_krsc,
+                                    int32_t *found_nonfinite, void *ws,
+                                    size_t ws_bytes, hipStream_t stream) {
+  if (!found_nonfinite) return FG_EINVAL;
+  return bwd_weight(d, x, dy, dw_krsc, found_nonfinite, ws, ws_bytes, stream);
 }
 
 // ---------------------------------------------------------------------------

@@ -43,4 +43,16 @@ __device__ __forceinline__ uint32_t pack_hi(uint32_t a, uint32_t b) {
   return (a >> 16) | (b & 0xFFFF0000u);
 }
 
+// True if either fp16 value packed in w is +-inf or NaN (exponent all ones).
+__device__ __forceinline__ bool nonfinite_h2(uint32_t w) {
+  return ((w & 0x7C00u) == 0x7C00u) | ((w & 0x7C000000u) == 0x7C000000u);
+}
+
+// *flag = 1 from one lane of each wave in which some lane has `bad` (a plain
+// store of the same value: no atomics needed). One-dimensional workgroups.
+__device__ __forceinline__ void flag_nonfinite(int32_t *flag, bool bad) {
+  const unsigned long long b = __ballot(bad);
+  if (b != 0 && (threadIdx.x & 63) == (unsigned)__builtin_ctzll(b)) *flag = 1;
+}
+
 }  // namespace fg

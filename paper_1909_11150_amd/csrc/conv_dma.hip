@@ -995,6 +995,7 @@ __device__ __forceinline__ void store_tile_w(f32x16 (&acc)[C::FM][C::FN],
     if (wave / WPA == k) buf = k < C::NS ? R.a[k] : R.b[k - C::NS];
   if (HM == 1) buf += (wave & 1) * 8192;
   constexpr int PASSES = SPLIT ? 2 : 1;
+  bool bad = false;  // an fp16 result is +-inf or NaN
 #pragma unroll
   for (int h = 0; h < HM; ++h) {
     uint8_t *hb = buf + h * 8192;
@@ -1038,11 +1039,14 @@ __device__ __forceinline__ void store_tile_w(f32x16 (&acc)[C::FM][C::FN],
 #pragma unroll
       for (int t = 0; t < 8; ++t) {
         const int k = k0 + 8 * t + (lane >> 3);
-        if (SPLIT)
+        if (SPLIT) {
           *reinterpret_cast<u32x4 *>(a.part + ((size_t)split * a.k + k) * rsc + rho +
                                      pass * 32 + 4 * q) = d[t];
-        else
+        } else {
+#pragma unroll
+          for (int w = 0; w < 4; ++w) bad |= nonfinite_h2(d[t][w]);
           *reinterpret_cast<u32x4 *>(a.dw + (size_t)k * rsc + rho + 8 * q) = d[t];
+        }
       }
       if (pass + 1 < PASSES || h + 1 < HM) {
         wait_lds();
@@ -1050,6 +1054,7 @@ __device__ __forceinline__ void store_tile_w(f32x16 (&acc)[C::FM][C::FN],
       }
     }
   }
+  if (!SPLIT && a.flag) flag_nonfinite(a.flag, bad);
 }
 
 // ---------------------------------------------------------------------------
@@ -1147,6 +1152,7 @@ __global__ __launch_bounds__(C::NT) void wgrad_dma_kernel(WgradArgs a, WgradDiv 
     store_tile_w<C, SPLIT>(acc, R, a, rsc, m0 + wm0, n0 + wn0, lane, wave, split);
   } else {
     // direct: each lane writes 4 consecutive rho of one output channel k
+    bool bad = false;
 #pragma unroll
     for (int j = 0; j < C::FN; ++j) {
       const int k = n0 + wn0 + j * 32 + (lane & 31);
@@ -1156,15 +1162,18 @@ __global__ __launch_bounds__(C::NT) void wgrad_dma_kernel(WgradArgs a, WgradDiv 
         for (int g = 0; g < 4; ++g) {
           const int rho = m0 + wm0 + i * 32 + 8 * g + 4 * (lane >> 5);
           const f32x16 &c = acc[i][j];
-          if (!SPLIT)
-            *reinterpret_cast<u32x2 *>(a.dw + (size_t)k * rsc + rho) =
-                to_h4(c[4 * g], c[4 * g + 1], c[4 * g + 2], c[4 * g + 3]);
-          else
+          if (!SPLIT) {
+            const u32x2 hv = to_h4(c[4 * g], c[4 * g + 1], c[4 * g + 2], c[4 * g + 3]);
+            bad |= nonfinite_h2(hv[0]) | nonfinite_h2(hv[1]);
+            *reinterpret_cast<u32x2 *>(a.dw + (size_t)k * rsc + rho) = hv;
+          } else {
             *reinterpret_cast<f32x4 *>(a.part + ((size_t)split * a.k + k) * rsc +
                                        rho) =
                 f32x4{c[4 * g], c[4 * g + 1], c[4 * g + 2], c[4 * g + 3]};
+          }
         }
     }
+    if (!SPLIT && a.flag) flag_nonfinite(a.flag, bad);
   }
 }
 

@@ -465,6 +465,7 @@ __global__ __launch_bounds__(C::NT) void wgrad_kernel(WgradArgs a) {
   }
 
   constexpr int FM = C::FM, FN = C::FN;
+  bool bad = false;
 #pragma unroll
   for (int j = 0; j < FN; ++j) {
     int k = n0 + wn0 + j * 32 + (lane & 31);
@@ -477,8 +478,9 @@ __global__ __launch_bounds__(C::NT) void wgrad_kernel(WgradArgs a) {
         if (rho >= rsc) continue;
         const f32x16 &c = core.acc[i][j];
         if (!SPLIT) {
-          *reinterpret_cast<u32x2 *>(a.dw + (size_t)k * rsc + rho) =
-              to_h4(c[4 * g], c[4 * g + 1], c[4 * g + 2], c[4 * g + 3]);
+          const u32x2 h = to_h4(c[4 * g], c[4 * g + 1], c[4 * g + 2], c[4 * g + 3]);
+          bad |= nonfinite_h2(h[0]) | nonfinite_h2(h[1]);
+          *reinterpret_cast<u32x2 *>(a.dw + (size_t)k * rsc + rho) = h;
         } else {
           f32x4 o = {c[4 * g], c[4 * g + 1], c[4 * g + 2], c[4 * g + 3]};
           *reinterpret_cast<f32x4 *>(
@@ -486,30 +488,38 @@ __global__ __launch_bounds__(C::NT) void wgrad_kernel(WgradArgs a) {
         }
       }
   }
+  if (!SPLIT && a.flag) flag_nonfinite(a.flag, bad);
 }
 
 // Sum nsplit fp32 partial arrays of len elements in split order, round to
-// fp16. len is a multiple of 4.
+// fp16. len is a multiple of 4. flag (or null): set to 1 if a result is
+// +-inf or NaN.
 __global__ __launch_bounds__(256) void split_reduce_kernel(const float *part,
                                                            int nsplit,
                                                            int64_t len,
-                                                           uint16_t *out) {
+                                                           uint16_t *out,
+                                                           int32_t *flag) {
   int64_t i4 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
-  if (i4 >= len) return;
-  f32x4 s = *reinterpret_cast<const f32x4 *>(part + i4);
-  for (int k = 1; k < nsplit; ++k) {
-    f32x4 v = *reinterpret_cast<const f32x4 *>(part + (size_t)k * len + i4);
+  bool bad = false;
+  if (i4 < len) {
+    f32x4 s = *reinterpret_cast<const f32x4 *>(part + i4);
+    for (int k = 1; k < nsplit; ++k) {
+      f32x4 v = *reinterpret_cast<const f32x4 *>(part + (size_t)k * len + i4);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) s[e] += v[e];
+      for (int e = 0; e < 4; ++e) s[e] += v[e];
+    }
+    const u32x2 h = to_h4(s[0], s[1], s[2], s[3]);
+    bad = nonfinite_h2(h[0]) | nonfinite_h2(h[1]);
+    *reinterpret_cast<u32x2 *>(out + i4) = h;
   }
-  *reinterpret_cast<u32x2 *>(out + i4) = to_h4(s[0], s[1], s[2], s[3]);
+  if (flag) flag_nonfinite(flag, bad);
 }
 
 // Same sum when the partials are many and short (nsplit large, len small):
 // one workgroup per 4 outputs; thread t adds splits t, t+256, ... in order,
 // then a fixed-shape tree in LDS combines the 256 thread sums.
 __global__ __launch_bounds__(256) void split_reduce_wide_kernel(
-    const float *part, int nsplit, int64_t len, uint16_t *out) {
+    const float *part, int nsplit, int64_t len, uint16_t *out, int32_t *flag) {
   __shared__ f32x4 red[256];
   const int64_t i4 = (int64_t)blockIdx.x * 4;
   f32x4 s = {0.f, 0.f, 0.f, 0.f};
@@ -531,7 +541,9 @@ __global__ __launch_bounds__(256) void split_reduce_wide_kernel(
   }
   if (threadIdx.x == 0) {
     f32x4 t = red[0];
-    *reinterpret_cast<u32x2 *>(out + i4) = to_h4(t[0], t[1], t[2], t[3]);
+    const u32x2 h = to_h4(t[0], t[1], t[2], t[3]);
+    *reinterpret_cast<u32x2 *>(out + i4) = h;
+    if (flag && (nonfinite_h2(h[0]) | nonfinite_h2(h[1]))) *flag = 1;
   }
 }
 
@@ -918,7 +930,7 @@ hipError_t launch_wgrad(const WgradArgs &a, bool big, hipStream_t st) {
   const int64_t len = (int64_t)a.k * rsc;
   dim3 g2((unsigned)((len / 4 + 255) / 256));
   hipLaunchKernelGGL(split_reduce_kernel, g2, dim3(256), 0, st, a.part,
-                     a.nsplit, len, a.dw);
+                     a.nsplit, len, a.dw, a.flag);
   return hipGetLastError();
 }
 
@@ -967,7 +979,7 @@ size_t head_wgrad_ws_bytes(const fg_conv_desc &d) {
 
 hipError_t launch_head_wgrad(const uint16_t *x, const uint16_t *dy,
                              uint16_t *dw, int64_t npix, int32_t c, float *ws,
-                             hipStream_t st) {
+                             int32_t *flag, hipStream_t st) {
   int64_t nb = head_wgrad_blocks(npix);
   int64_t chunk = (npix + nb - 1) / nb;
   hipLaunchKernelGGL(head_wgrad_kernel, dim3((unsigned)nb),
@@ -976,7 +988,7 @@ hipError_t launch_head_wgrad(const uint16_t *x, const uint16_t *dy,
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(split_reduce_wide_kernel, dim3((unsigned)(c / 4)),
-                     dim3(256), 0, st, ws, (int)nb, (int64_t)c, dw);
+                     dim3(256), 0, st, ws, (int)nb, (int64_t)c, dw, flag);
   return hipGetLastError();
 }
 

@@ -64,6 +64,7 @@ struct WgradArgs {
   int32_t mtot;          // n*p*q
   int32_t mchunk;        // reduction rows per split, multiple of 64
   int32_t nsplit;
+  int32_t *flag;         // set to 1 if an fp16 dW value is +-inf/NaN, or null
 };
 
 // Kernel selection for a shape; pure host logic, shared by the workspace
@@ -105,7 +106,7 @@ hipError_t launch_head_bwd_data(const uint16_t *dy, const uint16_t *w,
                                 hipStream_t st);
 hipError_t launch_head_wgrad(const uint16_t *x, const uint16_t *dy,
                              uint16_t *dw, int64_t npix, int32_t c,
-                             float *ws, hipStream_t st);
+                             float *ws, int32_t *flag, hipStream_t st);
 
 hipError_t launch_pack(const fg_segment *segs, int32_t nseg, uint16_t *group,
                        uint64_t group_numel, hipStream_t st);

@@ -18,7 +18,8 @@ import torch
 
 from . import (EPI_GATE, EPI_NONE, EPI_RELU, OP_BWD_DATA, OP_BWD_WEIGHT,
                OP_CONVT, OP_FWD, ConvDesc, FgError, Segment, kernel_name, lib,
-               conv2d_bwd_data, conv2d_bwd_weight, conv2d_fwd,
+               conv2d_bwd_data, conv2d_bwd_weight, conv2d_bwd_weight_checked,
+               conv2d_fwd,
                conv_transpose2d_fwd, grad_group_pack, grad_group_plan,
                grad_group_unpack, grad_unscale_check, l2_head_grad,
                relu_backward, workspace_bytes)
@@ -66,8 +67,14 @@ def chain_workspace_bytes(layers):
 
 class Chain:
     def __init__(self, layers, weights, x, device="cuda", loss_scale=2.0 ** 15,
-                 group_cap_bytes=None, group_align_bytes=256, stream=None):
+                 group_cap_bytes=None, group_align_bytes=256, stream=None,
+                 zero_copy=False):
+        """zero_copy (with groups): each layer's fp16 dW lives in its slot of
+        its group buffer, written there by conv2d_bwd_weight_checked (which
+        also raises the group's non-finite flag), so no pack is needed; the
+        gaps between slots are zeroed once here."""
         self.layers = list(layers)
+        self.zero_copy = bool(zero_copy)
         self.dev = torch.device(device)
         self.stream = stream
         self.loss_scale = float(loss_scale)
@@ -101,8 +108,16 @@ class Chain:
             groups.append({"members": [m for m, _ in mem],
                            "offsets": [o for _, o in mem], "numel": n})
         self.groups = groups
-        self.gbuf16 = [torch.empty(g["numel"], dtype=F16, device=self.dev)
+        alloc = torch.zeros if self.zero_copy else torch.empty
+        self.gbuf16 = [alloc(g["numel"], dtype=F16, device=self.dev)
                        for g in groups]
+        if self.zero_copy:  # dW tensors become views of their group slots
+            for gi, g in enumerate(groups):
+                for m, off in zip(g["members"], g["offsets"]):
+                    n = self.dw[m].numel()
+                    self.dw[m] = self.gbuf16[gi][off:off + n].view(self.dw[m].shape)
+        # group of each layer's dW
+        self._group_of = {m: gi for gi, g in enumerate(groups) for m in g["members"]}
         self.gbuf32 = [torch.empty(g["numel"], dtype=torch.float32, device=self.dev)
                        for g in groups]
         self.flags = torch.zeros(len(groups), dtype=torch.int32, device=self.dev)
@@ -113,8 +128,9 @@ class Chain:
 
     def run_group(self, gi):
         g = self.groups[gi]
-        grad_group_pack([self.dw[m] for m in g["members"]], g["offsets"],
-                        self.gbuf16[gi], stream=self.stream)
+        if not self.zero_copy:
+            grad_group_pack([self.dw[m] for m in g["members"]], g["offsets"],
+                            self.gbuf16[gi], stream=self.stream)
         grad_unscale_check(self.gbuf16[gi], 1.0 / self.loss_scale,
                            self.gbuf32[gi], self.flags[gi:gi + 1],
                            stream=self.stream)
@@ -149,7 +165,17 @@ class Chain:
         else:
             self.g[-1].copy_(dy)
 
+    def _bwd_weight(self, d, x, dy, i):
+        if self.zero_copy and self.groups is not None:
+            gi = self._group_of[i]
+            conv2d_bwd_weight_checked(d, x, dy, self.dw[i], self.flags[gi:gi + 1],
+                                      self.ws, stream=self.stream)
+        else:
+            conv2d_bwd_weight(d, x, dy, self.dw[i], self.ws, stream=self.stream)
+
     def backward(self, grad_path=False):
+        if self.zero_copy and self.groups is not None:
+            self.flags.zero_()
         for i in reversed(range(len(self.layers))):
             L = self.layers[i]
             dy = self.g[i + 1]
@@ -158,13 +184,11 @@ class Chain:
             gt = self.acts[i] if gate else None
             if L.kind == "conv":
                 d = fwd_desc(L)
-                conv2d_bwd_weight(d, self.acts[i], dy, self.dw[i], self.ws,
-                                  stream=self.stream)
+                self._bwd_weight(d, self.acts[i], dy, i)
                 conv2d_bwd_data(d, dy, self.w[i], self.g[i], epi, gt,
                                 ws=self.ws, stream=self.stream)
             else:
-                conv2d_bwd_weight(convt_dw_desc(L), dy, self.acts[i], self.dw[i],
-                                  self.ws, stream=self.stream)
+                self._bwd_weight(convt_dw_desc(L), dy, self.acts[i], i)
                 conv2d_fwd(convt_dx_desc(L), dy, self.w[i], self.g[i], epi, gt,
                            ws=self.ws, stream=self.stream)
             if grad_path and self.groups is not None and i in self._group_done_at:
@@ -288,7 +312,24 @@ class StepProgram:
                           (ptr(y), ptr(target), y.numel(),
                            2.0 * ch.loss_scale / y.numel(), ptr(ch.g[-1]), st)))
         writer = {nl: len(calls) - 1}  # call that writes g[i]
-        calls.append(Call("flags.zero", "", 0, None, (ch.flags.zero_,), False, sid=2))
+        # the non-finite flags are raised by the unscale calls (stream 2) and,
+        # with zero-copy groups, by the kernel gradients (stream 1)
+        calls.append(Call("flags.zero", "", 0, None, (ch.flags.zero_,), False,
+                          sid=1 if ch.zero_copy else 2))
+        zc = ch.zero_copy
+
+        def dw_call(label, kname, flops, d, x, dy, i):
+            if zc:
+                gi = ch._group_of[i]
+                flag = ch.flags[gi:gi + 1]
+                self._keep.append(flag)
+                return Call(label, kname, flops, L_.conv2d_bwd_weight_checked,
+                            (desc(d), ptr(x), ptr(dy), ptr(ch.dw[i]), flag.data_ptr(),
+                             ws2, wsb2, st), one(d, OP_BWD_WEIGHT),
+                            sid=1, deps=(writer[i + 1],))
+            return Call(label, kname, flops, L_.conv2d_bwd_weight,
+                        (desc(d), ptr(x), ptr(dy), ptr(ch.dw[i]), ws2, wsb2, st),
+                        one(d, OP_BWD_WEIGHT), sid=1, deps=(writer[i + 1],))
         last_dw = {}
         for i in reversed(range(nl)):
             L = ch.layers[i]
@@ -298,11 +339,8 @@ class StepProgram:
             gt = ptr(ch.acts[i]) if gate else None
             if L.kind == "conv":
                 d = fwd_desc(L)
-                calls.append(Call(f"{L.name}.dW", kernel_name(d, OP_BWD_WEIGHT),
-                                  L.flops, L_.conv2d_bwd_weight,
-                                  (desc(d), ptr(ch.acts[i]), ptr(dy), ptr(ch.dw[i]),
-                                   ws2, wsb2, st), one(d, OP_BWD_WEIGHT),
-                                  sid=1, deps=(writer[i + 1],)))
+                calls.append(dw_call(f"{L.name}.dW", kernel_name(d, OP_BWD_WEIGHT),
+                                     L.flops, d, ch.acts[i], dy, i))
                 last_dw[i] = len(calls) - 1
                 calls.append(Call(f"{L.name}.dx", kernel_name(d, OP_BWD_DATA),
                                   L.flops, L_.conv2d_bwd_data,
@@ -310,11 +348,8 @@ class StepProgram:
                                    gt, ws, wsb, st), one(d, OP_BWD_DATA)))
             else:
                 d = convt_dx_desc(L)
-                calls.append(Call(f"{L.name}.dW", kernel_name(d, OP_BWD_WEIGHT),
-                                  L.flops, L_.conv2d_bwd_weight,
-                                  (desc(d), ptr(dy), ptr(ch.acts[i]), ptr(ch.dw[i]),
-                                   ws2, wsb2, st), one(d, OP_BWD_WEIGHT),
-                                  sid=1, deps=(writer[i + 1],)))
+                calls.append(dw_call(f"{L.name}.dW", kernel_name(d, OP_BWD_WEIGHT),
+                                     L.flops, d, dy, ch.acts[i], i))
                 last_dw[i] = len(calls) - 1
                 calls.append(Call(f"{L.name}.dx", kernel_name(d, OP_FWD), L.flops,
                                   L_.conv2d_fwd,
@@ -350,9 +385,10 @@ class StepProgram:
         g16, g32 = ch.gbuf16[gi], ch.gbuf32[gi]
         flag = ch.flags[gi:gi + 1]
         self._keep.append(flag)
-        return [
+        pack = [] if ch.zero_copy else [
             Call(f"G{gi}.pack", "copy_pieces_kernel<2>", 4 * n, L_.grad_group_pack,
-                 (src, len(g["members"]), g16.data_ptr(), n, st), sid=2),
+                 (src, len(g["members"]), g16.data_ptr(), n, st), sid=2)]
+        return pack + [
             Call(f"G{gi}.unscale", "unscale_vec_kernel", 6 * n, L_.grad_unscale_check,
                  (g16.data_ptr(), n, 1.0 / ch.loss_scale, g32.data_ptr(),
                   flag.data_ptr(), st), sid=2),

@@ -72,6 +72,15 @@ def test_invalid_arguments_return_einval(L):
     for bad in (_desc(n=0), _desc(c=-8), _desc(r=11, pad=0), _desc(stride=0)):
         assert L.conv2d_fwd(ref(bad), FAKE, FAKE + (1 << 20), FAKE + (1 << 22), 0,
                             None, None, 0, None) == fg.FG_EINVAL
+    # kernel gradient with the non-finite flag: the flag is required and
+    # must not alias dW (x at FAKE, dy at +1 MiB, dW at +4 MiB)
+    x, dy, dw = FAKE, FAKE + (1 << 20), FAKE + (1 << 22)
+    assert L.conv2d_bwd_weight_checked(ref(d), x, dy, dw, None, None, 0,
+                                       None) == fg.FG_EINVAL
+    assert L.conv2d_bwd_weight_checked(ref(d), x, dy, dw, dw + 8, None, 0,
+                                       None) == fg.FG_EINVAL
+    assert L.conv2d_bwd_weight_checked(ref(d), x, dy, dw, x, None, 0,
+                                       None) == fg.FG_EINVAL
     # gradient path
     seg = (fg.Segment * 1)(fg.Segment(FAKE, 10, 0))
     assert L.grad_group_pack(seg, 0, FAKE + 4096, 10, None) == fg.FG_EINVAL
