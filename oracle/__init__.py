@@ -21,6 +21,9 @@ Contents
       with loss scaling).
   chain (module)
       the encoder-decoder forward and backward passes built from the above.
+  optim (module)
+      the layer-wise adaptive Adam update and the loss-scale backoff that
+      consume the unpacked fp32 gradients (Section 6.2).
 """
 import ctypes
 import os
