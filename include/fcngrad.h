@@ -218,6 +218,45 @@ fg_status relu_backward(const uint16_t *dy, const uint16_t *act,
 /* Workspace in bytes that the given pass needs for this shape (0 if none). */
 size_t fg_conv_workspace_bytes(const fg_conv_desc *d, int op);
 
+/* ---- optimizer (Section 6.2: layer-wise adaptive rates with Adam) ------ */
+
+/* One layer for lars_adam_update: device addresses of its fp32 master
+ * weights (w32, read and written), fp16 working weights (w16, written), fp32
+ * Adam moments (m, v, read and written) and fp32 unscaled gradient (g, read);
+ * numel elements each (1 .. 2^31 - 1). w32, m, v and g 16-byte aligned, w16
+ * 8-byte aligned; no two arrays of the call may overlap. */
+typedef struct {
+    uint64_t w32, w16, m, v, g;
+    uint64_t numel;
+} fg_opt_tensor;
+
+typedef struct {
+    float lr, beta1, beta2, eps, weight_decay;
+} fg_opt_params;
+
+/* Workspace (bytes, device) lars_adam_update needs for these layers. */
+size_t fg_lars_adam_workspace_bytes(const fg_opt_tensor *t, int32_t ntensors);
+
+/* Layer-wise adaptive Adam step on fp32 master weights. For each layer, with
+ * t = *step_count + 1: g~ = g + weight_decay * w; m = beta1 m + (1-beta1) g~;
+ * v = beta2 v + (1-beta2) g~^2; u = (m / (1-beta1^t)) / (sqrt(v /
+ * (1-beta2^t)) + eps); tau = ||w|| / ||u|| over the layer (1 if either is
+ * 0); w = w - lr * tau * u; w16 = nearest-even fp16 of the new w; then
+ * *step_count = t. If any of the nflags device int32 found_nonfinite flags
+ * (the unscale checks of the step's gradient groups) is non-zero, the step
+ * is skipped on the device: nothing is written and *step_count is kept.
+ * fp32 arithmetic; per-layer norms summed in a fixed order (the result is
+ * deterministic). t: host array of ntensors (1..FG_MAX_SEGMENTS) layers,
+ * read during the call only. FG_EINVAL for null or misaligned pointers,
+ * overlapping arrays, params outside lr >= 0, 0 <= beta < 1, eps >= 0,
+ * weight_decay >= 0, or nflags > 0 with null flags; FG_EWORKSPACE if
+ * ws_bytes is short. */
+fg_status lars_adam_update(const fg_opt_tensor *t, int32_t ntensors,
+                           const fg_opt_params *p,
+                           const int32_t *found_nonfinite, int32_t nflags,
+                           int32_t *step_count, void *ws, size_t ws_bytes,
+                           hipStream_t stream);
+
 /* Output spatial size: transpose = 0 gives the forward P, Q; 1 gives the
  * transposed convolution's output size. FG_EINVAL if it is not positive. */
 fg_status fg_conv_out_dims(const fg_conv_desc *d, int transpose, int32_t *p,

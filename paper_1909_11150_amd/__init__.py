@@ -24,7 +24,22 @@ ENTRY_POINTS = (
     "grad_group_unpack", "l2_head_grad", "relu_backward",
     "fg_conv_workspace_bytes", "fg_conv_out_dims", "grad_group_plan",
     "fg_conv_kernel_name", "fg_status_string",
+    "lars_adam_update", "fg_lars_adam_workspace_bytes",
 )
+
+
+class OptTensor(ctypes.Structure):
+    """fg_opt_tensor: one layer's device arrays for lars_adam_update."""
+    _fields_ = [("w32", ctypes.c_uint64), ("w16", ctypes.c_uint64),
+                ("m", ctypes.c_uint64), ("v", ctypes.c_uint64),
+                ("g", ctypes.c_uint64), ("numel", ctypes.c_uint64)]
+
+
+class OptParams(ctypes.Structure):
+    """fg_opt_params."""
+    _fields_ = [("lr", ctypes.c_float), ("beta1", ctypes.c_float),
+                ("beta2", ctypes.c_float), ("eps", ctypes.c_float),
+                ("weight_decay", ctypes.c_float)]
 
 
 class LibraryNotBuilt(RuntimeError):
@@ -90,6 +105,11 @@ def lib():
         fn = getattr(L, name)
         fn.argtypes = args
         fn.restype = ctypes.c_int
+    L.lars_adam_update.argtypes = [ctypes.POINTER(OptTensor), i32,
+                                   ctypes.POINTER(OptParams), vp, i32, vp, vp, sz, vp]
+    L.lars_adam_update.restype = ctypes.c_int
+    L.fg_lars_adam_workspace_bytes.argtypes = [ctypes.POINTER(OptTensor), i32]
+    L.fg_lars_adam_workspace_bytes.restype = ctypes.c_size_t
     L.fg_conv_workspace_bytes.argtypes = [pdesc, ctypes.c_int]
     L.fg_conv_workspace_bytes.restype = ctypes.c_size_t
     L.fg_conv_kernel_name.argtypes = [pdesc, ctypes.c_int]
@@ -175,6 +195,33 @@ def conv2d_bwd_weight_checked(desc, x, dy, dw, found_nonfinite, ws=None,
     _check("conv2d_bwd_weight_checked", lib().conv2d_bwd_weight_checked(
         ctypes.byref(desc), _p(x), _p(dy), _p(dw), _p(found_nonfinite), wp, wb,
         _s(stream)))
+
+
+def opt_tensors(w32, w16, m, v, g):
+    """fg_opt_tensor array for lists of per-layer torch tensors."""
+    n = len(w32)
+    arr = (OptTensor * n)(*[OptTensor(w32[i].data_ptr(), w16[i].data_ptr(),
+                                      m[i].data_ptr(), v[i].data_ptr(),
+                                      g[i].data_ptr(), w32[i].numel())
+                            for i in range(n)])
+    return arr
+
+
+def lars_adam_workspace_bytes(tensors):
+    return lib().fg_lars_adam_workspace_bytes(tensors, len(tensors))
+
+
+def lars_adam_update(tensors, lr, flags, step_count, ws, beta1=0.9, beta2=0.999,
+                     eps=1e-8, weight_decay=1e-4, stream=None):
+    """Layer-wise adaptive Adam step (see include/fcngrad.h). tensors: from
+    opt_tensors(); flags: device int32 tensor of the step's group flags (or
+    None); step_count: device int32 tensor of one element."""
+    p = OptParams(lr, beta1, beta2, eps, weight_decay)
+    wp, wb = _ws(ws)
+    nf = 0 if flags is None else flags.numel()
+    _check("lars_adam_update", lib().lars_adam_update(
+        tensors, len(tensors), ctypes.byref(p), _p(flags), nf, _p(step_count),
+        wp, wb, _s(stream)))
 
 
 def conv_transpose2d_fwd(desc, x, w, y, epi=EPI_NONE, gate=None, ws=None,

@@ -4,6 +4,8 @@
 // returns without touching the device.
 #include <string.h>
 
+#include <cmath>
+
 #include "internal.h"
 
 using namespace fg;
@@ -518,6 +520,67 @@ fg_status grad_unscale_check(const uint16_t *group, uint64_t numel,
     return FG_EINVAL;
   return launch_status(launch_unscale(group, numel, inv_scale, out_f32,
                                       found_nonfinite, stream));
+}
+
+// ---------------------------------------------------------------------------
+static bool opt_tensors_ok(const fg_opt_tensor *t, int32_t n) {
+  if (!t || n < 1 || n > FG_MAX_SEGMENTS) return false;
+  for (int i = 0; i < n; ++i) {
+    const fg_opt_tensor &a = t[i];
+    if (!a.w32 || !a.w16 || !a.m || !a.v || !a.g) return false;
+    if (a.numel == 0 || a.numel >= 0x7FFFFFFFull) return false;
+    if (((a.w32 | a.m | a.v | a.g) & 15) || (a.w16 & 7)) return false;
+  }
+  // no two arrays of the call overlap
+  for (int i = 0; i < n; ++i) {
+    const uint64_t pi[5] = {t[i].w32, t[i].m, t[i].v, t[i].g, t[i].w16};
+    const size_t bi[5] = {4, 4, 4, 4, 2};
+    for (int j = i; j < n; ++j) {
+      const uint64_t pj[5] = {t[j].w32, t[j].m, t[j].v, t[j].g, t[j].w16};
+      for (int a = 0; a < 5; ++a)
+        for (int b = (i == j ? a + 1 : 0); b < 5; ++b)
+          if (overlap((const void *)pi[a], t[i].numel * bi[a], (const void *)pj[b],
+                      t[j].numel * bi[b]))
+            return false;
+    }
+  }
+  return true;
+}
+
+size_t fg_lars_adam_workspace_bytes(const fg_opt_tensor *t, int32_t ntensors) {
+  if (!opt_tensors_ok(t, ntensors)) return 0;
+  return lars_adam_ws_bytes(t, ntensors);
+}
+
+fg_status lars_adam_update(const fg_opt_tensor *t, int32_t ntensors,
+                           const fg_opt_params *p,
+                           const int32_t *found_nonfinite, int32_t nflags,
+                           int32_t *step_count, void *ws, size_t ws_bytes,
+                           hipStream_t stream) {
+  if (!opt_tensors_ok(t, ntensors) || !p || !step_count) return FG_EINVAL;
+  if (nflags < 0 || (nflags > 0 && !found_nonfinite)) return FG_EINVAL;
+  const bool params_ok = std::isfinite(p->lr) && p->lr >= 0.f &&
+                         std::isfinite(p->beta1) && p->beta1 >= 0.f && p->beta1 < 1.f &&
+                         std::isfinite(p->beta2) && p->beta2 >= 0.f && p->beta2 < 1.f &&
+                         std::isfinite(p->eps) && p->eps >= 0.f &&
+                         std::isfinite(p->weight_decay) && p->weight_decay >= 0.f;
+  if (!params_ok) return FG_EINVAL;
+  const size_t need = lars_adam_ws_bytes(t, ntensors);
+  if (!ws || ws_bytes < need || ((uintptr_t)ws & 15)) return FG_EWORKSPACE;
+  // the step count and the workspace must not alias any layer array
+  for (int i = 0; i < ntensors; ++i) {
+    const uint64_t pa[5] = {t[i].w32, t[i].m, t[i].v, t[i].g, t[i].w16};
+    const size_t ba[5] = {4, 4, 4, 4, 2};
+    for (int a = 0; a < 5; ++a) {
+      if (overlap((const void *)pa[a], t[i].numel * ba[a], step_count, 4) ||
+          overlap((const void *)pa[a], t[i].numel * ba[a], ws, need))
+        return FG_EINVAL;
+    }
+  }
+  if (overlap(step_count, 4, ws, need)) return FG_EINVAL;
+  return launch_status(launch_lars_adam(t, ntensors, p->lr, p->beta1, p->beta2,
+                                        p->eps, p->weight_decay, found_nonfinite,
+                                        nflags, step_count, ws, stream));
 }
 
 fg_status l2_head_grad(const uint16_t *y, const float *t, uint64_t numel,

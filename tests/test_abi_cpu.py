@@ -161,3 +161,33 @@ def test_library_planner_matches_golden_and_oracle():
 
 def test_status_strings(L):
     assert fg.status_string(fg.FG_EWORKSPACE).startswith("FG_EWORKSPACE")
+
+
+def test_optimizer_argument_checks(L):
+    """lars_adam_update rejects bad layers, parameters and workspace before
+    touching the device (no pointer below is dereferenced)."""
+    ref = ctypes.byref
+    n = 1024
+
+    def layer(base):  # w32, w16, m, v, g laid out 64 KiB apart
+        return fg.OptTensor(base, base + (1 << 16), base + (2 << 16), base + (3 << 16),
+                            base + (4 << 16), n)
+
+    good = (fg.OptTensor * 2)(layer(FAKE), layer(FAKE + (1 << 20)))
+    p = fg.OptParams(1e-3, 0.9, 0.999, 1e-8, 1e-4)
+    sc, ws = FAKE + (1 << 24), FAKE + (1 << 25)
+    need = L.fg_lars_adam_workspace_bytes(good, 2)
+    assert need > 0
+    assert L.lars_adam_update(good, 0, ref(p), None, 0, sc, ws, need, None) == fg.FG_EINVAL
+    assert L.lars_adam_update(good, 2, ref(p), None, 0, None, ws, need, None) == fg.FG_EINVAL
+    assert L.lars_adam_update(good, 2, ref(p), None, 3, sc, ws, need, None) == fg.FG_EINVAL
+    assert L.lars_adam_update(good, 2, ref(p), None, 0, sc, ws, need - 4, None) == fg.FG_EWORKSPACE
+    for bad in (fg.OptParams(-1.0, 0.9, 0.999, 1e-8, 0.0), fg.OptParams(1e-3, 1.0, 0.999, 1e-8, 0.0),
+                fg.OptParams(1e-3, 0.9, 0.999, -1.0, 0.0), fg.OptParams(float("nan"), 0.9, 0.999, 0.0, 0.0)):
+        assert L.lars_adam_update(good, 2, ref(bad), None, 0, sc, ws, need, None) == fg.FG_EINVAL
+    mis = (fg.OptTensor * 1)(fg.OptTensor(FAKE + 4, FAKE + (1 << 16), FAKE + (2 << 16),
+                                          FAKE + (3 << 16), FAKE + (4 << 16), n))
+    assert L.lars_adam_update(mis, 1, ref(p), None, 0, sc, ws, need, None) == fg.FG_EINVAL
+    alias = (fg.OptTensor * 2)(layer(FAKE), layer(FAKE + 2048))  # second w32 inside the first
+    assert L.lars_adam_update(alias, 2, ref(p), None, 0, sc, ws, need, None) == fg.FG_EINVAL
+    assert L.lars_adam_update(good, 2, ref(p), None, 0, FAKE + 64, ws, need, None) == fg.FG_EINVAL
