@@ -58,6 +58,9 @@ def parse():
     ap.add_argument("--zero-copy", action="store_true",
                     help="kernel gradients write into their group slots (no pack; "
                          "the non-finite check fused into their store)")
+    ap.add_argument("--optimizer", action="store_true",
+                    help="end each step with the layer-wise adaptive Adam update of "
+                         "fp32 master weights under a backoff loss scale")
     ap.add_argument("--op", default=None,
                     help="time one pass of one layer, e.g. E2b.fwd, or 'copy'")
     ap.add_argument("--summarize-stats", default=None, metavar="CSV")
@@ -328,12 +331,14 @@ def main():
     import torch
 
     import synth
-    from paper_1909_11150_amd.fcn import Chain
+    from paper_1909_11150_amd.fcn import AdamLARS, Chain, LossScaler
 
     wl = synth.fcn()
     layers = wl.layers
+    opt = dict(optimizer=AdamLARS(), scaler=LossScaler(synth.LOSS_SCALE)) \
+        if args.optimizer else {}
     ch = Chain(layers, wl.weights, wl.x, loss_scale=synth.LOSS_SCALE,
-               group_cap_bytes=synth.GROUP_CAP_BYTES, zero_copy=args.zero_copy)
+               group_cap_bytes=synth.GROUP_CAP_BYTES, zero_copy=args.zero_copy, **opt)
     target = torch.from_numpy(wl.target).cuda()
     # per-call accounting on one stream, where a call's duration is its own
     prog = ch.program(target, streams=1)
@@ -387,6 +392,9 @@ def main():
     dom_ev = [{i: (ev(), ev()) for i in dom_idx} for _ in range(args.steps)]
     e_start, e_end = ev(), ev()
     torch.cuda.synchronize()
+    if args.optimizer:
+        ch.observe()
+        applied0, scale0 = ch.applied, ch.loss_scale
     t0 = time.perf_counter()
     e_start.record()
     for s_ev in dom_ev:
@@ -441,7 +449,8 @@ def main():
                                "13 layers (99,483,904 weights), L2 head, loss scale 2^15, "
                                "25 MiB gradient groups (9)",
                    "global_batch": 4, "conv_tflop_per_step": round(flops_step / 1e12, 4),
-                   "streams": args.streams, "zero_copy_groups": args.zero_copy},
+                   "streams": args.streams, "zero_copy_groups": args.zero_copy,
+                   "optimizer": "lars_adam" if args.optimizer else None},
         "mfma_peak_frac": round(value / MFMA_F16_PEAK_TFLOPS, 4),
         "conv_kernels_tflops": round(flops_step / (conv_ms * 1e-3) / 1e12, 2),
         "grad_pack_GBps": bw("copy_pieces_kernel<2>"),
@@ -451,6 +460,14 @@ def main():
         "roofline": roof,
         "roofline_alone": roof_alone,
     }
+    if args.optimizer:
+        ch.observe()
+        o = per_op["opt.update"]
+        out["optimizer"] = {
+            "update_ms": round(o[0], 4), "update_GBps": round(o[1] / (o[0] * 1e-3) / 1e9, 1),
+            "bytes_per_param": "30 (w, m, v, fp32 gradient read; w, m, v, fp16 copy written)",
+            "timed_updates_applied": ch.applied - applied0,
+            "loss_scale_start": scale0, "loss_scale_end": ch.loss_scale}
     if args.detail:
         det = {"per_kernel": {k: {"launches_per_step": v[0], "ms_per_step": v[1],
                                   "work_per_step": v[2], "single_launch": v[3]}

@@ -19,7 +19,11 @@ names these ingredients but not how they combine; the readings taken here:
     the unscale check) is skipped: weights, moments and t stay unchanged;
   * loss-scale backoff: a skipped step halves S (not below s_min) and
     restarts the clean count; `interval` consecutive clean steps double S
-    (not above s_max).
+    (not above s_max);
+  * learning rate: linear warm-up from the initial rate (1e-4 in the paper)
+    to the peak (N times it for N ranks), then a staircase decay; the paper
+    gives neither the warm-up length nor the decay interval and rate, so
+    they are parameters. The step index counts applied updates from 0.
 """
 import numpy as np
 
@@ -55,3 +59,15 @@ def loss_scale_next(scale, clean, found, interval=2000, s_min=1.0, s_max=2.0 ** 
     if clean >= interval:
         return min(scale * 2.0, s_max), 0, True
     return scale, clean, True
+
+
+def lr_at(k, base=1e-4, peak=None, warmup=0, every=0, rate=1.0):
+    """Learning rate of the k-th applied update (k from 0): linear warm-up
+    from base to peak over `warmup` updates, then the peak multiplied by
+    rate once per `every` updates (every = 0: no decay)."""
+    peak = base if peak is None else peak
+    if k < warmup:
+        return base + (peak - base) * (k / warmup)
+    if every == 0:
+        return peak
+    return peak * rate ** ((k - warmup) // every)

@@ -6,7 +6,9 @@ with fused ReLUs, the loss-scaled L2 head gradient, the backward pass with
 fused ReLU gradients, and — per complete gradient group, in backward
 completion order — fusion-buffer pack, unscale with overflow check and
 unpack to fp32 master gradients (Section 4.2 Grouping; Section 6.2 loss
-scaling). Device memory comes from torch; every step is a libfcngrad call.
+scaling) — and, with an optimizer, the layer-wise adaptive Adam update of
+fp32 master weights under a backoff loss scale (Section 6.2). Device memory
+comes from torch; every step is a libfcngrad call.
 
 Layers are duck-typed: ``kind`` ("conv" | "convT"), ``x_shape``/``y_shape``
 (NHWC), ``r``, ``s``, ``stride``, ``pad``, ``relu`` and ``w_shape``.
@@ -17,11 +19,13 @@ from collections import namedtuple
 import torch
 
 from . import (EPI_GATE, EPI_NONE, EPI_RELU, OP_BWD_DATA, OP_BWD_WEIGHT,
-               OP_CONVT, OP_FWD, ConvDesc, FgError, Segment, kernel_name, lib,
+               OP_CONVT, OP_FWD, ConvDesc, FgError, OptParams, Segment,
+               kernel_name, lib,
                conv2d_bwd_data, conv2d_bwd_weight, conv2d_bwd_weight_checked,
                conv2d_fwd,
                conv_transpose2d_fwd, grad_group_pack, grad_group_plan,
                grad_group_unpack, grad_unscale_check, l2_head_grad,
+               lars_adam_update, lars_adam_workspace_bytes, opt_tensors,
                relu_backward, workspace_bytes)
 
 F16 = torch.float16
@@ -65,19 +69,89 @@ def chain_workspace_bytes(layers):
     return ws
 
 
+class LossScaler:
+    """Backoff loss scaling (Section 6.2: the loss is scaled before the
+    gradient computation, with OpenSeq2Seq's adaptive strategy). A step whose
+    gradients hold a non-finite value is not applied; it halves the scale
+    (not below s_min) and restarts the count of clean steps. After
+    `interval` clean steps in a row the scale doubles (not above s_max).
+    Powers of two keep scaling and unscaling exact."""
+
+    def __init__(self, scale=2.0 ** 15, interval=2000, s_min=1.0, s_max=2.0 ** 24):
+        if interval < 1 or not 0 < s_min <= scale <= s_max:
+            raise ValueError("need interval >= 1 and 0 < s_min <= scale <= s_max")
+        self.scale, self.interval = float(scale), int(interval)
+        self.s_min, self.s_max = float(s_min), float(s_max)
+        self.clean = 0
+
+    def update(self, found_nonfinite):
+        """Record one step's outcome; returns whether its update applied."""
+        if found_nonfinite:
+            self.scale = max(self.scale * 0.5, self.s_min)
+            self.clean = 0
+            return False
+        self.clean += 1
+        if self.clean >= self.interval:
+            self.scale = min(self.scale * 2.0, self.s_max)
+            self.clean = 0
+        return True
+
+
+class LRSchedule:
+    """Learning rate per applied step (Section 6.2): a linear warm-up from
+    `base` to `peak` (the paper's N * base for N ranks) over `warmup` steps,
+    then a staircase decay by `rate` every `every` steps (every = 0: none).
+    The step index counts applied updates from 0."""
+
+    def __init__(self, base=1e-4, peak=None, warmup=0, every=0, rate=1.0):
+        self.base = float(base)
+        self.peak = self.base if peak is None else float(peak)
+        self.warmup, self.every, self.rate = int(warmup), int(every), float(rate)
+        if self.warmup < 0 or self.every < 0 or self.base < 0 or self.peak < 0:
+            raise ValueError("negative schedule parameter")
+
+    def __call__(self, k):
+        if k < self.warmup:
+            return self.base + (self.peak - self.base) * k / self.warmup
+        steps = (k - self.warmup) // self.every if self.every else 0
+        return self.peak * self.rate ** steps
+
+
+class AdamLARS:
+    """Hyperparameters of the layer-wise adaptive Adam update (Section 6.2:
+    Adam with beta1 0.9, beta2 0.999; L2 weight decay 1e-4). lr: a float or
+    a schedule called with the number of applied steps."""
+
+    def __init__(self, lr=1e-4, beta1=0.9, beta2=0.999, eps=1e-8,
+                 weight_decay=1e-4):
+        self.lr = lr
+        self.beta1, self.beta2 = float(beta1), float(beta2)
+        self.eps, self.weight_decay = float(eps), float(weight_decay)
+
+    def lr_at(self, k):
+        return float(self.lr(k)) if callable(self.lr) else float(self.lr)
+
+
 class Chain:
     def __init__(self, layers, weights, x, device="cuda", loss_scale=2.0 ** 15,
                  group_cap_bytes=None, group_align_bytes=256, stream=None,
-                 zero_copy=False):
+                 zero_copy=False, optimizer=None, scaler=None):
         """zero_copy (with groups): each layer's fp16 dW lives in its slot of
         its group buffer, written there by conv2d_bwd_weight_checked (which
         also raises the group's non-finite flag), so no pack is needed; the
-        gaps between slots are zeroed once here."""
+        gaps between slots are zeroed once here.
+        optimizer (an AdamLARS; needs groups): the step ends with the update
+        of fp32 master weights (initialised from the given weights), their
+        Adam moments and the fp16 working weights the passes read; a step
+        with a flagged group is skipped on the device.
+        scaler (a LossScaler): the loss scale follows the flags of each step
+        (loss_scale is then taken from it)."""
         self.layers = list(layers)
         self.zero_copy = bool(zero_copy)
         self.dev = torch.device(device)
         self.stream = stream
-        self.loss_scale = float(loss_scale)
+        self.scaler = scaler
+        self.loss_scale = float(scaler.scale if scaler is not None else loss_scale)
         self.w = [torch.as_tensor(w).to(self.dev).contiguous() for w in weights]
         self.x = torch.as_tensor(x).to(self.dev).contiguous()
         nl = len(self.layers)
@@ -96,6 +170,33 @@ class Chain:
         if group_cap_bytes is not None:
             self._plan_groups(group_cap_bytes, group_align_bytes)
         self._nl = nl
+        self.opt = optimizer
+        self.applied = 0  # updates applied (host count, known after a step)
+        if optimizer is not None:
+            self._init_optimizer()
+
+    # ---- optimizer state ----------------------------------------------------------
+    def _init_optimizer(self):
+        if self.groups is None:
+            raise ValueError("the optimizer needs gradient groups (group_cap_bytes)")
+        if any(w.dtype != F16 for w in self.w):
+            raise ValueError("the optimizer writes fp16 working weights")
+        f32 = torch.float32
+        self.w32 = [w.to(f32).contiguous() for w in self.w]
+        self.m = [torch.zeros_like(w) for w in self.w32]
+        self.v = [torch.zeros_like(w) for w in self.w32]
+        self.step_count = torch.zeros(1, dtype=torch.int32, device=self.dev)
+        self.opt_tensors = opt_tensors(self.w32, self.w, self.m, self.v, self.master)
+        self.opt_ws = torch.empty(max(lars_adam_workspace_bytes(self.opt_tensors), 16),
+                                  dtype=torch.uint8, device=self.dev)
+
+    def update(self):
+        """The optimizer step on the unpacked gradients (skipped on the device
+        when a group flag is set)."""
+        o = self.opt
+        lars_adam_update(self.opt_tensors, o.lr_at(self.applied), self.flags,
+                         self.step_count, self.opt_ws, o.beta1, o.beta2, o.eps,
+                         o.weight_decay, stream=self.stream)
 
     # ---- gradient groups ---------------------------------------------------
     def _plan_groups(self, cap, align):
@@ -194,8 +295,29 @@ class Chain:
             if grad_path and self.groups is not None and i in self._group_done_at:
                 self.run_group(self._group_done_at[i])
 
+    def observe(self):
+        """Outcome of the last step a program ran: wait for its flag copy,
+        then advance the loss scaler and the count of applied updates. A
+        program does this by itself before each step's head call (the next
+        forward pass is queued by then); call it after the last step to bring
+        the host state up to date."""
+        pend = getattr(self, "_pending", None)
+        if pend is None:
+            return
+        self._pending = None
+        ev, hf = pend
+        ev.synchronize()
+        found = bool(hf.any())
+        self.last_found = found
+        if self.scaler is not None:
+            self.scaler.update(found)
+            self.loss_scale = self.scaler.scale
+        if not found and self.opt is not None:
+            self.applied += 1
+
     def step(self, target):
-        """Forward, loss head, backward and the grouped gradient path."""
+        """Forward, loss head, backward, the grouped gradient path and, with
+        an optimizer, the update."""
         if self.groups is not None:
             key = target.data_ptr()
             if getattr(self, "_prog_key", None) != key:
@@ -220,6 +342,10 @@ class Chain:
         the streams."""
         return StepProgram(self, target, streams)
 
+
+# algorithmic HBM bytes of the optimizer per parameter: w, m, v and the fp32
+# gradient read (16), w, m, v and the fp16 copy written (14)
+OPT_BYTES_PER_PARAM = 30
 
 # label, main kernel, algorithmic work (flops, or bytes for the gradient
 # path), C function (None: a Python callable), argument tuple (the stream
@@ -253,7 +379,14 @@ class StepProgram:
     the next step's forward pass cannot overwrite activations a kernel
     gradient still reads, nor its kernel gradients a buffer a pack still
     reads. Every kernel is deterministic and reads only finished inputs, so
-    the results are identical to the one-stream order (``streams=1``)."""
+    the results are identical to the one-stream order (``streams=1``).
+
+    With an optimizer, stream 2 ends with the update (after the last
+    unpack and the main stream's last pass, which reads the fp16 weights).
+    With an optimizer or a loss scaler, it then copies the group flags to
+    pinned host memory; the next run waits for that copy just before its
+    head call (its forward pass already queued), updates the scaler and the
+    applied count, and patches the loss-scale and learning-rate arguments."""
 
     def __init__(self, ch, target, streams=3):
         if ch.groups is None:
@@ -307,15 +440,21 @@ class StepProgram:
                                    ptr(ch.acts[i + 1]), epi, None, ws, wsb, st),
                                   one(d, OP_CONVT)))
         y = ch.acts[-1]
+        # loss-scale arguments, patched in place before each run
+        self._ny = y.numel()
+        self._head_scale = ctypes.c_double(2.0 * ch.loss_scale / self._ny)
+        self._inv_scale = ctypes.c_float(1.0 / ch.loss_scale)
         calls.append(Call("head_grad", "head_grad_kernel", 6 * y.numel(),
                           L_.l2_head_grad,
-                          (ptr(y), ptr(target), y.numel(),
-                           2.0 * ch.loss_scale / y.numel(), ptr(ch.g[-1]), st)))
+                          (ptr(y), ptr(target), y.numel(), self._head_scale,
+                           ptr(ch.g[-1]), st)))
+        self._head = len(calls) - 1
         writer = {nl: len(calls) - 1}  # call that writes g[i]
         # the non-finite flags are raised by the unscale calls (stream 2) and,
-        # with zero-copy groups, by the kernel gradients (stream 1)
+        # with zero-copy groups, by the kernel gradients (stream 1); cleared
+        # after the head call, which follows the previous step's last reads
         calls.append(Call("flags.zero", "", 0, None, (ch.flags.zero_,), False,
-                          sid=1 if ch.zero_copy else 2))
+                          sid=1 if ch.zero_copy else 2, deps=(self._head,)))
         zc = ch.zero_copy
 
         def dw_call(label, kname, flops, d, x, dy, i):
@@ -361,6 +500,32 @@ class StepProgram:
                 gc = self._group_calls(ch, gi, L_, st)
                 gc[0] = gc[0]._replace(deps=(last_dw[i],))
                 calls += gc
+        self.params = None
+        if ch.opt is not None:
+            # after the last group's unpack (stream order) and the last pass
+            # that reads the fp16 weights (the main stream's last call)
+            o = ch.opt
+            self.params = OptParams(o.lr_at(ch.applied), o.beta1, o.beta2, o.eps,
+                                    o.weight_decay)
+            ntot = sum(w.numel() for w in ch.w32)
+            calls.append(Call("opt.update", "lars_adam_moments_kernel",
+                              OPT_BYTES_PER_PARAM * ntot, L_.lars_adam_update,
+                              (ch.opt_tensors, nl, ctypes.byref(self.params),
+                               ch.flags.data_ptr(), len(ch.groups),
+                               ch.step_count.data_ptr(), ch.opt_ws.data_ptr(),
+                               ch.opt_ws.numel(), st), False, sid=2,
+                              deps=(writer[0],)))
+        self._copy = None
+        if ch.opt is not None or ch.scaler is not None:
+            # the step's flags to pinned host memory; read before the next
+            # step's head call, by which time the next forward pass is queued
+            self.host_flags = torch.zeros(len(ch.groups), dtype=torch.int32,
+                                          pin_memory=True)
+            calls.append(Call("flags.copy", "", 0, None,
+                              (lambda: self.host_flags.copy_(ch.flags,
+                                                             non_blocking=True),),
+                              False, sid=2))
+            self._copy = len(calls) - 1
         if streams == 1:  # program order already respects every dependency
             calls = [c._replace(sid=0, deps=()) for c in calls]
         # the stream argument of each library call
@@ -369,8 +534,11 @@ class StepProgram:
         self.final = tuple(max(j for j, c in enumerate(calls) if c.sid == sid)
                            for sid in range(1, len(self.streams)))
         needed = {d for c in calls for d in c.deps} | set(self.final)
+        if self._copy is not None:
+            needed.add(self._copy)
         self.events = {j: torch.cuda.Event() for j in sorted(needed)}
         self.calls = calls
+        self.ch = ch
 
     def _group_calls(self, ch, gi, L_, st):
         g = ch.groups[gi]
@@ -390,17 +558,27 @@ class StepProgram:
                  (src, len(g["members"]), g16.data_ptr(), n, st), sid=2)]
         return pack + [
             Call(f"G{gi}.unscale", "unscale_vec_kernel", 6 * n, L_.grad_unscale_check,
-                 (g16.data_ptr(), n, 1.0 / ch.loss_scale, g32.data_ptr(),
+                 (g16.data_ptr(), n, self._inv_scale, g32.data_ptr(),
                   flag.data_ptr(), st), sid=2),
             Call(f"G{gi}.unpack", "copy_pieces_kernel<4>", 8 * n, L_.grad_group_unpack,
                  (g32.data_ptr(), n, dst, len(g["members"]), st), sid=2),
         ]
+
+    def _patch(self):
+        ch = self.ch
+        self._head_scale.value = 2.0 * ch.loss_scale / self._ny
+        self._inv_scale.value = 1.0 / ch.loss_scale
+        if self.params is not None:
+            self.params.lr = ch.opt.lr_at(ch.applied)
 
     def run(self, events=None):
         """Run the step once. events: {call index: (start, end)} HIP events
         recorded around those calls on the call's stream."""
         streams, evs = self.streams, self.events
         for i, c in enumerate(self.calls):
+            if i == self._head:
+                self.ch.observe()
+                self._patch()
             s = streams[c.sid]
             for d in c.deps:
                 s.wait_event(evs[d])
@@ -420,3 +598,5 @@ class StepProgram:
                 evs[i].record(s)
         for j in self.final:
             streams[0].wait_event(evs[j])
+        if self._copy is not None:
+            self.ch._pending = (evs[self._copy], self.host_flags)

@@ -10,10 +10,16 @@ max error of about 2^-11 * max|o|; fp32 accumulation adds ~sqrt(K)*2^-24
 relative. The bound leaves ~18x headroom on the L2 term.
 """
 import numpy as np
+import pytest
 import torch
+
+from oracle import optim as O
 
 REL_L2 = 5e-3
 MAX_ABS_RMS = 2e-2
+
+# the optimizer hyperparameters of Section 6.2 (Adam betas, weight decay)
+OPT_HP = dict(beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=1e-4)
 
 
 def dev(a, dtype=None):
@@ -75,3 +81,33 @@ def workspace(desc, op):
     import paper_1909_11150_amd as fg
     return torch.empty(max(16, fg.workspace_bytes(desc, op)), dtype=torch.uint8,
                        device="cuda")
+
+
+def check_opt_layer(w0, m0, v0, g0, t, lr, w1, m1, v1, h1, hp=OPT_HP):
+    """One layer of lars_adam_update from (w0, m0, v0, g0) at step t against
+    the fp64 oracle: moments to a few fp32 roundings of each term, the step
+    as lr * tau * u of the stored moments, tau within 1e-4 of the oracle's,
+    the fp16 copy bit for bit."""
+    # the kernel's inputs are the fp32 values of the hyperparameters
+    f = lambda x: float(np.float32(x))
+    b1, b2, eps, wd = f(hp["beta1"]), f(hp["beta2"]), f(hp["eps"]), f(hp["weight_decay"])
+    lr = f(lr)
+    rw, rm, rv, tau = O.lars_adam_update(w0, m0, v0, g0, t, lr, b1=b1, b2=b2, eps=eps, wd=wd)
+    # moments: a few fp32 roundings of each term (b1 m and (1-b1) g~ may cancel)
+    w0d, g0d = w0.astype(np.float64), g0.astype(np.float64)
+    gt = g0d + wd * w0d
+    ulp = 2.0 ** -24
+    mb = 8 * ulp * (b1 * np.abs(m0) + (1 - b1) * np.abs(gt)) + 1e-38
+    assert (np.abs(m1 - rm) <= mb).all(), float((np.abs(m1 - rm) / mb).max())
+    vb = 8 * ulp * (b2 * v0 + (1 - b2) * gt * gt) + 1e-38
+    assert (np.abs(v1 - rv) <= vb).all(), float((np.abs(v1 - rv) / vb).max())
+    # the applied step is lr * tau * u of the stored moments, tau = ||w|| / ||u||
+    m1d, v1d = m1.astype(np.float64), v1.astype(np.float64)
+    u = (m1d / (1 - b1 ** t)) / (np.sqrt(v1d / (1 - b2 ** t)) + eps)
+    tg = np.linalg.norm(w0d) / np.linalg.norm(u) if np.linalg.norm(w0d) > 0 else 1.0
+    assert tg == pytest.approx(tau, rel=1e-4)
+    step = lr * tg * u
+    err = np.abs(w1.astype(np.float64) - (w0d - step))
+    bound = 1e-5 * np.abs(step) + np.abs(w0d - step) * 2.0 ** -23 + 1e-38
+    assert (err <= bound).all(), float((err / bound).max())
+    assert np.array_equal(h1.view(np.uint16), O.fp16_copy(w1).view(np.uint16))

@@ -18,12 +18,11 @@ import pytest
 import torch
 
 import paper_1909_11150_amd as fg
-from oracle import optim as O
+from gpu_util import OPT_HP as HP, check_opt_layer
 
 pytestmark = pytest.mark.gpu
 
 SIZES = [1, 5, 4096, 4099, 100003, 262144 + 3]
-HP = dict(beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=1e-4)
 
 
 def _state(seed, sizes=SIZES, wscale=0.05):
@@ -55,32 +54,6 @@ class Dev:
         return c(self.w32), c(self.m), c(self.v), c(self.w16), int(self.step.item())
 
 
-def _check_layer(w0, m0, v0, g0, t, lr, w1, m1, v1, h1):
-    # the kernel's inputs are the fp32 values of the hyperparameters
-    f = lambda x: float(np.float32(x))
-    b1, b2, eps, wd = f(HP["beta1"]), f(HP["beta2"]), f(HP["eps"]), f(HP["weight_decay"])
-    lr = f(lr)
-    rw, rm, rv, tau = O.lars_adam_update(w0, m0, v0, g0, t, lr, b1=b1, b2=b2, eps=eps, wd=wd)
-    # moments: a few fp32 roundings of each term (b1 m and (1-b1) g~ may cancel)
-    w0d, g0d = w0.astype(np.float64), g0.astype(np.float64)
-    gt = g0d + wd * w0d
-    ulp = 2.0 ** -24
-    mb = 8 * ulp * (b1 * np.abs(m0) + (1 - b1) * np.abs(gt)) + 1e-38
-    assert (np.abs(m1 - rm) <= mb).all(), float((np.abs(m1 - rm) / mb).max())
-    vb = 8 * ulp * (b2 * v0 + (1 - b2) * gt * gt) + 1e-38
-    assert (np.abs(v1 - rv) <= vb).all(), float((np.abs(v1 - rv) / vb).max())
-    # the applied step is lr * tau * u of the stored moments, tau = ||w|| / ||u||
-    m1d, v1d = m1.astype(np.float64), v1.astype(np.float64)
-    u = (m1d / (1 - b1 ** t)) / (np.sqrt(v1d / (1 - b2 ** t)) + eps)
-    tg = np.linalg.norm(w0d) / np.linalg.norm(u) if np.linalg.norm(w0d) > 0 else 1.0
-    assert tg == pytest.approx(tau, rel=1e-4)
-    step = lr * tg * u
-    err = np.abs(w1.astype(np.float64) - (w0d - step))
-    bound = 1e-5 * np.abs(step) + np.abs(w0d - step) * 2.0 ** -23 + 1e-38
-    assert (err <= bound).all(), float((err / bound).max())
-    assert np.array_equal(h1.view(np.uint16), O.fp16_copy(w1).view(np.uint16))
-
-
 def test_update_matches_oracle():
     w, m, v, g = _state(1)
     d = Dev(w, m, v, g, step=6)
@@ -89,7 +62,7 @@ def test_update_matches_oracle():
     w1, m1, v1, h1, step = d.host()
     assert step == 7
     for i in range(len(SIZES)):
-        _check_layer(w[i], m[i], v[i], g[i], 7, lr, w1[i], m1[i], v1[i], h1[i])
+        check_opt_layer(w[i], m[i], v[i], g[i], 7, lr, w1[i], m1[i], v1[i], h1[i])
 
 
 def test_three_steps_follow_the_oracle():
@@ -105,7 +78,7 @@ def test_three_steps_follow_the_oracle():
         w1, m1, v1, h1, step = d.host()
         assert step == t
         for i in range(2):
-            _check_layer(w0[i], m0[i], v0[i], gs[i], t, 1e-2, w1[i], m1[i], v1[i], h1[i])
+            check_opt_layer(w0[i], m0[i], v0[i], gs[i], t, 1e-2, w1[i], m1[i], v1[i], h1[i])
 
 
 def test_flagged_step_changes_nothing():
@@ -136,4 +109,4 @@ def test_zero_weight_layer_and_determinism():
     for a, b in zip(outs[0][0], outs[1][0]):
         assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
     w1, m1, v1, h1, _ = outs[0]
-    _check_layer(w[0], m[0], v[0], g[0], 1, 1e-3, w1[0], m1[0], v1[0], h1[0])
+    check_opt_layer(w[0], m[0], v[0], g[0], 1, 1e-3, w1[0], m1[0], v1[0], h1[0])

@@ -98,3 +98,31 @@ def test_loss_scale_backoff_sequence():
                      (2.0 ** 14, 0, False), (2.0 ** 13, 0, False)]
     s, clean, _ = O.loss_scale_next(2.0 ** 13, 0, True, s_min=2.0 ** 13)
     assert s == 2.0 ** 13
+
+
+def test_lr_schedule_hand_values():
+    # warm-up 1e-4 -> 8e-4 over 7 updates: +1e-4 per update, exactly the
+    # peak at k = 7; then x0.5 every 3 updates
+    f = lambda k: O.lr_at(k, base=1e-4, peak=8e-4, warmup=7, every=3, rate=0.5)
+    np.testing.assert_allclose([f(k) for k in range(7)],
+                               [1e-4 * (1 + k) for k in range(7)], rtol=1e-14)
+    assert [f(k) for k in (7, 8, 9, 10, 12, 13, 16)] == \
+        [8e-4, 8e-4, 8e-4, 4e-4, 4e-4, 2e-4, 1e-4]
+    # one rank, no warm-up, no decay: the paper's initial rate throughout
+    assert {O.lr_at(k) for k in range(50)} == {1e-4}
+
+
+def test_lr_schedule_shape():
+    rng = np.random.default_rng(9)
+    for _ in range(20):
+        base = 10.0 ** rng.uniform(-5, -3)
+        n = int(rng.integers(1, 64))
+        wu, ev = int(rng.integers(1, 40)), int(rng.integers(1, 30))
+        rate = float(rng.uniform(0.1, 0.99))
+        lr = [O.lr_at(k, base, n * base, wu, ev, rate) for k in range(wu + 5 * ev)]
+        d = np.diff(lr[:wu + 1])
+        assert np.all(d >= 0) and np.allclose(d, d[0], rtol=1e-9)   # linear
+        assert lr[wu] == n * base
+        tail = np.array(lr[wu:])
+        assert np.all(np.diff(tail) <= 0)                          # decays
+        assert len(set(np.round(tail / (n * base), 12))) == 5      # 5 stairs
