@@ -462,10 +462,15 @@ def main():
     }
     if args.optimizer:
         ch.observe()
-        o = per_op["opt.update"]
+        nrm = [v for k, v in per_op.items() if k.endswith(".norms")]
+        ap = per_op["opt.apply"]
+        n_ms, n_b = sum(v[0] for v in nrm), sum(v[1] for v in nrm)
         out["optimizer"] = {
-            "update_ms": round(o[0], 4), "update_GBps": round(o[1] / (o[0] * 1e-3) / 1e9, 1),
-            "bytes_per_param": "30 (w, m, v, fp32 gradient read; w, m, v, fp16 copy written)",
+            "norms_ms": round(n_ms, 4), "norms_GBps": round(n_b / (n_ms * 1e-3) / 1e9, 1),
+            "apply_ms": round(ap[0], 4), "apply_GBps": round(ap[1] / (ap[0] * 1e-3) / 1e9, 1),
+            "gradients": "fp16 group slots" if args.zero_copy else "fp32 unpacked",
+            "bytes_per_param": "norms: w, m, v, gradient read; apply: the same read, "
+                               "w, m, v, fp16 copy written",
             "timed_updates_applied": ch.applied - applied0,
             "loss_scale_start": scale0, "loss_scale_end": ch.loss_scale}
     if args.detail:

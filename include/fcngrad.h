@@ -234,10 +234,19 @@ typedef struct {
     float lr, beta1, beta2, eps, weight_decay;
 } fg_opt_params;
 
-/* Workspace (bytes, device) lars_adam_update needs for these layers. */
+/* Workspace (bytes, device) the optimizer calls need for these layers (it
+ * depends on the element counts only); 0 for a count outside
+ * 1..FG_MAX_SEGMENTS or a numel outside 1..2^31 - 2. */
 size_t fg_lars_adam_workspace_bytes(const fg_opt_tensor *t, int32_t ntensors);
 
-/* Layer-wise adaptive Adam step on fp32 master weights. For each layer, with
+/* Form of the gradient t[i].g of the optimizer calls: fp32 unscaled
+ * (16-byte aligned), or fp16 loss-scaled (8-byte aligned, e.g. the layer's
+ * slot in its gradient group buffer), read as fp16 * grad_inv_scale — the
+ * fp32 value grad_unscale_check writes for it. */
+enum { FG_GRAD_F32 = 0, FG_GRAD_F16_SCALED = 1 };
+
+/* Layer-wise adaptive Adam step on fp32 master weights (Section 6.2: LARS
+ * layer-wise rates with Adam, L2 weight decay). For each layer, with
  * t = *step_count + 1: g~ = g + weight_decay * w; m = beta1 m + (1-beta1) g~;
  * v = beta2 v + (1-beta2) g~^2; u = (m / (1-beta1^t)) / (sqrt(v /
  * (1-beta2^t)) + eps); tau = ||w|| / ||u|| over the layer (1 if either is
@@ -246,16 +255,47 @@ size_t fg_lars_adam_workspace_bytes(const fg_opt_tensor *t, int32_t ntensors);
  * (the unscale checks of the step's gradient groups) is non-zero, the step
  * is skipped on the device: nothing is written and *step_count is kept.
  * fp32 arithmetic; per-layer norms summed in a fixed order (the result is
- * deterministic). t: host array of ntensors (1..FG_MAX_SEGMENTS) layers,
- * read during the call only. FG_EINVAL for null or misaligned pointers,
- * overlapping arrays, params outside lr >= 0, 0 <= beta < 1, eps >= 0,
- * weight_decay >= 0, or nflags > 0 with null flags; FG_EWORKSPACE if
- * ws_bytes is short. */
+ * deterministic). The square root and the quotient of u are the hardware
+ * ones (a few ulps). t: host array of ntensors (1..FG_MAX_SEGMENTS) layers
+ * with fp32 gradients, read during the call only. FG_EINVAL for null or
+ * misaligned pointers, overlapping arrays, params outside lr >= 0,
+ * 0 <= beta < 1, eps >= 0, weight_decay >= 0, or nflags > 0 with null
+ * flags; FG_EWORKSPACE if ws_bytes is short or ws is not 16-byte aligned.
+ * Same as lars_adam_norms over all layers followed by lars_adam_apply. */
 fg_status lars_adam_update(const fg_opt_tensor *t, int32_t ntensors,
                            const fg_opt_params *p,
                            const int32_t *found_nonfinite, int32_t nflags,
                            int32_t *step_count, void *ws, size_t ws_bytes,
                            hipStream_t stream);
+
+/* The update of lars_adam_update in two parts, so that the part that reads
+ * each layer's gradient can run as soon as that gradient exists (e.g. per
+ * gradient group, beside the rest of the backward pass) and only the writes
+ * remain after it. lars_adam_norms reads layers [first, first + count) of
+ * the table t (weights, moments, gradient; nothing is written but ws) and
+ * stores their partial sums of u^2 and w^2 in ws; t = *step_count + 1 as
+ * lars_adam_update. lars_adam_apply then forms every layer's tau, skips the
+ * step if any flag is set, and otherwise writes m, v, w, the fp16 copy and
+ * the step count as lars_adam_update. Between the norms calls that cover
+ * every layer and the apply, the caller passes the same table, params
+ * (lr aside), gradient form, grad_inv_scale, step_count and ws, and changes
+ * none of the layer arrays; the apply must be ordered after every norms
+ * call on the device (same stream or an event). Validation as
+ * lars_adam_update, with the gradient form (FG_GRAD_*) and, for fp16
+ * gradients, a finite grad_inv_scale > 0; lars_adam_norms also returns
+ * FG_EINVAL for a range outside the table, and lars_adam_apply returns
+ * FG_EINVAL, before any launch, unless norms calls with these arguments
+ * have covered every layer since the last apply on this ws (tracked on the
+ * host per workspace address; a lars_adam_update on ws clears it). */
+fg_status lars_adam_norms(const fg_opt_tensor *t, int32_t ntensors, int32_t first,
+                          int32_t count, const fg_opt_params *p, int32_t grad_format,
+                          float grad_inv_scale, const int32_t *step_count, void *ws,
+                          size_t ws_bytes, hipStream_t stream);
+fg_status lars_adam_apply(const fg_opt_tensor *t, int32_t ntensors,
+                          const fg_opt_params *p, int32_t grad_format,
+                          float grad_inv_scale, const int32_t *found_nonfinite,
+                          int32_t nflags, int32_t *step_count, void *ws,
+                          size_t ws_bytes, hipStream_t stream);
 
 /* Output spatial size: transpose = 0 gives the forward P, Q; 1 gives the
  * transposed convolution's output size. FG_EINVAL if it is not positive. */

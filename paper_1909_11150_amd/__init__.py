@@ -17,6 +17,7 @@ FG_OK, FG_EINVAL, FG_EUNSUPPORTED, FG_EWORKSPACE, FG_ELAUNCH = range(5)
 EPI_NONE, EPI_RELU, EPI_GATE = 0, 1, 2
 OP_FWD, OP_BWD_DATA, OP_BWD_WEIGHT, OP_CONVT = 0, 1, 2, 3
 MAX_SEGMENTS = 64
+GRAD_F32, GRAD_F16_SCALED = 0, 1
 
 ENTRY_POINTS = (
     "conv2d_fwd", "conv2d_bwd_data", "conv2d_bwd_weight",
@@ -24,7 +25,8 @@ ENTRY_POINTS = (
     "grad_group_unpack", "l2_head_grad", "relu_backward",
     "fg_conv_workspace_bytes", "fg_conv_out_dims", "grad_group_plan",
     "fg_conv_kernel_name", "fg_status_string",
-    "lars_adam_update", "fg_lars_adam_workspace_bytes",
+    "lars_adam_update", "lars_adam_norms", "lars_adam_apply",
+    "fg_lars_adam_workspace_bytes",
 )
 
 
@@ -108,6 +110,14 @@ def lib():
     L.lars_adam_update.argtypes = [ctypes.POINTER(OptTensor), i32,
                                    ctypes.POINTER(OptParams), vp, i32, vp, vp, sz, vp]
     L.lars_adam_update.restype = ctypes.c_int
+    L.lars_adam_norms.argtypes = [ctypes.POINTER(OptTensor), i32, i32, i32,
+                                  ctypes.POINTER(OptParams), i32, ctypes.c_float, vp,
+                                  vp, sz, vp]
+    L.lars_adam_norms.restype = ctypes.c_int
+    L.lars_adam_apply.argtypes = [ctypes.POINTER(OptTensor), i32,
+                                  ctypes.POINTER(OptParams), i32, ctypes.c_float, vp,
+                                  i32, vp, vp, sz, vp]
+    L.lars_adam_apply.restype = ctypes.c_int
     L.fg_lars_adam_workspace_bytes.argtypes = [ctypes.POINTER(OptTensor), i32]
     L.fg_lars_adam_workspace_bytes.restype = ctypes.c_size_t
     L.fg_conv_workspace_bytes.argtypes = [pdesc, ctypes.c_int]
@@ -222,6 +232,30 @@ def lars_adam_update(tensors, lr, flags, step_count, ws, beta1=0.9, beta2=0.999,
     _check("lars_adam_update", lib().lars_adam_update(
         tensors, len(tensors), ctypes.byref(p), _p(flags), nf, _p(step_count),
         wp, wb, _s(stream)))
+
+
+def lars_adam_norms(tensors, first, count, step_count, ws, grad_format=GRAD_F32,
+                    grad_inv_scale=1.0, beta1=0.9, beta2=0.999, eps=1e-8,
+                    weight_decay=1e-4, stream=None):
+    """Partial norms of layers [first, first + count) (see include/fcngrad.h);
+    the learning rate does not enter."""
+    p = OptParams(0.0, beta1, beta2, eps, weight_decay)
+    wp, wb = _ws(ws)
+    _check("lars_adam_norms", lib().lars_adam_norms(
+        tensors, len(tensors), first, count, ctypes.byref(p), grad_format,
+        grad_inv_scale, _p(step_count), wp, wb, _s(stream)))
+
+
+def lars_adam_apply(tensors, lr, flags, step_count, ws, grad_format=GRAD_F32,
+                    grad_inv_scale=1.0, beta1=0.9, beta2=0.999, eps=1e-8,
+                    weight_decay=1e-4, stream=None):
+    """Ratio and update after lars_adam_norms has covered every layer."""
+    p = OptParams(lr, beta1, beta2, eps, weight_decay)
+    wp, wb = _ws(ws)
+    nf = 0 if flags is None else flags.numel()
+    _check("lars_adam_apply", lib().lars_adam_apply(
+        tensors, len(tensors), ctypes.byref(p), grad_format, grad_inv_scale, _p(flags),
+        nf, _p(step_count), wp, wb, _s(stream)))
 
 
 def conv_transpose2d_fwd(desc, x, w, y, epi=EPI_NONE, gate=None, ws=None,

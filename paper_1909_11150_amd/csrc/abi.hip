@@ -5,6 +5,8 @@
 #include <string.h>
 
 #include <cmath>
+#include <mutex>
+#include <unordered_map>
 
 #include "internal.h"
 
@@ -523,32 +525,104 @@ fg_status grad_unscale_check(const uint16_t *group, uint64_t numel,
 }
 
 // ---------------------------------------------------------------------------
-static bool opt_tensors_ok(const fg_opt_tensor *t, int32_t n) {
+// gbytes: bytes per gradient element (4: fp32, 2: fp16)
+static bool opt_tensors_ok(const fg_opt_tensor *t, int32_t n, size_t gbytes = 4) {
   if (!t || n < 1 || n > FG_MAX_SEGMENTS) return false;
+  const uint64_t galign = gbytes == 4 ? 15 : 7;
   for (int i = 0; i < n; ++i) {
     const fg_opt_tensor &a = t[i];
     if (!a.w32 || !a.w16 || !a.m || !a.v || !a.g) return false;
     if (a.numel == 0 || a.numel >= 0x7FFFFFFFull) return false;
-    if (((a.w32 | a.m | a.v | a.g) & 15) || (a.w16 & 7)) return false;
+    if (((a.w32 | a.m | a.v) & 15) || (a.g & galign) || (a.w16 & 7)) return false;
   }
   // no two arrays of the call overlap
+  const size_t bytes[5] = {4, 4, 4, gbytes, 2};
   for (int i = 0; i < n; ++i) {
     const uint64_t pi[5] = {t[i].w32, t[i].m, t[i].v, t[i].g, t[i].w16};
-    const size_t bi[5] = {4, 4, 4, 4, 2};
     for (int j = i; j < n; ++j) {
       const uint64_t pj[5] = {t[j].w32, t[j].m, t[j].v, t[j].g, t[j].w16};
       for (int a = 0; a < 5; ++a)
         for (int b = (i == j ? a + 1 : 0); b < 5; ++b)
-          if (overlap((const void *)pi[a], t[i].numel * bi[a], (const void *)pj[b],
-                      t[j].numel * bi[b]))
+          if (overlap((const void *)pi[a], t[i].numel * bytes[a], (const void *)pj[b],
+                      t[j].numel * bytes[b]))
             return false;
     }
   }
   return true;
 }
 
+static bool opt_params_ok(const fg_opt_params *p) {
+  return p && std::isfinite(p->lr) && p->lr >= 0.f && std::isfinite(p->beta1) &&
+         p->beta1 >= 0.f && p->beta1 < 1.f && std::isfinite(p->beta2) &&
+         p->beta2 >= 0.f && p->beta2 < 1.f && std::isfinite(p->eps) && p->eps >= 0.f &&
+         std::isfinite(p->weight_decay) && p->weight_decay >= 0.f;
+}
+
+// Shared checks of the optimizer calls: the table, the gradient format, the
+// step count and the workspace (size, alignment, no aliasing of any array).
+static fg_status opt_call_ok(const fg_opt_tensor *t, int32_t n, const fg_opt_params *p,
+                             int32_t grad_format, float inv_scale,
+                             const int32_t *step_count, const void *ws,
+                             size_t ws_bytes) {
+  if (grad_format != FG_GRAD_F32 && grad_format != FG_GRAD_F16_SCALED) return FG_EINVAL;
+  if (grad_format == FG_GRAD_F16_SCALED && !(std::isfinite(inv_scale) && inv_scale > 0.f))
+    return FG_EINVAL;
+  const size_t gb = grad_format == FG_GRAD_F32 ? 4 : 2;
+  if (!opt_tensors_ok(t, n, gb) || !opt_params_ok(p) || !step_count) return FG_EINVAL;
+  const size_t need = lars_adam_ws_bytes(t, n);
+  if (!ws || ws_bytes < need || ((uintptr_t)ws & 15)) return FG_EWORKSPACE;
+  const size_t bytes[5] = {4, 4, 4, gb, 2};
+  for (int i = 0; i < n; ++i) {
+    const uint64_t pa[5] = {t[i].w32, t[i].m, t[i].v, t[i].g, t[i].w16};
+    for (int a = 0; a < 5; ++a) {
+      if (overlap((const void *)pa[a], t[i].numel * bytes[a], step_count, 4) ||
+          overlap((const void *)pa[a], t[i].numel * bytes[a], ws, need))
+        return FG_EINVAL;
+    }
+  }
+  if (overlap(step_count, 4, ws, need)) return FG_EINVAL;
+  return FG_OK;
+}
+
+// Which tensors have partial norms in a workspace since its last apply, for
+// one table, gradient form and set of parameters (a hash of them): an apply
+// is accepted only when every tensor is covered, so a missing norms call is
+// an error at the call instead of a wrong update.
+namespace {
+struct NormsRecord {
+  uint64_t key;
+  uint64_t mask;
+};
+std::mutex g_norms_mu;
+std::unordered_map<uintptr_t, NormsRecord> g_norms;
+
+uint64_t fnv(uint64_t h, const void *p, size_t n) {
+  const unsigned char *c = static_cast<const unsigned char *>(p);
+  for (size_t i = 0; i < n; ++i) h = (h ^ c[i]) * 0x100000001b3ull;
+  return h;
+}
+
+uint64_t norms_key(const fg_opt_tensor *t, int32_t n, const fg_opt_params *p,
+                   int32_t grad_format, float inv_scale, const int32_t *step_count) {
+  uint64_t h = 0xcbf29ce484222325ull;
+  h = fnv(h, &n, sizeof n);
+  h = fnv(h, t, sizeof(fg_opt_tensor) * (size_t)n);
+  const float f[4] = {p->beta1, p->beta2, p->eps, p->weight_decay};
+  h = fnv(h, f, sizeof f);
+  h = fnv(h, &grad_format, sizeof grad_format);
+  const float inv = grad_format == FG_GRAD_F32 ? 0.f : inv_scale;
+  h = fnv(h, &inv, sizeof inv);
+  const uintptr_t sc = (uintptr_t)step_count;
+  return fnv(h, &sc, sizeof sc);
+}
+
+uint64_t full_mask(int32_t n) { return n >= 64 ? ~0ull : (1ull << n) - 1; }
+}  // namespace
+
 size_t fg_lars_adam_workspace_bytes(const fg_opt_tensor *t, int32_t ntensors) {
-  if (!opt_tensors_ok(t, ntensors)) return 0;
+  if (!t || ntensors < 1 || ntensors > FG_MAX_SEGMENTS) return 0;
+  for (int i = 0; i < ntensors; ++i)
+    if (t[i].numel == 0 || t[i].numel >= 0x7FFFFFFFull) return 0;
   return lars_adam_ws_bytes(t, ntensors);
 }
 
@@ -557,30 +631,65 @@ fg_status lars_adam_update(const fg_opt_tensor *t, int32_t ntensors,
                            const int32_t *found_nonfinite, int32_t nflags,
                            int32_t *step_count, void *ws, size_t ws_bytes,
                            hipStream_t stream) {
-  if (!opt_tensors_ok(t, ntensors) || !p || !step_count) return FG_EINVAL;
   if (nflags < 0 || (nflags > 0 && !found_nonfinite)) return FG_EINVAL;
-  const bool params_ok = std::isfinite(p->lr) && p->lr >= 0.f &&
-                         std::isfinite(p->beta1) && p->beta1 >= 0.f && p->beta1 < 1.f &&
-                         std::isfinite(p->beta2) && p->beta2 >= 0.f && p->beta2 < 1.f &&
-                         std::isfinite(p->eps) && p->eps >= 0.f &&
-                         std::isfinite(p->weight_decay) && p->weight_decay >= 0.f;
-  if (!params_ok) return FG_EINVAL;
-  const size_t need = lars_adam_ws_bytes(t, ntensors);
-  if (!ws || ws_bytes < need || ((uintptr_t)ws & 15)) return FG_EWORKSPACE;
-  // the step count and the workspace must not alias any layer array
-  for (int i = 0; i < ntensors; ++i) {
-    const uint64_t pa[5] = {t[i].w32, t[i].m, t[i].v, t[i].g, t[i].w16};
-    const size_t ba[5] = {4, 4, 4, 4, 2};
-    for (int a = 0; a < 5; ++a) {
-      if (overlap((const void *)pa[a], t[i].numel * ba[a], step_count, 4) ||
-          overlap((const void *)pa[a], t[i].numel * ba[a], ws, need))
-        return FG_EINVAL;
-    }
+  const fg_status st =
+      opt_call_ok(t, ntensors, p, FG_GRAD_F32, 1.f, step_count, ws, ws_bytes);
+  if (st != FG_OK) return st;
+  {  // this call overwrites any partial norms held in the workspace
+    std::lock_guard<std::mutex> lk(g_norms_mu);
+    g_norms.erase((uintptr_t)ws);
   }
-  if (overlap(step_count, 4, ws, need)) return FG_EINVAL;
-  return launch_status(launch_lars_adam(t, ntensors, p->lr, p->beta1, p->beta2,
-                                        p->eps, p->weight_decay, found_nonfinite,
-                                        nflags, step_count, ws, stream));
+  hipError_t e = launch_lars_adam_norms(t, ntensors, 0, ntensors, *p, false, 1.f,
+                                        step_count, ws, stream);
+  if (e != hipSuccess) return launch_status(e);
+  return launch_status(launch_lars_adam_apply(t, ntensors, *p, false, 1.f,
+                                              found_nonfinite, nflags, step_count, ws,
+                                              stream));
+}
+
+fg_status lars_adam_norms(const fg_opt_tensor *t, int32_t ntensors, int32_t first,
+                          int32_t count, const fg_opt_params *p, int32_t grad_format,
+                          float grad_inv_scale, const int32_t *step_count, void *ws,
+                          size_t ws_bytes, hipStream_t stream) {
+  const fg_status st =
+      opt_call_ok(t, ntensors, p, grad_format, grad_inv_scale, step_count, ws, ws_bytes);
+  if (st != FG_OK) return st;
+  if (first < 0 || count < 1 || first > ntensors - count) return FG_EINVAL;
+  const uint64_t key = norms_key(t, ntensors, p, grad_format, grad_inv_scale, step_count);
+  const hipError_t e =
+      launch_lars_adam_norms(t, ntensors, first, count, *p,
+                             grad_format == FG_GRAD_F16_SCALED, grad_inv_scale,
+                             step_count, ws, stream);
+  if (e != hipSuccess) return launch_status(e);
+  std::lock_guard<std::mutex> lk(g_norms_mu);
+  NormsRecord &r = g_norms[(uintptr_t)ws];
+  if (r.key != key) r = NormsRecord{key, 0};
+  r.mask |= full_mask(first + count) & ~full_mask(first);
+  return FG_OK;
+}
+
+fg_status lars_adam_apply(const fg_opt_tensor *t, int32_t ntensors,
+                          const fg_opt_params *p, int32_t grad_format,
+                          float grad_inv_scale, const int32_t *found_nonfinite,
+                          int32_t nflags, int32_t *step_count, void *ws,
+                          size_t ws_bytes, hipStream_t stream) {
+  if (nflags < 0 || (nflags > 0 && !found_nonfinite)) return FG_EINVAL;
+  const fg_status st =
+      opt_call_ok(t, ntensors, p, grad_format, grad_inv_scale, step_count, ws, ws_bytes);
+  if (st != FG_OK) return st;
+  const uint64_t key = norms_key(t, ntensors, p, grad_format, grad_inv_scale, step_count);
+  {
+    std::lock_guard<std::mutex> lk(g_norms_mu);
+    auto it = g_norms.find((uintptr_t)ws);
+    if (it == g_norms.end() || it->second.key != key ||
+        it->second.mask != full_mask(ntensors))
+      return FG_EINVAL;
+    g_norms.erase(it);
+  }
+  return launch_status(launch_lars_adam_apply(t, ntensors, *p,
+                                              grad_format == FG_GRAD_F16_SCALED,
+                                              grad_inv_scale, found_nonfinite, nflags,
+                                              step_count, ws, stream));
 }
 
 fg_status l2_head_grad(const uint16_t *y, const float *t, uint64_t numel,

@@ -105,10 +105,14 @@ hipError_t launch_head_bwd_data(const uint16_t *dy, const uint16_t *w,
                                 int32_t epi, const uint16_t *gate,
                                 hipStream_t st);
 size_t lars_adam_ws_bytes(const fg_opt_tensor *ts, int32_t n);
-hipError_t launch_lars_adam(const fg_opt_tensor *ts, int32_t n, float lr, float b1,
-                            float b2, float eps, float wd, const int32_t *flags,
-                            int32_t nflags, int32_t *step_count, void *ws,
-                            hipStream_t st);
+hipError_t launch_lars_adam_norms(const fg_opt_tensor *ts, int32_t n, int32_t first,
+                                  int32_t count, const fg_opt_params &p, bool fp16_grad,
+                                  float inv_scale, const int32_t *step_count, void *ws,
+                                  hipStream_t st);
+hipError_t launch_lars_adam_apply(const fg_opt_tensor *ts, int32_t n,
+                                  const fg_opt_params &p, bool fp16_grad, float inv_scale,
+                                  const int32_t *flags, int32_t nflags,
+                                  int32_t *step_count, void *ws, hipStream_t st);
 hipError_t launch_head_wgrad(const uint16_t *x, const uint16_t *dy,
                              uint16_t *dw, int64_t npix, int32_t c,
                              float *ws, int32_t *flag, hipStream_t st);

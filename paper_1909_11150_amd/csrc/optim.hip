@@ -1,20 +1,27 @@
 // Layer-wise adaptive Adam update of the fp32 master weights (Section 6.2,
 // Model Implementation: LARS layer-wise rates used with Adam, beta1 0.9 and
-// beta2 0.999), consuming the unscaled fp32 gradients the unpack writes.
-// Per layer, with t the count of applied steps including this one:
+// beta2 0.999, L2 weight decay). Per layer, with t the count of applied
+// steps including this one:
 //   g~ = g + wd w;  m = b1 m + (1-b1) g~;  v = b2 v + (1-b2) g~^2;
 //   u = (m / (1-b1^t)) / (sqrt(v / (1-b2^t)) + eps);
 //   tau = ||w|| / ||u|| over the layer (1 if either is 0);
 //   w = w - lr tau u, and the fp16 working copy = w rounded nearest-even.
-// A step whose gradient groups were flagged non-finite is skipped on the
-// device: every kernel reads the flags and returns, so the host never waits.
+// The gradient g is either the fp32 unscaled gradient, or the fp16
+// loss-scaled gradient (a group-buffer slot) times 1/S, which is the same
+// fp32 value the unscale kernel writes.
+//
 // Three launches, all bandwidth-bound:
-//   1. moments: new m, v; per-workgroup sums of u^2 and w^2 (fixed-shape
-//      reduction) into the workspace;
-//   2. ratio: one thread per layer adds its workgroups' sums in order (fp64)
-//      and forms tau; thread 0 advances the step count;
-//   3. apply: recomputes u from the stored moments (the same fp32
-//      operations, so the same value) and writes w and its fp16 copy.
+//   1. norms: reads w, m, v, g and sums u^2 and w^2 per workgroup (fixed
+//      shape) into the workspace; writes nothing else, so it may run for a
+//      group of layers as soon as their gradients exist, while the backward
+//      pass still runs;
+//   2. ratio: one workgroup per layer adds its partial sums in a fixed order
+//      (fp64) and forms tau; the first advances the step count;
+//   3. apply: recomputes the new moments and u with the same fp32 operations
+//      and writes m, v, w and the fp16 copy.
+// A step whose gradient groups were flagged non-finite is skipped on the
+// device: the ratio and apply kernels read the flags and return, so the host
+// never waits.
 #include <cmath>
 
 #include "common.h"
@@ -23,7 +30,7 @@
 namespace fg {
 
 constexpr int kOptThreads = 256;
-constexpr int kOptIters = 4;                            // float4 per thread
+constexpr int kOptIters = 4;                            // 4-element chunks per thread
 constexpr int kOptElems = kOptThreads * 4 * kOptIters;  // per workgroup
 
 struct OptPiece {
@@ -32,6 +39,7 @@ struct OptPiece {
 };
 struct OptTable {
   int32_t n;
+  uint32_t nblocks;
   OptPiece p[FG_MAX_SEGMENTS];
 };
 struct OptParams {
@@ -53,12 +61,29 @@ __device__ __forceinline__ bool opt_skip(const int32_t *flags, int nflags) {
   return any;
 }
 
+// Per-step constants. The bias corrections 1 - b^t are formed in fp64 (in
+// fp32 the rounding of b^t would be amplified ~1/(1-b2) times for small t)
+// and enter as reciprocals; u uses the hardware square root and reciprocal
+// (about one ulp each), a few ulps from the correctly rounded quotient.
 struct OptStep {
-  float lr, b1, b2, eps, wd, bc1, bc2;
+  float b1, c1, b2, c2, eps, wd, rbc1, rbc2;
+  __device__ __forceinline__ void moments(float g, float w, float &m, float &v) const {
+    const float gt = g + wd * w;
+    m = b1 * m + c1 * gt;
+    v = b2 * v + c2 * (gt * gt);
+  }
   __device__ __forceinline__ float u(float m, float v) const {
-    return (m / bc1) / (sqrtf(v / bc2) + eps);
+    const float den = __builtin_amdgcn_sqrtf(v * rbc2) + eps;
+    return (m * rbc1) * __builtin_amdgcn_rcpf(den);
   }
 };
+
+__device__ __forceinline__ OptStep opt_step(const OptParams &p, int t) {
+  const double bc1 = 1.0 - pow((double)p.b1, (double)t);
+  const double bc2 = 1.0 - pow((double)p.b2, (double)t);
+  return OptStep{p.b1, 1.f - p.b1, p.b2, 1.f - p.b2, p.eps, p.wd,
+                 (float)(1.0 / bc1), (float)(1.0 / bc2)};
+}
 
 // The fp16 copy must be the rounding of the fp32 weight as stored. Without a
 // barrier the compiler folds the conversion into the update's fma (a mixed
@@ -69,15 +94,70 @@ __device__ __forceinline__ uint16_t stored_f32_to_h(float v) {
   return f32_to_h(v);
 }
 
-__device__ __forceinline__ OptStep opt_step(const OptParams &p, int t) {
-  return OptStep{p.lr, p.b1, p.b2, p.eps, p.wd,
-                 1.f - powf(p.b1, (float)t), 1.f - powf(p.b2, (float)t)};
+// Gradient access: fp32 as stored, or fp16 times 1/S (materialised before
+// use, so that the update sees the same fp32 value in both forms).
+template <bool H>
+struct Grad {
+  uint64_t p;
+  float inv;
+  __device__ __forceinline__ f32x4 load4(uint32_t i) const {
+    if constexpr (H) {
+      const u32x2 h = *reinterpret_cast<const u32x2 *>(
+          reinterpret_cast<const uint16_t *>(p) + i);
+      f32x4 g;
+      g[0] = h_to_f32((uint16_t)h[0]) * inv;
+      g[1] = h_to_f32((uint16_t)(h[0] >> 16)) * inv;
+      g[2] = h_to_f32((uint16_t)h[1]) * inv;
+      g[3] = h_to_f32((uint16_t)(h[1] >> 16)) * inv;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) asm volatile("" : "+v"(g[e]));
+      return g;
+    } else {
+      return *reinterpret_cast<const f32x4 *>(reinterpret_cast<const float *>(p) + i);
+    }
+  }
+  __device__ __forceinline__ float load1(uint32_t j) const {
+    if constexpr (H) {
+      float g = h_to_f32(reinterpret_cast<const uint16_t *>(p)[j]) * inv;
+      asm volatile("" : "+v"(g));
+      return g;
+    } else {
+      return reinterpret_cast<const float *>(p)[j];
+    }
+  }
+};
+
+// One 4-element chunk of a layer's arrays, zero beyond the layer's end
+// (zeros add nothing to either sum).
+template <bool H>
+__device__ __forceinline__ void load_chunk(const OptPiece &pc, const Grad<H> &gr,
+                                           uint32_t i, uint32_t end, f32x4 &g,
+                                           f32x4 &w, f32x4 &m, f32x4 &v) {
+  const float *wp = reinterpret_cast<const float *>(pc.w32);
+  const float *mp = reinterpret_cast<const float *>(pc.m);
+  const float *vp = reinterpret_cast<const float *>(pc.v);
+  if (i + 4 <= end) {
+    g = gr.load4(i);
+    w = *reinterpret_cast<const f32x4 *>(wp + i);
+    m = *reinterpret_cast<const f32x4 *>(mp + i);
+    v = *reinterpret_cast<const f32x4 *>(vp + i);
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const bool in = i + e < end;
+      g[e] = in ? gr.load1(i + e) : 0.f;
+      w[e] = in ? wp[i + e] : 0.f;
+      m[e] = in ? mp[i + e] : 0.f;
+      v[e] = in ? vp[i + e] : 0.f;
+    }
+  }
 }
 
 // sums of two values over the workgroup, fixed order: wave shuffles, then
-// the four wave results in order
-__device__ __forceinline__ void block_sum2(float &a, float &b) {
-  __shared__ float red[2][kOptThreads / 64];
+// the four wave results in order (thread 0 holds the result)
+template <typename T>
+__device__ __forceinline__ void block_sum2(T &a, T &b) {
+  __shared__ T red[2][kOptThreads / 64];
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
     a += __shfl_down(a, o, 64);
@@ -99,118 +179,127 @@ __device__ __forceinline__ void block_sum2(float &a, float &b) {
   }
 }
 
-__global__ __launch_bounds__(kOptThreads) void lars_adam_moments_kernel(
-    OptTable t, OptParams p, const int32_t *flags, int nflags,
-    const int32_t *step_count, float *part) {
-  if (opt_skip(flags, nflags)) return;
-  const OptPiece pc = t.p[opt_piece(t, blockIdx.x)];
+// Workgroup b0 + blockIdx.x of the table: sum of u^2 and of w^2 over its
+// kOptElems elements into part[2b], part[2b+1].
+template <bool H>
+__global__ __launch_bounds__(kOptThreads) void lars_adam_norms_kernel(
+    OptTable t, OptParams p, float inv, const int32_t *step_count, uint32_t b0,
+    float *part) {
+  const uint32_t b = b0 + blockIdx.x;
+  const OptPiece pc = t.p[opt_piece(t, b)];
   const OptStep s = opt_step(p, *step_count + 1);
-  const float *g = reinterpret_cast<const float *>(pc.g);
-  const float *w = reinterpret_cast<const float *>(pc.w32);
-  float *m = reinterpret_cast<float *>(pc.m);
-  float *v = reinterpret_cast<float *>(pc.v);
-  const uint32_t beg = (blockIdx.x - pc.block0) * (uint32_t)kOptElems;
+  const Grad<H> gr{pc.g, inv};
+  const uint32_t beg = (b - pc.block0) * (uint32_t)kOptElems;
   const uint32_t end = min(pc.numel, beg + (uint32_t)kOptElems);
-  float su = 0.f, sw = 0.f;
-  for (uint32_t i = beg + threadIdx.x * 4; i < end; i += kOptThreads * 4) {
-    if (i + 4 <= end) {
-      const f32x4 gv = *reinterpret_cast<const f32x4 *>(g + i);
-      const f32x4 wv = *reinterpret_cast<const f32x4 *>(w + i);
-      f32x4 mv = *reinterpret_cast<const f32x4 *>(m + i);
-      f32x4 vv = *reinterpret_cast<const f32x4 *>(v + i);
+  f32x4 g[kOptIters], w[kOptIters], m[kOptIters], v[kOptIters];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float gt = gv[e] + s.wd * wv[e];
-        mv[e] = s.b1 * mv[e] + (1.f - s.b1) * gt;
-        vv[e] = s.b2 * vv[e] + (1.f - s.b2) * gt * gt;
-        const float u = s.u(mv[e], vv[e]);
-        su += u * u;
-        sw += wv[e] * wv[e];
-      }
-      *reinterpret_cast<f32x4 *>(m + i) = mv;
-      *reinterpret_cast<f32x4 *>(v + i) = vv;
-    } else {
-      for (uint32_t j = i; j < end; ++j) {
-        const float gt = g[j] + s.wd * w[j];
-        const float mj = s.b1 * m[j] + (1.f - s.b1) * gt;
-        const float vj = s.b2 * v[j] + (1.f - s.b2) * gt * gt;
-        const float u = s.u(mj, vj);
-        m[j] = mj;
-        v[j] = vj;
-        su += u * u;
-        sw += w[j] * w[j];
-      }
+  for (int c = 0; c < kOptIters; ++c) {
+    const uint32_t i = beg + (c * kOptThreads + threadIdx.x) * 4;
+    load_chunk<H>(pc, gr, i, end, g[c], w[c], m[c], v[c]);
+  }
+  float su = 0.f, sw = 0.f;
+#pragma unroll
+  for (int c = 0; c < kOptIters; ++c) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float mm = m[c][e], vv = v[c][e];
+      s.moments(g[c][e], w[c][e], mm, vv);
+      const float u = s.u(mm, vv);
+      su += u * u;
+      sw += w[c][e] * w[c][e];
     }
   }
   block_sum2(su, sw);
   if (threadIdx.x == 0) {
-    part[2 * blockIdx.x] = su;
-    part[2 * blockIdx.x + 1] = sw;
+    part[2 * b] = su;
+    part[2 * b + 1] = sw;
   }
 }
 
-__global__ __launch_bounds__(64) void lars_adam_ratio_kernel(
+// One workgroup per layer: tau from the layer's partial sums (fp64, fixed
+// order). Workgroup 0 advances the step count.
+__global__ __launch_bounds__(kOptThreads) void lars_adam_ratio_kernel(
     OptTable t, const int32_t *flags, int nflags, int32_t *step_count,
-    const float *part, uint32_t nblocks, float *ratio, int32_t *t_cur) {
+    const float *part, float *ratio, int32_t *t_cur) {
   if (opt_skip(flags, nflags)) return;
-  const int l = threadIdx.x;
-  if (l < t.n) {
-    const uint32_t b0 = t.p[l].block0;
-    const uint32_t b1 = l + 1 < t.n ? t.p[l + 1].block0 : nblocks;
-    double su = 0.0, sw = 0.0;
-    for (uint32_t b = b0; b < b1; ++b) {
-      su += (double)part[2 * b];
-      sw += (double)part[2 * b + 1];
-    }
-    ratio[l] = su > 0.0 && sw > 0.0 ? (float)(sqrt(sw) / sqrt(su)) : 1.f;
+  const int l = blockIdx.x;
+  const uint32_t b0 = t.p[l].block0;
+  const uint32_t b1 = l + 1 < t.n ? t.p[l + 1].block0 : t.nblocks;
+  double su = 0.0, sw = 0.0;
+  for (uint32_t b = b0 + threadIdx.x; b < b1; b += kOptThreads) {
+    su += (double)part[2 * b];
+    sw += (double)part[2 * b + 1];
   }
-  if (l == 0) {
-    const int32_t tn = *step_count + 1;
-    *t_cur = tn;
-    *step_count = tn;
+  block_sum2(su, sw);
+  if (threadIdx.x == 0) {
+    ratio[l] = su > 0.0 && sw > 0.0 ? (float)(sqrt(sw) / sqrt(su)) : 1.f;
+    if (l == 0) {
+      const int32_t tn = *step_count + 1;
+      *t_cur = tn;
+      *step_count = tn;
+    }
   }
 }
 
+template <bool H>
 __global__ __launch_bounds__(kOptThreads) void lars_adam_apply_kernel(
-    OptTable t, OptParams p, const int32_t *flags, int nflags,
+    OptTable t, OptParams p, float inv, const int32_t *flags, int nflags,
     const float *ratio, const int32_t *t_cur) {
   if (opt_skip(flags, nflags)) return;
   const int pi = opt_piece(t, blockIdx.x);
   const OptPiece pc = t.p[pi];
   const OptStep s = opt_step(p, *t_cur);
-  const float step = s.lr * ratio[pi];
-  const float *m = reinterpret_cast<const float *>(pc.m);
-  const float *v = reinterpret_cast<const float *>(pc.v);
-  float *w = reinterpret_cast<float *>(pc.w32);
-  uint16_t *w16 = reinterpret_cast<uint16_t *>(pc.w16);
+  const float step = p.lr * ratio[pi];
+  const Grad<H> gr{pc.g, inv};
+  float *wp = reinterpret_cast<float *>(pc.w32);
+  float *mp = reinterpret_cast<float *>(pc.m);
+  float *vp = reinterpret_cast<float *>(pc.v);
+  uint16_t *hp = reinterpret_cast<uint16_t *>(pc.w16);
   const uint32_t beg = (blockIdx.x - pc.block0) * (uint32_t)kOptElems;
   const uint32_t end = min(pc.numel, beg + (uint32_t)kOptElems);
-  for (uint32_t i = beg + threadIdx.x * 4; i < end; i += kOptThreads * 4) {
-    if (i + 4 <= end) {
-      const f32x4 mv = *reinterpret_cast<const f32x4 *>(m + i);
-      const f32x4 vv = *reinterpret_cast<const f32x4 *>(v + i);
-      f32x4 wv = *reinterpret_cast<const f32x4 *>(w + i);
+  f32x4 g[kOptIters], w[kOptIters], m[kOptIters], v[kOptIters];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) wv[e] = wv[e] - step * s.u(mv[e], vv[e]);
-      *reinterpret_cast<f32x4 *>(w + i) = wv;
+  for (int c = 0; c < kOptIters; ++c) {
+    const uint32_t i = beg + (c * kOptThreads + threadIdx.x) * 4;
+    load_chunk<H>(pc, gr, i, end, g[c], w[c], m[c], v[c]);
+  }
+#pragma unroll
+  for (int c = 0; c < kOptIters; ++c) {
+    const uint32_t i = beg + (c * kOptThreads + threadIdx.x) * 4;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float mm = m[c][e], vv = v[c][e];
+      s.moments(g[c][e], w[c][e], mm, vv);
+      m[c][e] = mm;
+      v[c][e] = vv;
+      w[c][e] = w[c][e] - step * s.u(mm, vv);
+    }
+    if (i + 4 <= end) {
+      *reinterpret_cast<f32x4 *>(mp + i) = m[c];
+      *reinterpret_cast<f32x4 *>(vp + i) = v[c];
+      *reinterpret_cast<f32x4 *>(wp + i) = w[c];
       u32x2 h;
-      h[0] = (uint32_t)stored_f32_to_h(wv[0]) |
-             ((uint32_t)stored_f32_to_h(wv[1]) << 16);
-      h[1] = (uint32_t)stored_f32_to_h(wv[2]) |
-             ((uint32_t)stored_f32_to_h(wv[3]) << 16);
-      *reinterpret_cast<u32x2 *>(w16 + i) = h;
+      h[0] = (uint32_t)stored_f32_to_h(w[c][0]) |
+             ((uint32_t)stored_f32_to_h(w[c][1]) << 16);
+      h[1] = (uint32_t)stored_f32_to_h(w[c][2]) |
+             ((uint32_t)stored_f32_to_h(w[c][3]) << 16);
+      *reinterpret_cast<u32x2 *>(hp + i) = h;
     } else {
-      for (uint32_t j = i; j < end; ++j) {
-        const float wj = w[j] - step * s.u(m[j], v[j]);
-        w[j] = wj;
-        w16[j] = stored_f32_to_h(wj);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if (i + e < end) {
+          mp[i + e] = m[c][e];
+          vp[i + e] = v[c][e];
+          wp[i + e] = w[c][e];
+          hp[i + e] = stored_f32_to_h(w[c][e]);
+        }
       }
     }
   }
 }
 
 // ---------------------------------------------------------------------------
-static uint32_t opt_table(const fg_opt_tensor *ts, int32_t n, OptTable &t) {
+static void opt_table(const fg_opt_tensor *ts, int32_t n, OptTable &t) {
   uint32_t nb = 0;
   t.n = n;
   for (int i = 0; i < n; ++i) {
@@ -218,36 +307,69 @@ static uint32_t opt_table(const fg_opt_tensor *ts, int32_t n, OptTable &t) {
                       (uint32_t)ts[i].numel, nb};
     nb += (uint32_t)((ts[i].numel + kOptElems - 1) / kOptElems);
   }
-  return nb;
+  t.nblocks = nb;
 }
+
+struct OptWs {
+  float *part, *ratio;
+  int32_t *t_cur;
+};
 
 // workspace: [2 * nblocks floats of partial sums][ratio per layer][t]
-size_t lars_adam_ws_bytes(const fg_opt_tensor *ts, int32_t n) {
-  OptTable t;
-  const uint32_t nb = opt_table(ts, n, t);
-  return (size_t)nb * 2 * sizeof(float) + (size_t)FG_MAX_SEGMENTS * sizeof(float) + 16;
-}
-
-hipError_t launch_lars_adam(const fg_opt_tensor *ts, int32_t n, float lr, float b1,
-                            float b2, float eps, float wd, const int32_t *flags,
-                            int32_t nflags, int32_t *step_count, void *ws,
-                            hipStream_t st) {
-  OptTable t;
-  const uint32_t nb = opt_table(ts, n, t);
-  const OptParams p{lr, b1, b2, eps, wd};
+static OptWs opt_ws(void *ws, uint32_t nb) {
   float *part = reinterpret_cast<float *>(ws);
   float *ratio = part + 2 * (size_t)nb;
-  int32_t *t_cur = reinterpret_cast<int32_t *>(ratio + FG_MAX_SEGMENTS);
-  hipLaunchKernelGGL(lars_adam_moments_kernel, dim3(nb), dim3(kOptThreads), 0, st,
-                     t, p, flags, nflags, step_count, part);
+  return OptWs{part, ratio, reinterpret_cast<int32_t *>(ratio + FG_MAX_SEGMENTS)};
+}
+
+size_t lars_adam_ws_bytes(const fg_opt_tensor *ts, int32_t n) {
+  OptTable t;
+  opt_table(ts, n, t);
+  return (size_t)t.nblocks * 2 * sizeof(float) + (size_t)FG_MAX_SEGMENTS * sizeof(float) +
+         16;
+}
+
+static OptParams opt_params(const fg_opt_params &p) {
+  return OptParams{p.lr, p.beta1, p.beta2, p.eps, p.weight_decay};
+}
+
+hipError_t launch_lars_adam_norms(const fg_opt_tensor *ts, int32_t n, int32_t first,
+                                  int32_t count, const fg_opt_params &pp, bool fp16_grad,
+                                  float inv_scale, const int32_t *step_count, void *ws,
+                                  hipStream_t st) {
+  OptTable t;
+  opt_table(ts, n, t);
+  const OptParams p = opt_params(pp);
+  const uint32_t b0 = t.p[first].block0;
+  const uint32_t b1 = first + count < n ? t.p[first + count].block0 : t.nblocks;
+  const OptWs w = opt_ws(ws, t.nblocks);
+  if (fp16_grad)
+    hipLaunchKernelGGL(lars_adam_norms_kernel<true>, dim3(b1 - b0), dim3(kOptThreads), 0,
+                       st, t, p, inv_scale, step_count, b0, w.part);
+  else
+    hipLaunchKernelGGL(lars_adam_norms_kernel<false>, dim3(b1 - b0), dim3(kOptThreads), 0,
+                       st, t, p, inv_scale, step_count, b0, w.part);
+  return hipGetLastError();
+}
+
+hipError_t launch_lars_adam_apply(const fg_opt_tensor *ts, int32_t n,
+                                  const fg_opt_params &pp, bool fp16_grad, float inv_scale,
+                                  const int32_t *flags, int32_t nflags,
+                                  int32_t *step_count, void *ws, hipStream_t st) {
+  OptTable t;
+  opt_table(ts, n, t);
+  const OptParams p = opt_params(pp);
+  const OptWs w = opt_ws(ws, t.nblocks);
+  hipLaunchKernelGGL(lars_adam_ratio_kernel, dim3(n), dim3(kOptThreads), 0, st, t, flags,
+                     nflags, step_count, w.part, w.ratio, w.t_cur);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(lars_adam_ratio_kernel, dim3(1), dim3(64), 0, st, t, flags,
-                     nflags, step_count, part, nb, ratio, t_cur);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(lars_adam_apply_kernel, dim3(nb), dim3(kOptThreads), 0, st,
-                     t, p, flags, nflags, ratio, t_cur);
+  if (fp16_grad)
+    hipLaunchKernelGGL(lars_adam_apply_kernel<true>, dim3(t.nblocks), dim3(kOptThreads), 0,
+                       st, t, p, inv_scale, flags, nflags, w.ratio, w.t_cur);
+  else
+    hipLaunchKernelGGL(lars_adam_apply_kernel<false>, dim3(t.nblocks), dim3(kOptThreads), 0,
+                       st, t, p, inv_scale, flags, nflags, w.ratio, w.t_cur);
   return hipGetLastError();
 }
 

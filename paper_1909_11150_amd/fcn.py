@@ -20,7 +20,7 @@ import torch
 
 from . import (EPI_GATE, EPI_NONE, EPI_RELU, OP_BWD_DATA, OP_BWD_WEIGHT,
                OP_CONVT, OP_FWD, ConvDesc, FgError, OptParams, Segment,
-               kernel_name, lib,
+               GRAD_F16_SCALED, GRAD_F32, kernel_name, lib,
                conv2d_bwd_data, conv2d_bwd_weight, conv2d_bwd_weight_checked,
                conv2d_fwd,
                conv_transpose2d_fwd, grad_group_pack, grad_group_plan,
@@ -343,9 +343,12 @@ class Chain:
         return StepProgram(self, target, streams)
 
 
-# algorithmic HBM bytes of the optimizer per parameter: w, m, v and the fp32
-# gradient read (16), w, m, v and the fp16 copy written (14)
-OPT_BYTES_PER_PARAM = 30
+# algorithmic HBM bytes of the optimizer per parameter: w, m, v and the
+# gradient read (12 + 4 for fp32 gradients, 12 + 2 for fp16 ones) and w, m,
+# v and the fp16 copy written (14). The norms pass reads, the apply pass
+# reads and writes.
+OPT_READ_BYTES = 12
+OPT_WRITE_BYTES = 14
 
 # label, main kernel, algorithmic work (flops, or bytes for the gradient
 # path), C function (None: a Python callable), argument tuple (the stream
@@ -381,9 +384,13 @@ class StepProgram:
     reads. Every kernel is deterministic and reads only finished inputs, so
     the results are identical to the one-stream order (``streams=1``).
 
-    With an optimizer, stream 2 ends with the update (after the last
-    unpack and the main stream's last pass, which reads the fp16 weights).
-    With an optimizer or a loss scaler, it then copies the group flags to
+    With an optimizer, stream 2 also runs each group's optimizer norms pass
+    (the part that reads the gradients; it writes only the workspace) right
+    after the group's gradient path, and ends with the ratio and apply
+    launches (after the main stream's last pass, which reads the fp16
+    weights). With zero-copy groups the norms and apply read the fp16
+    loss-scaled gradients in the group slots, and the unscale and unpack
+    are left out (the kernel gradients raise the flags). With an optimizer or a loss scaler, it then copies the group flags to
     pinned host memory; the next run waits for that copy just before its
     head call (its forward pass already queued), updates the scaler and the
     applied count, and patches the loss-scale and learning-rate arguments."""
@@ -469,6 +476,22 @@ class StepProgram:
             return Call(label, kname, flops, L_.conv2d_bwd_weight,
                         (desc(d), ptr(x), ptr(dy), ptr(ch.dw[i]), ws2, wsb2, st),
                         one(d, OP_BWD_WEIGHT), sid=1, deps=(writer[i + 1],))
+        self.params = None
+        if ch.opt is not None:
+            # with zero-copy groups the optimizer reads each layer's fp16
+            # loss-scaled gradient in its group slot (flags come from the
+            # kernel gradients, so no unscale or unpack is needed); otherwise
+            # the fp32 gradients the unpack writes
+            o = ch.opt
+            self.params = OptParams(o.lr_at(ch.applied), o.beta1, o.beta2, o.eps,
+                                    o.weight_decay)
+            fused = ch.zero_copy
+            tab = opt_tensors(ch.w32, ch.w, ch.m, ch.v, ch.dw) if fused else ch.opt_tensors
+            self._opt = dict(tab=tab, fmt=GRAD_F16_SCALED if fused else GRAD_F32,
+                             inv=self._inv_scale if fused else ctypes.c_float(1.0),
+                             gb=2 if fused else 4, h="true" if fused else "false",
+                             fused=fused, n=sum(w.numel() for w in ch.w32))
+            self._keep.append(tab)
         last_dw = {}
         for i in reversed(range(nl)):
             L = ch.layers[i]
@@ -497,20 +520,18 @@ class StepProgram:
             writer[i] = len(calls) - 1
             gi = ch._group_done_at.get(i)
             if gi is not None:
-                gc = self._group_calls(ch, gi, L_, st)
+                gc = self._group_calls(ch, gi, L_, st) + self._norms_calls(ch, gi, L_, st)
                 gc[0] = gc[0]._replace(deps=(last_dw[i],))
                 calls += gc
-        self.params = None
         if ch.opt is not None:
-            # after the last group's unpack (stream order) and the last pass
-            # that reads the fp16 weights (the main stream's last call)
-            o = ch.opt
-            self.params = OptParams(o.lr_at(ch.applied), o.beta1, o.beta2, o.eps,
-                                    o.weight_decay)
-            ntot = sum(w.numel() for w in ch.w32)
-            calls.append(Call("opt.update", "lars_adam_moments_kernel",
-                              OPT_BYTES_PER_PARAM * ntot, L_.lars_adam_update,
-                              (ch.opt_tensors, nl, ctypes.byref(self.params),
+            # ratio and apply: after the last group's norms (stream order) and
+            # the last pass that reads the fp16 weights (the main stream's
+            # last call)
+            o = self._opt
+            calls.append(Call("opt.apply", f"lars_adam_apply_kernel<{o['h']}>",
+                              (OPT_READ_BYTES + o["gb"] + OPT_WRITE_BYTES) * o["n"],
+                              L_.lars_adam_apply,
+                              (o["tab"], nl, ctypes.byref(self.params), o["fmt"], o["inv"],
                                ch.flags.data_ptr(), len(ch.groups),
                                ch.step_count.data_ptr(), ch.opt_ws.data_ptr(),
                                ch.opt_ws.numel(), st), False, sid=2,
@@ -540,7 +561,23 @@ class StepProgram:
         self.calls = calls
         self.ch = ch
 
+    def _norms_calls(self, ch, gi, L_, st):
+        if ch.opt is None:
+            return []
+        mem = sorted(ch.groups[gi]["members"])
+        first, count = mem[0], len(mem)
+        assert mem == list(range(first, first + count)), "a group is a layer range"
+        o = self._opt
+        n = sum(ch.w32[i].numel() for i in mem)
+        return [Call(f"G{gi}.norms", f"lars_adam_norms_kernel<{o['h']}>",
+                     (OPT_READ_BYTES + o["gb"]) * n, L_.lars_adam_norms,
+                     (o["tab"], len(ch.layers), first, count, ctypes.byref(self.params),
+                      o["fmt"], o["inv"], ch.step_count.data_ptr(), ch.opt_ws.data_ptr(),
+                      ch.opt_ws.numel(), st), sid=2)]
+
     def _group_calls(self, ch, gi, L_, st):
+        if ch.opt is not None and self._opt["fused"]:
+            return []
         g = ch.groups[gi]
         n = g["numel"]
         src = (Segment * len(g["members"]))(

@@ -191,3 +191,39 @@ def test_optimizer_argument_checks(L):
     alias = (fg.OptTensor * 2)(layer(FAKE), layer(FAKE + 2048))  # second w32 inside the first
     assert L.lars_adam_update(alias, 2, ref(p), None, 0, sc, ws, need, None) == fg.FG_EINVAL
     assert L.lars_adam_update(good, 2, ref(p), None, 0, FAKE + 64, ws, need, None) == fg.FG_EINVAL
+
+
+def test_optimizer_split_argument_checks(L):
+    """lars_adam_norms / lars_adam_apply reject bad ranges, gradient forms
+    and scales, and an apply without norms, before touching the device."""
+    ref = ctypes.byref
+    n = 1024
+
+    def layer(base, g_off=4 << 16):
+        return fg.OptTensor(base, base + (1 << 16), base + (2 << 16), base + (3 << 16),
+                            base + g_off, n)
+
+    good = (fg.OptTensor * 2)(layer(FAKE), layer(FAKE + (1 << 20)))
+    p = fg.OptParams(1e-3, 0.9, 0.999, 1e-8, 1e-4)
+    sc, ws = FAKE + (1 << 24), FAKE + (1 << 25)
+    need = L.fg_lars_adam_workspace_bytes(good, 2)
+    F32, F16 = fg.GRAD_F32, fg.GRAD_F16_SCALED
+    for first, count in ((-1, 1), (0, 0), (1, 2), (2, 1)):
+        assert L.lars_adam_norms(good, 2, first, count, ref(p), F32, 1.0, sc, ws, need,
+                                 None) == fg.FG_EINVAL
+    assert L.lars_adam_norms(good, 2, 0, 2, ref(p), 2, 1.0, sc, ws, need, None) == fg.FG_EINVAL
+    for inv in (0.0, -1.0, float("nan"), float("inf")):
+        assert L.lars_adam_norms(good, 2, 0, 2, ref(p), F16, inv, sc, ws, need,
+                                 None) == fg.FG_EINVAL
+    assert L.lars_adam_norms(good, 2, 0, 2, ref(p), F32, 1.0, sc, ws, need - 4,
+                             None) == fg.FG_EWORKSPACE
+    # an fp16 gradient needs 8-byte alignment, an fp32 one 16
+    g8 = (fg.OptTensor * 1)(layer(FAKE, (4 << 16) + 8))
+    assert L.lars_adam_norms(g8, 1, 0, 1, ref(p), F32, 1.0, sc, ws, need, None) == fg.FG_EINVAL
+    g4 = (fg.OptTensor * 1)(layer(FAKE, (4 << 16) + 4))
+    assert L.lars_adam_norms(g4, 1, 0, 1, ref(p), F16, 0.5, sc, ws, need, None) == fg.FG_EINVAL
+    # no norms on this workspace yet: the apply is refused before any launch
+    assert L.lars_adam_apply(good, 2, ref(p), F32, 1.0, None, 0, sc, ws, need,
+                             None) == fg.FG_EINVAL
+    assert L.lars_adam_apply(good, 2, ref(p), F32, 1.0, None, 2, sc, ws, need,
+                             None) == fg.FG_EINVAL

@@ -110,3 +110,68 @@ def test_zero_weight_layer_and_determinism():
         assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
     w1, m1, v1, h1, _ = outs[0]
     check_opt_layer(w[0], m[0], v[0], g[0], 1, 1e-3, w1[0], m1[0], v1[0], h1[0])
+
+
+def _split(d, lr, ranges, flags=None, fmt=fg.GRAD_F32, inv=1.0, g=None):
+    """The update as norms over the given layer ranges, then the apply."""
+    tens = d.tens if g is None else fg.opt_tensors(d.w32, d.w16, d.m, d.v, g)
+    for first, count in ranges:
+        fg.lars_adam_norms(tens, first, count, d.step, d.ws, fmt, inv, **HP)
+    fg.lars_adam_apply(tens, lr, flags, d.step, d.ws, fmt, inv, **HP)
+    torch.cuda.synchronize()
+
+
+def _bits_equal(a, b):
+    return all(np.array_equal(x.view(np.uint8), y.view(np.uint8))
+               for xs, ys in zip(a[:4], b[:4]) for x, y in zip(xs, ys)) and a[4] == b[4]
+
+
+def test_split_update_equals_update():
+    """Norms per range of layers (any split) then apply: the same bits as
+    lars_adam_update."""
+    w, m, v, g = _state(6)
+    ref = Dev(w, m, v, g, step=2)
+    ref.update(3e-3)
+    for ranges in ([(0, len(SIZES))], [(3, 3), (0, 1), (1, 2)],
+                   [(i, 1) for i in reversed(range(len(SIZES)))]):
+        d = Dev(w, m, v, g, step=2)
+        _split(d, 3e-3, ranges)
+        assert _bits_equal(d.host(), ref.host()), ranges
+
+
+def test_fp16_scaled_gradients_equal_unscaled_fp32():
+    """The optimizer reading fp16 loss-scaled gradients with 1/S gives the
+    bits it gives on the fp32 gradients the unscale check writes for them."""
+    sizes = [3, 4096, 70001, 262147]
+    w, m, v, _ = _state(7, sizes)
+    rng = np.random.default_rng(8)
+    S = 2.0 ** 13
+    g16 = [(rng.normal(size=n) * 1e-3 * S).astype(np.float16) for n in sizes]
+    g32 = [x.astype(np.float32) * np.float32(1.0 / S) for x in g16]
+    a = Dev(w, m, v, g32, step=4)
+    a.update(1e-3)
+    b = Dev(w, m, v, g32, step=4)
+    gd = [torch.from_numpy(x).cuda() for x in g16]
+    _split(b, 1e-3, [(2, 2), (0, 2)], fmt=fg.GRAD_F16_SCALED, inv=1.0 / S, g=gd)
+    assert _bits_equal(a.host(), b.host())
+    w1, m1, v1, h1, _ = b.host()
+    for i in range(len(sizes)):
+        check_opt_layer(w[i], m[i], v[i], g32[i], 5, 1e-3, w1[i], m1[i], v1[i], h1[i])
+
+
+def test_apply_needs_norms_of_every_layer():
+    w, m, v, g = _state(9, [100, 5000, 17])
+    d = Dev(w, m, v, g)
+    before = d.host()
+    fg.lars_adam_norms(d.tens, 0, 2, d.step, d.ws, **HP)
+    with pytest.raises(fg.FgError):      # layer 2 not covered
+        fg.lars_adam_apply(d.tens, 1e-3, None, d.step, d.ws, **HP)
+    fg.lars_adam_norms(d.tens, 2, 1, d.step, d.ws, fg.GRAD_F16_SCALED, 0.5, **HP)
+    with pytest.raises(fg.FgError):      # another gradient form: coverage restarts
+        fg.lars_adam_apply(d.tens, 1e-3, None, d.step, d.ws, **HP)
+    torch.cuda.synchronize()
+    assert _bits_equal(d.host(), before)
+    _split(d, 1e-3, [(1, 2), (0, 1)])
+    assert d.host()[4] == 1
+    with pytest.raises(fg.FgError):      # consumed by the apply
+        fg.lars_adam_apply(d.tens, 1e-3, None, d.step, d.ws, **HP)

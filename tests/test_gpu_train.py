@@ -5,7 +5,8 @@ fp32 master weights and the backoff loss scale, run by the step program.
 Each step is checked against the oracle on the GPU's own inputs of that
 step: the head gradient against fp16(2 S (y - t) / numel) with the scale S
 the step was given (bit for bit: both round one fp64 value), the unpacked
-gradients against fp16 dW / S (exact), the group flags against the
+gradients against fp16 dW / S (exact; with zero-copy groups the optimizer
+reads dW / S from the fp16 slots itself), the group flags against the
 non-finite entries of dW, a skipped step against the state before it (bit
 for bit), an applied step layer by layer against the optimizer oracle (the
 rule of the optimizer's own parity tests), and the loss-scale sequence
@@ -76,10 +77,13 @@ def _run(ch, t, nsteps, lr_of, program=None):
                                       ref.view(np.uint16))
         # unpacked gradients, flags
         dws = [host(d).ravel() for d in ch.dw]
-        gs = [host(m).ravel() for m in ch.master]
         inv = np.float32(1.0 / S)
-        for d, g in zip(dws, gs):
-            np.testing.assert_array_equal(g, d.astype(np.float32) * inv)
+        if ch.zero_copy:  # the optimizer reads the fp16 slots: dW / S
+            gs = [d.astype(np.float32) * inv for d in dws]
+        else:
+            gs = [host(m).ravel() for m in ch.master]
+            for d, g in zip(dws, gs):
+                np.testing.assert_array_equal(g, d.astype(np.float32) * inv)
         assert found == any(not np.isfinite(d.astype(np.float32)).all() for d in dws)
         if found:
             assert _same(before, after), "a flagged step changed the state"
@@ -134,6 +138,28 @@ def test_overflow_backs_off_and_skips(zero_copy):
     assert (sc.scale, sc.clean) == (s, c)
     assert ch.applied == found.count(False)
     assert any(b > a for (a, _), (b, _) in zip(seq, seq[1:])), "the scale never grew"
+
+
+def test_fp16_slot_optimizer_equals_fp32_gradient_path():
+    """Zero-copy groups (optimizer on the fp16 slots, no unscale/unpack) and
+    packed groups (optimizer on the unpacked fp32 gradients) give the same
+    bits over steps with skips and scale changes."""
+    layers, x, w, t = _reduced()
+    td = dev(t - np.float32(40.0))
+    out = []
+    for zc in (False, True):
+        ch = Chain(layers, w, x, group_cap_bytes=CAP, zero_copy=zc,
+                   optimizer=_opt(1e-3), scaler=LossScaler(2.0 ** 15, interval=2))
+        prog = ch.program(td)
+        labels = [c.label for c in prog.calls]
+        assert any(".norms" in c for c in labels)
+        assert any(".unscale" in c for c in labels) == (not zc)
+        for _ in range(8):
+            prog.run()
+        ch.observe()
+        out.append((_state(ch), ch.loss_scale, ch.applied))
+    assert _same(out[0][0], out[1][0])
+    assert out[0][1:] == out[1][1:]
 
 
 @pytest.mark.parametrize("zero_copy", [False, True])
