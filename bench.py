@@ -399,6 +399,7 @@ def main():
     e_start.record()
     for s_ev in dom_ev:
         prog.run(s_ev)
+    prog.join()
     e_end.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -463,7 +464,8 @@ def main():
     if args.optimizer:
         ch.observe()
         nrm = [v for k, v in per_op.items() if k.endswith(".norms")]
-        ap = per_op["opt.apply"]
+        aps = [v for k, v in per_op.items() if k.endswith(".apply")]
+        ap = (sum(v[0] for v in aps), sum(v[1] for v in aps))
         n_ms, n_b = sum(v[0] for v in nrm), sum(v[1] for v in nrm)
         out["optimizer"] = {
             "norms_ms": round(n_ms, 4), "norms_GBps": round(n_b / (n_ms * 1e-3) / 1e9, 1),
@@ -471,6 +473,7 @@ def main():
             "gradients": "fp16 group slots" if args.zero_copy else "fp32 unpacked",
             "bytes_per_param": "norms: w, m, v, gradient read; apply: the same read, "
                                "w, m, v, fp16 copy written",
+            "apply_overlap": "per layer, beside the next step's forward pass",
             "timed_updates_applied": ch.applied - applied0,
             "loss_scale_start": scale0, "loss_scale_end": ch.loss_scale}
     if args.detail:

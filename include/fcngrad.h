@@ -268,31 +268,37 @@ fg_status lars_adam_update(const fg_opt_tensor *t, int32_t ntensors,
                            int32_t *step_count, void *ws, size_t ws_bytes,
                            hipStream_t stream);
 
-/* The update of lars_adam_update in two parts, so that the part that reads
- * each layer's gradient can run as soon as that gradient exists (e.g. per
- * gradient group, beside the rest of the backward pass) and only the writes
- * remain after it. lars_adam_norms reads layers [first, first + count) of
- * the table t (weights, moments, gradient; nothing is written but ws) and
- * stores their partial sums of u^2 and w^2 in ws; t = *step_count + 1 as
- * lars_adam_update. lars_adam_apply then forms every layer's tau, skips the
- * step if any flag is set, and otherwise writes m, v, w, the fp16 copy and
- * the step count as lars_adam_update. Between the norms calls that cover
- * every layer and the apply, the caller passes the same table, params
- * (lr aside), gradient form, grad_inv_scale, step_count and ws, and changes
- * none of the layer arrays; the apply must be ordered after every norms
- * call on the device (same stream or an event). Validation as
- * lars_adam_update, with the gradient form (FG_GRAD_*) and, for fp16
- * gradients, a finite grad_inv_scale > 0; lars_adam_norms also returns
- * FG_EINVAL for a range outside the table, and lars_adam_apply returns
- * FG_EINVAL, before any launch, unless norms calls with these arguments
- * have covered every layer since the last apply on this ws (tracked on the
- * host per workspace address; a lars_adam_update on ws clears it). */
+/* The update of lars_adam_update in parts, so that the part that reads each
+ * layer's gradient can run as soon as that gradient exists (e.g. per
+ * gradient group, beside the rest of the backward pass), and each layer's
+ * writes just before that layer's weights are next read (e.g. the next
+ * forward pass, layer by layer).
+ * lars_adam_norms reads layers [first, first + count) of the table t
+ * (weights, moments, gradient; nothing is written but ws) and stores their
+ * partial sums of u^2 and w^2 in ws; t = *step_count + 1 as in
+ * lars_adam_update. lars_adam_apply, once norms calls have covered every
+ * layer, writes m, v, w and the fp16 copy of layers [first, first + count)
+ * as lars_adam_update does, or nothing if a flag is set; the first apply
+ * call of a step also forms every layer's tau and advances *step_count (or
+ * leaves it if a flag is set). Between the first norms call and the apply
+ * call that completes the table, the caller passes the same table, params
+ * (lr aside), gradient form, grad_inv_scale, step_count and ws, changes
+ * none of the layer arrays, and orders every apply after every norms call
+ * and later applies after the first on the device (same stream, or
+ * events). Validation as lars_adam_update, with the gradient form
+ * (FG_GRAD_*), for fp16 gradients a finite grad_inv_scale > 0, and a range
+ * inside the table. Tracked on the host per workspace address, before any
+ * launch: lars_adam_apply returns FG_EINVAL unless norms calls with these
+ * arguments have covered every layer since the last completed apply and
+ * its range holds no layer already applied in this step; lars_adam_norms
+ * returns FG_EINVAL while the apply of a step is incomplete. A
+ * lars_adam_update on ws clears the record. */
 fg_status lars_adam_norms(const fg_opt_tensor *t, int32_t ntensors, int32_t first,
                           int32_t count, const fg_opt_params *p, int32_t grad_format,
                           float grad_inv_scale, const int32_t *step_count, void *ws,
                           size_t ws_bytes, hipStream_t stream);
-fg_status lars_adam_apply(const fg_opt_tensor *t, int32_t ntensors,
-                          const fg_opt_params *p, int32_t grad_format,
+fg_status lars_adam_apply(const fg_opt_tensor *t, int32_t ntensors, int32_t first,
+                          int32_t count, const fg_opt_params *p, int32_t grad_format,
                           float grad_inv_scale, const int32_t *found_nonfinite,
                           int32_t nflags, int32_t *step_count, void *ws,
                           size_t ws_bytes, hipStream_t stream);

@@ -114,7 +114,7 @@ def lib():
                                   ctypes.POINTER(OptParams), i32, ctypes.c_float, vp,
                                   vp, sz, vp]
     L.lars_adam_norms.restype = ctypes.c_int
-    L.lars_adam_apply.argtypes = [ctypes.POINTER(OptTensor), i32,
+    L.lars_adam_apply.argtypes = [ctypes.POINTER(OptTensor), i32, i32, i32,
                                   ctypes.POINTER(OptParams), i32, ctypes.c_float, vp,
                                   i32, vp, vp, sz, vp]
     L.lars_adam_apply.restype = ctypes.c_int
@@ -248,14 +248,17 @@ def lars_adam_norms(tensors, first, count, step_count, ws, grad_format=GRAD_F32,
 
 def lars_adam_apply(tensors, lr, flags, step_count, ws, grad_format=GRAD_F32,
                     grad_inv_scale=1.0, beta1=0.9, beta2=0.999, eps=1e-8,
-                    weight_decay=1e-4, stream=None):
-    """Ratio and update after lars_adam_norms has covered every layer."""
+                    weight_decay=1e-4, first=0, count=None, stream=None):
+    """Update of layers [first, first + count) (default: all) once
+    lars_adam_norms has covered every layer."""
     p = OptParams(lr, beta1, beta2, eps, weight_decay)
     wp, wb = _ws(ws)
     nf = 0 if flags is None else flags.numel()
+    if count is None:
+        count = len(tensors) - first
     _check("lars_adam_apply", lib().lars_adam_apply(
-        tensors, len(tensors), ctypes.byref(p), grad_format, grad_inv_scale, _p(flags),
-        nf, _p(step_count), wp, wb, _s(stream)))
+        tensors, len(tensors), first, count, ctypes.byref(p), grad_format, grad_inv_scale,
+        _p(flags), nf, _p(step_count), wp, wb, _s(stream)))
 
 
 def conv_transpose2d_fwd(desc, x, w, y, epi=EPI_NONE, gate=None, ws=None,

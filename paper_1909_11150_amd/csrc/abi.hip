@@ -584,14 +584,17 @@ static fg_status opt_call_ok(const fg_opt_tensor *t, int32_t n, const fg_opt_par
   return FG_OK;
 }
 
-// Which tensors have partial norms in a workspace since its last apply, for
-// one table, gradient form and set of parameters (a hash of them): an apply
-// is accepted only when every tensor is covered, so a missing norms call is
-// an error at the call instead of a wrong update.
+// Per workspace: which tensors have partial norms for the step in progress
+// and which have been applied, for one table, gradient form and set of
+// parameters (a hash of them). An apply is accepted only once every tensor
+// has norms, and each tensor is applied once; norms are refused while an
+// apply is incomplete. A missing or repeated call is thus an error at the
+// call instead of a wrong update.
 namespace {
 struct NormsRecord {
   uint64_t key;
-  uint64_t mask;
+  uint64_t norms;
+  uint64_t applied;
 };
 std::mutex g_norms_mu;
 std::unordered_map<uintptr_t, NormsRecord> g_norms;
@@ -642,9 +645,9 @@ fg_status lars_adam_update(const fg_opt_tensor *t, int32_t ntensors,
   hipError_t e = launch_lars_adam_norms(t, ntensors, 0, ntensors, *p, false, 1.f,
                                         step_count, ws, stream);
   if (e != hipSuccess) return launch_status(e);
-  return launch_status(launch_lars_adam_apply(t, ntensors, *p, false, 1.f,
-                                              found_nonfinite, nflags, step_count, ws,
-                                              stream));
+  return launch_status(launch_lars_adam_apply(t, ntensors, 0, ntensors, true, *p, false,
+                                              1.f, found_nonfinite, nflags, step_count,
+                                              ws, stream));
 }
 
 fg_status lars_adam_norms(const fg_opt_tensor *t, int32_t ntensors, int32_t first,
@@ -656,20 +659,21 @@ fg_status lars_adam_norms(const fg_opt_tensor *t, int32_t ntensors, int32_t firs
   if (st != FG_OK) return st;
   if (first < 0 || count < 1 || first > ntensors - count) return FG_EINVAL;
   const uint64_t key = norms_key(t, ntensors, p, grad_format, grad_inv_scale, step_count);
+  std::lock_guard<std::mutex> lk(g_norms_mu);
+  NormsRecord &r = g_norms[(uintptr_t)ws];
+  if (r.applied) return FG_EINVAL;  // the previous step's apply is incomplete
+  if (r.key != key) r = NormsRecord{key, 0, 0};
   const hipError_t e =
       launch_lars_adam_norms(t, ntensors, first, count, *p,
                              grad_format == FG_GRAD_F16_SCALED, grad_inv_scale,
                              step_count, ws, stream);
   if (e != hipSuccess) return launch_status(e);
-  std::lock_guard<std::mutex> lk(g_norms_mu);
-  NormsRecord &r = g_norms[(uintptr_t)ws];
-  if (r.key != key) r = NormsRecord{key, 0};
-  r.mask |= full_mask(first + count) & ~full_mask(first);
+  r.norms |= full_mask(first + count) & ~full_mask(first);
   return FG_OK;
 }
 
-fg_status lars_adam_apply(const fg_opt_tensor *t, int32_t ntensors,
-                          const fg_opt_params *p, int32_t grad_format,
+fg_status lars_adam_apply(const fg_opt_tensor *t, int32_t ntensors, int32_t first,
+                          int32_t count, const fg_opt_params *p, int32_t grad_format,
                           float grad_inv_scale, const int32_t *found_nonfinite,
                           int32_t nflags, int32_t *step_count, void *ws,
                           size_t ws_bytes, hipStream_t stream) {
@@ -677,19 +681,22 @@ fg_status lars_adam_apply(const fg_opt_tensor *t, int32_t ntensors,
   const fg_status st =
       opt_call_ok(t, ntensors, p, grad_format, grad_inv_scale, step_count, ws, ws_bytes);
   if (st != FG_OK) return st;
+  if (first < 0 || count < 1 || first > ntensors - count) return FG_EINVAL;
   const uint64_t key = norms_key(t, ntensors, p, grad_format, grad_inv_scale, step_count);
-  {
-    std::lock_guard<std::mutex> lk(g_norms_mu);
-    auto it = g_norms.find((uintptr_t)ws);
-    if (it == g_norms.end() || it->second.key != key ||
-        it->second.mask != full_mask(ntensors))
-      return FG_EINVAL;
-    g_norms.erase(it);
-  }
-  return launch_status(launch_lars_adam_apply(t, ntensors, *p,
-                                              grad_format == FG_GRAD_F16_SCALED,
-                                              grad_inv_scale, found_nonfinite, nflags,
-                                              step_count, ws, stream));
+  const uint64_t range = full_mask(first + count) & ~full_mask(first);
+  std::lock_guard<std::mutex> lk(g_norms_mu);
+  auto it = g_norms.find((uintptr_t)ws);
+  if (it == g_norms.end() || it->second.key != key ||
+      it->second.norms != full_mask(ntensors) || (it->second.applied & range))
+    return FG_EINVAL;
+  const hipError_t e = launch_lars_adam_apply(
+      t, ntensors, first, count, it->second.applied == 0, *p,
+      grad_format == FG_GRAD_F16_SCALED, grad_inv_scale, found_nonfinite, nflags,
+      step_count, ws, stream);
+  if (e != hipSuccess) return launch_status(e);
+  it->second.applied |= range;
+  if (it->second.applied == full_mask(ntensors)) g_norms.erase(it);
+  return FG_OK;
 }
 
 fg_status l2_head_grad(const uint16_t *y, const float *t, uint64_t numel,

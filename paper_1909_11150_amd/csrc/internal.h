@@ -109,10 +109,11 @@ hipError_t launch_lars_adam_norms(const fg_opt_tensor *ts, int32_t n, int32_t fi
                                   int32_t count, const fg_opt_params &p, bool fp16_grad,
                                   float inv_scale, const int32_t *step_count, void *ws,
                                   hipStream_t st);
-hipError_t launch_lars_adam_apply(const fg_opt_tensor *ts, int32_t n,
-                                  const fg_opt_params &p, bool fp16_grad, float inv_scale,
-                                  const int32_t *flags, int32_t nflags,
-                                  int32_t *step_count, void *ws, hipStream_t st);
+hipError_t launch_lars_adam_apply(const fg_opt_tensor *ts, int32_t n, int32_t first,
+                                  int32_t count, bool with_ratio, const fg_opt_params &p,
+                                  bool fp16_grad, float inv_scale, const int32_t *flags,
+                                  int32_t nflags, int32_t *step_count, void *ws,
+                                  hipStream_t st);
 hipError_t launch_head_wgrad(const uint16_t *x, const uint16_t *dy,
                              uint16_t *dw, int64_t npix, int32_t c,
                              float *ws, int32_t *flag, hipStream_t st);

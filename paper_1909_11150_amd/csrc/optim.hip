@@ -18,7 +18,8 @@
 //   2. ratio: one workgroup per layer adds its partial sums in a fixed order
 //      (fp64) and forms tau; the first advances the step count;
 //   3. apply: recomputes the new moments and u with the same fp32 operations
-//      and writes m, v, w and the fp16 copy.
+//      and writes m, v, w and the fp16 copy; it may run per range of layers
+//      (e.g. each just before the next forward pass reads that layer).
 // A step whose gradient groups were flagged non-finite is skipped on the
 // device: the ratio and apply kernels read the flags and return, so the host
 // never waits.
@@ -241,12 +242,14 @@ __global__ __launch_bounds__(kOptThreads) void lars_adam_ratio_kernel(
   }
 }
 
+// Workgroup b0 + blockIdx.x of the table.
 template <bool H>
 __global__ __launch_bounds__(kOptThreads) void lars_adam_apply_kernel(
     OptTable t, OptParams p, float inv, const int32_t *flags, int nflags,
-    const float *ratio, const int32_t *t_cur) {
+    const float *ratio, const int32_t *t_cur, uint32_t b0) {
   if (opt_skip(flags, nflags)) return;
-  const int pi = opt_piece(t, blockIdx.x);
+  const uint32_t b = b0 + blockIdx.x;
+  const int pi = opt_piece(t, b);
   const OptPiece pc = t.p[pi];
   const OptStep s = opt_step(p, *t_cur);
   const float step = p.lr * ratio[pi];
@@ -255,7 +258,7 @@ __global__ __launch_bounds__(kOptThreads) void lars_adam_apply_kernel(
   float *mp = reinterpret_cast<float *>(pc.m);
   float *vp = reinterpret_cast<float *>(pc.v);
   uint16_t *hp = reinterpret_cast<uint16_t *>(pc.w16);
-  const uint32_t beg = (blockIdx.x - pc.block0) * (uint32_t)kOptElems;
+  const uint32_t beg = (b - pc.block0) * (uint32_t)kOptElems;
   const uint32_t end = min(pc.numel, beg + (uint32_t)kOptElems);
   f32x4 g[kOptIters], w[kOptIters], m[kOptIters], v[kOptIters];
 #pragma unroll
@@ -333,6 +336,13 @@ static OptParams opt_params(const fg_opt_params &p) {
   return OptParams{p.lr, p.beta1, p.beta2, p.eps, p.weight_decay};
 }
 
+// blocks of layers [first, first + count)
+static void block_range(const OptTable &t, int32_t first, int32_t count, uint32_t &b0,
+                        uint32_t &b1) {
+  b0 = t.p[first].block0;
+  b1 = first + count < t.n ? t.p[first + count].block0 : t.nblocks;
+}
+
 hipError_t launch_lars_adam_norms(const fg_opt_tensor *ts, int32_t n, int32_t first,
                                   int32_t count, const fg_opt_params &pp, bool fp16_grad,
                                   float inv_scale, const int32_t *step_count, void *ws,
@@ -340,8 +350,8 @@ hipError_t launch_lars_adam_norms(const fg_opt_tensor *ts, int32_t n, int32_t fi
   OptTable t;
   opt_table(ts, n, t);
   const OptParams p = opt_params(pp);
-  const uint32_t b0 = t.p[first].block0;
-  const uint32_t b1 = first + count < n ? t.p[first + count].block0 : t.nblocks;
+  uint32_t b0, b1;
+  block_range(t, first, count, b0, b1);
   const OptWs w = opt_ws(ws, t.nblocks);
   if (fp16_grad)
     hipLaunchKernelGGL(lars_adam_norms_kernel<true>, dim3(b1 - b0), dim3(kOptThreads), 0,
@@ -352,24 +362,29 @@ hipError_t launch_lars_adam_norms(const fg_opt_tensor *ts, int32_t n, int32_t fi
   return hipGetLastError();
 }
 
-hipError_t launch_lars_adam_apply(const fg_opt_tensor *ts, int32_t n,
-                                  const fg_opt_params &pp, bool fp16_grad, float inv_scale,
-                                  const int32_t *flags, int32_t nflags,
-                                  int32_t *step_count, void *ws, hipStream_t st) {
+hipError_t launch_lars_adam_apply(const fg_opt_tensor *ts, int32_t n, int32_t first,
+                                  int32_t count, bool with_ratio, const fg_opt_params &pp,
+                                  bool fp16_grad, float inv_scale, const int32_t *flags,
+                                  int32_t nflags, int32_t *step_count, void *ws,
+                                  hipStream_t st) {
   OptTable t;
   opt_table(ts, n, t);
   const OptParams p = opt_params(pp);
   const OptWs w = opt_ws(ws, t.nblocks);
-  hipLaunchKernelGGL(lars_adam_ratio_kernel, dim3(n), dim3(kOptThreads), 0, st, t, flags,
-                     nflags, step_count, w.part, w.ratio, w.t_cur);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (with_ratio) {
+    hipLaunchKernelGGL(lars_adam_ratio_kernel, dim3(n), dim3(kOptThreads), 0, st, t,
+                       flags, nflags, step_count, w.part, w.ratio, w.t_cur);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  uint32_t b0, b1;
+  block_range(t, first, count, b0, b1);
   if (fp16_grad)
-    hipLaunchKernelGGL(lars_adam_apply_kernel<true>, dim3(t.nblocks), dim3(kOptThreads), 0,
-                       st, t, p, inv_scale, flags, nflags, w.ratio, w.t_cur);
+    hipLaunchKernelGGL(lars_adam_apply_kernel<true>, dim3(b1 - b0), dim3(kOptThreads), 0,
+                       st, t, p, inv_scale, flags, nflags, w.ratio, w.t_cur, b0);
   else
-    hipLaunchKernelGGL(lars_adam_apply_kernel<false>, dim3(t.nblocks), dim3(kOptThreads), 0,
-                       st, t, p, inv_scale, flags, nflags, w.ratio, w.t_cur);
+    hipLaunchKernelGGL(lars_adam_apply_kernel<false>, dim3(b1 - b0), dim3(kOptThreads), 0,
+                       st, t, p, inv_scale, flags, nflags, w.ratio, w.t_cur, b0);
   return hipGetLastError();
 }
 

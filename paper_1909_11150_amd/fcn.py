@@ -324,6 +324,7 @@ class Chain:
                 self._prog = self.program(target)
                 self._prog_key = key
             self._prog.run()
+            self._prog.join()
             return
         self.forward()
         self.head_grad(target)
@@ -353,10 +354,11 @@ OPT_WRITE_BYTES = 14
 # label, main kernel, algorithmic work (flops, or bytes for the gradient
 # path), C function (None: a Python callable), argument tuple (the stream
 # last), whether the call is exactly one launch of that kernel, its stream
-# (0: main, 1: kernel gradients, 2: gradient path) and the calls (indices)
-# that must finish before it starts
-Call = namedtuple("Call", "label kernel work fn args single sid deps",
-                  defaults=(True, 0, ()))
+# (0: main, 1: kernel gradients, 2: gradient path), the calls (indices)
+# that must finish before it starts, and the later calls whose launch in the
+# previous run must finish before it starts
+Call = namedtuple("Call", "label kernel work fn args single sid deps prev_deps",
+                  defaults=(True, 0, (), ()))
 
 
 def kernel_gradient_workspace_bytes(layers):
@@ -386,14 +388,19 @@ class StepProgram:
 
     With an optimizer, stream 2 also runs each group's optimizer norms pass
     (the part that reads the gradients; it writes only the workspace) right
-    after the group's gradient path, and ends with the ratio and apply
-    launches (after the main stream's last pass, which reads the fp16
-    weights). With zero-copy groups the norms and apply read the fp16
-    loss-scaled gradients in the group slots, and the unscale and unpack
-    are left out (the kernel gradients raise the flags). With an optimizer or a loss scaler, it then copies the group flags to
-    pinned host memory; the next run waits for that copy just before its
+    after the group's gradient path. With zero-copy groups the norms and
+    updates read the fp16 loss-scaled gradients in the group slots, and the
+    unscale and unpack are left out (the kernel gradients raise the flags).
+    With an optimizer or a loss scaler, stream 2 then copies the group flags
+    to pinned host memory; the next run waits for that copy just before its
     head call (its forward pass already queued), updates the scaler and the
-    applied count, and patches the loss-scale and learning-rate arguments."""
+    applied count, and patches the loss-scale and learning-rate arguments.
+    The updates follow, one call per layer in forward order (layer 0's on
+    stream 1, after the main stream's last pass, which reads its fp16
+    weights). The main stream does not wait for them at the end of the
+    run: the next run's forward pass of each layer waits for that layer's
+    update, so the updates overlap the next forward pass. ``join()`` makes
+    the main stream wait for everything."""
 
     def __init__(self, ch, target, streams=3):
         if ch.groups is None:
@@ -523,23 +530,11 @@ class StepProgram:
                 gc = self._group_calls(ch, gi, L_, st) + self._norms_calls(ch, gi, L_, st)
                 gc[0] = gc[0]._replace(deps=(last_dw[i],))
                 calls += gc
-        if ch.opt is not None:
-            # ratio and apply: after the last group's norms (stream order) and
-            # the last pass that reads the fp16 weights (the main stream's
-            # last call)
-            o = self._opt
-            calls.append(Call("opt.apply", f"lars_adam_apply_kernel<{o['h']}>",
-                              (OPT_READ_BYTES + o["gb"] + OPT_WRITE_BYTES) * o["n"],
-                              L_.lars_adam_apply,
-                              (o["tab"], nl, ctypes.byref(self.params), o["fmt"], o["inv"],
-                               ch.flags.data_ptr(), len(ch.groups),
-                               ch.step_count.data_ptr(), ch.opt_ws.data_ptr(),
-                               ch.opt_ws.numel(), st), False, sid=2,
-                              deps=(writer[0],)))
         self._copy = None
         if ch.opt is not None or ch.scaler is not None:
-            # the step's flags to pinned host memory; read before the next
-            # step's head call, by which time the next forward pass is queued
+            # the step's flags to pinned host memory once every flag is final
+            # (after the last kernel gradient and unscale); read before the
+            # next step's head call, by which time its forward pass is queued
             self.host_flags = torch.zeros(len(ch.groups), dtype=torch.int32,
                                           pin_memory=True)
             calls.append(Call("flags.copy", "", 0, None,
@@ -547,14 +542,47 @@ class StepProgram:
                                                              non_blocking=True),),
                               False, sid=2))
             self._copy = len(calls) - 1
+        self._apply = {}
+        if ch.opt is not None:
+            # each layer's update after every group's norms, in forward order
+            # (the first apply call also forms tau): layers 1.. on stream 2,
+            # layer 0 on stream 1 once the main stream's last pass (layer 0's
+            # input gradient, which reads its fp16 weights) is done. The next
+            # run's forward pass of layer i waits for the apply of layer i
+            # only, so the updates overlap the next forward pass.
+            o = self._opt
+            order = [(i, 2) for i in range(1, nl)] + [(0, 1 if nl > 1 else 2)]
+            for i, sid in order:
+                deps = () if i else (writer[0],) + \
+                    ((self._apply[1],) if nl > 1 else ())
+                n_i = ch.w32[i].numel()
+                calls.append(Call(f"{ch.layers[i].name}.apply",
+                                  f"lars_adam_apply_kernel<{o['h']}>",
+                                  (OPT_READ_BYTES + o["gb"] + OPT_WRITE_BYTES) * n_i,
+                                  L_.lars_adam_apply,
+                                  (o["tab"], nl, i, 1, ctypes.byref(self.params), o["fmt"],
+                                   o["inv"], ch.flags.data_ptr(), len(ch.groups),
+                                   ch.step_count.data_ptr(), ch.opt_ws.data_ptr(),
+                                   ch.opt_ws.numel(), st), i != order[0][0], sid=sid,
+                                  deps=deps))
+                self._apply[i] = len(calls) - 1
+            fwd = {f"{L.name}.fwd": i for i, L in enumerate(ch.layers)}
+            calls = [c._replace(prev_deps=(self._apply[fwd[c.label]],))
+                     if c.label in fwd else c for c in calls]
         if streams == 1:  # program order already respects every dependency
-            calls = [c._replace(sid=0, deps=()) for c in calls]
+            calls = [c._replace(sid=0, deps=(), prev_deps=()) for c in calls]
         # the stream argument of each library call
         calls = [c if c.fn is None else
                  c._replace(args=c.args[:-1] + (sptr[c.sid],)) for c in calls]
         self.final = tuple(max(j for j, c in enumerate(calls) if c.sid == sid)
                            for sid in range(1, len(self.streams)))
-        needed = {d for c in calls for d in c.deps} | set(self.final)
+        # what the main stream waits for at the end of a run: every side
+        # stream's last call, except the per-layer updates on stream 2, which
+        # the next run's forward pass waits for layer by layer (join() waits
+        # for everything)
+        self.step_final = tuple(j for j in self.final
+                                if not (self._apply and calls[j].sid == 2))
+        needed = {d for c in calls for d in c.deps + c.prev_deps} | set(self.final)
         if self._copy is not None:
             needed.add(self._copy)
         self.events = {j: torch.cuda.Event() for j in sorted(needed)}
@@ -617,7 +645,7 @@ class StepProgram:
                 self.ch.observe()
                 self._patch()
             s = streams[c.sid]
-            for d in c.deps:
+            for d in c.deps + c.prev_deps:
                 s.wait_event(evs[d])
             ev = events.get(i) if events else None
             if ev:
@@ -633,7 +661,13 @@ class StepProgram:
                 ev[1].record(s)
             if i in evs:
                 evs[i].record(s)
-        for j in self.final:
+        for j in self.step_final:
             streams[0].wait_event(evs[j])
         if self._copy is not None:
             self.ch._pending = (evs[self._copy], self.host_flags)
+
+    def join(self):
+        """Make the main stream wait for all of the last run's work (the
+        per-layer updates included)."""
+        for j in self.final:
+            self.streams[0].wait_event(self.events[j])

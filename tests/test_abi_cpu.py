@@ -223,7 +223,10 @@ def test_optimizer_split_argument_checks(L):
     g4 = (fg.OptTensor * 1)(layer(FAKE, (4 << 16) + 4))
     assert L.lars_adam_norms(g4, 1, 0, 1, ref(p), F16, 0.5, sc, ws, need, None) == fg.FG_EINVAL
     # no norms on this workspace yet: the apply is refused before any launch
-    assert L.lars_adam_apply(good, 2, ref(p), F32, 1.0, None, 0, sc, ws, need,
+    assert L.lars_adam_apply(good, 2, 0, 2, ref(p), F32, 1.0, None, 0, sc, ws, need,
                              None) == fg.FG_EINVAL
-    assert L.lars_adam_apply(good, 2, ref(p), F32, 1.0, None, 2, sc, ws, need,
+    assert L.lars_adam_apply(good, 2, 0, 2, ref(p), F32, 1.0, None, 2, sc, ws, need,
                              None) == fg.FG_EINVAL
+    for first, count in ((-1, 1), (0, 0), (1, 2)):
+        assert L.lars_adam_apply(good, 2, first, count, ref(p), F32, 1.0, None, 0, sc, ws,
+                                 need, None) == fg.FG_EINVAL
