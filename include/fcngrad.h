@@ -303,6 +303,56 @@ fg_status lars_adam_apply(const fg_opt_tensor *t, int32_t ntensors, int32_t firs
                           int32_t nflags, int32_t *step_count, void *ws,
                           size_t ws_bytes, hipStream_t stream);
 
+/* ---- FC-DenseNet variant (Section 6.2, Neural Network Architecture and
+ * Model Implementation) ---------------------------------------------------- */
+
+/* Gradient of the loss-scaled mean Huber loss (Section 6.2, the loss
+ * equation, with cutoff delta): dy[j] = fp16(scale * clamp(y[j] - t[j],
+ * -delta, delta)), evaluated in fp64 and rounded once (nearest-even,
+ * overflow to infinity). For the loss S * mean(huber_delta(y - t)) over
+ * numel outputs, where huber_delta(d) = d^2/2 for |d| <= delta and
+ * delta (|d| - delta/2) beyond, the caller passes scale = S/numel. y fp16,
+ * t fp32, dy fp16; numel 1..2^31-1. FG_EINVAL for null pointers, delta not
+ * > 0 (+inf is allowed and gives scale * (y - t)), a non-finite scale, or dy
+ * overlapping y or t. */
+fg_status huber_head_grad(const uint16_t *y, const float *t, uint64_t numel,
+                          double scale, double delta, uint16_t *dy,
+                          hipStream_t stream);
+
+/* 2x2 average pooling with stride 2 (Section 6.2: average pooling in place
+ * of max pooling). x: N x H x W x C fp16 (NHWC), H and W even; y: N x H/2 x
+ * W/2 x C, the mean of the four inputs computed exactly and rounded once.
+ * FG_EINVAL for null or overlapping buffers or a non-positive size;
+ * FG_EUNSUPPORTED for odd H or W, C not a multiple of 8, 2^31 or more
+ * elements, or a pointer not 16-byte aligned. */
+fg_status avg_pool2d_fwd(const uint16_t *x, int32_t n, int32_t h, int32_t w, int32_t c,
+                         uint16_t *y, hipStream_t stream);
+
+/* Gradient of avg_pool2d_fwd: dx[n, 2p+i, 2q+j, c] = fp16(dy[n, p, q, c] / 4),
+ * or +0 where gate (N x H x W x C fp16, e.g. the ReLU output that was
+ * pooled; may be null) is <= 0. n, h, w, c are the forward input's sizes.
+ * Same checks as the forward; dx may not overlap dy or gate. */
+fg_status avg_pool2d_bwd(const uint16_t *dy, const uint16_t *gate, int32_t n, int32_t h,
+                         int32_t w, int32_t c, uint16_t *dx, hipStream_t stream);
+
+/* Channel slice copy between NHWC buffers with their own pixel strides
+ * (Section 6.2: dense blocks concatenate their layers' outputs along the
+ * channels, growth rate 256). For npix pixels p and channels k < nch:
+ * v = src[p*src_ld + k], or +0 where gate[p*gate_ld + k] <= 0 (gate may be
+ * null); dst[p*dst_ld + k] = v, or fp16(dst[p*dst_ld + k] + v) (exact sum,
+ * one rounding) when accumulate is non-zero. A slice at channel offset o is
+ * addressed by offsetting the pointer by o. The concatenation of a dense
+ * block is a copy of each piece into its slice; backward, a slice's
+ * gradient is read out (gated by the piece's ReLU output) and a layer's
+ * input gradient is accumulated into the slices it read. FG_EINVAL for a
+ * null src or dst, non-positive sizes or strides, nch above a stride, or
+ * dst's span ((npix-1)*dst_ld + nch elements) overlapping src's or gate's;
+ * FG_EUNSUPPORTED for nch or a stride not a multiple of 8, a pointer not
+ * 16-byte aligned, or npix times a stride of 2^31 or more. */
+fg_status channel_slice_copy(const uint16_t *src, int32_t src_ld, const uint16_t *gate,
+                             int32_t gate_ld, uint16_t *dst, int32_t dst_ld, int64_t npix,
+                             int32_t nch, int32_t accumulate, hipStream_t stream);
+
 /* Output spatial size: transpose = 0 gives the forward P, Q; 1 gives the
  * transposed convolution's output size. FG_EINVAL if it is not positive. */
 fg_status fg_conv_out_dims(const fg_conv_desc *d, int transpose, int32_t *p,

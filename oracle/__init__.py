@@ -24,6 +24,10 @@ Contents
   optim (module)
       the layer-wise adaptive Adam update and the loss-scale backoff that
       consume the unpacked fp32 gradients (Section 6.2).
+  dense (module)
+      the FC-DenseNet variant's glue: Huber head gradient, 2 x 2 average
+      pooling and its gradient, channel concatenation and slice copies
+      (Section 6.2).
 """
 import ctypes
 import os

@@ -27,6 +27,7 @@ ENTRY_POINTS = (
     "fg_conv_kernel_name", "fg_status_string",
     "lars_adam_update", "lars_adam_norms", "lars_adam_apply",
     "fg_lars_adam_workspace_bytes",
+    "huber_head_grad", "avg_pool2d_fwd", "avg_pool2d_bwd", "channel_slice_copy",
 )
 
 
@@ -96,6 +97,10 @@ def lib():
         "grad_group_unpack": [vp, u64, pseg, i32, vp],
         "l2_head_grad": [vp, vp, u64, ctypes.c_double, vp, vp],
         "relu_backward": [vp, vp, u64, vp, vp],
+        "huber_head_grad": [vp, vp, u64, ctypes.c_double, ctypes.c_double, vp, vp],
+        "avg_pool2d_fwd": [vp, i32, i32, i32, i32, vp, vp],
+        "avg_pool2d_bwd": [vp, vp, i32, i32, i32, i32, vp, vp],
+        "channel_slice_copy": [vp, i32, vp, i32, vp, i32, ctypes.c_int64, i32, i32, vp],
         "fg_conv_out_dims": [pdesc, ctypes.c_int, ctypes.POINTER(i32),
                              ctypes.POINTER(i32)],
         "grad_group_plan": [ctypes.POINTER(u64), i32, u64, ctypes.c_uint32,
@@ -299,6 +304,39 @@ def grad_group_unpack(group_f32, dsts, offsets, stream=None):
 def l2_head_grad(y, t, scale, dy, stream=None):
     _check("l2_head_grad", lib().l2_head_grad(
         _p(y), _p(t), y.numel(), float(scale), _p(dy), _s(stream)))
+
+
+def huber_head_grad(y, t, scale, delta, dy, stream=None):
+    """dy = fp16(scale * clamp(y - t, -delta, delta)); scale = S / numel for
+    the loss-scaled mean Huber loss."""
+    _check("huber_head_grad", lib().huber_head_grad(
+        _p(y), _p(t), y.numel(), float(scale), float(delta), _p(dy), _s(stream)))
+
+
+def avg_pool2d_fwd(x, y, stream=None):
+    """2x2 stride-2 mean pooling of an N x H x W x C fp16 tensor."""
+    n, h, w, c = x.shape
+    _check("avg_pool2d_fwd", lib().avg_pool2d_fwd(_p(x), n, h, w, c, _p(y), _s(stream)))
+
+
+def avg_pool2d_bwd(dy, dx, gate=None, stream=None):
+    """Gradient of avg_pool2d_fwd into dx (the forward input's shape),
+    zero where gate <= 0 if a gate is given."""
+    n, h, w, c = dx.shape
+    _check("avg_pool2d_bwd", lib().avg_pool2d_bwd(
+        _p(dy), _p(gate), n, h, w, c, _p(dx), _s(stream)))
+
+
+def channel_slice_copy(src, src_ld, dst, dst_ld, npix, nch, gate=None, gate_ld=0,
+                       accumulate=False, stream=None):
+    """Per pixel, nch channels from src (pixel stride src_ld) to dst (pixel
+    stride dst_ld); src, dst, gate: tensors or device addresses (a channel
+    offset is an address offset)."""
+    def a(x):
+        return None if x is None else (x if isinstance(x, int) else x.data_ptr())
+    _check("channel_slice_copy", lib().channel_slice_copy(
+        a(src), src_ld, a(gate), gate_ld, a(dst), dst_ld, npix, nch, int(accumulate),
+        _s(stream)))
 
 
 def relu_backward(dy, act, out, stream=None):

@@ -4,6 +4,7 @@
 // returns without touching the device.
 #include <string.h>
 
+#include <algorithm>
 #include <cmath>
 #include <mutex>
 #include <unordered_map>
@@ -706,6 +707,67 @@ fg_status l2_head_grad(const uint16_t *y, const float *t, uint64_t numel,
   if (overlap(dy, numel * 2, y, numel * 2) || overlap(dy, numel * 2, t, numel * 4))
     return FG_EINVAL;
   return launch_status(launch_head_grad(y, t, numel, scale, dy, stream));
+}
+
+// ---- FC-DenseNet variant glue -------------------------------------------
+fg_status huber_head_grad(const uint16_t *y, const float *t, uint64_t numel,
+                          double scale, double delta, uint16_t *dy,
+                          hipStream_t stream) {
+  if (!y || !t || !dy || numel == 0) return FG_EINVAL;
+  if (!(delta > 0.0) || !std::isfinite(scale)) return FG_EINVAL;
+  if (numel >= (uint64_t)kMaxElems) return FG_EUNSUPPORTED;
+  if (overlap(dy, numel * 2, y, numel * 2) || overlap(dy, numel * 2, t, numel * 4))
+    return FG_EINVAL;
+  return launch_status(launch_huber_head_grad(y, t, numel, scale, delta, dy, stream));
+}
+
+static fg_status pool_ok(const void *a, const void *b, int32_t n, int32_t h, int32_t w,
+                         int32_t c) {
+  if (!a || !b || !pos(n) || !pos(h) || !pos(w) || !pos(c)) return FG_EINVAL;
+  if (h % 2 || w % 2 || c % 8 || elems4(n, h, w, c) >= kMaxElems) return FG_EUNSUPPORTED;
+  if (((uintptr_t)a | (uintptr_t)b) & 15) return FG_EUNSUPPORTED;
+  return FG_OK;
+}
+
+fg_status avg_pool2d_fwd(const uint16_t *x, int32_t n, int32_t h, int32_t w, int32_t c,
+                         uint16_t *y, hipStream_t stream) {
+  const fg_status st = pool_ok(x, y, n, h, w, c);
+  if (st != FG_OK) return st;
+  const size_t big = (size_t)elems4(n, h, w, c) * 2;
+  if (overlap(x, big, y, big / 4)) return FG_EINVAL;
+  return launch_status(launch_avg_pool2d_fwd(x, n, h, w, c, y, stream));
+}
+
+fg_status avg_pool2d_bwd(const uint16_t *dy, const uint16_t *gate, int32_t n, int32_t h,
+                         int32_t w, int32_t c, uint16_t *dx, hipStream_t stream) {
+  fg_status st = pool_ok(dy, dx, n, h, w, c);
+  if (st != FG_OK) return st;
+  if (gate && ((uintptr_t)gate & 15)) return FG_EUNSUPPORTED;
+  const size_t big = (size_t)elems4(n, h, w, c) * 2;
+  if (overlap(dx, big, dy, big / 4) || (gate && overlap(dx, big, gate, big)))
+    return FG_EINVAL;
+  return launch_status(launch_avg_pool2d_bwd(dy, gate, n, h, w, c, dx, stream));
+}
+
+fg_status channel_slice_copy(const uint16_t *src, int32_t src_ld, const uint16_t *gate,
+                             int32_t gate_ld, uint16_t *dst, int32_t dst_ld, int64_t npix,
+                             int32_t nch, int32_t accumulate, hipStream_t stream) {
+  if (!src || !dst || npix <= 0 || !pos(nch) || !pos(src_ld) || !pos(dst_ld) ||
+      (gate && !pos(gate_ld)))
+    return FG_EINVAL;
+  if (nch > src_ld || nch > dst_ld || (gate && nch > gate_ld)) return FG_EINVAL;
+  if (nch % 8 || src_ld % 8 || dst_ld % 8 || (gate && gate_ld % 8)) return FG_EUNSUPPORTED;
+  if ((((uintptr_t)src | (uintptr_t)dst | (uintptr_t)gate) & 15)) return FG_EUNSUPPORTED;
+  const int64_t ld_max = std::max<int64_t>(std::max(src_ld, dst_ld), gate ? gate_ld : 0);
+  if (npix * ld_max >= kMaxElems) return FG_EUNSUPPORTED;
+  // spans of the three buffers: (npix - 1) * ld + nch elements each
+  const size_t ssrc = ((size_t)(npix - 1) * src_ld + nch) * 2;
+  const size_t sdst = ((size_t)(npix - 1) * dst_ld + nch) * 2;
+  const size_t sgate = gate ? ((size_t)(npix - 1) * gate_ld + nch) * 2 : 0;
+  if (overlap(dst, sdst, src, ssrc) || (gate && overlap(dst, sdst, gate, sgate)))
+    return FG_EINVAL;
+  return launch_status(launch_channel_slice_copy(src, src_ld, gate, gate_ld, dst, dst_ld,
+                                                 npix, nch, accumulate != 0, stream));
 }
 
 fg_status relu_backward(const uint16_t *dy, const uint16_t *act,

@@ -23,6 +23,28 @@ __device__ __forceinline__ float h_to_f32(uint16_t b) {
   return (float)__builtin_bit_cast(_Float16, b);
 }
 
+// fp64 -> fp16 bits, one nearest-even rounding (overflow to infinity).
+// The value is first rounded in fp64 to a multiple of the fp16 spacing at its
+// magnitude (rint rounds half to even); the result is an fp16 number, so the
+// remaining conversions are exact.
+__device__ __forceinline__ uint16_t f64_to_h(double d) {
+  if (d != d) return 0x7E00;
+  double ad = fabs(d);
+  double r;
+  if (ad >= 65520.0) {
+    r = __builtin_inf();
+  } else if (ad == 0.0) {
+    r = 0.0;
+  } else {
+    int e = ilogb(ad);                 // ad in [2^e, 2^(e+1))
+    int ue = (e < -14 ? -14 : e) - 10; // spacing 2^ue of fp16 at this size
+    r = ldexp(rint(ldexp(ad, -ue)), ue);
+  }
+  r = copysign(r, d);
+  _Float16 h = (_Float16)(float)r;
+  return __builtin_bit_cast(uint16_t, h);
+}
+
 // 32x32x16 fp16 MFMA with fp32 accumulate. Operand lane layout: lane l holds
 // row (A) / column (B) l % 32 and the 8 reduction elements 8*(l/32)..+7.
 // Accumulator layout: lane l, register v holds C[8*(v/4) + 4*(l/32) + v%4]

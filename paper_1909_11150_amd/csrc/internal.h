@@ -114,6 +114,18 @@ hipError_t launch_lars_adam_apply(const fg_opt_tensor *ts, int32_t n, int32_t fi
                                   bool fp16_grad, float inv_scale, const int32_t *flags,
                                   int32_t nflags, int32_t *step_count, void *ws,
                                   hipStream_t st);
+hipError_t launch_huber_head_grad(const uint16_t *y, const float *t, uint64_t numel,
+                                  double scale, double delta, uint16_t *dy,
+                                  hipStream_t st);
+hipError_t launch_avg_pool2d_fwd(const uint16_t *x, int32_t n, int32_t h, int32_t w,
+                                 int32_t c, uint16_t *y, hipStream_t st);
+hipError_t launch_avg_pool2d_bwd(const uint16_t *dy, const uint16_t *gate, int32_t n,
+                                 int32_t h, int32_t w, int32_t c, uint16_t *dx,
+                                 hipStream_t st);
+hipError_t launch_channel_slice_copy(const uint16_t *src, int32_t src_ld,
+                                     const uint16_t *gate, int32_t gate_ld, uint16_t *dst,
+                                     int32_t dst_ld, int64_t npix, int32_t nch,
+                                     bool accumulate, hipStream_t st);
 hipError_t launch_head_wgrad(const uint16_t *x, const uint16_t *dy,
                              uint16_t *dw, int64_t npix, int32_t c,
                              float *ws, int32_t *flag, hipStream_t st);

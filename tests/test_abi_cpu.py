@@ -230,3 +230,30 @@ def test_optimizer_split_argument_checks(L):
     for first, count in ((-1, 1), (0, 0), (1, 2)):
         assert L.lars_adam_apply(good, 2, first, count, ref(p), F32, 1.0, None, 0, sc, ws,
                                  need, None) == fg.FG_EINVAL
+
+
+def test_dense_glue_argument_checks(L):
+    """Huber head, pooling and channel slice copies reject bad arguments
+    before touching the device."""
+    a, b, g = FAKE, FAKE + (1 << 24), FAKE + (1 << 25)
+    E, U = fg.FG_EINVAL, fg.FG_EUNSUPPORTED
+    assert L.huber_head_grad(a, b, 0, 1.0, 10.0, g, None) == E
+    assert L.huber_head_grad(a, b, 64, 1.0, 0.0, g, None) == E
+    assert L.huber_head_grad(a, b, 64, 1.0, -1.0, g, None) == E
+    assert L.huber_head_grad(a, b, 64, float("nan"), 10.0, g, None) == E
+    assert L.huber_head_grad(a, b, 64, 1.0, 10.0, a + 64, None) == E   # dy inside y
+    assert L.avg_pool2d_fwd(a, 1, 5, 4, 8, b, None) == U               # odd H
+    assert L.avg_pool2d_fwd(a, 1, 4, 4, 12, b, None) == U              # C % 8
+    assert L.avg_pool2d_fwd(a + 8, 1, 4, 4, 8, b, None) == U           # alignment
+    assert L.avg_pool2d_fwd(a, 0, 4, 4, 8, b, None) == E
+    assert L.avg_pool2d_fwd(a, 1, 4, 4, 8, a + 64, None) == E          # overlap
+    assert L.avg_pool2d_bwd(a, None, 1, 4, 4, 8, a + 32, None) == E    # dx over dy
+    assert L.avg_pool2d_bwd(a, g, 1, 4, 4, 8, g + 64, None) == E       # dx over gate
+    assert L.channel_slice_copy(a, 64, None, 0, b, 64, 10, 72, 0, None) == E   # nch > ld
+    assert L.channel_slice_copy(a, 64, None, 0, b, 64, 0, 8, 0, None) == E
+    assert L.channel_slice_copy(a, 60, None, 0, b, 64, 10, 8, 0, None) == U
+    assert L.channel_slice_copy(a, 64, None, 0, b, 64, 10, 12, 0, None) == U
+    assert L.channel_slice_copy(a + 2, 64, None, 0, b, 64, 10, 8, 0, None) == U
+    assert L.channel_slice_copy(a, 64, None, 0, a + 16, 64, 10, 8, 0, None) == E  # spans overlap
+    assert L.channel_slice_copy(a, 64, g, 64, g + 128, 64, 10, 8, 0, None) == E
+    assert L.channel_slice_copy(a, 1 << 20, None, 0, b, 64, 1 << 12, 8, 0, None) == U
