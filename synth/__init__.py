@@ -88,6 +88,50 @@ def fcn_layers(n=4, h=256, c_in=256, widths=(512, 1024, 1024, 1024),
     return L
 
 
+def densenet_layers(n=4, h=128, c_in=256, c0=256, growth=256, levels=2, per_block=2):
+    """Conv layers of the FC-DenseNet variant (Section 6.2: dense blocks
+    with growth rate 256, average pooling), forward order. The paper gives
+    no layer counts; this Tiramisu-shaped reading has:
+      C0       3x3 stem conv, c_in -> c0, at h;
+      D{d}.{l} dense layers of down level d (3x3, -> growth channels), each
+               reading the concatenation of the block input and the
+               block's earlier outputs;
+      TD{d}    transition down: 1x1 conv over the block's full
+               concatenation (channels kept), then 2x2 average pooling;
+      B.{l}    dense layers of the bottleneck block;
+      TU{d}    transition up: 4x4 stride-2 transposed conv of the previous
+               block's new features (per_block * growth channels, kept);
+      U{d}.{l} dense layers of up level d, whose block input is the
+               concatenation of TU{d}'s output and the skip (the full
+               concatenation of down level d);
+      F1x1     1x1 head over the last block's new features -> 1 channel.
+    A ReLU follows every layer except the head. Defaults: 4 x 128 x 128 x
+    256 input, 38,928,896 weights."""
+    L = [_conv("C0", n, h, c_in, c0, 3, 1, 1, True)]
+    hh, c = h, c0
+    skips = []
+    for d in range(1, levels + 1):
+        for l in range(1, per_block + 1):
+            L.append(_conv(f"D{d}.{l}", n, hh, c, growth, 3, 1, 1, True))
+            c += growth
+        skips.append(c)
+        L.append(_conv(f"TD{d}", n, hh, c, c, 1, 1, 0, True))
+        hh //= 2
+    for l in range(1, per_block + 1):
+        L.append(_conv(f"B.{l}", n, hh, c, growth, 3, 1, 1, True))
+        c += growth
+    new = per_block * growth
+    for d in range(levels, 0, -1):
+        L.append(_convt(f"TU{d}", n, hh, new, new, True))
+        hh *= 2
+        c = new + skips[d - 1]
+        for l in range(1, per_block + 1):
+            L.append(_conv(f"U{d}.{l}", n, hh, c, growth, 3, 1, 1, True))
+            c += growth
+    L.append(_conv("F1x1", n, hh, new, 1, 1, 1, 0, False))
+    return L
+
+
 def single_conv_layer():
     """One 3x3 s1 p1 conv, N=2, C=K=16, 64x64, no epilogue."""
     return [_conv("C1", 2, 64, 16, 16, 3, 1, 1, False)]
@@ -212,6 +256,15 @@ def decoder_block():
     x = normal(np.random.default_rng(2), layers[0].x_shape)
     dy = normal(np.random.default_rng(3), layers[-1].y_shape, 1e-2)
     return Workload("decoder_block_n8_c256_32", layers, x, he_weights(layers), dy=dy)
+
+
+def densenet(n=4, h=128, c_in=256, c0=256, growth=256, levels=2, per_block=2):
+    layers = densenet_layers(n, h, c_in, c0, growth, levels, per_block)
+    x = diffraction_like(n, h, c_in, seed=0)
+    w = he_weights(layers, seed=1)
+    t = smooth_target(n, h, seed=4)
+    return Workload(f"densenet_n{n}_c{c_in}_{h}_k{growth}", layers, x, w, target=t,
+                    extra=dict(levels=levels, per_block=per_block, growth=growth))
 
 
 def fcn(n=4, h=256, c_in=256, widths=(512, 1024, 1024, 1024),

@@ -111,3 +111,28 @@ def check_opt_layer(w0, m0, v0, g0, t, lr, w1, m1, v1, h1, hp=OPT_HP):
     bound = 1e-5 * np.abs(step) + np.abs(w0d - step) * 2.0 ** -23 + 1e-38
     assert (err <= bound).all(), float((err / bound).max())
     assert np.array_equal(h1.view(np.uint16), O.fp16_copy(w1).view(np.uint16))
+
+
+def _dist(a, b):
+    a = np.asarray(a, np.float64).ravel()
+    b = np.asarray(b, np.float64).ravel()
+    d = a - b
+    rel = np.linalg.norm(d) / max(np.linalg.norm(b), 1e-30)
+    ratio = np.max(np.abs(d)) / max(np.sqrt(np.mean(b ** 2)), 1e-30)
+    return rel, ratio
+
+
+def chain_parity(g16, o16, o64, t32, what):
+    """Chained outputs: rel_L2(GPU, O16) <= max(5e-3, 2 * fp16 noise), the
+    noise being the larger of rel_L2(O16, O64) and rel_L2(T32, O16) (t32 may
+    be None); the largest single difference is printed, not gated."""
+    assert np.all(np.isfinite(np.asarray(g16, np.float64))), what
+    rel, ratio = _dist(g16, o16)
+    rel_n, ratio_n = _dist(o16, o64)
+    if t32 is not None:
+        rel_n = max(rel_n, _dist(t32, o16)[0])
+    print(f"{what}: rel_L2 {rel:.3e} (fp16 noise {rel_n:.3e}), "
+          f"max_abs/RMS {ratio:.3e} (fp16 noise {ratio_n:.3e})")
+    assert rel <= max(5e-3, 2 * rel_n), \
+        f"{what}: rel_L2 {rel:.3e} (fp16 noise {rel_n:.3e})"
+    return rel, ratio

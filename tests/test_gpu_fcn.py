@@ -27,33 +27,12 @@ import oracle
 import paper_1909_11150_amd as fg
 import synth
 import fp32_chain as T32
-from gpu_util import conv_parity, dev, host, sample_indices
+from gpu_util import chain_parity, conv_parity, dev, host, sample_indices
 from oracle import chain as OC
 from oracle import grad as G
 from paper_1909_11150_amd.fcn import Chain
 
 pytestmark = pytest.mark.gpu
-
-
-def _dist(a, b):
-    a = np.asarray(a, np.float64).ravel()
-    b = np.asarray(b, np.float64).ravel()
-    d = a - b
-    rel = np.linalg.norm(d) / max(np.linalg.norm(b), 1e-30)
-    ratio = np.max(np.abs(d)) / max(np.sqrt(np.mean(b ** 2)), 1e-30)
-    return rel, ratio
-
-
-def chain_parity(g16, o16, o64, t32, what):
-    assert np.all(np.isfinite(np.asarray(g16, np.float64))), what
-    rel, ratio = _dist(g16, o16)
-    rel_n, ratio_n = _dist(o16, o64)
-    rel_n = max(rel_n, _dist(t32, o16)[0])
-    print(f"{what}: rel_L2 {rel:.3e} (fp16 noise {rel_n:.3e}), "
-          f"max_abs/RMS {ratio:.3e} (fp16 noise {ratio_n:.3e})")
-    assert rel <= max(5e-3, 2 * rel_n), \
-        f"{what}: rel_L2 {rel:.3e} (fp16 noise {rel_n:.3e})"
-    return rel, ratio
 
 
 def test_single_conv_workload():
