@@ -58,6 +58,9 @@ def parse():
     ap.add_argument("--zero-copy", action="store_true",
                     help="kernel gradients write into their group slots (no pack; "
                          "the non-finite check fused into their store)")
+    ap.add_argument("--workload", default="fcn", choices=("fcn", "densenet"),
+                    help="fcn: the encoder-decoder step; densenet: the FC-DenseNet "
+                         "variant's step (one stream, no gradient groups)")
     ap.add_argument("--optimizer", action="store_true",
                     help="end each step with the layer-wise adaptive Adam update of "
                          "fp32 master weights under a backoff loss scale")
@@ -66,10 +69,22 @@ def parse():
     ap.add_argument("--summarize-stats", default=None, metavar="CSV")
     ap.add_argument("--summarize-pmc", default=None, metavar="DIR")
     ap.add_argument("--summarize-trace", nargs=2, default=None, metavar=("CSV", "KERNEL"),
-                    help="durations of KERNEL in a kernel trace of the default bench "
-                         "(6 launches per step; pass the traced run's --steps and --warmup)")
+                    help="durations of KERNEL in a kernel trace of a bench run (pass the "
+                         "traced run's --steps, --warmup and the kernel's "
+                         "--launches-per-step)")
+    ap.add_argument("--launches-per-step", type=int, default=6,
+                    help="with --summarize-trace: the kernel's launches per step")
     return ap.parse_args()
 
+
+WORKLOADS = {
+    "fcn": "fcn encoder-decoder step, N=4 x 256x256 x 256ch input, 13 layers "
+           "(99,483,904 weights), L2 head, loss scale 2^15, 25 MiB gradient groups (9)",
+    "densenet": "FC-DenseNet variant step, N=4 x 128x128 x 256ch input, growth 256, "
+                "2 levels of 2-layer dense blocks + bottleneck, average pooling, "
+                "16 conv layers (38,928,896 weights), Huber head (delta 10), "
+                "loss scale 2^15, dense concatenation by channel-slice copies",
+}
 
 COPY_KIB = 256 * 1024  # bytes read (and written) by `--op copy`, in KiB
 
@@ -114,7 +129,7 @@ def summarize_trace(path, kernel, per_step, timed_steps, one_stream_steps):
     """Launch durations of one kernel from a rocprofv3 kernel trace of the
     default bench command: all launches, the first per_step *
     one_stream_steps (warm-up and detail pass, one stream) and the last
-    per_step * timed_steps (the timed region, three streams)."""
+    per_step * timed_steps (the timed region)."""
     import csv
     rows = [r for r in csv.DictReader(open(path))
             if short_kernel_name(r["Kernel_Name"]) == kernel]
@@ -233,12 +248,13 @@ def op_bench(label, steps, warmup):
                       "unit": unit, "launches": steps}), flush=True)
 
 
-def recorded_traffic(kernel):
-    """HBM bytes per launch of `kernel` from profiles/fcn_step_hbm_traffic.md
-    (rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled by a plain copy's reading),
-    or None when no record exists for it or the kernel's source file has
-    changed since the counters were taken."""
-    path = os.path.join(ROOT, "profiles", "fcn_step_hbm_traffic.md")
+def recorded_traffic(kernel, workload="fcn"):
+    """HBM bytes per launch of `kernel` in the workload's step, from
+    profiles/<workload>_step_hbm_traffic.md (rocprofv3 FETCH_SIZE +
+    WRITE_SIZE, scaled by a plain copy's reading), or None when no record
+    exists for it or the kernel's source file has changed since the counters
+    were taken."""
+    path = os.path.join(ROOT, "profiles", f"{workload}_step_hbm_traffic.md")
     try:
         lines = open(path).read().splitlines()
         sha = source_hash(kernel)
@@ -318,8 +334,8 @@ def main():
         summarize_pmc(args.summarize_pmc)
         return
     if args.summarize_trace:
-        summarize_trace(args.summarize_trace[0], args.summarize_trace[1], 6, args.steps,
-                        args.warmup + 2)
+        summarize_trace(args.summarize_trace[0], args.summarize_trace[1],
+                        args.launches_per_step, args.steps, args.warmup + 2)
         return
     if args.op:
         op_bench(args.op, args.steps, args.warmup)
@@ -333,12 +349,23 @@ def main():
     import synth
     from paper_1909_11150_amd.fcn import AdamLARS, Chain, LossScaler
 
-    wl = synth.fcn()
-    layers = wl.layers
-    opt = dict(optimizer=AdamLARS(), scaler=LossScaler(synth.LOSS_SCALE)) \
-        if args.optimizer else {}
-    ch = Chain(layers, wl.weights, wl.x, loss_scale=synth.LOSS_SCALE,
-               group_cap_bytes=synth.GROUP_CAP_BYTES, zero_copy=args.zero_copy, **opt)
+    if args.workload == "densenet":
+        from paper_1909_11150_amd.densenet import DenseNet
+        if args.optimizer or args.zero_copy:
+            print(json.dumps({"error": "the dense workload runs without gradient groups"}))
+            sys.exit(2)
+        args.streams = 1
+        wl = synth.densenet()
+        layers = wl.layers
+        ch = DenseNet(layers, wl.weights, wl.x, loss_scale=synth.LOSS_SCALE,
+                      delta=synth.HUBER_DELTA)
+    else:
+        wl = synth.fcn()
+        layers = wl.layers
+        opt = dict(optimizer=AdamLARS(), scaler=LossScaler(synth.LOSS_SCALE)) \
+            if args.optimizer else {}
+        ch = Chain(layers, wl.weights, wl.x, loss_scale=synth.LOSS_SCALE,
+                   group_cap_bytes=synth.GROUP_CAP_BYTES, zero_copy=args.zero_copy, **opt)
     target = torch.from_numpy(wl.target).cuda()
     # per-call accounting on one stream, where a call's duration is its own
     prog = ch.program(target, streams=1)
@@ -416,7 +443,7 @@ def main():
             "peak": MFMA_F16_PEAK_TFLOPS, "unit": "TFLOP/s",
             "frac": round(achieved / MFMA_F16_PEAK_TFLOPS, 4),
             "avg_launch_us": round(avg_s * 1e6, 2), "launches_per_step": len(dom_idx),
-            "traffic": recorded_traffic(dom)}
+            "traffic": recorded_traffic(dom, args.workload)}
     v = per_kernel[dom]
     alone_s = v[1] / v[0] * 1e-3
     alone = v[2] / v[0] / alone_s / 1e12
@@ -446,9 +473,7 @@ def main():
         "vs_baseline": None,
         "dtype": "f16",
         "data": "synthetic",
-        "config": {"workload": "fcn encoder-decoder step, N=4 x 256x256 x 256ch input, "
-                               "13 layers (99,483,904 weights), L2 head, loss scale 2^15, "
-                               "25 MiB gradient groups (9)",
+        "config": {"workload": WORKLOADS[args.workload],
                    "global_batch": 4, "conv_tflop_per_step": round(flops_step / 1e12, 4),
                    "streams": args.streams, "zero_copy_groups": args.zero_copy,
                    "optimizer": "lars_adam" if args.optimizer else None},

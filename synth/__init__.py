@@ -19,6 +19,7 @@ import numpy as np
 LOSS_SCALE = 2.0 ** 15
 GROUP_CAP_BYTES = 25 * 1024 * 1024
 GROUP_ALIGN_BYTES = 256
+HUBER_DELTA = 10.0   # the Huber cutoff the paper starts from (Section 6.2)
 
 
 @dataclass(frozen=True)
