@@ -60,7 +60,8 @@ def parse():
                          "the non-finite check fused into their store)")
     ap.add_argument("--workload", default="fcn", choices=("fcn", "densenet"),
                     help="fcn: the encoder-decoder step; densenet: the FC-DenseNet "
-                         "variant's step (one stream, no gradient groups)")
+                         "variant's step (no gradient groups; --streams above 1 runs its "
+                         "kernel gradients on a second stream)")
     ap.add_argument("--optimizer", action="store_true",
                     help="end each step with the layer-wise adaptive Adam update of "
                          "fp32 master weights under a backoff loss scale")
@@ -83,7 +84,8 @@ WORKLOADS = {
     "densenet": "FC-DenseNet variant step, N=4 x 128x128 x 256ch input, growth 256, "
                 "2 levels of 2-layer dense blocks + bottleneck, average pooling, "
                 "16 conv layers (38,928,896 weights), Huber head (delta 10), "
-                "loss scale 2^15, dense concatenation by channel-slice copies",
+                "loss scale 2^15, dense concatenation by channel-slice copies, "
+                "kernel gradients on a second stream",
 }
 
 COPY_KIB = 256 * 1024  # bytes read (and written) by `--op copy`, in KiB
@@ -354,7 +356,7 @@ def main():
         if args.optimizer or args.zero_copy:
             print(json.dumps({"error": "the dense workload runs without gradient groups"}))
             sys.exit(2)
-        args.streams = 1
+        args.streams = 2 if args.streams > 1 else 1   # kernel gradients beside
         wl = synth.densenet()
         layers = wl.layers
         ch = DenseNet(layers, wl.weights, wl.x, loss_scale=synth.LOSS_SCALE,

@@ -24,8 +24,9 @@ import ctypes
 import torch
 
 from . import (EPI_NONE, EPI_RELU, OP_BWD_DATA, OP_BWD_WEIGHT, OP_CONVT, OP_FWD,
-               ConvDesc, FgError, kernel_name, lib, workspace_bytes)
-from .fcn import Call, chain_workspace_bytes, convt_dw_desc, convt_dx_desc, fwd_desc
+               FgError, kernel_name, lib, workspace_bytes)
+from .fcn import (Call, chain_workspace_bytes, convt_dw_desc, convt_dx_desc, fwd_desc,
+                  kernel_gradient_workspace_bytes)
 
 F16 = torch.float16
 
@@ -71,14 +72,19 @@ class DenseNet:
         self._block_bufs("B")
         for d in range(1, self.levels + 1):
             self._block_bufs(f"U{d}")
-        # gradient scratch, one per resolution (the step runs in order)
+        # gradient buffers (the input-gradient scratch dZin is one per
+        # resolution: the main stream uses it in order)
         self.g_out = e(self.L["F1x1"].y_shape)
         self.dX = e(self.x.shape)
+        # a layer's output gradient has a buffer of its own: its kernel
+        # gradient may still read it on the side stream while the next
+        # layer's is written
         self.dY, self.dZin, self.dT, self.dP, self.dU = {}, {}, {}, {}, {}
         for blk in self._blocks():
             n, h, w, _ = self.L[f"{blk}.1"].x_shape
             cmax = max(self.L[f"{blk}.{l}"].x_shape[3] for l in range(1, self.per + 1))
-            self.dY.setdefault(h, e((n, h, w, self.k)))
+            for l in range(1, self.per + 1):
+                self.dY[f"{blk}.{l}"] = e((n, h, w, self.k))
             old = self.dZin.get(h)
             if old is None or old.shape[3] < cmax:
                 self.dZin[h] = e((n, h, w, cmax))
@@ -107,10 +113,12 @@ class DenseNet:
             self.dNF[blk] = e((n, h, w, self.per * self.k))
 
     # ---- prepared calls ----------------------------------------------------------
-    def program(self, target, streams=1):
-        if streams != 1:
-            raise ValueError("the dense network's step runs on one stream")
-        return _DenseProgram(self, target)
+    def program(self, target, streams=2):
+        """streams = 1: every call in order on one stream; 2 (or more): the
+        kernel gradients on a second stream."""
+        if streams < 1:
+            raise ValueError("streams must be >= 1")
+        return _DenseProgram(self, target, min(streams, 2))
 
     def step(self, target):
         key = target.data_ptr()
@@ -118,26 +126,45 @@ class DenseNet:
             self._prog = self.program(target)
             self._prog_key = key
         self._prog.run()
+        self._prog.join()
 
     def conv_flops(self):
         return sum(3 * L.flops for L in self.layers)
 
 
 class _DenseProgram:
-    """The step as a list of prepared library calls on one stream (the
-    chain step program's interface: calls, streams, events, run, join)."""
+    """The step as a list of prepared library calls (the chain step
+    program's interface: calls, streams, events, run, join). With two
+    streams each kernel gradient runs on the second one as soon as its
+    output gradient is written (an event after the writing call), beside the
+    main stream's input gradients and copies, with a workspace of its own;
+    the main stream waits for the second stream's last call at the end of
+    the step, before the next forward pass overwrites what the kernel
+    gradients read. Every kernel reads only finished inputs, so the results
+    equal the one-stream order's."""
 
-    def __init__(self, net, target):
+    def __init__(self, net, target, streams=1):
         self.net = net
         self._keep = [target]
         self.calls = []
         self._L = lib()
         main = torch.cuda.ExternalStream(net.stream, device=net.dev) \
             if net.stream is not None else torch.cuda.current_stream(net.dev)
-        self.streams = (main,)
-        self._sp = ctypes.c_void_p(main.cuda_stream)
+        self.streams = (main,) if streams == 1 else (main, torch.cuda.Stream(device=net.dev))
+        self._sp = [ctypes.c_void_p(x.cuda_stream) for x in self.streams]
+        if streams > 1:
+            self._ws_side = torch.empty(
+                max(16, kernel_gradient_workspace_bytes(net.layers)), dtype=torch.uint8,
+                device=net.dev)
         self._build(target)
-        self.final, self.step_final, self.events = (), (), {}
+        if streams == 1:
+            self.calls = [c._replace(sid=0, deps=()) for c in self.calls]
+        self.calls = [c._replace(args=c.args + (self._sp[c.sid],)) for c in self.calls]
+        self.final = tuple(max(j for j, c in enumerate(self.calls) if c.sid == sid)
+                           for sid in range(1, len(self.streams)))
+        self.step_final = self.final
+        needed = {d for c in self.calls for d in c.deps} | set(self.final)
+        self.events = {j: torch.cuda.Event() for j in sorted(needed)}
 
     # -- checks: every buffer a call touches holds what the call addresses --
     @staticmethod
@@ -155,8 +182,9 @@ class _DenseProgram:
         self._keep.append(d)
         return ctypes.byref(d)
 
-    def _add(self, label, kernel, work, fn, args, single=True):
-        self.calls.append(Call(label, kernel, work, fn, args + (self._sp,), single))
+    def _add(self, label, kernel, work, fn, args, single=True, sid=0, deps=()):
+        """Append a call; the stream argument is added once all are built."""
+        self.calls.append(Call(label, kernel, work, fn, args, single, sid, deps))
 
     # -- ops --
     def conv_fwd(self, name, x, y, relu):
@@ -179,19 +207,24 @@ class _DenseProgram:
                       workspace_bytes(d, OP_CONVT) == 0)
 
     def conv_bwd(self, name, x, dy, dx):
-        """Kernel gradient into dw[name]; input gradient into dx (no gate)."""
+        """Kernel gradient into dw[name] (second stream, after the call that
+        wrote dy, which is the last one appended); input gradient into dx
+        (no gate)."""
         L = self.net.L[name]
         n = self.net
         self._shape_ok(x, L.x_shape)
         self._shape_ok(dy, L.y_shape)
         self._shape_ok(dx, L.x_shape)
         wsp, wsb = n.ws.data_ptr(), n.ws.numel()
+        side = len(self.streams) > 1
+        dws, dwb = (self._ws_side.data_ptr(), self._ws_side.numel()) if side else (wsp, wsb)
+        dwk = dict(sid=1 if side else 0, deps=(len(self.calls) - 1,))
         if L.kind == "conv":
             d = fwd_desc(L)
             self._add(f"{name}.dW", kernel_name(d, OP_BWD_WEIGHT), L.flops,
                       self._L.conv2d_bwd_weight,
                       (self._desc(d), x.data_ptr(), dy.data_ptr(), n.dw[name].data_ptr(),
-                       wsp, wsb), workspace_bytes(d, OP_BWD_WEIGHT) == 0)
+                       dws, dwb), workspace_bytes(d, OP_BWD_WEIGHT) == 0, **dwk)
             self._add(f"{name}.dx", kernel_name(d, OP_BWD_DATA), L.flops,
                       self._L.conv2d_bwd_data,
                       (self._desc(d), dy.data_ptr(), n.w[name].data_ptr(), dx.data_ptr(),
@@ -201,7 +234,7 @@ class _DenseProgram:
             self._add(f"{name}.dW", kernel_name(d, OP_BWD_WEIGHT), L.flops,
                       self._L.conv2d_bwd_weight,
                       (self._desc(d), dy.data_ptr(), x.data_ptr(), n.dw[name].data_ptr(),
-                       wsp, wsb), workspace_bytes(d, OP_BWD_WEIGHT) == 0)
+                       dws, dwb), workspace_bytes(d, OP_BWD_WEIGHT) == 0, **dwk)
             d = convt_dx_desc(L)
             self._add(f"{name}.dx", kernel_name(d, OP_FWD), L.flops, self._L.conv2d_fwd,
                       (self._desc(d), dy.data_ptr(), n.w[name].data_ptr(), dx.data_ptr(),
@@ -251,7 +284,7 @@ class _DenseProgram:
             name = f"{blk}.{l}"
             lo = c0 + (l - 1) * n.k
             h = n.L[name].x_shape[1]
-            dY = n.dY[h]
+            dY = n.dY[name]
             zin = n.Z[(blk, l - 1)] if l > 1 or blk.startswith("U") else self._block_input[blk]
             self.copy(f"{name}.dy", G, lo, cl, dY, 0, n.k, n.k, gate=n.act[name], gld=n.k)
             dZ = n.dZin[h]
@@ -351,15 +384,26 @@ class _DenseProgram:
         self._head_args[3].value = s / self.net.act["F1x1"].numel()
 
     def run(self, events=None):
+        """Run the step once. events: {call index: (start, end)} HIP events
+        recorded around those calls on the call's stream."""
+        streams, evs = self.streams, self.events
         for i, c in enumerate(self.calls):
+            s = streams[c.sid]
+            for d in c.deps:
+                s.wait_event(evs[d])
             ev = events.get(i) if events else None
             if ev:
-                ev[0].record(self.streams[0])
+                ev[0].record(s)
             st = c.fn(*c.args)
             if st:
                 raise FgError(c.label, st)
             if ev:
-                ev[1].record(self.streams[0])
+                ev[1].record(s)
+            if i in evs:
+                evs[i].record(s)
+        for j in self.step_final:
+            streams[0].wait_event(evs[j])
 
     def join(self):
-        pass
+        """The main stream already waits for the other stream's last call
+        at the end of each run."""

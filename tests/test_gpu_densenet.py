@@ -102,6 +102,26 @@ def test_reduced_densenet_program_is_deterministic():
         assert np.array_equal(outs[0][k], outs[1][k]), k
 
 
+def test_two_streams_match_one_stream():
+    """Kernel gradients on a second stream give the bits of the one-stream
+    order, over two steps."""
+    layers, x, w, t = _reduced()
+    td = dev(t)
+    out = []
+    for streams in (1, 2):
+        net = DenseNet(layers, w, x, loss_scale=S_RED, delta=DELTA)
+        prog = net.program(td, streams=streams)
+        assert len(prog.streams) == streams
+        for _ in range(2):
+            prog.run()
+        prog.join()
+        torch.cuda.synchronize()
+        out.append({k: host(v).view(np.uint16).copy() for k, v in net.dw.items()})
+        out[-1]["dX"] = host(net.dX).view(np.uint16).copy()
+    for k in out[0]:
+        assert np.array_equal(out[0][k], out[1][k]), k
+
+
 def _unique_layers():
     seen, out = set(), []
     for L in synth.densenet_layers():
