@@ -259,8 +259,9 @@ enum { FG_GRAD_F32 = 0, FG_GRAD_F16_SCALED = 1 };
  * ones (a few ulps). t: host array of ntensors (1..FG_MAX_SEGMENTS) layers
  * with fp32 gradients, read during the call only. FG_EINVAL for null or
  * misaligned pointers, overlapping arrays, params outside lr >= 0,
- * 0 <= beta < 1, eps >= 0, weight_decay >= 0, or nflags > 0 with null
- * flags; FG_EWORKSPACE if ws_bytes is short or ws is not 16-byte aligned.
+ * 0 <= beta < 1, eps >= 0, weight_decay >= 0, nflags > 0 with null flags,
+ * or flags overlapping ws, the step count or an array the update writes;
+ * FG_EWORKSPACE if ws_bytes is short or ws is not 16-byte aligned.
  * Same as lars_adam_norms over all layers followed by lars_adam_apply. */
 fg_status lars_adam_update(const fg_opt_tensor *t, int32_t ntensors,
                            const fg_opt_params *p,

@@ -585,6 +585,23 @@ static fg_status opt_call_ok(const fg_opt_tensor *t, int32_t n, const fg_opt_par
   return FG_OK;
 }
 
+// The flags the update reads may not lie in memory the update writes.
+static bool opt_flags_ok(const fg_opt_tensor *t, int32_t n, const int32_t *flags,
+                         int32_t nflags, const int32_t *step_count, const void *ws) {
+  if (nflags < 0 || (nflags > 0 && !flags)) return false;
+  if (nflags == 0) return true;
+  const size_t fb = (size_t)nflags * 4;
+  if (overlap(flags, fb, step_count, 4) || overlap(flags, fb, ws, lars_adam_ws_bytes(t, n)))
+    return false;
+  for (int i = 0; i < n; ++i) {
+    const uint64_t pa[4] = {t[i].w32, t[i].m, t[i].v, t[i].w16};
+    const size_t ba[4] = {4, 4, 4, 2};
+    for (int a = 0; a < 4; ++a)
+      if (overlap((const void *)pa[a], t[i].numel * ba[a], flags, fb)) return false;
+  }
+  return true;
+}
+
 // Per workspace: which tensors have partial norms for the step in progress
 // and which have been applied, for one table, gradient form and set of
 // parameters (a hash of them). An apply is accepted only once every tensor
@@ -639,6 +656,7 @@ fg_status lars_adam_update(const fg_opt_tensor *t, int32_t ntensors,
   const fg_status st =
       opt_call_ok(t, ntensors, p, FG_GRAD_F32, 1.f, step_count, ws, ws_bytes);
   if (st != FG_OK) return st;
+  if (!opt_flags_ok(t, ntensors, found_nonfinite, nflags, step_count, ws)) return FG_EINVAL;
   {  // this call overwrites any partial norms held in the workspace
     std::lock_guard<std::mutex> lk(g_norms_mu);
     g_norms.erase((uintptr_t)ws);
@@ -682,6 +700,7 @@ fg_status lars_adam_apply(const fg_opt_tensor *t, int32_t ntensors, int32_t firs
   const fg_status st =
       opt_call_ok(t, ntensors, p, grad_format, grad_inv_scale, step_count, ws, ws_bytes);
   if (st != FG_OK) return st;
+  if (!opt_flags_ok(t, ntensors, found_nonfinite, nflags, step_count, ws)) return FG_EINVAL;
   if (first < 0 || count < 1 || first > ntensors - count) return FG_EINVAL;
   const uint64_t key = norms_key(t, ntensors, p, grad_format, grad_inv_scale, step_count);
   const uint64_t range = full_mask(first + count) & ~full_mask(first);

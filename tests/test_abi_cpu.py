@@ -191,6 +191,10 @@ def test_optimizer_argument_checks(L):
     alias = (fg.OptTensor * 2)(layer(FAKE), layer(FAKE + 2048))  # second w32 inside the first
     assert L.lars_adam_update(alias, 2, ref(p), None, 0, sc, ws, need, None) == fg.FG_EINVAL
     assert L.lars_adam_update(good, 2, ref(p), None, 0, FAKE + 64, ws, need, None) == fg.FG_EINVAL
+    # flags inside memory the update writes: the step count, the workspace, a weight
+    for bad_flags in (sc, ws + 16, FAKE + 8):
+        assert L.lars_adam_update(good, 2, ref(p), bad_flags, 2, sc, ws, need,
+                                  None) == fg.FG_EINVAL
 
 
 def test_optimizer_split_argument_checks(L):

@@ -71,7 +71,6 @@ def test_gradient_path_at_maximum_size():
     off1 = grp["offsets"][grp["members"].index(1)]
     assert off1 == n0
     # the group holds member 0 then member 1, bit for bit
-    want = np.where(idx < n0, 0, 1)
     got16 = _take(gbuf, idx).view(np.uint16)
     src16 = np.empty_like(got16)
     m0 = idx < n0
@@ -87,7 +86,7 @@ def test_gradient_path_at_maximum_size():
     got1 = _take(dsts[1], idx[~m0] - n0)
     np.testing.assert_array_equal(got0.view(np.uint32), r32[m0].view(np.uint32))
     np.testing.assert_array_equal(got1.view(np.uint32), r32[~m0].view(np.uint32))
-    assert np.isinf(got1[-1]) and want[-1] == 1
+    assert np.isinf(got1[-1]) and idx[-1] == total - 1
 
 
 def test_conv_at_maximum_size():
