@@ -60,8 +60,8 @@ def parse():
                          "the non-finite check fused into their store)")
     ap.add_argument("--workload", default="fcn", choices=("fcn", "densenet"),
                     help="fcn: the encoder-decoder step; densenet: the FC-DenseNet "
-                         "variant's step (no gradient groups; --streams above 1 runs its "
-                         "kernel gradients on a second stream)")
+                         "variant's step (no gradient groups; with --streams 3 its kernel "
+                         "gradients run on a second stream)")
     ap.add_argument("--optimizer", action="store_true",
                     help="end each step with the layer-wise adaptive Adam update of "
                          "fp32 master weights under a backoff loss scale")
@@ -356,7 +356,9 @@ def main():
         if args.optimizer or args.zero_copy:
             print(json.dumps({"error": "the dense workload runs without gradient groups"}))
             sys.exit(2)
-        args.streams = 2 if args.streams > 1 else 1   # kernel gradients beside
+        # kernel gradients on a second stream (a third stream for the
+        # concatenation copies measures slower)
+        args.streams = min(args.streams, 2)
         wl = synth.densenet()
         layers = wl.layers
         ch = DenseNet(layers, wl.weights, wl.x, loss_scale=synth.LOSS_SCALE,

@@ -40,22 +40,30 @@ def _reduced():
 
 
 def _gpu_forward_state(net):
-    """The GPU's stored forward tensors, keyed as the oracle network's."""
+    """The GPU's stored forward tensors, keyed as the oracle network's. The
+    last concatenation of the bottleneck and up blocks, which nothing reads
+    and the GPU does not keep, is rebuilt on the host from the block's
+    tensors (the oracle's backward pass takes only its shape)."""
     fw = {name: host(a) for name, a in net.act.items()}
     fw["y"] = fw["F1x1"]
     lv, per = net.levels, net.per
-    for blk in net._blocks():
-        for l in range(1, per + 1):
-            fw[f"Z:{blk}:{l}"] = host(net.Z[(blk, l)])
     fw["Z:D1:0"] = fw["C0"]
     for d in range(1, lv + 1):
         fw[f"P{d}"] = host(net.P[d])
-        fw[f"skip{d}"] = fw[f"Z:D{d}:{per}"]
         fw[f"Z:U{d}:0"] = host(net.Z[(f"U{d}", 0)])
         if d > 1:
             fw[f"Z:D{d}:0"] = fw[f"P{d - 1}"]
         fw[f"in:TU{d}"] = host(net.NF["B" if d == lv else f"U{d + 1}"])
     fw["Z:B:0"] = fw[f"P{lv}"]
+    for blk in net._blocks():
+        for l in range(1, per + 1):
+            if (blk, l) in net.Z:
+                fw[f"Z:{blk}:{l}"] = host(net.Z[(blk, l)])
+            else:
+                fw[f"Z:{blk}:{l}"] = np.concatenate([fw[f"Z:{blk}:{l - 1}"],
+                                                     fw[f"{blk}.{l}"]], axis=-1)
+    for d in range(1, lv + 1):
+        fw[f"skip{d}"] = fw[f"Z:D{d}:{per}"]
     fw["in:F1x1"] = host(net.NF["U1"])
     return fw
 
@@ -102,13 +110,13 @@ def test_reduced_densenet_program_is_deterministic():
         assert np.array_equal(outs[0][k], outs[1][k]), k
 
 
-def test_two_streams_match_one_stream():
-    """Kernel gradients on a second stream give the bits of the one-stream
-    order, over two steps."""
+def test_streams_match_one_stream():
+    """Kernel gradients on a second stream, and concatenation copies on a
+    third, give the bits of the one-stream order, over two steps."""
     layers, x, w, t = _reduced()
     td = dev(t)
     out = []
-    for streams in (1, 2):
+    for streams in (1, 2, 3):
         net = DenseNet(layers, w, x, loss_scale=S_RED, delta=DELTA)
         prog = net.program(td, streams=streams)
         assert len(prog.streams) == streams
@@ -118,8 +126,9 @@ def test_two_streams_match_one_stream():
         torch.cuda.synchronize()
         out.append({k: host(v).view(np.uint16).copy() for k, v in net.dw.items()})
         out[-1]["dX"] = host(net.dX).view(np.uint16).copy()
-    for k in out[0]:
-        assert np.array_equal(out[0][k], out[1][k]), k
+    for o in out[1:]:
+        for k in out[0]:
+            assert np.array_equal(out[0][k], o[k]), k
 
 
 def _unique_layers():
