@@ -71,12 +71,18 @@ typedef enum {
 /* Epilogue fused into the convolution's output.
  *   FG_EPI_NONE  out = fp16(acc)
  *   FG_EPI_RELU  out = fp16(acc > 0 ? acc : +0)          (forward ReLU)
+ *   FG_EPI_ACC   out = fp16(out + acc): the result is added to what the
+ *                output holds (gradient contributions summed in place; the
+ *                staged store rounds acc to fp16 before the addition). Not
+ *                for the K = 1 head (FG_EUNSUPPORTED).
  *   FG_EPI_GATE  out = fp16(gate > 0 ? acc : +0)         (ReLU backward;
  *                gate = the forward ReLU output at the same index, an fp16
  *                tensor with the output's shape)
  * acc is the fp32 accumulator; fp16() rounds to nearest-even with overflow
  * to +-infinity (no saturation) and keeps subnormals. */
-typedef enum { FG_EPI_NONE = 0, FG_EPI_RELU = 1, FG_EPI_GATE = 2 } fg_epilogue;
+typedef enum {
+    FG_EPI_NONE = 0, FG_EPI_RELU = 1, FG_EPI_GATE = 2, FG_EPI_ACC = 3
+} fg_epilogue;
 
 /* Shape of a convolution, always described by its forward direction:
  *   n, h, w, c   the input image (NHWC); for the transposed convolution, its
@@ -88,6 +94,17 @@ typedef struct {
     int32_t n, h, w, c;
     int32_t k, r, s;
     int32_t stride_h, stride_w, pad_h, pad_w;
+    /* Pixel strides, in elements, of the x-shaped tensors (x, dx) and the
+     * y-shaped ones (y, dy); 0 means dense (c, resp. k). A stride other
+     * than dense is honoured where that tensor is the pass's output (y of
+     * conv2d_fwd and conv_transpose2d_fwd, dx of conv2d_bwd_data), so that
+     * a pass can write into a channel slice of a wider buffer (the pointer
+     * then addresses the slice's first channel): it must be >= the channel
+     * count and a multiple of 8, the output pointer 16-byte aligned, and
+     * pixels * stride below 2^31 (else FG_EUNSUPPORTED; below the channel
+     * count, FG_EINVAL). A gate is laid out like the output. Inputs, and
+     * the K = 1 head's tensors, are dense (FG_EUNSUPPORTED otherwise). */
+    int32_t x_ld, y_ld;
 } fg_conv_desc;
 
 /* One member of a gradient group: `ptr` is a device address (fp16 dW for

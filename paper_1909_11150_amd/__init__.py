@@ -14,7 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libfcngrad.so")
 
 FG_OK, FG_EINVAL, FG_EUNSUPPORTED, FG_EWORKSPACE, FG_ELAUNCH = range(5)
-EPI_NONE, EPI_RELU, EPI_GATE = 0, 1, 2
+EPI_NONE, EPI_RELU, EPI_GATE, EPI_ACC = 0, 1, 2, 3
 OP_FWD, OP_BWD_DATA, OP_BWD_WEIGHT, OP_CONVT = 0, 1, 2, 3
 MAX_SEGMENTS = 64
 GRAD_F32, GRAD_F16_SCALED = 0, 1
@@ -56,13 +56,15 @@ class FgError(RuntimeError):
 
 
 class ConvDesc(ctypes.Structure):
+    """fg_conv_desc. x_ld / y_ld: pixel strides of the x- and y-shaped
+    tensors (0: dense), honoured where that tensor is the pass's output."""
     _fields_ = [(f, ctypes.c_int32) for f in
                 ("n", "h", "w", "c", "k", "r", "s", "stride_h", "stride_w",
-                 "pad_h", "pad_w")]
+                 "pad_h", "pad_w", "x_ld", "y_ld")]
 
     @classmethod
-    def make(cls, n, h, w, c, k, r, s, stride=1, pad=0):
-        return cls(n, h, w, c, k, r, s, stride, stride, pad, pad)
+    def make(cls, n, h, w, c, k, r, s, stride=1, pad=0, x_ld=0, y_ld=0):
+        return cls(n, h, w, c, k, r, s, stride, stride, pad, pad, x_ld, y_ld)
 
 
 class Segment(ctypes.Structure):

@@ -39,7 +39,7 @@ fg_status check_desc(const fg_conv_desc *d) {
   if (!d) return FG_EINVAL;
   if (!pos(d->n) || !pos(d->h) || !pos(d->w) || !pos(d->c) || !pos(d->k) ||
       !pos(d->r) || !pos(d->s) || !pos(d->stride_h) || !pos(d->stride_w) ||
-      d->pad_h < 0 || d->pad_w < 0)
+      d->pad_h < 0 || d->pad_w < 0 || d->x_ld < 0 || d->y_ld < 0)
     return FG_EINVAL;
   return FG_OK;
 }
@@ -70,6 +70,32 @@ bool sizes_ok(int64_t a, int64_t b, int64_t c) {
 
 fg_status launch_status(hipError_t e) {
   return e == hipSuccess ? FG_OK : FG_ELAUNCH;
+}
+
+// Pixel stride (elements) of a tensor with ch channels: ld, 0 meaning dense.
+int64_t ld_or(int32_t ld, int32_t ch) { return ld ? ld : ch; }
+
+// Inputs are read dense.
+bool dense_ld(int32_t ld, int32_t ch) { return ld == 0 || ld == ch; }
+
+// An output written at pixel stride ld: dense, or ld >= ch, a multiple of 8
+// elements, a 16-byte aligned pointer and npix * ld below 2^31.
+fg_status out_ld_ok(int32_t ld, int32_t ch, int64_t npix, const void *p) {
+  if (dense_ld(ld, ch)) return FG_OK;
+  if (ld < ch) return FG_EINVAL;
+  if (ld % 8 != 0 || ((uintptr_t)p & 15) != 0) return FG_EUNSUPPORTED;
+  if (npix * (int64_t)ld >= kMaxElems) return FG_EUNSUPPORTED;
+  return FG_OK;
+}
+
+// Bytes from the first to the last element of npix pixels at stride ld.
+size_t span_bytes(int64_t npix, int64_t ld, int64_t ch) {
+  return (size_t)((npix - 1) * ld + ch) * 2;
+}
+
+bool epi_ok(int epi) {
+  return epi == FG_EPI_NONE || epi == FG_EPI_RELU || epi == FG_EPI_GATE ||
+         epi == FG_EPI_ACC;
 }
 
 // Phase description for an input-gradient style convolution (scatter form
@@ -124,6 +150,7 @@ DataConvArgs fwd_args(const fg_conv_desc *d, int32_t P, int32_t Q) {
   memset(&a, 0, sizeof(a));
   a.n = d->n; a.hi = d->h; a.wi = d->w; a.cr = d->c;
   a.ho = P; a.wo = Q; a.co = d->k;
+  a.ldo = (int32_t)ld_or(d->y_ld, d->k);
   a.istr = d->stride_h;
   a.ostr = 1;
   a.s = d->s;
@@ -145,6 +172,7 @@ DataConvArgs bwd_data_args(const fg_conv_desc *d, int32_t P, int32_t Q) {
   memset(&a, 0, sizeof(a));
   a.n = d->n; a.hi = P; a.wi = Q; a.cr = d->k;
   a.ho = d->h; a.wo = d->w; a.co = d->c;
+  a.ldo = (int32_t)ld_or(d->x_ld, d->c);
   a.istr = 1;
   a.ostr = d->stride_h;
   a.s = d->s;
@@ -163,6 +191,7 @@ DataConvArgs convt_args(const fg_conv_desc *d, int32_t HO, int32_t WO) {
   memset(&a, 0, sizeof(a));
   a.n = d->n; a.hi = d->h; a.wi = d->w; a.cr = d->c;
   a.ho = HO; a.wo = WO; a.co = d->k;
+  a.ldo = (int32_t)ld_or(d->y_ld, d->k);
   a.istr = 1;
   a.ostr = d->stride_h;
   a.s = d->s;
@@ -297,8 +326,7 @@ fg_status conv2d_fwd(const fg_conv_desc *d, const uint16_t *x,
   fg_status st = check_desc(d);
   if (st != FG_OK) return st;
   if (!x || !w_krsc || !y) return FG_EINVAL;
-  if (epi != FG_EPI_NONE && epi != FG_EPI_RELU && epi != FG_EPI_GATE)
-    return FG_EINVAL;
+  if (!epi_ok(epi)) return FG_EINVAL;
   if (epi == FG_EPI_GATE && !gate) return FG_EINVAL;
   int32_t P, Q;
   if (fg_conv_out_dims(d, 0, &P, &Q) != FG_OK) return FG_EINVAL;
@@ -306,17 +334,23 @@ fg_status conv2d_fwd(const fg_conv_desc *d, const uint16_t *x,
   const int64_t nw = elems4(d->k, d->r, d->s, d->c);
   const int64_t ny = elems4(d->n, P, Q, d->k);
   if (!sizes_ok(nx, nw, ny)) return FG_EUNSUPPORTED;
-  if (overlap(y, ny * 2, x, nx * 2) || overlap(y, ny * 2, w_krsc, nw * 2))
+  if (!dense_ld(d->x_ld, d->c)) return FG_EUNSUPPORTED;
+  const int64_t npy = (int64_t)d->n * P * Q;
+  if ((st = out_ld_ok(d->y_ld, d->k, npy, y)) != FG_OK) return st;
+  const size_t sy = span_bytes(npy, ld_or(d->y_ld, d->k), d->k);
+  if (overlap(y, sy, x, nx * 2) || overlap(y, sy, w_krsc, nw * 2))
     return FG_EINVAL;
   if ((st = check_conv_support(d)) != FG_OK) return st;
   // one input step per output position for both image axes
   if (d->stride_h != d->stride_w) return FG_EUNSUPPORTED;
 
-  if (d->k == 1)
+  if (d->k == 1) {
+    if (!dense_ld(d->y_ld, d->k) || epi == FG_EPI_ACC) return FG_EUNSUPPORTED;
     return launch_status(launch_head_fwd(x, w_krsc, y, (int64_t)d->n * P * Q,
                                          d->c, epi, gate, stream));
+  }
   if ((st = check_ws(d, FG_OP_FWD, ws, ws_bytes, x, nx * 2, w_krsc, nw * 2, y,
-                     ny * 2, gate, ny * 2)) != FG_OK)
+                     sy, gate, sy)) != FG_OK)
     return st;
   DataConvArgs a = fwd_args(d, P, Q);
   a.act = x;
@@ -335,8 +369,7 @@ fg_status conv2d_bwd_data(const fg_conv_desc *d, const uint16_t *dy,
   fg_status st = check_desc(d);
   if (st != FG_OK) return st;
   if (!dy || !w_krsc || !dx) return FG_EINVAL;
-  if (epi != FG_EPI_NONE && epi != FG_EPI_RELU && epi != FG_EPI_GATE)
-    return FG_EINVAL;
+  if (!epi_ok(epi)) return FG_EINVAL;
   if (epi == FG_EPI_GATE && !gate) return FG_EINVAL;
   int32_t P, Q;
   if (fg_conv_out_dims(d, 0, &P, &Q) != FG_OK) return FG_EINVAL;
@@ -344,16 +377,22 @@ fg_status conv2d_bwd_data(const fg_conv_desc *d, const uint16_t *dy,
   const int64_t nw = elems4(d->k, d->r, d->s, d->c);
   const int64_t ny = elems4(d->n, P, Q, d->k);
   if (!sizes_ok(nx, nw, ny)) return FG_EUNSUPPORTED;
-  if (overlap(dx, nx * 2, dy, ny * 2) || overlap(dx, nx * 2, w_krsc, nw * 2))
+  if (!dense_ld(d->y_ld, d->k)) return FG_EUNSUPPORTED;
+  const int64_t npx = (int64_t)d->n * d->h * d->w;
+  if ((st = out_ld_ok(d->x_ld, d->c, npx, dx)) != FG_OK) return st;
+  const size_t sx = span_bytes(npx, ld_or(d->x_ld, d->c), d->c);
+  if (overlap(dx, sx, dy, ny * 2) || overlap(dx, sx, w_krsc, nw * 2))
     return FG_EINVAL;
   if ((st = check_conv_support(d)) != FG_OK) return st;
   if (d->stride_h != d->stride_w || d->stride_h > 2) return FG_EUNSUPPORTED;
 
-  if (d->k == 1)
+  if (d->k == 1) {
+    if (!dense_ld(d->x_ld, d->c) || epi == FG_EPI_ACC) return FG_EUNSUPPORTED;
     return launch_status(launch_head_bwd_data(
         dy, w_krsc, dx, (int64_t)d->n * d->h * d->w, d->c, epi, gate, stream));
+  }
   if ((st = check_ws(d, FG_OP_BWD_DATA, ws, ws_bytes, dy, ny * 2, w_krsc, nw * 2,
-                     dx, nx * 2, gate, nx * 2)) != FG_OK)
+                     dx, sx, gate, sx)) != FG_OK)
     return st;
   DataConvArgs a = bwd_data_args(d, P, Q);
   a.act = dy;
@@ -372,8 +411,7 @@ fg_status conv_transpose2d_fwd(const fg_conv_desc *d, const uint16_t *x,
   fg_status st = check_desc(d);
   if (st != FG_OK) return st;
   if (!x || !w_crsk || !y) return FG_EINVAL;
-  if (epi != FG_EPI_NONE && epi != FG_EPI_RELU && epi != FG_EPI_GATE)
-    return FG_EINVAL;
+  if (!epi_ok(epi)) return FG_EINVAL;
   if (epi == FG_EPI_GATE && !gate) return FG_EINVAL;
   int32_t HO, WO;
   if (fg_conv_out_dims(d, 1, &HO, &WO) != FG_OK) return FG_EINVAL;
@@ -381,11 +419,15 @@ fg_status conv_transpose2d_fwd(const fg_conv_desc *d, const uint16_t *x,
   const int64_t nw = elems4(d->c, d->r, d->s, d->k);
   const int64_t ny = elems4(d->n, HO, WO, d->k);
   if (!sizes_ok(nx, nw, ny)) return FG_EUNSUPPORTED;
-  if (overlap(y, ny * 2, x, nx * 2) || overlap(y, ny * 2, w_crsk, nw * 2))
+  if (!dense_ld(d->x_ld, d->c)) return FG_EUNSUPPORTED;
+  const int64_t npy = (int64_t)d->n * HO * WO;
+  if ((st = out_ld_ok(d->y_ld, d->k, npy, y)) != FG_OK) return st;
+  const size_t sy = span_bytes(npy, ld_or(d->y_ld, d->k), d->k);
+  if (overlap(y, sy, x, nx * 2) || overlap(y, sy, w_crsk, nw * 2))
     return FG_EINVAL;
   if (!convt_supported(d)) return FG_EUNSUPPORTED;
   if ((st = check_ws(d, FG_OP_CONVT, ws, ws_bytes, x, nx * 2, w_crsk, nw * 2, y,
-                     ny * 2, gate, ny * 2)) != FG_OK)
+                     sy, gate, sy)) != FG_OK)
     return st;
   DataConvArgs a = convt_args(d, HO, WO);
   a.act = x;
@@ -404,6 +446,7 @@ static fg_status bwd_weight(const fg_conv_desc *d, const uint16_t *x,
   fg_status st = check_desc(d);
   if (st != FG_OK) return st;
   if (!x || !dy || !dw_krsc) return FG_EINVAL;
+  if (!dense_ld(d->x_ld, d->c) || !dense_ld(d->y_ld, d->k)) return FG_EUNSUPPORTED;
   int32_t P, Q;
   if (fg_conv_out_dims(d, 0, &P, &Q) != FG_OK) return FG_EINVAL;
   const int64_t nx = elems4(d->n, d->h, d->w, d->c);

@@ -274,8 +274,10 @@ __device__ __forceinline__ u32x2 to_h4(float a, float b, float c, float d) {
   return o;
 }
 
-__device__ __forceinline__ void epilogue4(float v[4], int epi,
-                                          const uint16_t *gate) {
+// Apply the epilogue to 4 consecutive channels; gate and out point at them
+// (out is read for FG_EPI_ACC only).
+__device__ __forceinline__ void epilogue4(float v[4], int epi, const uint16_t *gate,
+                                          const uint16_t *out) {
   if (epi == FG_EPI_RELU) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) v[e] = v[e] > 0.f ? v[e] : 0.f;
@@ -286,7 +288,26 @@ __device__ __forceinline__ void epilogue4(float v[4], int epi,
       uint16_t gb = (uint16_t)(gw[e >> 1] >> (16 * (e & 1)));
       v[e] = h_to_f32(gb) > 0.f ? v[e] : 0.f;
     }
+  } else if (epi == FG_EPI_ACC) {
+    u32x2 ow = *reinterpret_cast<const u32x2 *>(out);
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      v[e] += h_to_f32((uint16_t)(ow[e >> 1] >> (16 * (e & 1))));
   }
+}
+
+// fp16(a + b) for 8 packed pairs (fp32 sum of two fp16 values, one rounding
+// to fp16; the sum of two fp16 values is exact in fp32 unless it is far
+// below the larger's last bit, where the rounding is the same)
+__device__ __forceinline__ u32x4 add_h8(const u32x4 &a, const u32x4 &b) {
+  u32x4 o;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const float lo = h_to_f32((uint16_t)(a[w] & 0xFFFFu)) + h_to_f32((uint16_t)(b[w] & 0xFFFFu));
+    const float hi = h_to_f32((uint16_t)(a[w] >> 16)) + h_to_f32((uint16_t)(b[w] >> 16));
+    o[w] = (uint32_t)f32_to_h(lo) | ((uint32_t)f32_to_h(hi) << 16);
+  }
+  return o;
 }
 
 // The ring: stage s of operand X lives in its own LDS array so that the
@@ -481,7 +502,9 @@ __device__ __forceinline__ void store_tile(f32x16 (&acc)[C::FM][C::FN],
       if (col < npix) {
         const int b = col % P.mw, t = col / P.mw;
         const int aa = t % P.mh, nn = t / P.mh;
-        ob = ((nn * a.ho + aa * a.ostr + P.ooh) * a.wo + b * a.ostr + P.oow) * a.co;
+        // split partials are dense; the output has its own pixel stride
+        ob = ((nn * a.ho + aa * a.ostr + P.ooh) * a.wo + b * a.ostr + P.oow) *
+             (SPLIT ? a.co : a.ldo);
       }
       pos[j * 32 + lane] = ob;
     }
@@ -553,6 +576,14 @@ __device__ __forceinline__ void store_tile(f32x16 (&acc)[C::FM][C::FN],
           d[k][w] &= lo | hi;
         }
     }
+    if (!SPLIT && a.epi == FG_EPI_ACC) {  // add what the output holds
+      u32x4 ow[16];
+#pragma unroll
+      for (int k = 0; k < 16; ++k)
+        ow[k] = *reinterpret_cast<const u32x4 *>(a.out + (ob[k] < 0 ? 0 : ob[k] + cw + ch));
+#pragma unroll
+      for (int k = 0; k < 16; ++k) d[k] = add_h8(d[k], ow[k]);
+    }
 #pragma unroll
     for (int k = 0; k < 16; ++k) {
       if (ob[k] < 0) continue;
@@ -584,7 +615,8 @@ __device__ __forceinline__ void store_direct(f32x16 (&acc)[C::FM][C::FN],
     const int b = col % P.mw, t = col / P.mw;
     const int aa = t % P.mh, nn = t / P.mh;
     const size_t obase =
-        ((size_t)(nn * a.ho + aa * a.ostr + P.ooh) * a.wo + b * a.ostr + P.oow) * a.co;
+        ((size_t)(nn * a.ho + aa * a.ostr + P.ooh) * a.wo + b * a.ostr + P.oow) *
+        (SPLIT ? a.co : a.ldo);
 #pragma unroll
     for (int i = 0; i < C::FM; ++i)
 #pragma unroll
@@ -598,7 +630,7 @@ __device__ __forceinline__ void store_direct(f32x16 (&acc)[C::FM][C::FN],
           *reinterpret_cast<f32x4 *>(a.part + split * out_total + obase + co) =
               f32x4{v[0], v[1], v[2], v[3]};
         } else {
-          epilogue4(v, a.epi, a.gate + obase + co);
+          epilogue4(v, a.epi, a.gate + obase + co, a.out + obase + co);
           *reinterpret_cast<u32x2 *>(a.out + obase + co) =
               to_h4(v[0], v[1], v[2], v[3]);
         }

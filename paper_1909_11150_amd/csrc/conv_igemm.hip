@@ -113,9 +113,10 @@ __device__ __forceinline__ u32x2 to_h4(float a, float b, float c, float d) {
   return o;
 }
 
-// Apply the epilogue to 4 consecutive channels; gate word holds 4 halves.
-__device__ __forceinline__ void epilogue4(float v[4], int epi,
-                                          const uint16_t *gate) {
+// Apply the epilogue to 4 consecutive channels; gate and out point at them
+// (out is read for FG_EPI_ACC only).
+__device__ __forceinline__ void epilogue4(float v[4], int epi, const uint16_t *gate,
+                                          const uint16_t *out) {
   if (epi == FG_EPI_RELU) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) v[e] = v[e] > 0.f ? v[e] : 0.f;
@@ -126,6 +127,11 @@ __device__ __forceinline__ void epilogue4(float v[4], int epi,
       uint16_t gb = (uint16_t)(gw[e >> 1] >> (16 * (e & 1)));
       v[e] = h_to_f32(gb) > 0.f ? v[e] : 0.f;
     }
+  } else if (epi == FG_EPI_ACC) {
+    u32x2 ow = *reinterpret_cast<const u32x2 *>(out);
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      v[e] += h_to_f32((uint16_t)(ow[e >> 1] >> (16 * (e & 1))));
   }
 }
 
@@ -311,9 +317,10 @@ __global__ __launch_bounds__(C::NT) void data_conv_kernel(DataConvArgs a) {
     if (col >= npix) continue;
     int b = col % P.mw, t = col / P.mw;
     int aa = t % P.mh, nn = t / P.mh;
+    // split partials are dense; the output has its own pixel stride
     size_t obase = ((size_t)(nn * a.ho + aa * a.ostr + P.ooh) * a.wo +
                     b * a.ostr + P.oow) *
-                   a.co;
+                   (SPLIT ? a.co : a.ldo);
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -327,7 +334,7 @@ __global__ __launch_bounds__(C::NT) void data_conv_kernel(DataConvArgs a) {
           f32x4 o = {v[0], v[1], v[2], v[3]};
           *reinterpret_cast<f32x4 *>(a.part + split * out_total + obase + co) = o;
         } else {
-          epilogue4(v, a.epi, a.gate + obase + co);
+          epilogue4(v, a.epi, a.gate + obase + co, a.out + obase + co);
           *reinterpret_cast<u32x2 *>(a.out + obase + co) =
               to_h4(v[0], v[1], v[2], v[3]);
         }
@@ -335,11 +342,12 @@ __global__ __launch_bounds__(C::NT) void data_conv_kernel(DataConvArgs a) {
   }
 }
 
-// Sum nsplit fp32 partial arrays of len elements in split order, apply the
-// epilogue, round to fp16. len is a multiple of 4.
+// Sum nsplit fp32 partial arrays of len elements (dense, co channels per
+// pixel) in split order, apply the epilogue, round to fp16 into out (and
+// read gate) at pixel stride ldo. len and co are multiples of 4.
 __global__ __launch_bounds__(256) void split_epilogue_kernel(
-    const float *part, int nsplit, int64_t len, int epi, const uint16_t *gate,
-    uint16_t *out) {
+    const float *part, int nsplit, int64_t len, int co, int ldo, int epi,
+    const uint16_t *gate, uint16_t *out) {
   int64_t i4 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
   if (i4 >= len) return;
   f32x4 s = *reinterpret_cast<const f32x4 *>(part + i4);
@@ -348,9 +356,11 @@ __global__ __launch_bounds__(256) void split_epilogue_kernel(
 #pragma unroll
     for (int e = 0; e < 4; ++e) s[e] += v[e];
   }
+  const int64_t pix = i4 / co;
+  const int64_t o = pix * ldo + (i4 - pix * co);
   float v[4] = {s[0], s[1], s[2], s[3]};
-  epilogue4(v, epi, gate + i4);
-  *reinterpret_cast<u32x2 *>(out + i4) = to_h4(v[0], v[1], v[2], v[3]);
+  epilogue4(v, epi, gate + o, out + o);
+  *reinterpret_cast<u32x2 *>(out + o) = to_h4(v[0], v[1], v[2], v[3]);
 }
 
 // ---------------------------------------------------------------------------
@@ -813,7 +823,7 @@ hipError_t launch_data_conv(const DataConvArgs &a0, bool w_kmajor,
   const int64_t len = (int64_t)a.n * a.ho * a.wo * a.co;
   hipLaunchKernelGGL(split_epilogue_kernel,
                      dim3((unsigned)((len / 4 + 255) / 256)), dim3(256), 0, st,
-                     a.part, a.nsplit, len, a.epi, a.gate, a.out);
+                     a.part, a.nsplit, len, a.co, a.ldo, a.epi, a.gate, a.out);
   return hipGetLastError();
 }
 

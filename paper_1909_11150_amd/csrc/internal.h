@@ -28,10 +28,11 @@ struct Phase {
 struct DataConvArgs {
   const uint16_t *act;   // input image  [n][hi][wi][cr]
   const uint16_t *wgt;   // weights (layout per w_kmajor)
-  uint16_t *out;         // output image [n][ho][wo][co]
-  const uint16_t *gate;  // shaped like out (FG_EPI_GATE) or null
+  uint16_t *out;         // output image [n][ho][wo][co], pixel stride ldo
+  const uint16_t *gate;  // laid out like out (FG_EPI_GATE) or null
   int32_t n, hi, wi, cr;
   int32_t ho, wo, co;
+  int32_t ldo;           // pixel stride of out (and gate), elements (>= co)
   int32_t istr, ostr;
   int32_t s;             // kernel width
   // weight element (co, r, s, cr):
