@@ -261,3 +261,32 @@ def test_dense_glue_argument_checks(L):
     assert L.channel_slice_copy(a, 64, None, 0, a + 16, 64, 10, 8, 0, None) == E  # spans overlap
     assert L.channel_slice_copy(a, 64, g, 64, g + 128, 64, 10, 8, 0, None) == E
     assert L.channel_slice_copy(a, 1 << 20, None, 0, b, 64, 1 << 12, 8, 0, None) == U
+
+
+def test_strided_output_checks(L):
+    """Pixel strides: honoured for a pass's output only, at least the
+    channel count, a multiple of 8, a 16-byte aligned output; the K = 1 head
+    takes neither strides nor the accumulate epilogue. All refused before
+    any launch (nothing below is dereferenced)."""
+    ref = ctypes.byref
+    x, w, y = FAKE, FAKE + (1 << 20), FAKE + (1 << 26)
+    mk = lambda **k: fg.ConvDesc.make(2, 8, 8, 16, 16, 3, 3, 1, 1, **k)
+    fwd = lambda d, out=y, epi=0: L.conv2d_fwd(ref(d), x, w, out, epi, None, None, 0, None)
+    bwd = lambda d, out=y, epi=0: L.conv2d_bwd_data(ref(d), x, w, out, epi, None, None, 0,
+                                                   None)
+    assert fwd(mk(y_ld=8)) == fg.FG_EINVAL             # below the channel count
+    assert fwd(mk(y_ld=20)) == fg.FG_EUNSUPPORTED      # not a multiple of 8
+    assert fwd(mk(y_ld=24), out=y + 8) == fg.FG_EUNSUPPORTED   # output not 16-byte aligned
+    assert fwd(mk(x_ld=24)) == fg.FG_EUNSUPPORTED      # strided input
+    assert bwd(mk(y_ld=24)) == fg.FG_EUNSUPPORTED      # strided dy (an input)
+    assert bwd(mk(x_ld=8)) == fg.FG_EINVAL
+    assert fwd(mk(x_ld=-8)) == fg.FG_EINVAL
+    assert L.conv2d_bwd_weight(ref(mk(x_ld=24)), x, FAKE + (1 << 24), y, None, 0,
+                               None) == fg.FG_EUNSUPPORTED
+    # at stride 4096 the output's span (127 pixels * 4096 + 16 elements, ~1 MiB)
+    # from 64 KiB past x reaches the weights at 1 MiB; dense, it would not
+    assert bwd(mk(x_ld=4096), out=x + (1 << 16)) == fg.FG_EINVAL
+    head = lambda **k: fg.ConvDesc.make(2, 8, 8, 16, 1, 1, 1, 1, 0, **k)
+    assert fwd(head(y_ld=8)) == fg.FG_EUNSUPPORTED
+    assert fwd(head(), epi=fg.EPI_ACC) == fg.FG_EUNSUPPORTED
+    assert bwd(head(x_ld=24)) == fg.FG_EUNSUPPORTED
