@@ -84,8 +84,8 @@ WORKLOADS = {
     "densenet": "FC-DenseNet variant step, N=4 x 128x128 x 256ch input, growth 256, "
                 "2 levels of 2-layer dense blocks + bottleneck, average pooling, "
                 "16 conv layers (38,928,896 weights), Huber head (delta 10), "
-                "loss scale 2^15, dense concatenation by channel-slice copies, "
-                "kernel gradients on a second stream",
+                "loss scale 2^15, layers write into their concatenation slices and add their "
+                "input gradients in place, kernel gradients on a second stream",
 }
 
 COPY_KIB = 256 * 1024  # bytes read (and written) by `--op copy`, in KiB

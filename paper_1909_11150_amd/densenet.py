@@ -10,25 +10,41 @@ block, transposed-conv transitions up with skip concatenations, a 1x1 head)
 entirely through libfcngrad calls, prepared once as a call list like the
 chain's step program.
 
-Dense concatenation: the convolution kernels read dense NHWC inputs, so a
-block keeps one buffer per layer input, Z_l = concat(Z_{l-1}, Y_l), written
-by two channel-slice copies. Backward, each block keeps a gradient buffer G
-in the layout of its last concatenation: a layer's output gradient is its
-slice of G, gated by its ReLU output; the layer's input gradient is added
-into the slices it read. A skip connection's gradient (a slice of the up
-block's G) is added to the down block's G, which the transition-down conv
-writes first. fp16 storage throughout; every addition is one rounding.
+Dense concatenation. The convolutions read dense NHWC inputs and can write
+into a channel slice of a wider buffer (a pixel stride), and add into it:
+  * forward: a block keeps one buffer per layer input, Z_l = concat(Z_{l-1},
+    Y_l); layer l writes Y_l straight into its slice of Z_l and Z_{l-1} is
+    copied into Z_l's prefix; a transition up writes into the first channels
+    of its block's input, whose other channels are a copy of the skip; the
+    last layer of a bottleneck or up block writes into the block's
+    new-feature buffer;
+  * backward: a bottleneck or up block keeps a gradient buffer G in the
+    layout of its last concatenation. A layer's output gradient is its slice
+    of G (of the new-feature gradient, for the last layer), gated by its ReLU
+    output; its input gradient is added into the slices it read by the
+    convolution itself (the accumulate epilogue). A down block's G is the
+    skip's slice of its up block's G (a strided view), so the skip gradient
+    is in place when the transition conv adds its input gradient to it.
+fp16 storage throughout; every addition is one rounding.
 """
 import ctypes
+from collections import namedtuple
 
 import torch
 
-from . import (EPI_NONE, EPI_RELU, OP_BWD_DATA, OP_BWD_WEIGHT, OP_CONVT, OP_FWD,
-               FgError, kernel_name, lib, workspace_bytes)
-from .fcn import (Call, chain_workspace_bytes, convt_dw_desc, convt_dx_desc, fwd_desc,
-                  kernel_gradient_workspace_bytes)
+from . import (EPI_ACC, EPI_NONE, EPI_RELU, OP_BWD_DATA, OP_BWD_WEIGHT, OP_CONVT,
+               OP_FWD, ConvDesc, FgError, kernel_name, lib, workspace_bytes)
+from .fcn import (Call, chain_workspace_bytes, kernel_gradient_workspace_bytes)
 
 F16 = torch.float16
+
+# a channel slice of a buffer: base tensor, element offset of the first
+# channel, pixel stride, channels
+Slice = namedtuple("Slice", "t off ld ch")
+
+
+def _dense(t):
+    return Slice(t, 0, t.shape[-1], t.shape[-1])
 
 
 def _structure(layers):
@@ -40,6 +56,17 @@ def _structure(layers):
         if req not in names:
             raise ValueError(f"layer {req} missing from the dense network")
     return levels, per
+
+
+def _desc(L, op, x_ld=0, y_ld=0):
+    """Descriptor of one pass; for a transposed conv's input gradient and
+    kernel gradient, the conv of dy (the big image) with Wt read as KRSC."""
+    n, h, w, c = L.x_shape
+    if L.kind == "conv" or op == OP_CONVT:
+        return ConvDesc.make(n, h, w, c, L.y_shape[3], L.r, L.s, L.stride, L.pad,
+                             x_ld, y_ld)
+    n, ho, wo, co = L.y_shape
+    return ConvDesc.make(n, ho, wo, co, c, L.r, L.s, L.stride, L.pad, x_ld, y_ld)
 
 
 class DenseNet:
@@ -57,44 +84,52 @@ class DenseNet:
         self.w = {L.name: torch.as_tensor(w).to(self.dev).contiguous()
                   for L, w in zip(self.layers, weights)}
         self.dw = {L.name: e(L.w_shape) for L in self.layers}
-        self.act = {L.name: e(L.y_shape) for L in self.layers}   # post-ReLU outputs
         self.ws = torch.empty(max(chain_workspace_bytes(self.layers), 16),
                               dtype=torch.uint8, device=self.dev)
         # forward buffers: Z[(block, l)] = input of layer l + 1 of the block
-        # (l = 0: the block input), pooled outputs, new-feature buffers
-        self.Z, self.P, self.NF = {}, {}, {}
-        self.G, self.dNF = {}, {}
+        # (l = 0: an up block's input), pooled maps, new-feature buffers
+        self.Z, self.P, self.NF, self.G, self.dNF = {}, {}, {}, {}, {}
+        for blk in self._blocks():
+            self._block_bufs(blk)
         for d in range(1, self.levels + 1):
-            self._block_bufs(f"D{d}")
-            td = self.L[f"TD{d}"]
-            n, h, w, c = td.y_shape
+            n, h, w, c = self.L[f"TD{d}"].y_shape
             self.P[d] = e((n, h // 2, w // 2, c))
-        self._block_bufs("B")
+        # where each layer's (post-ReLU) output lives
+        self.out = {}
+        for name in ("C0", "F1x1") + tuple(f"TD{d}" for d in range(1, self.levels + 1)):
+            self.out[name] = _dense(e(self.L[name].y_shape))
+        for blk in self._blocks():
+            c0 = self.L[f"{blk}.1"].x_shape[3]
+            for l in range(1, self.per + 1):
+                if (blk, l) in self.Z:
+                    z = self.Z[(blk, l)]
+                    self.out[f"{blk}.{l}"] = Slice(z, c0 + (l - 1) * self.k, z.shape[3],
+                                                   self.k)
+                else:          # a bottleneck or up block's last layer
+                    nf = self.NF[blk]
+                    self.out[f"{blk}.{l}"] = Slice(nf, (l - 1) * self.k, nf.shape[3],
+                                                   self.k)
         for d in range(1, self.levels + 1):
-            self._block_bufs(f"U{d}")
-        # gradient buffers (the input-gradient scratch dZin is one per
-        # resolution: the main stream uses it in order)
+            z0 = self.Z[(f"U{d}", 0)]
+            self.out[f"TU{d}"] = Slice(z0, 0, z0.shape[3], self.per * self.k)
+        # post-ReLU outputs as (possibly strided) tensor views
+        self.act = {name: self._view(s) for name, s in self.out.items()}
+        # gradients: one output-gradient buffer per layer (its kernel
+        # gradient may still read it on the side stream)
         self.g_out = e(self.L["F1x1"].y_shape)
         self.dX = e(self.x.shape)
-        # a layer's output gradient has a buffer of its own: its kernel
-        # gradient may still read it on the side stream while the next
-        # layer's is written
-        self.dY, self.dZin, self.dT, self.dP, self.dU = {}, {}, {}, {}, {}
-        for blk in self._blocks():
-            n, h, w, _ = self.L[f"{blk}.1"].x_shape
-            cmax = max(self.L[f"{blk}.{l}"].x_shape[3] for l in range(1, self.per + 1))
-            for l in range(1, self.per + 1):
-                self.dY[f"{blk}.{l}"] = e((n, h, w, self.k))
-            old = self.dZin.get(h)
-            if old is None or old.shape[3] < cmax:
-                self.dZin[h] = e((n, h, w, cmax))
-        for d in range(1, self.levels + 1):
-            self.dT[d] = e(self.L[f"TD{d}"].y_shape)
-            n, h, w, c = self.L[f"TD{d}"].y_shape
-            self.dP[d] = e((n, h // 2, w // 2, c))
-            self.dU[d] = e(self.L[f"TU{d}"].y_shape)
+        self.dY = {f"{b}.{l}": e(self.L[f"{b}.{l}"].y_shape)
+                   for b in self._blocks() for l in range(1, self.per + 1)}
+        self.dT = {d: e(self.L[f"TD{d}"].y_shape) for d in range(1, self.levels + 1)}
+        self.dP = {d: e(self.P[d].shape) for d in range(1, self.levels + 1)}
+        self.dU = {d: e(self.L[f"TU{d}"].y_shape) for d in range(1, self.levels + 1)}
         self.dC0 = e(self.L["C0"].y_shape)
         self._L = lib()
+
+    @staticmethod
+    def _view(s):
+        n, h, w = s.t.shape[:3]
+        return s.t.view(n, h, w, s.ld)[..., s.off:s.off + s.ch]
 
     def _blocks(self):
         return [f"D{d}" for d in range(1, self.levels + 1)] + ["B"] + \
@@ -109,19 +144,16 @@ class DenseNet:
         last = self.per if blk.startswith("D") else self.per - 1
         for l in range(1, last + 1):
             self.Z[(blk, l)] = e((n, h, w, c0 + l * self.k))
-        self.G[blk] = e((n, h, w, c0 + self.per * self.k))
         if not blk.startswith("D"):
+            self.G[blk] = e((n, h, w, c0 + self.per * self.k))
             self.NF[blk] = e((n, h, w, self.per * self.k))
             self.dNF[blk] = e((n, h, w, self.per * self.k))
 
     # ---- prepared calls ----------------------------------------------------------
     def program(self, target, streams=2):
         """streams = 1: every call in order on one stream; 2: the kernel
-        gradients on a second stream; 3: also the forward pass's
-        concatenation copies that do not wait for the layer they follow on a
-        third. Measured on the full network: 6.73, 6.51 and 6.70 ms per step
-        (the copy stream slows the forward convolutions it runs beside by
-        more than it saves), so 2 is the default."""
+        gradients on a second stream; 3: also the forward pass's copies that
+        do not wait for the layer they follow on a third."""
         if streams < 1:
             raise ValueError("streams must be >= 1")
         return _DenseProgram(self, target, min(streams, 3))
@@ -144,13 +176,12 @@ class _DenseProgram:
     streams each kernel gradient runs on the second one as soon as its
     output gradient is written (an event after the writing call), beside the
     main stream's input gradients and copies, with a workspace of its own.
-    With three, the copy of a dense layer's input into the prefix of its
-    block's next concatenation, and of its output into the block's
-    new-feature buffer, run on the third beside the layer's convolution
-    (each after the calls that complete what it reads; the convolution that
-    reads a concatenation waits for both of its copies). The main stream
-    waits for the other streams' last calls at the end of the step, before
-    the next forward pass overwrites what they read. Every kernel reads only
+    With three, the forward pass's copies that need not wait for the layer
+    they follow (a concatenation's prefix, the skip into an up block's
+    input, an output into the new-feature buffer) run on the third, each
+    after the calls that complete what it reads. The main stream waits for
+    the other streams' last calls at the end of the step, before the next
+    forward pass overwrites what they read. Every kernel reads only
     finished inputs, so the results equal the one-stream order's."""
 
     def __init__(self, net, target, streams=1):
@@ -165,10 +196,9 @@ class _DenseProgram:
         self._dw_sid = 1 if streams > 1 else 0
         self._cp_sid = 2 if streams > 2 else 0
         self._sp = [ctypes.c_void_p(x.cuda_stream) for x in self.streams]
-        if streams > 1:
-            self._ws_side = torch.empty(
-                max(16, kernel_gradient_workspace_bytes(net.layers)), dtype=torch.uint8,
-                device=net.dev)
+        self._ws_side = torch.empty(
+            max(16, kernel_gradient_workspace_bytes(net.layers)), dtype=torch.uint8,
+            device=net.dev) if streams > 1 else net.ws
         self._build(target)
         if streams == 1:
             self.calls = [c._replace(sid=0, deps=()) for c in self.calls]
@@ -184,227 +214,229 @@ class _DenseProgram:
 
     # -- checks: every buffer a call touches holds what the call addresses --
     @staticmethod
-    def _span_ok(t, off, ld, npix, nch):
-        need = off + (npix - 1) * ld + nch
-        if t.dtype != F16 or not t.is_contiguous() or t.numel() < need:
-            raise ValueError(f"buffer of {t.numel()} fp16 elements, call reaches {need}")
+    def _span_ok(s, npix):
+        need = s.off + (npix - 1) * s.ld + s.ch
+        if s.t.dtype != F16 or not s.t.is_contiguous() or s.t.numel() < need or \
+                s.ch > s.ld:
+            raise ValueError(f"buffer of {s.t.numel()} fp16 elements, call reaches {need}")
 
     @staticmethod
     def _shape_ok(t, shape):
         if tuple(t.shape) != tuple(shape) or not t.is_contiguous():
             raise ValueError(f"tensor {tuple(t.shape)} where {tuple(shape)} is needed")
 
-    def _desc(self, d):
+    def _keep_desc(self, d):
         self._keep.append(d)
         return ctypes.byref(d)
 
     def _add(self, label, kernel, work, fn, args, single=True, sid=0, deps=()):
         """Append a call; the stream argument is added once all are built."""
         self.calls.append(Call(label, kernel, work, fn, args, single, sid, deps))
+        return len(self.calls) - 1
+
+    @staticmethod
+    def _ptr(s):
+        return s.t.data_ptr() + 2 * s.off
 
     # -- ops --
-    def conv_fwd(self, name, x, y, relu, deps=()):
+    def conv_fwd(self, name, x, out, relu, deps=()):
+        """Forward pass of a layer: dense input x, output into slice out."""
         L = self.net.L[name]
         n = self.net
         self._shape_ok(x, L.x_shape)
-        self._shape_ok(y, L.y_shape)
-        d = fwd_desc(L)
-        epi = EPI_RELU if relu else EPI_NONE
-        if L.kind == "conv":
-            self._add(f"{name}.fwd", kernel_name(d, OP_FWD), L.flops, self._L.conv2d_fwd,
-                      (self._desc(d), x.data_ptr(), n.w[name].data_ptr(), y.data_ptr(), epi,
-                       None, n.ws.data_ptr(), n.ws.numel()),
-                      workspace_bytes(d, OP_FWD) == 0, deps=deps)
-        else:
-            self._add(f"{name}.fwd", kernel_name(d, OP_CONVT), L.flops,
-                      self._L.conv_transpose2d_fwd,
-                      (self._desc(d), x.data_ptr(), n.w[name].data_ptr(), y.data_ptr(), epi,
-                       None, n.ws.data_ptr(), n.ws.numel()),
-                      workspace_bytes(d, OP_CONVT) == 0, deps=deps)
+        npix = L.y_shape[0] * L.y_shape[1] * L.y_shape[2]
+        assert out.ch == L.y_shape[3]
+        self._span_ok(out, npix)
+        op = OP_FWD if L.kind == "conv" else OP_CONVT
+        d = _desc(L, op, y_ld=out.ld)
+        fn = self._L.conv2d_fwd if L.kind == "conv" else self._L.conv_transpose2d_fwd
+        return self._add(f"{name}.fwd", kernel_name(d, op), L.flops, fn,
+                         (self._keep_desc(d), x.data_ptr(), n.w[name].data_ptr(),
+                          self._ptr(out), EPI_RELU if relu else EPI_NONE, None,
+                          n.ws.data_ptr(), n.ws.numel()), workspace_bytes(d, op) == 0,
+                         deps=deps)
 
-    def conv_bwd(self, name, x, dy, dx):
+    def conv_bwd(self, name, x, dy, dx, acc):
         """Kernel gradient into dw[name] (second stream, after the call that
-        wrote dy, which is the last one appended); input gradient into dx
-        (no gate)."""
+        wrote dy, which is the last one appended); input gradient into slice
+        dx, added to what it holds when acc (no gate)."""
         L = self.net.L[name]
         n = self.net
         self._shape_ok(x, L.x_shape)
         self._shape_ok(dy, L.y_shape)
-        self._shape_ok(dx, L.x_shape)
+        npix = L.x_shape[0] * L.x_shape[1] * L.x_shape[2]
+        assert dx.ch == L.x_shape[3]
+        self._span_ok(dx, npix)
         wsp, wsb = n.ws.data_ptr(), n.ws.numel()
-        side = len(self.streams) > 1
-        dws, dwb = (self._ws_side.data_ptr(), self._ws_side.numel()) if side else (wsp, wsb)
+        dws, dwb = self._ws_side.data_ptr(), self._ws_side.numel()
+        epi = EPI_ACC if acc else EPI_NONE
         dwk = dict(sid=self._dw_sid, deps=(len(self.calls) - 1,))
         if L.kind == "conv":
-            d = fwd_desc(L)
-            self._add(f"{name}.dW", kernel_name(d, OP_BWD_WEIGHT), L.flops,
+            d = _desc(L, OP_FWD, x_ld=dx.ld)
+            dw_d = _desc(L, OP_FWD)
+            self._add(f"{name}.dW", kernel_name(dw_d, OP_BWD_WEIGHT), L.flops,
                       self._L.conv2d_bwd_weight,
-                      (self._desc(d), x.data_ptr(), dy.data_ptr(), n.dw[name].data_ptr(),
-                       dws, dwb), workspace_bytes(d, OP_BWD_WEIGHT) == 0, **dwk)
+                      (self._keep_desc(dw_d), x.data_ptr(), dy.data_ptr(),
+                       n.dw[name].data_ptr(), dws, dwb),
+                      workspace_bytes(dw_d, OP_BWD_WEIGHT) == 0, **dwk)
             self._add(f"{name}.dx", kernel_name(d, OP_BWD_DATA), L.flops,
                       self._L.conv2d_bwd_data,
-                      (self._desc(d), dy.data_ptr(), n.w[name].data_ptr(), dx.data_ptr(),
-                       EPI_NONE, None, wsp, wsb), workspace_bytes(d, OP_BWD_DATA) == 0)
-        else:
-            d = convt_dw_desc(L)
-            self._add(f"{name}.dW", kernel_name(d, OP_BWD_WEIGHT), L.flops,
+                      (self._keep_desc(d), dy.data_ptr(), n.w[name].data_ptr(),
+                       self._ptr(dx), epi, None, wsp, wsb),
+                      workspace_bytes(d, OP_BWD_DATA) == 0)
+        else:   # transposed conv: both passes are convs of dy with Wt as KRSC
+            dw_d = _desc(L, OP_BWD_WEIGHT)
+            self._add(f"{name}.dW", kernel_name(dw_d, OP_BWD_WEIGHT), L.flops,
                       self._L.conv2d_bwd_weight,
-                      (self._desc(d), dy.data_ptr(), x.data_ptr(), n.dw[name].data_ptr(),
-                       dws, dwb), workspace_bytes(d, OP_BWD_WEIGHT) == 0, **dwk)
-            d = convt_dx_desc(L)
+                      (self._keep_desc(dw_d), dy.data_ptr(), x.data_ptr(),
+                       n.dw[name].data_ptr(), dws, dwb),
+                      workspace_bytes(dw_d, OP_BWD_WEIGHT) == 0, **dwk)
+            d = _desc(L, OP_BWD_DATA, y_ld=dx.ld)
             self._add(f"{name}.dx", kernel_name(d, OP_FWD), L.flops, self._L.conv2d_fwd,
-                      (self._desc(d), dy.data_ptr(), n.w[name].data_ptr(), dx.data_ptr(),
-                       EPI_NONE, None, wsp, wsb), workspace_bytes(d, OP_FWD) == 0)
+                      (self._keep_desc(d), dy.data_ptr(), n.w[name].data_ptr(),
+                       self._ptr(dx), epi, None, wsp, wsb),
+                      workspace_bytes(d, OP_FWD) == 0)
 
-    def copy(self, label, src, soff, sld, dst, doff, dld, nch, gate=None, gld=0,
-             acc=False, sid=0, deps=()):
-        """nch channels per pixel; the pixel count is dst's over its stride."""
-        npix = dst.numel() // dld
-        self._span_ok(src, soff, sld, npix, nch)
-        self._span_ok(dst, doff, dld, npix, nch)
-        if gate is not None:
-            self._span_ok(gate, 0, gld, npix, nch)
+    def copy(self, label, src, dst, gate=None, acc=False, sid=0, deps=()):
+        """Per pixel, dst.ch channels from slice src to slice dst (gated by
+        slice gate; added to dst when acc)."""
+        npix = dst.t.numel() // dst.ld
+        nch = dst.ch
+        for s in (src, dst) + ((gate,) if gate is not None else ()):
+            assert s.ch == nch
+            self._span_ok(s, npix)
         rd = 2 * nch * npix * (2 if acc else 1) + (2 * nch * npix if gate is not None else 0)
-        self._add(label, f"channel_slice_copy_kernel<{'true' if acc else 'false'}>",
-                  rd + 2 * nch * npix, self._L.channel_slice_copy,
-                  (src.data_ptr() + 2 * soff, sld,
-                   None if gate is None else gate.data_ptr(), gld,
-                   dst.data_ptr() + 2 * doff, dld, npix, nch, int(acc)),
-                  sid=sid, deps=deps)
-        return len(self.calls) - 1
+        return self._add(label, f"channel_slice_copy_kernel<{'true' if acc else 'false'}>",
+                         rd + 2 * nch * npix, self._L.channel_slice_copy,
+                         (self._ptr(src), src.ld,
+                          None if gate is None else self._ptr(gate),
+                          0 if gate is None else gate.ld,
+                          self._ptr(dst), dst.ld, npix, nch, int(acc)),
+                         sid=sid, deps=deps)
 
     # -- the step --
     def _block_fwd(self, blk, z0, ready):
-        """Dense layers of a block whose input z0 is complete once the calls
-        in `ready` are. Returns the last concatenation (down blocks) and the
-        calls that complete it; for other blocks, the calls that complete
-        the new-feature buffer."""
+        """Dense layers of a block whose input z0 (dense) is complete once
+        the calls in `ready` are. Returns the calls that complete the last
+        concatenation (down blocks) or the new-feature buffer (others)."""
         n = self.net
         z = z0
         nf_ready = []
         for l in range(1, n.per + 1):
             name = f"{blk}.{l}"
-            self.conv_fwd(name, z, n.act[name], True, deps=ready)
-            conv = len(self.calls) - 1
+            conv = self.conv_fwd(name, z, n.out[name], True, deps=ready)
             if not blk.startswith("D"):     # new features: the block's outputs
-                nf_ready.append(self.copy(f"{name}.new", n.act[name], 0, n.k, n.NF[blk],
-                                          (l - 1) * n.k, n.per * n.k, n.k,
-                                          sid=self._cp_sid, deps=(conv,)))
+                if (blk, l) in n.Z:
+                    nf = n.NF[blk]
+                    nf_ready.append(self.copy(
+                        f"{name}.new", n.out[name],
+                        Slice(nf, (l - 1) * n.k, nf.shape[3], n.k),
+                        sid=self._cp_sid, deps=(conv,)))
+                else:
+                    nf_ready.append(conv)
             if (blk, l) not in n.Z:
                 continue
-            out = n.Z[(blk, l)]
-            cz, co = z.shape[3], out.shape[3]
-            cat0 = self.copy(f"{name}.cat0", z, 0, cz, out, 0, co, cz,
+            zl = n.Z[(blk, l)]
+            cat0 = self.copy(f"{name}.cat0", _dense(z), Slice(zl, 0, zl.shape[3], z.shape[3]),
                              sid=self._cp_sid, deps=ready)
-            cat1 = self.copy(f"{name}.cat1", n.act[name], 0, n.k, out, cz, co, n.k)
-            z, ready = out, (cat0, cat1)
-        return (z, ready) if blk.startswith("D") else tuple(nf_ready)
+            z, ready = zl, (cat0, conv)
+        return ready if blk.startswith("D") else tuple(nf_ready)
 
-    def _block_bwd(self, blk, fresh):
-        """G[blk] holds the gradient of the block's last concatenation (for a
-        fresh block only its new-feature channels); leaves the gradient of
-        the block input in G[blk][..., :c0]."""
+    def _block_bwd(self, blk, G, c0, block_input, fresh, dnf=None):
+        """G: slice over the layout of the block's last concatenation (ld =
+        its pixel stride). For a fresh block (bottleneck, up) nothing is in G
+        yet and dnf holds the new-feature gradient; otherwise G holds the
+        whole gradient. Leaves the block input's gradient in G's first c0
+        channels."""
         n = self.net
-        G = n.G[blk]
-        cl = G.shape[3]
-        c0 = n.L[f"{blk}.1"].x_shape[3]
+        nk = n.per * n.k
         for l in range(n.per, 0, -1):
             name = f"{blk}.{l}"
             lo = c0 + (l - 1) * n.k
-            h = n.L[name].x_shape[1]
+            zin = n.Z[(blk, l - 1)] if (blk, l - 1) in n.Z else block_input
             dY = n.dY[name]
-            zin = n.Z[(blk, l - 1)] if l > 1 or blk.startswith("U") else self._block_input[blk]
-            self.copy(f"{name}.dy", G, lo, cl, dY, 0, n.k, n.k, gate=n.act[name], gld=n.k)
-            dZ = n.dZin[h]
-            dZv = dZ.view(-1)[:zin.numel()].view(zin.shape)
-            self.conv_bwd(name, zin, dY, dZv)
-            if fresh and l == n.per:  # the block input's slice of G is still empty
-                self.copy(f"{name}.dz0", dZv, 0, lo, G, 0, cl, c0)
-                if lo > c0:
-                    self.copy(f"{name}.dzacc", dZv, c0, lo, G, c0, cl, lo - c0, acc=True)
-            else:
-                self.copy(f"{name}.dzacc", dZv, 0, lo, G, 0, cl, lo, acc=True)
+            src = Slice(dnf, (l - 1) * n.k, nk, n.k) if fresh and l == n.per else \
+                Slice(G.t, G.off + lo, G.ld, n.k)
+            self.copy(f"{name}.dy", src, _dense(dY), gate=n.out[name])
+            first = fresh and l == n.per          # nothing in G to add to yet
+            self.conv_bwd(name, zin, dY, Slice(G.t, G.off, G.ld, lo), acc=not first)
+            if first and n.per > 1:   # the earlier layers' new-feature gradients
+                self.copy(f"{blk}.dnew", Slice(dnf, 0, nk, lo - c0),
+                          Slice(G.t, G.off + c0, G.ld, lo - c0), acc=True)
 
     def _build(self, target):
         n = self.net
         Lb = self._L
-        self._block_input = {}
-        # forward
-        self.conv_fwd("C0", n.x, n.act["C0"], True)
+        nk = n.per * n.k
+        # ---- forward
+        self.conv_fwd("C0", n.x, n.out["C0"], True)
         bin_, ready = n.act["C0"], (len(self.calls) - 1,)
         skips, skip_ready = {}, {}
         for d in range(1, n.levels + 1):
-            self._block_input[f"D{d}"] = bin_
-            z, zr = self._block_fwd(f"D{d}", bin_, ready)
-            skips[d], skip_ready[d] = z, zr
-            self.conv_fwd(f"TD{d}", z, n.act[f"TD{d}"], True, deps=zr)
+            zr = self._block_fwd(f"D{d}", bin_, ready)
+            skips[d], skip_ready[d] = n.Z[(f"D{d}", n.per)], zr
+            self.conv_fwd(f"TD{d}", skips[d], n.out[f"TD{d}"], True, deps=zr)
             td = n.act[f"TD{d}"]
             self._add(f"TD{d}.pool", "avg_pool2d_fwd_kernel", 2 * td.numel() * 5 // 4,
                       Lb.avg_pool2d_fwd,
                       (td.data_ptr(), *td.shape, n.P[d].data_ptr()))
             bin_, ready = n.P[d], (len(self.calls) - 1,)
-        self._block_input["B"] = bin_
         nf_ready = self._block_fwd("B", bin_, ready)
         nf = n.NF["B"]
-        self._tu_in = {}
+        tu_in = {}
         for d in range(n.levels, 0, -1):
             tu = f"TU{d}"
-            self._tu_in[d] = nf
-            self.conv_fwd(tu, nf, n.act[tu], True, deps=nf_ready)
+            tu_in[d] = nf
             z0 = n.Z[(f"U{d}", 0)]
-            nk, c0 = n.act[tu].shape[3], z0.shape[3]
-            cat1 = self.copy(f"{tu}.cat1", skips[d], 0, skips[d].shape[3], z0, nk, c0,
-                             c0 - nk, sid=self._cp_sid, deps=skip_ready[d])
-            cat0 = self.copy(f"{tu}.cat0", n.act[tu], 0, nk, z0, 0, c0, nk)
-            nf_ready = self._block_fwd(f"U{d}", z0, (cat0, cat1))
+            c0 = z0.shape[3]
+            tconv = self.conv_fwd(tu, nf, n.out[tu], True, deps=nf_ready)
+            skip = self.copy(f"{tu}.skip", _dense(skips[d]),
+                             Slice(z0, nk, c0, c0 - nk), sid=self._cp_sid,
+                             deps=skip_ready[d])
+            nf_ready = self._block_fwd(f"U{d}", z0, (tconv, skip))
             nf = n.NF[f"U{d}"]
         y = n.act["F1x1"]
-        self.conv_fwd("F1x1", nf, y, False, deps=nf_ready)
-        # head: loss-scaled mean Huber loss
+        self.conv_fwd("F1x1", nf, n.out["F1x1"], False, deps=nf_ready)
+        # ---- head: loss-scaled mean Huber loss
         self._head_args = [y.data_ptr(), target.data_ptr(), y.numel(),
                            ctypes.c_double(n.loss_scale / y.numel()),
                            ctypes.c_double(n.delta), n.g_out.data_ptr()]
         self._add("head_grad", "huber_head_grad_kernel", 10 * y.numel(),
                   Lb.huber_head_grad, tuple(self._head_args))
-        # backward: head, up blocks (level 1 first), bottleneck, down path
-        self.conv_bwd("F1x1", nf, n.g_out, n.dNF["U1"])
-        up_skip = {}
+        # ---- backward: head, up blocks (level 1 first), bottleneck, down path
+        self.conv_bwd("F1x1", nf, n.g_out, _dense(n.dNF["U1"]), acc=False)
         for d in range(1, n.levels + 1):
-            blk = f"U{d}"
-            G = n.G[blk]
-            cl, c0 = G.shape[3], n.L[f"{blk}.1"].x_shape[3]
-            self.copy(f"{blk}.dnew", n.dNF[blk], 0, n.per * n.k, G, c0, cl, n.per * n.k)
-            self._block_bwd(blk, fresh=True)
-            tu = f"TU{d}"
-            nk = n.per * n.k
-            self.copy(f"{tu}.dy", G, 0, cl, n.dU[d], 0, nk, nk, gate=n.act[tu], gld=nk)
+            blk, tu = f"U{d}", f"TU{d}"
+            G = _dense(n.G[blk])
+            self._block_bwd(blk, G, n.Z[(blk, 0)].shape[3], n.Z[(blk, 0)], True,
+                            n.dNF[blk])
+            self.copy(f"{tu}.dy", Slice(G.t, 0, G.ld, nk), _dense(n.dU[d]),
+                      gate=n.out[tu])
             below = "B" if d == n.levels else f"U{d + 1}"
-            self.conv_bwd(tu, self._tu_in[d], n.dU[d], n.dNF[below])
-            up_skip[d] = (G, nk, cl)
-        G = n.G["B"]
-        cl, c0 = G.shape[3], n.L["B.1"].x_shape[3]
-        self.copy("B.dnew", n.dNF["B"], 0, n.per * n.k, G, c0, cl, n.per * n.k)
-        self._block_bwd("B", fresh=True)
-        dP_src, dP_off, dP_ld = G, 0, cl
+            self.conv_bwd(tu, tu_in[d], n.dU[d], _dense(n.dNF[below]), acc=False)
+        G = _dense(n.G["B"])
+        c0 = n.P[n.levels].shape[3]
+        self._block_bwd("B", G, c0, n.P[n.levels], True, n.dNF["B"])
+        dP_src = Slice(G.t, 0, G.ld, c0)
         for d in range(n.levels, 0, -1):
             # gradient of the pooled output -> dense, then through the pool
-            # (gated by the transition's ReLU output) and the 1x1 conv
-            c = n.P[d].shape[3]
-            self.copy(f"P{d}.dy", dP_src, dP_off, dP_ld, n.dP[d], 0, c, c)
+            # (gated by the transition's ReLU output) and the 1x1 conv, whose
+            # input gradient is added to the skip's gradient already in place
+            self.copy(f"P{d}.dy", dP_src, _dense(n.dP[d]))
             td = n.act[f"TD{d}"]
             self._add(f"TD{d}.dpool", "avg_pool2d_bwd_kernel", 2 * td.numel() * 9 // 4,
                       Lb.avg_pool2d_bwd,
                       (n.dP[d].data_ptr(), td.data_ptr(), *td.shape, n.dT[d].data_ptr()))
-            blk = f"D{d}"
-            G = n.G[blk]
-            self.conv_bwd(f"TD{d}", skips[d], n.dT[d], G)
-            Gu, off, ldu = up_skip[d]
-            self.copy(f"{blk}.dskip", Gu, off, ldu, G, 0, G.shape[3], G.shape[3], acc=True)
-            self._block_bwd(blk, fresh=False)
-            dP_src, dP_off, dP_ld = G, 0, G.shape[3]
-        c0 = n.act["C0"].shape[3]
-        self.copy("C0.dy", dP_src, 0, dP_ld, n.dC0, 0, c0, c0, gate=n.act["C0"], gld=c0)
-        self.conv_bwd("C0", n.x, n.dC0, n.dX)
+            Gu = n.G[f"U{d}"]
+            G = Slice(Gu, nk, Gu.shape[3], skips[d].shape[3])
+            self.conv_bwd(f"TD{d}", skips[d], n.dT[d], G, acc=True)
+            c0 = n.L[f"D{d}.1"].x_shape[3]
+            block_input = n.act["C0"] if d == 1 else n.P[d - 1]
+            self._block_bwd(f"D{d}", G, c0, block_input, False)
+            dP_src = Slice(G.t, G.off, G.ld, c0)
+        c0 = n.L["C0"].y_shape[3]
+        self.copy("C0.dy", dP_src, _dense(n.dC0), gate=n.out["C0"])
+        self.conv_bwd("C0", n.x, n.dC0, _dense(n.dX), acc=False)
 
     def set_loss_scale(self, s):
         self.net.loss_scale = float(s)
@@ -432,5 +464,5 @@ class _DenseProgram:
             streams[0].wait_event(evs[j])
 
     def join(self):
-        """The main stream already waits for the other stream's last call
+        """The main stream already waits for the other streams' last calls
         at the end of each run."""
