@@ -96,14 +96,20 @@ typedef struct {
     int32_t stride_h, stride_w, pad_h, pad_w;
     /* Pixel strides, in elements, of the x-shaped tensors (x, dx) and the
      * y-shaped ones (y, dy); 0 means dense (c, resp. k). A stride other
-     * than dense is honoured where that tensor is the pass's output (y of
-     * conv2d_fwd and conv_transpose2d_fwd, dx of conv2d_bwd_data), so that
-     * a pass can write into a channel slice of a wider buffer (the pointer
-     * then addresses the slice's first channel): it must be >= the channel
-     * count and a multiple of 8, the output pointer 16-byte aligned, and
-     * pixels * stride below 2^31 (else FG_EUNSUPPORTED; below the channel
-     * count, FG_EINVAL). A gate is laid out like the output. Inputs, and
-     * the K = 1 head's tensors, are dense (FG_EUNSUPPORTED otherwise). */
+     * than dense is honoured for
+     *   - the pass's output (y of conv2d_fwd and conv_transpose2d_fwd, dx
+     *     of conv2d_bwd_data), so that a pass can write into a channel
+     *     slice of a wider buffer;
+     *   - x where conv2d_fwd and conv2d_bwd_weight read it, so that a pass
+     *     can read a channel slice (a dense block's layer reads the
+     *     channels before those it writes, in the same buffer).
+     * The pointer then addresses the slice's first channel. The stride
+     * must be >= the channel count and a multiple of 8, the pointer 16-byte
+     * aligned, and pixels * stride below 2^31 (else FG_EUNSUPPORTED; below
+     * the channel count, FG_EINVAL). A gate is laid out like the output.
+     * An input and an output at one stride whose channel ranges are
+     * disjoint within each pixel do not overlap. Other tensors, and the
+     * K = 1 head's, are dense (FG_EUNSUPPORTED otherwise). */
     int32_t x_ld, y_ld;
 } fg_conv_desc;
 

@@ -93,6 +93,28 @@ size_t span_bytes(int64_t npix, int64_t ld, int64_t ch) {
   return (size_t)((npix - 1) * ld + ch) * 2;
 }
 
+// Two channel slices at one pixel stride ld: ch1 channels from a, ch2 from
+// b. Their elements are disjoint, whatever their pixel ranges, when b's
+// first channel lies at least ch1 channels past a's and its last one before
+// a's next pixel (b - a taken modulo the pixel stride).
+bool slices_disjoint(const void *a, int64_t ch1, const void *b, int64_t ch2,
+                     int64_t ld) {
+  const int64_t db = (int64_t)((uintptr_t)b - (uintptr_t)a);
+  if (db % 2 != 0) return false;
+  const int64_t r = ((db / 2) % ld + ld) % ld;
+  return ch1 <= r && r + ch2 <= ld;
+}
+
+// Overlap of an input slice (x, npx pixels at stride ldx, cx channels) with
+// an output slice (y, npy at ldy, cy): interleaved slices of one buffer
+// (a dense block's layer reading the channels before the ones it writes)
+// do not overlap.
+bool slices_overlap(const void *x, int64_t npx, int64_t ldx, int64_t cx,
+                    const void *y, int64_t npy, int64_t ldy, int64_t cy) {
+  if (ldx == ldy && slices_disjoint(x, cx, y, cy, ldx)) return false;
+  return overlap(x, span_bytes(npx, ldx, cx), y, span_bytes(npy, ldy, cy));
+}
+
 bool epi_ok(int epi) {
   return epi == FG_EPI_NONE || epi == FG_EPI_RELU || epi == FG_EPI_GATE ||
          epi == FG_EPI_ACC;
@@ -149,6 +171,7 @@ DataConvArgs fwd_args(const fg_conv_desc *d, int32_t P, int32_t Q) {
   DataConvArgs a;
   memset(&a, 0, sizeof(a));
   a.n = d->n; a.hi = d->h; a.wi = d->w; a.cr = d->c;
+  a.ldi = (int32_t)ld_or(d->x_ld, d->c);
   a.ho = P; a.wo = Q; a.co = d->k;
   a.ldo = (int32_t)ld_or(d->y_ld, d->k);
   a.istr = d->stride_h;
@@ -171,6 +194,7 @@ DataConvArgs bwd_data_args(const fg_conv_desc *d, int32_t P, int32_t Q) {
   DataConvArgs a;
   memset(&a, 0, sizeof(a));
   a.n = d->n; a.hi = P; a.wi = Q; a.cr = d->k;
+  a.ldi = d->k;
   a.ho = d->h; a.wo = d->w; a.co = d->c;
   a.ldo = (int32_t)ld_or(d->x_ld, d->c);
   a.istr = 1;
@@ -190,6 +214,7 @@ DataConvArgs convt_args(const fg_conv_desc *d, int32_t HO, int32_t WO) {
   DataConvArgs a;
   memset(&a, 0, sizeof(a));
   a.n = d->n; a.hi = d->h; a.wi = d->w; a.cr = d->c;
+  a.ldi = d->c;
   a.ho = HO; a.wo = WO; a.co = d->k;
   a.ldo = (int32_t)ld_or(d->y_ld, d->k);
   a.istr = 1;
@@ -334,22 +359,28 @@ fg_status conv2d_fwd(const fg_conv_desc *d, const uint16_t *x,
   const int64_t nw = elems4(d->k, d->r, d->s, d->c);
   const int64_t ny = elems4(d->n, P, Q, d->k);
   if (!sizes_ok(nx, nw, ny)) return FG_EUNSUPPORTED;
-  if (!dense_ld(d->x_ld, d->c)) return FG_EUNSUPPORTED;
+  const int64_t npx = (int64_t)d->n * d->h * d->w;
   const int64_t npy = (int64_t)d->n * P * Q;
+  // the input may be a channel prefix of a wider buffer, like the output
+  if ((st = out_ld_ok(d->x_ld, d->c, npx, x)) != FG_OK) return st;
   if ((st = out_ld_ok(d->y_ld, d->k, npy, y)) != FG_OK) return st;
-  const size_t sy = span_bytes(npy, ld_or(d->y_ld, d->k), d->k);
-  if (overlap(y, sy, x, nx * 2) || overlap(y, sy, w_krsc, nw * 2))
+  const int64_t ldx = ld_or(d->x_ld, d->c), ldy = ld_or(d->y_ld, d->k);
+  const size_t sx = span_bytes(npx, ldx, d->c);
+  const size_t sy = span_bytes(npy, ldy, d->k);
+  if (slices_overlap(x, npx, ldx, d->c, y, npy, ldy, d->k) ||
+      overlap(y, sy, w_krsc, nw * 2))
     return FG_EINVAL;
   if ((st = check_conv_support(d)) != FG_OK) return st;
   // one input step per output position for both image axes
   if (d->stride_h != d->stride_w) return FG_EUNSUPPORTED;
 
   if (d->k == 1) {
-    if (!dense_ld(d->y_ld, d->k) || epi == FG_EPI_ACC) return FG_EUNSUPPORTED;
+    if (!dense_ld(d->x_ld, d->c) || !dense_ld(d->y_ld, d->k) || epi == FG_EPI_ACC)
+      return FG_EUNSUPPORTED;
     return launch_status(launch_head_fwd(x, w_krsc, y, (int64_t)d->n * P * Q,
                                          d->c, epi, gate, stream));
   }
-  if ((st = check_ws(d, FG_OP_FWD, ws, ws_bytes, x, nx * 2, w_krsc, nw * 2, y,
+  if ((st = check_ws(d, FG_OP_FWD, ws, ws_bytes, x, sx, w_krsc, nw * 2, y,
                      sy, gate, sy)) != FG_OK)
     return st;
   DataConvArgs a = fwd_args(d, P, Q);
@@ -446,24 +477,29 @@ static fg_status bwd_weight(const fg_conv_desc *d, const uint16_t *x,
   fg_status st = check_desc(d);
   if (st != FG_OK) return st;
   if (!x || !dy || !dw_krsc) return FG_EINVAL;
-  if (!dense_ld(d->x_ld, d->c) || !dense_ld(d->y_ld, d->k)) return FG_EUNSUPPORTED;
+  if (!dense_ld(d->y_ld, d->k)) return FG_EUNSUPPORTED;
   int32_t P, Q;
   if (fg_conv_out_dims(d, 0, &P, &Q) != FG_OK) return FG_EINVAL;
   const int64_t nx = elems4(d->n, d->h, d->w, d->c);
+  // x may be a channel prefix of a wider buffer; sx is its span
+  const int64_t npx = (int64_t)d->n * d->h * d->w;
+  if (out_ld_ok(d->x_ld, d->c, npx, x) != FG_OK) return out_ld_ok(d->x_ld, d->c, npx, x);
+  if (d->k == 1 && !dense_ld(d->x_ld, d->c)) return FG_EUNSUPPORTED;
+  const size_t sx = span_bytes(npx, ld_or(d->x_ld, d->c), d->c);
   const int64_t nw = elems4(d->k, d->r, d->s, d->c);
   const int64_t ny = elems4(d->n, P, Q, d->k);
   if (!sizes_ok(nx, nw, ny)) return FG_EUNSUPPORTED;
-  if (overlap(dw_krsc, nw * 2, x, nx * 2) ||
+  if (overlap(dw_krsc, nw * 2, x, sx) ||
       overlap(dw_krsc, nw * 2, dy, ny * 2))
     return FG_EINVAL;
   if (found_nonfinite &&
       (overlap(found_nonfinite, 4, dw_krsc, nw * 2) ||
-       overlap(found_nonfinite, 4, x, nx * 2) ||
+       overlap(found_nonfinite, 4, x, sx) ||
        overlap(found_nonfinite, 4, dy, ny * 2) ||
        overlap(found_nonfinite, 4, ws, ws_bytes)))
     return FG_EINVAL;
   if ((st = check_conv_support(d)) != FG_OK) return st;
-  if ((st = check_ws(d, FG_OP_BWD_WEIGHT, ws, ws_bytes, x, nx * 2, dy, ny * 2,
+  if ((st = check_ws(d, FG_OP_BWD_WEIGHT, ws, ws_bytes, x, sx, dy, ny * 2,
                      dw_krsc, nw * 2, nullptr, 0)) != FG_OK)
     return st;
 
@@ -479,6 +515,7 @@ static fg_status bwd_weight(const fg_conv_desc *d, const uint16_t *x,
   a.dw = dw_krsc;
   a.part = (float *)ws;
   a.n = d->n; a.h = d->h; a.w = d->w; a.c = d->c; a.k = d->k;
+  a.ldx = (int32_t)ld_or(d->x_ld, d->c);
   a.r = d->r; a.s = d->s; a.p = P; a.q = Q;
   a.sh = d->stride_h; a.sw = d->stride_w; a.ph = d->pad_h; a.pw = d->pad_w;
   a.mtot = d->n * P * Q;

@@ -666,7 +666,7 @@ __global__ __launch_bounds__(C::NT, C::WPE) void data_conv_dma_kernel(DataConvAr
   const int wm0 = (wave / C::WGN) * C::WM, wn0 = (wave % C::WGN) * C::WN;
 
   const __amdgpu_buffer_rsrc_t rs_act = __builtin_amdgcn_make_buffer_rsrc(
-      (void *)a.act, 0, (int)((size_t)a.n * a.hi * a.wi * a.cr * 2), kRsrcFlags);
+      (void *)a.act, 0, (int)act_span_bytes(a), kRsrcFlags);
   const __amdgpu_buffer_rsrc_t rs_w = __builtin_amdgcn_make_buffer_rsrc(
       (void *)a.wgt, 0, a.wbytes, kRsrcFlags);
 
@@ -682,7 +682,7 @@ __global__ __launch_bounds__(C::NT, C::WPE) void data_conv_dma_kernel(DataConvAr
       int aa = t % P.mh, nn = t / P.mh;
       bh[jj] = aa * a.istr;
       bw[jj] = b * a.istr;
-      bbase[jj] = ((nn * a.hi + bh[jj]) * a.wi + bw[jj]) * a.cr + bs.coff[jj];
+      bbase[jj] = ((nn * a.hi + bh[jj]) * a.wi + bw[jj]) * a.ldi + bs.coff[jj];
     } else {
       bh[jj] = -(1 << 29);  // never inside the image
       bw[jj] = 0;
@@ -721,7 +721,7 @@ __global__ __launch_bounds__(C::NT, C::WPE) void data_conv_dma_kernel(DataConvAr
   auto issue = [&](int, int slot) __attribute__((always_inline)) {
     const int dh = P.dh0 + P.dstep * ti, dw = P.dw0 + P.dstep * tj;
     const int woff = (P.r0 + P.rstep * ti) * a.s + (P.s0 + P.rstep * tj);
-    const int delta = (dh * a.wi + dw) * a.cr + cr0;
+    const int delta = (dh * a.wi + dw) * a.ldi + cr0;
     const int wst = WK ? woff * a.cr + cr0 : cr0 * a.w_red + woff * a.w_tap;
     uint8_t *ta = R.a[slot], *tb = R.b[slot];
 #pragma unroll
@@ -848,7 +848,7 @@ __global__ __launch_bounds__(C::NT) void data_conv_halo_kernel(DataConvArgs a,
   const int wm0 = (wave / C::WGN) * C::WM, wn0 = (wave % C::WGN) * C::WN;
 
   const __amdgpu_buffer_rsrc_t rs_act = __builtin_amdgcn_make_buffer_rsrc(
-      (void *)a.act, 0, (int)((size_t)a.n * a.hi * a.wi * a.cr * 2), kRsrcFlags);
+      (void *)a.act, 0, (int)act_span_bytes(a), kRsrcFlags);
   const __amdgpu_buffer_rsrc_t rs_w = __builtin_amdgcn_make_buffer_rsrc(
       (void *)a.wgt, 0, a.wbytes, kRsrcFlags);
 
@@ -869,7 +869,7 @@ __global__ __launch_bounds__(C::NT) void data_conv_halo_kernel(DataConvArgs a,
     const int h = h0 + r / pwid, w = w0 + r % pwid;
     const bool v = r < prows && (unsigned)h < (unsigned)a.hi &&
                    (unsigned)w < (unsigned)a.wi;
-    pbase[jj] = v ? (((img * a.hi + h) * a.wi + w) * a.cr +
+    pbase[jj] = v ? (((img * a.hi + h) * a.wi + w) * a.ldi +
                      8 * ((lane & 3) ^ kmaj_swz<32>(r))) * 2
                   : -1;
   }
@@ -1114,7 +1114,7 @@ __global__ __launch_bounds__(C::NT) void wgrad_dma_kernel(WgradArgs a, WgradDiv 
   const int tr = tap / a.s, ts = tap - tr * a.s;
 
   const __amdgpu_buffer_rsrc_t rs_x = __builtin_amdgcn_make_buffer_rsrc(
-      (void *)a.x, 0, (int)((size_t)a.n * a.h * a.w * a.c * 2), kRsrcFlags);
+      (void *)a.x, 0, (int)x_span_bytes(a), kRsrcFlags);
   const __amdgpu_buffer_rsrc_t rs_dy = __builtin_amdgcn_make_buffer_rsrc(
       (void *)a.dy, 0, (int)((size_t)a.mtot * a.k * 2), kRsrcFlags);
 
@@ -1127,7 +1127,7 @@ __global__ __launch_bounds__(C::NT) void wgrad_dma_kernel(WgradArgs a, WgradDiv 
   // stage cost more VALU time than the stage's MFMAs leave free.
   const MnSlot<C> sl = mn_slots<C>(wave, lane);
   const int h0 = tr - a.ph, w0 = ts - a.pw;
-  const int pixb = a.c * 2, rowb = a.w * pixb, imgb = a.h * rowb;
+  const int pixb = a.ldx * 2, rowb = a.w * pixb, imgb = a.h * rowb;
   int hh[PW], ww[PW], ox[PW], od[PW];
 #pragma unroll
   for (int jj = 0; jj < PW; ++jj) {
@@ -1214,13 +1214,13 @@ __global__ __launch_bounds__(C::NT) void wgrad_dma_kernel(WgradArgs a, WgradDiv 
 // ---------------------------------------------------------------------------
 bool data_dma_ok(const DataConvArgs &a) {
   return a.cr % dma::DataRun::BK == 0 &&
-         (size_t)a.n * a.hi * a.wi * a.cr * 2 < 0x7FFFFFFFull &&
+         act_span_bytes(a) < 0x7FFFFFFFull &&
          (size_t)a.wbytes < 0x7FFFFFFFull;
 }
 
 bool wgrad_dma_ok(const WgradArgs &a) {
   return a.c % dma::TM == 0 && a.k % dma::TN == 0 &&
-         (size_t)a.n * a.h * a.w * a.c * 2 < 0x7FFFFFFFull &&
+         x_span_bytes(a) < 0x7FFFFFFFull &&
          (size_t)a.mtot * a.k * 2 < 0x7FFFFFFFull;
 }
 
@@ -1232,7 +1232,7 @@ bool data_halo_ok(const DataConvArgs &a) {
     return false;
   const int rt = dma::TN / P.mw;  // output rows per tile
   if (P.mh % rt != 0 || (rt + 2) * (P.mw + 2) > dma::kPatchRows) return false;
-  return (size_t)a.n * a.hi * a.wi * a.cr * 2 < 0x7FFFFFFFull &&
+  return act_span_bytes(a) < 0x7FFFFFFFull &&
          (size_t)a.wbytes < 0x7FFFFFFFull;
 }
 

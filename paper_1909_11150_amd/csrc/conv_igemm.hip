@@ -178,7 +178,7 @@ __global__ __launch_bounds__(C::NT) void data_conv_kernel(DataConvArgs a) {
       int aa = t % P.mh, nn = t / P.mh;
       bh[i] = aa * a.istr;
       bw[i] = b * a.istr;
-      bbase[i] = ((nn * a.hi + bh[i]) * a.wi + bw[i]) * a.cr;
+      bbase[i] = ((nn * a.hi + bh[i]) * a.wi + bw[i]) * a.ldi;
     } else {
       bh[i] = -(1 << 29);  // fails every bounds check
       bw[i] = 0;
@@ -219,7 +219,7 @@ __global__ __launch_bounds__(C::NT) void data_conv_kernel(DataConvArgs a) {
         cr = kv ? kk - t * a.cr : 0;
         tap_geom(t, dh, dw, woff);
       }
-      const int delta = (dh * a.wi + dw) * a.cr + cr;
+      const int delta = (dh * a.wi + dw) * a.ldi + cr;
 #pragma unroll
       for (int i = 0; i < BCOL; ++i) {
         int hh = bh[i] + dh, ww = bw[i] + dw;
@@ -417,7 +417,7 @@ __global__ __launch_bounds__(C::NT) void wgrad_kernel(WgradArgs a) {
         bool v = arv[u] && (m + e) < mend && hh >= 0 && hh < a.h && ww >= 0 &&
                  ww < a.w;
         ra[4 * u + e] =
-            v ? ldg16(a.x + ((size_t)((nn * a.h + hh) * a.w + ww)) * a.c + ac[u])
+            v ? ldg16(a.x + ((size_t)((nn * a.h + hh) * a.w + ww)) * a.ldx + ac[u])
               : u32x4{0, 0, 0, 0};
         // next reduction row: advance (n, p, q)
         if (++q == a.q) {
@@ -885,6 +885,7 @@ const char *wgrad_kernel_name(const fg_conv_desc &d) {
   const WgradPlan pl = plan_wgrad(d, p, q);
   WgradArgs wa;
   wa.n = d.n; wa.h = d.h; wa.w = d.w; wa.c = d.c; wa.k = d.k;
+  wa.ldx = d.x_ld ? d.x_ld : d.c;
   wa.mtot = d.n * p * q;
   if (pl.big && wgrad_dma_ok(wa))
     return pl.nsplit > 1 ? "wgrad_dma_kernel<true>" : "wgrad_dma_kernel<false>";

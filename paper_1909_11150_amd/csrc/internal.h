@@ -31,6 +31,7 @@ struct DataConvArgs {
   uint16_t *out;         // output image [n][ho][wo][co], pixel stride ldo
   const uint16_t *gate;  // laid out like out (FG_EPI_GATE) or null
   int32_t n, hi, wi, cr;
+  int32_t ldi;           // pixel stride of act, elements (>= cr)
   int32_t ho, wo, co;
   int32_t ldo;           // pixel stride of out (and gate), elements (>= co)
   int32_t istr, ostr;
@@ -55,12 +56,20 @@ struct DataPlan {
 };
 DataPlan plan_data_conv(const DataConvArgs &a);
 
+// Bytes from the first element of act to the last one a convolution reads
+// (the span a buffer resource must cover).
+__host__ __device__ inline size_t act_span_bytes(const DataConvArgs &a) {
+  const size_t npix = (size_t)a.n * a.hi * a.wi;
+  return npix ? ((npix - 1) * (size_t)a.ldi + (size_t)a.cr) * 2 : 0;
+}
+
 struct WgradArgs {
   const uint16_t *x;     // [n][h][w][c]
   const uint16_t *dy;    // [n][p][q][k]
   uint16_t *dw;          // [k][r][s][c] fp16 (single split)
   float *part;           // [nsplit][k][r*s*c] fp32 partials (nsplit > 1)
   int32_t n, h, w, c, k, r, s, p, q;
+  int32_t ldx;           // pixel stride of x, elements (>= c)
   int32_t sh, sw, ph, pw;
   int32_t mtot;          // n*p*q
   int32_t mchunk;        // reduction rows per split, multiple of 64
@@ -76,6 +85,12 @@ struct WgradPlan {
   size_t ws_bytes;
 };
 WgradPlan plan_wgrad(const fg_conv_desc &d, int32_t p, int32_t q);
+
+// The same span for the kernel gradient's x.
+__host__ __device__ inline size_t x_span_bytes(const WgradArgs &a) {
+  const size_t npix = (size_t)a.n * a.h * a.w;
+  return npix ? ((npix - 1) * (size_t)a.ldx + (size_t)a.c) * 2 : 0;
+}
 size_t head_wgrad_ws_bytes(const fg_conv_desc &d);
 
 hipError_t launch_data_conv(const DataConvArgs &a, bool w_kmajor,

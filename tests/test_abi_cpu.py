@@ -264,10 +264,12 @@ def test_dense_glue_argument_checks(L):
 
 
 def test_strided_output_checks(L):
-    """Pixel strides: honoured for a pass's output only, at least the
-    channel count, a multiple of 8, a 16-byte aligned output; the K = 1 head
-    takes neither strides nor the accumulate epilogue. All refused before
-    any launch (nothing below is dereferenced)."""
+    """Pixel strides: honoured for a pass's output and for x where the
+    forward pass and the kernel gradient read it; at least the channel
+    count, a multiple of 8, a 16-byte aligned pointer; an input and output
+    slice of one buffer must not share channels; the K = 1 head takes
+    neither strides nor the accumulate epilogue. All refused before any
+    launch (nothing below is dereferenced)."""
     ref = ctypes.byref
     x, w, y = FAKE, FAKE + (1 << 20), FAKE + (1 << 26)
     mk = lambda **k: fg.ConvDesc.make(2, 8, 8, 16, 16, 3, 3, 1, 1, **k)
@@ -277,12 +279,19 @@ def test_strided_output_checks(L):
     assert fwd(mk(y_ld=8)) == fg.FG_EINVAL             # below the channel count
     assert fwd(mk(y_ld=20)) == fg.FG_EUNSUPPORTED      # not a multiple of 8
     assert fwd(mk(y_ld=24), out=y + 8) == fg.FG_EUNSUPPORTED   # output not 16-byte aligned
-    assert fwd(mk(x_ld=24)) == fg.FG_EUNSUPPORTED      # strided input
+    assert fwd(mk(x_ld=20)) == fg.FG_EUNSUPPORTED      # input stride not a multiple of 8
+    assert fwd(mk(x_ld=8)) == fg.FG_EINVAL             # input stride below the channel count
+    # input channels 0..15 and output channels 8..23 of one buffer at stride 32
+    assert fwd(mk(x_ld=32, y_ld=32), out=x + 16) == fg.FG_EINVAL
+    # output channels 16..31 but at stride 40: the slices interleave and collide
+    assert fwd(mk(x_ld=32, y_ld=40), out=x + 32) == fg.FG_EINVAL
     assert bwd(mk(y_ld=24)) == fg.FG_EUNSUPPORTED      # strided dy (an input)
     assert bwd(mk(x_ld=8)) == fg.FG_EINVAL
     assert fwd(mk(x_ld=-8)) == fg.FG_EINVAL
-    assert L.conv2d_bwd_weight(ref(mk(x_ld=24)), x, FAKE + (1 << 24), y, None, 0,
-                               None) == fg.FG_EUNSUPPORTED
+    wgt = lambda d: L.conv2d_bwd_weight(ref(d), x, FAKE + (1 << 24), y, None, 0, None)
+    assert wgt(mk(x_ld=20)) == fg.FG_EUNSUPPORTED
+    assert wgt(mk(x_ld=8)) == fg.FG_EINVAL
+    assert wgt(mk(y_ld=24)) == fg.FG_EUNSUPPORTED       # strided dy
     # at stride 4096 the output's span (127 pixels * 4096 + 16 elements, ~1 MiB)
     # from 64 KiB past x reaches the weights at 1 MiB; dense, it would not
     assert bwd(mk(x_ld=4096), out=x + (1 << 16)) == fg.FG_EINVAL
@@ -290,3 +299,5 @@ def test_strided_output_checks(L):
     assert fwd(head(y_ld=8)) == fg.FG_EUNSUPPORTED
     assert fwd(head(), epi=fg.EPI_ACC) == fg.FG_EUNSUPPORTED
     assert bwd(head(x_ld=24)) == fg.FG_EUNSUPPORTED
+    assert fwd(head(x_ld=24)) == fg.FG_EUNSUPPORTED
+    assert wgt(head(x_ld=24)) == fg.FG_EUNSUPPORTED

@@ -131,3 +131,82 @@ def test_strided_convt_and_gate():
     np.testing.assert_array_equal(got[:, OFF:OFF + co].view(np.uint16),
                                   host(dense).reshape(npix, co).view(np.uint16))
     assert not np.any(got[:, :OFF]) and not np.any(got[:, OFF + co:])
+
+
+# strided inputs: the forward pass and the kernel gradient reading x from a
+# channel slice of a wider buffer, on each kernel path
+IN_CASES = [(s, f) for s, op, f in CASES if op == fg.OP_FWD] + \
+    [((1, 127, 129, 512, 256, 3, 2, 1), "")]
+WG_FRAGS = ("wgrad_dma_kernel<false>", "wgrad_dma_kernel<true>", "wgrad_kernel<")
+
+
+@pytest.mark.parametrize("shape,frag", IN_CASES, ids=[f"{f}-{s}" for s, f in IN_CASES])
+def test_strided_input(shape, frag):
+    """x at channel OFF of a buffer of pixel stride c + PAD: the forward
+    output (with ReLU) and the kernel gradient equal the dense calls' bit
+    for bit, and the buffer is left as it was."""
+    n, h, w, c, k, r, st, pd = shape
+    rng = np.random.default_rng(h * w + c + k + 1)
+    p = (h + 2 * pd - r) // st + 1
+    q = (w + 2 * pd - r) // st + 1
+    x = synth.uniform(rng, (n, h, w, c))
+    W = synth.normal(rng, (k, r, r, c), np.sqrt(2.0 / (r * r * c)))
+    dy = synth.uniform(rng, (n, p, q, k))
+    ld = c + PAD
+    npx = n * h * w
+    big = synth.normal(rng, (npx, ld))
+    big[:, OFF:OFF + c] = x.reshape(npx, c)
+    bigd = dev(big)
+    xs = bigd.view(-1)[OFF:]
+    dd = fg.ConvDesc.make(n, h, w, c, k, r, r, st, pd)
+    ds = fg.ConvDesc.make(n, h, w, c, k, r, r, st, pd, x_ld=ld)
+    assert frag in fg.kernel_name(ds, fg.OP_FWD)
+    print(fg.kernel_name(ds, fg.OP_FWD), fg.kernel_name(ds, fg.OP_BWD_WEIGHT))
+    Ws, dys, xd = dev(W), dev(dy), dev(x)
+    ys = [torch.empty((n, p, q, k), dtype=torch.float16, device="cuda") for _ in range(2)]
+    dws = [torch.empty((k, r, r, c), dtype=torch.float16, device="cuda") for _ in range(2)]
+    for d, xx, y, dw in ((dd, xd, ys[0], dws[0]), (ds, xs, ys[1], dws[1])):
+        fg.conv2d_fwd(d, xx, Ws, y, fg.EPI_RELU, None, workspace(d, fg.OP_FWD))
+        fg.conv2d_bwd_weight(d, xx, dys, dw, workspace(d, fg.OP_BWD_WEIGHT))
+    np.testing.assert_array_equal(host(ys[1]).view(np.uint16), host(ys[0]).view(np.uint16))
+    np.testing.assert_array_equal(host(dws[1]).view(np.uint16), host(dws[0]).view(np.uint16))
+    np.testing.assert_array_equal(host(bigd).view(np.uint16), big.view(np.uint16))
+
+
+def test_strided_kernel_gradient_paths_covered():
+    names = {fg.kernel_name(fg.ConvDesc.make(*s, x_ld=s[3] + PAD), fg.OP_BWD_WEIGHT)
+             for s, _ in IN_CASES}
+    for f in WG_FRAGS:
+        assert any(f in nm for nm in names), (f, names)
+
+
+def test_interleaved_input_and_output():
+    """A dense block's layer: x = channels [0, c) of a buffer, the output
+    written (then added, FG_EPI_ACC) into channels [c, c + k) of the same
+    buffer at the same pixel stride."""
+    n, h, w, c, k = 2, 64, 64, 256, 256
+    rng = np.random.default_rng(17)
+    ld = c + k + 8
+    npx = n * h * w
+    big = synth.normal(rng, (npx, ld))
+    x = np.ascontiguousarray(big[:, :c]).reshape(n, h, w, c)
+    W = synth.normal(rng, (k, 3, 3, c), np.sqrt(2.0 / (9 * c)))
+    dd = fg.ConvDesc.make(n, h, w, c, k, 3, 3, 1, 1)
+    ds = fg.ConvDesc.make(n, h, w, c, k, 3, 3, 1, 1, x_ld=ld, y_ld=ld)
+    Ws = dev(W)
+    ref = torch.empty((n, h, w, k), dtype=torch.float16, device="cuda")
+    fg.conv2d_fwd(dd, dev(x), Ws, ref, fg.EPI_NONE, None, workspace(dd, fg.OP_FWD))
+    r16 = host(ref).reshape(npx, k)
+    bigd = dev(big)
+    fg.conv2d_fwd(ds, bigd, Ws, bigd.view(-1)[c:], fg.EPI_NONE, None,
+                  workspace(ds, fg.OP_FWD))
+    got = host(bigd)
+    np.testing.assert_array_equal(got[:, c:c + k].view(np.uint16), r16.view(np.uint16))
+    keep = np.ones(ld, bool)
+    keep[c:c + k] = False
+    np.testing.assert_array_equal(got[:, keep].view(np.uint16), big[:, keep].view(np.uint16))
+    fg.conv2d_fwd(ds, bigd, Ws, bigd.view(-1)[c:], fg.EPI_ACC, None,
+                  workspace(ds, fg.OP_FWD))
+    g = host(bigd)[:, c:c + k].astype(np.float64)
+    err = np.abs(g - 2.0 * r16.astype(np.float64))
+    assert np.all(err <= 0.5 * _ulp16(2.0 * r16) + 0.5 * _ulp16(g)), float(err.max())
