@@ -10,14 +10,17 @@ block, transposed-conv transitions up with skip concatenations, a 1x1 head)
 entirely through libfcngrad calls, prepared once as a call list like the
 chain's step program.
 
-Dense concatenation. The convolutions read dense NHWC inputs and can write
-into a channel slice of a wider buffer (a pixel stride), and add into it:
-  * forward: a block keeps one buffer per layer input, Z_l = concat(Z_{l-1},
-    Y_l); layer l writes Y_l straight into its slice of Z_l and Z_{l-1} is
-    copied into Z_l's prefix; a transition up writes into the first channels
-    of its block's input, whose other channels are a copy of the skip; the
-    last layer of a bottleneck or up block writes into the block's
-    new-feature buffer;
+Dense concatenation. The convolutions read a channel prefix of a wider
+buffer and write, or add, into a channel slice of one (pixel strides):
+  * forward: each level d keeps one buffer laid out as [transition-up
+    output | the down block's input and layer outputs (the skip) | the up
+    block's layer outputs], the bottleneck one as [pooled input | layer
+    outputs]. A layer reads the channels before its own slice and writes
+    its slice, so every concatenation is in place; the stem writes the first
+    down block's input slice, and a pooled map is copied into the next
+    block's input slice. The last layer of a bottleneck or up block writes
+    into the block's new-feature buffer, to which the other layers' outputs
+    are copied (a transition up reads it dense);
   * backward: a bottleneck or up block keeps a gradient buffer G in the
     layout of its last concatenation. A layer's output gradient is its slice
     of G (of the new-feature gradient, for the last layer), gated by its ReLU
@@ -86,32 +89,33 @@ class DenseNet:
         self.dw = {L.name: e(L.w_shape) for L in self.layers}
         self.ws = torch.empty(max(chain_workspace_bytes(self.layers), 16),
                               dtype=torch.uint8, device=self.dev)
-        # forward buffers: Z[(block, l)] = input of layer l + 1 of the block
-        # (l = 0: an up block's input), pooled maps, new-feature buffers
+        # forward buffers: one per level (Z["U<d>"]) and the bottleneck's
+        # (Z["B"]), pooled maps, new-feature buffers; where each layer reads
+        # its input (inp) and writes its (post-ReLU) output (out)
         self.Z, self.P, self.NF, self.G, self.dNF = {}, {}, {}, {}, {}
-        for blk in self._blocks():
-            self._block_bufs(blk)
+        self.inp, self.out = {}, {}
+        k, per = self.k, self.per
+        nk = per * k
         for d in range(1, self.levels + 1):
-            n, h, w, c = self.L[f"TD{d}"].y_shape
-            self.P[d] = e((n, h // 2, w // 2, c))
-        # where each layer's (post-ReLU) output lives
-        self.out = {}
-        for name in ("C0", "F1x1") + tuple(f"TD{d}" for d in range(1, self.levels + 1)):
-            self.out[name] = _dense(e(self.L[name].y_shape))
-        for blk in self._blocks():
-            c0 = self.L[f"{blk}.1"].x_shape[3]
-            for l in range(1, self.per + 1):
-                if (blk, l) in self.Z:
-                    z = self.Z[(blk, l)]
-                    self.out[f"{blk}.{l}"] = Slice(z, c0 + (l - 1) * self.k, z.shape[3],
-                                                   self.k)
-                else:          # a bottleneck or up block's last layer
-                    nf = self.NF[blk]
-                    self.out[f"{blk}.{l}"] = Slice(nf, (l - 1) * self.k, nf.shape[3],
-                                                   self.k)
-        for d in range(1, self.levels + 1):
-            z0 = self.Z[(f"U{d}", 0)]
-            self.out[f"TU{d}"] = Slice(z0, 0, z0.shape[3], self.per * self.k)
+            n_, h, w, c0u = self.L[f"U{d}.1"].x_shape
+            c0d = self.L[f"D{d}.1"].x_shape[3]
+            z = e((n_, h, w, c0u + (per - 1) * k))
+            self.Z[f"U{d}"] = z
+            ld = z.shape[3]
+            for l in range(1, per + 1):
+                self.inp[f"D{d}.{l}"] = Slice(z, nk, ld, c0d + (l - 1) * k)
+                self.out[f"D{d}.{l}"] = Slice(z, nk + c0d + (l - 1) * k, ld, k)
+            self.inp[f"TD{d}"] = Slice(z, nk, ld, c0d + per * k)     # the skip
+            self.out[f"TU{d}"] = Slice(z, 0, ld, nk)
+            self._block_tail(f"U{d}", z, c0u)
+            tdy = self.L[f"TD{d}"].y_shape
+            self.out[f"TD{d}"] = _dense(e(tdy))
+            self.P[d] = e((tdy[0], tdy[1] // 2, tdy[2] // 2, tdy[3]))
+        n_, h, w, c0b = self.L["B.1"].x_shape
+        self.Z["B"] = e((n_, h, w, c0b + (per - 1) * k))
+        self._block_tail("B", self.Z["B"], c0b)
+        self.out["C0"] = self.inp["D1.1"]._replace(ch=self.L["C0"].y_shape[3])
+        self.out["F1x1"] = _dense(e(self.L["F1x1"].y_shape))
         # post-ReLU outputs as (possibly strided) tensor views
         self.act = {name: self._view(s) for name, s in self.out.items()}
         # gradients: one output-gradient buffer per layer (its kernel
@@ -135,25 +139,25 @@ class DenseNet:
         return [f"D{d}" for d in range(1, self.levels + 1)] + ["B"] + \
                [f"U{d}" for d in range(1, self.levels + 1)]
 
-    def _block_bufs(self, blk):
+    def _block_tail(self, blk, z, c0):
+        """Slices of a bottleneck or up block whose input is the first c0
+        channels of z, its new-feature and gradient buffers."""
         e = lambda s: torch.empty(s, dtype=F16, device=self.dev)
-        n, h, w, c0 = self.L[f"{blk}.1"].x_shape
-        if blk.startswith("U"):           # block input: concat(TU out, skip)
-            self.Z[(blk, 0)] = e((n, h, w, c0))
-        # the last concatenation is read only where it is a skip (down blocks)
-        last = self.per if blk.startswith("D") else self.per - 1
-        for l in range(1, last + 1):
-            self.Z[(blk, l)] = e((n, h, w, c0 + l * self.k))
-        if not blk.startswith("D"):
-            self.G[blk] = e((n, h, w, c0 + self.per * self.k))
-            self.NF[blk] = e((n, h, w, self.per * self.k))
-            self.dNF[blk] = e((n, h, w, self.per * self.k))
+        n, h, w = z.shape[:3]
+        k, per, ld = self.k, self.per, z.shape[3]
+        self.NF[blk] = e((n, h, w, per * k))
+        self.dNF[blk] = e((n, h, w, per * k))
+        self.G[blk] = e((n, h, w, c0 + per * k))
+        for l in range(1, per + 1):
+            self.inp[f"{blk}.{l}"] = Slice(z, 0, ld, c0 + (l - 1) * k)
+            self.out[f"{blk}.{l}"] = Slice(z, c0 + (l - 1) * k, ld, k) if l < per else \
+                Slice(self.NF[blk], (l - 1) * k, per * k, k)
 
     # ---- prepared calls ----------------------------------------------------------
     def program(self, target, streams=2):
         """streams = 1: every call in order on one stream; 2: the kernel
-        gradients on a second stream; 3: also the forward pass's copies that
-        do not wait for the layer they follow on a third."""
+        gradients on a second stream; 3: also the forward pass's copies into
+        the new-feature buffers on a third."""
         if streams < 1:
             raise ValueError("streams must be >= 1")
         return _DenseProgram(self, target, min(streams, 3))
@@ -176,10 +180,9 @@ class _DenseProgram:
     streams each kernel gradient runs on the second one as soon as its
     output gradient is written (an event after the writing call), beside the
     main stream's input gradients and copies, with a workspace of its own.
-    With three, the forward pass's copies that need not wait for the layer
-    they follow (a concatenation's prefix, the skip into an up block's
-    input, an output into the new-feature buffer) run on the third, each
-    after the calls that complete what it reads. The main stream waits for
+    With three, the forward pass's copies into the new-feature buffers,
+    which no later layer of the block waits for, run on the third, each
+    after the layer it copies. The main stream waits for
     the other streams' last calls at the end of the step, before the next
     forward pass overwrites what they read. Every kernel reads only
     finished inputs, so the results equal the one-stream order's."""
@@ -239,19 +242,27 @@ class _DenseProgram:
         return s.t.data_ptr() + 2 * s.off
 
     # -- ops --
+    def _in_ok(self, x, L):
+        """x: the slice a layer reads as its input (L.x_shape)."""
+        assert x.ch == L.x_shape[3]
+        self._span_ok(x, L.x_shape[0] * L.x_shape[1] * L.x_shape[2])
+
     def conv_fwd(self, name, x, out, relu, deps=()):
-        """Forward pass of a layer: dense input x, output into slice out."""
+        """Forward pass of a layer: input from slice x (dense for a
+        transposed conv), output into slice out."""
         L = self.net.L[name]
         n = self.net
-        self._shape_ok(x, L.x_shape)
+        self._in_ok(x, L)
         npix = L.y_shape[0] * L.y_shape[1] * L.y_shape[2]
         assert out.ch == L.y_shape[3]
         self._span_ok(out, npix)
         op = OP_FWD if L.kind == "conv" else OP_CONVT
-        d = _desc(L, op, y_ld=out.ld)
+        if op == OP_CONVT:
+            assert x.ld == x.ch
+        d = _desc(L, op, x_ld=x.ld, y_ld=out.ld)
         fn = self._L.conv2d_fwd if L.kind == "conv" else self._L.conv_transpose2d_fwd
         return self._add(f"{name}.fwd", kernel_name(d, op), L.flops, fn,
-                         (self._keep_desc(d), x.data_ptr(), n.w[name].data_ptr(),
+                         (self._keep_desc(d), self._ptr(x), n.w[name].data_ptr(),
                           self._ptr(out), EPI_RELU if relu else EPI_NONE, None,
                           n.ws.data_ptr(), n.ws.numel()), workspace_bytes(d, op) == 0,
                          deps=deps)
@@ -262,7 +273,7 @@ class _DenseProgram:
         dx, added to what it holds when acc (no gate)."""
         L = self.net.L[name]
         n = self.net
-        self._shape_ok(x, L.x_shape)
+        self._in_ok(x, L)
         self._shape_ok(dy, L.y_shape)
         npix = L.x_shape[0] * L.x_shape[1] * L.x_shape[2]
         assert dx.ch == L.x_shape[3]
@@ -273,10 +284,10 @@ class _DenseProgram:
         dwk = dict(sid=self._dw_sid, deps=(len(self.calls) - 1,))
         if L.kind == "conv":
             d = _desc(L, OP_FWD, x_ld=dx.ld)
-            dw_d = _desc(L, OP_FWD)
+            dw_d = _desc(L, OP_FWD, x_ld=x.ld)
             self._add(f"{name}.dW", kernel_name(dw_d, OP_BWD_WEIGHT), L.flops,
                       self._L.conv2d_bwd_weight,
-                      (self._keep_desc(dw_d), x.data_ptr(), dy.data_ptr(),
+                      (self._keep_desc(dw_d), self._ptr(x), dy.data_ptr(),
                        n.dw[name].data_ptr(), dws, dwb),
                       workspace_bytes(dw_d, OP_BWD_WEIGHT) == 0, **dwk)
             self._add(f"{name}.dx", kernel_name(d, OP_BWD_DATA), L.flops,
@@ -285,10 +296,11 @@ class _DenseProgram:
                        self._ptr(dx), epi, None, wsp, wsb),
                       workspace_bytes(d, OP_BWD_DATA) == 0)
         else:   # transposed conv: both passes are convs of dy with Wt as KRSC
+            assert x.ld == x.ch
             dw_d = _desc(L, OP_BWD_WEIGHT)
             self._add(f"{name}.dW", kernel_name(dw_d, OP_BWD_WEIGHT), L.flops,
                       self._L.conv2d_bwd_weight,
-                      (self._keep_desc(dw_d), dy.data_ptr(), x.data_ptr(),
+                      (self._keep_desc(dw_d), dy.data_ptr(), self._ptr(x),
                        n.dw[name].data_ptr(), dws, dwb),
                       workspace_bytes(dw_d, OP_BWD_WEIGHT) == 0, **dwk)
             d = _desc(L, OP_BWD_DATA, y_ld=dx.ld)
@@ -315,34 +327,30 @@ class _DenseProgram:
                          sid=sid, deps=deps)
 
     # -- the step --
-    def _block_fwd(self, blk, z0, ready):
-        """Dense layers of a block whose input z0 (dense) is complete once
-        the calls in `ready` are. Returns the calls that complete the last
-        concatenation (down blocks) or the new-feature buffer (others)."""
+    def _block_fwd(self, blk, ready):
+        """Dense layers of a block whose input slice is complete once the
+        calls in `ready` are. Each layer reads the channels before its own
+        slice and writes its slice. Returns the calls that complete the
+        block's outputs: its last layer (down blocks; the skip is then
+        whole) or the new-feature buffer (others)."""
         n = self.net
-        z = z0
         nf_ready = []
         for l in range(1, n.per + 1):
             name = f"{blk}.{l}"
-            conv = self.conv_fwd(name, z, n.out[name], True, deps=ready)
-            if not blk.startswith("D"):     # new features: the block's outputs
-                if (blk, l) in n.Z:
-                    nf = n.NF[blk]
-                    nf_ready.append(self.copy(
-                        f"{name}.new", n.out[name],
-                        Slice(nf, (l - 1) * n.k, nf.shape[3], n.k),
-                        sid=self._cp_sid, deps=(conv,)))
-                else:
-                    nf_ready.append(conv)
-            if (blk, l) not in n.Z:
+            conv = self.conv_fwd(name, n.inp[name], n.out[name], True, deps=ready)
+            ready = (conv,)
+            if blk.startswith("D"):
                 continue
-            zl = n.Z[(blk, l)]
-            cat0 = self.copy(f"{name}.cat0", _dense(z), Slice(zl, 0, zl.shape[3], z.shape[3]),
-                             sid=self._cp_sid, deps=ready)
-            z, ready = zl, (cat0, conv)
+            if l < n.per:     # copied into the new-feature buffer
+                nf = n.NF[blk]
+                nf_ready.append(self.copy(f"{name}.new", n.out[name],
+                                          Slice(nf, (l - 1) * n.k, nf.shape[3], n.k),
+                                          sid=self._cp_sid, deps=(conv,)))
+            else:
+                nf_ready.append(conv)
         return ready if blk.startswith("D") else tuple(nf_ready)
 
-    def _block_bwd(self, blk, G, c0, block_input, fresh, dnf=None):
+    def _block_bwd(self, blk, G, c0, fresh, dnf=None):
         """G: slice over the layout of the block's last concatenation (ld =
         its pixel stride). For a fresh block (bottleneck, up) nothing is in G
         yet and dnf holds the new-feature gradient; otherwise G holds the
@@ -353,13 +361,13 @@ class _DenseProgram:
         for l in range(n.per, 0, -1):
             name = f"{blk}.{l}"
             lo = c0 + (l - 1) * n.k
-            zin = n.Z[(blk, l - 1)] if (blk, l - 1) in n.Z else block_input
             dY = n.dY[name]
             src = Slice(dnf, (l - 1) * n.k, nk, n.k) if fresh and l == n.per else \
                 Slice(G.t, G.off + lo, G.ld, n.k)
             self.copy(f"{name}.dy", src, _dense(dY), gate=n.out[name])
             first = fresh and l == n.per          # nothing in G to add to yet
-            self.conv_bwd(name, zin, dY, Slice(G.t, G.off, G.ld, lo), acc=not first)
+            self.conv_bwd(name, n.inp[name], dY, Slice(G.t, G.off, G.ld, lo),
+                          acc=not first)
             if first and n.per > 1:   # the earlier layers' new-feature gradients
                 self.copy(f"{blk}.dnew", Slice(dnf, 0, nk, lo - c0),
                           Slice(G.t, G.off + c0, G.ld, lo - c0), acc=True)
@@ -369,34 +377,31 @@ class _DenseProgram:
         Lb = self._L
         nk = n.per * n.k
         # ---- forward
-        self.conv_fwd("C0", n.x, n.out["C0"], True)
-        bin_, ready = n.act["C0"], (len(self.calls) - 1,)
-        skips, skip_ready = {}, {}
+        self.conv_fwd("C0", _dense(n.x), n.out["C0"], True)
+        ready = (len(self.calls) - 1,)
+        skip_ready = {}
         for d in range(1, n.levels + 1):
-            zr = self._block_fwd(f"D{d}", bin_, ready)
-            skips[d], skip_ready[d] = n.Z[(f"D{d}", n.per)], zr
-            self.conv_fwd(f"TD{d}", skips[d], n.out[f"TD{d}"], True, deps=zr)
+            skip_ready[d] = self._block_fwd(f"D{d}", ready)
+            self.conv_fwd(f"TD{d}", n.inp[f"TD{d}"], n.out[f"TD{d}"], True,
+                          deps=skip_ready[d])
             td = n.act[f"TD{d}"]
             self._add(f"TD{d}.pool", "avg_pool2d_fwd_kernel", 2 * td.numel() * 5 // 4,
                       Lb.avg_pool2d_fwd,
                       (td.data_ptr(), *td.shape, n.P[d].data_ptr()))
-            bin_, ready = n.P[d], (len(self.calls) - 1,)
-        nf_ready = self._block_fwd("B", bin_, ready)
+            # the pooled map into the next block's input slice
+            nxt = n.inp[f"D{d + 1}.1" if d < n.levels else "B.1"]
+            ready = (self.copy(f"P{d}.cat", _dense(n.P[d]), nxt),)
+        nf_ready = self._block_fwd("B", ready)
         nf = n.NF["B"]
         tu_in = {}
         for d in range(n.levels, 0, -1):
             tu = f"TU{d}"
             tu_in[d] = nf
-            z0 = n.Z[(f"U{d}", 0)]
-            c0 = z0.shape[3]
-            tconv = self.conv_fwd(tu, nf, n.out[tu], True, deps=nf_ready)
-            skip = self.copy(f"{tu}.skip", _dense(skips[d]),
-                             Slice(z0, nk, c0, c0 - nk), sid=self._cp_sid,
-                             deps=skip_ready[d])
-            nf_ready = self._block_fwd(f"U{d}", z0, (tconv, skip))
+            tconv = self.conv_fwd(tu, _dense(nf), n.out[tu], True, deps=nf_ready)
+            nf_ready = self._block_fwd(f"U{d}", (tconv,) + tuple(skip_ready[d]))
             nf = n.NF[f"U{d}"]
         y = n.act["F1x1"]
-        self.conv_fwd("F1x1", nf, n.out["F1x1"], False, deps=nf_ready)
+        self.conv_fwd("F1x1", _dense(nf), n.out["F1x1"], False, deps=nf_ready)
         # ---- head: loss-scaled mean Huber loss
         self._head_args = [y.data_ptr(), target.data_ptr(), y.numel(),
                            ctypes.c_double(n.loss_scale / y.numel()),
@@ -404,19 +409,18 @@ class _DenseProgram:
         self._add("head_grad", "huber_head_grad_kernel", 10 * y.numel(),
                   Lb.huber_head_grad, tuple(self._head_args))
         # ---- backward: head, up blocks (level 1 first), bottleneck, down path
-        self.conv_bwd("F1x1", nf, n.g_out, _dense(n.dNF["U1"]), acc=False)
+        self.conv_bwd("F1x1", _dense(nf), n.g_out, _dense(n.dNF["U1"]), acc=False)
         for d in range(1, n.levels + 1):
             blk, tu = f"U{d}", f"TU{d}"
             G = _dense(n.G[blk])
-            self._block_bwd(blk, G, n.Z[(blk, 0)].shape[3], n.Z[(blk, 0)], True,
-                            n.dNF[blk])
+            self._block_bwd(blk, G, n.inp[f"{blk}.1"].ch, True, n.dNF[blk])
             self.copy(f"{tu}.dy", Slice(G.t, 0, G.ld, nk), _dense(n.dU[d]),
                       gate=n.out[tu])
             below = "B" if d == n.levels else f"U{d + 1}"
-            self.conv_bwd(tu, tu_in[d], n.dU[d], _dense(n.dNF[below]), acc=False)
+            self.conv_bwd(tu, _dense(tu_in[d]), n.dU[d], _dense(n.dNF[below]), acc=False)
         G = _dense(n.G["B"])
         c0 = n.P[n.levels].shape[3]
-        self._block_bwd("B", G, c0, n.P[n.levels], True, n.dNF["B"])
+        self._block_bwd("B", G, c0, True, n.dNF["B"])
         dP_src = Slice(G.t, 0, G.ld, c0)
         for d in range(n.levels, 0, -1):
             # gradient of the pooled output -> dense, then through the pool
@@ -428,15 +432,14 @@ class _DenseProgram:
                       Lb.avg_pool2d_bwd,
                       (n.dP[d].data_ptr(), td.data_ptr(), *td.shape, n.dT[d].data_ptr()))
             Gu = n.G[f"U{d}"]
-            G = Slice(Gu, nk, Gu.shape[3], skips[d].shape[3])
-            self.conv_bwd(f"TD{d}", skips[d], n.dT[d], G, acc=True)
+            G = Slice(Gu, nk, Gu.shape[3], n.inp[f"TD{d}"].ch)
+            self.conv_bwd(f"TD{d}", n.inp[f"TD{d}"], n.dT[d], G, acc=True)
             c0 = n.L[f"D{d}.1"].x_shape[3]
-            block_input = n.act["C0"] if d == 1 else n.P[d - 1]
-            self._block_bwd(f"D{d}", G, c0, block_input, False)
+            self._block_bwd(f"D{d}", G, c0, False)
             dP_src = Slice(G.t, G.off, G.ld, c0)
         c0 = n.L["C0"].y_shape[3]
         self.copy("C0.dy", dP_src, _dense(n.dC0), gate=n.out["C0"])
-        self.conv_bwd("C0", n.x, n.dC0, _dense(n.dX), acc=False)
+        self.conv_bwd("C0", _dense(n.x), n.dC0, _dense(n.dX), acc=False)
 
     def set_loss_scale(self, s):
         self.net.loss_scale = float(s)

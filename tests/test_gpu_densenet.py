@@ -40,30 +40,25 @@ def _reduced():
 
 
 def _gpu_forward_state(net):
-    """The GPU's stored forward tensors, keyed as the oracle network's. The
+    """The GPU's stored forward tensors, keyed as the oracle network's: each
+    layer's input and output are views of the network's level buffers. The
     last concatenation of the bottleneck and up blocks, which nothing reads
     and the GPU does not keep, is rebuilt on the host from the block's
     tensors (the oracle's backward pass takes only its shape)."""
+    view = lambda s: host(net._view(s))
     fw = {name: host(a) for name, a in net.act.items()}
     fw["y"] = fw["F1x1"]
     lv, per = net.levels, net.per
-    fw["Z:D1:0"] = fw["C0"]
     for d in range(1, lv + 1):
         fw[f"P{d}"] = host(net.P[d])
-        fw[f"Z:U{d}:0"] = host(net.Z[(f"U{d}", 0)])
-        if d > 1:
-            fw[f"Z:D{d}:0"] = fw[f"P{d - 1}"]
         fw[f"in:TU{d}"] = host(net.NF["B" if d == lv else f"U{d + 1}"])
-    fw["Z:B:0"] = fw[f"P{lv}"]
+        fw[f"skip{d}"] = fw[f"Z:D{d}:{per}"] = view(net.inp[f"TD{d}"])
     for blk in net._blocks():
         for l in range(1, per + 1):
-            if (blk, l) in net.Z:
-                fw[f"Z:{blk}:{l}"] = host(net.Z[(blk, l)])
-            else:
-                fw[f"Z:{blk}:{l}"] = np.concatenate([fw[f"Z:{blk}:{l - 1}"],
-                                                     fw[f"{blk}.{l}"]], axis=-1)
-    for d in range(1, lv + 1):
-        fw[f"skip{d}"] = fw[f"Z:D{d}:{per}"]
+            fw[f"Z:{blk}:{l - 1}"] = view(net.inp[f"{blk}.{l}"])
+        if not blk.startswith("D"):
+            fw[f"Z:{blk}:{per}"] = np.concatenate([fw[f"Z:{blk}:{per - 1}"],
+                                                   fw[f"{blk}.{per}"]], axis=-1)
     fw["in:F1x1"] = host(net.NF["U1"])
     return fw
 
