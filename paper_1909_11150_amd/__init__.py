@@ -57,7 +57,8 @@ class FgError(RuntimeError):
 
 class ConvDesc(ctypes.Structure):
     """fg_conv_desc. x_ld / y_ld: pixel strides of the x- and y-shaped
-    tensors (0: dense), honoured where that tensor is the pass's output."""
+    tensors (0: dense), honoured where that tensor is the pass's output and
+    for x where the forward pass and the kernel gradient read it."""
     _fields_ = [(f, ctypes.c_int32) for f in
                 ("n", "h", "w", "c", "k", "r", "s", "stride_h", "stride_w",
                  "pad_h", "pad_w", "x_ld", "y_ld")]
