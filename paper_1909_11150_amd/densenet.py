@@ -36,7 +36,8 @@ from collections import namedtuple
 import torch
 
 from . import (EPI_ACC, EPI_NONE, EPI_RELU, OP_BWD_DATA, OP_BWD_WEIGHT, OP_CONVT,
-               OP_FWD, ConvDesc, FgError, kernel_name, lib, workspace_bytes)
+               OP_FWD, ConvDesc, FgError, Segment, grad_group_plan, kernel_name, lib,
+               workspace_bytes)
 from .fcn import (Call, chain_workspace_bytes, kernel_gradient_workspace_bytes)
 
 F16 = torch.float16
@@ -74,7 +75,7 @@ def _desc(L, op, x_ld=0, y_ld=0):
 
 class DenseNet:
     def __init__(self, layers, weights, x, loss_scale=2.0 ** 15, delta=10.0,
-                 device="cuda", stream=None):
+                 device="cuda", stream=None, group_cap_bytes=None, group_align_bytes=256):
         self.layers = list(layers)
         self.L = {L.name: L for L in self.layers}
         self.levels, self.per = _structure(self.layers)
@@ -128,7 +129,41 @@ class DenseNet:
         self.dP = {d: e(self.P[d].shape) for d in range(1, self.levels + 1)}
         self.dU = {d: e(self.L[f"TU{d}"].y_shape) for d in range(1, self.levels + 1)}
         self.dC0 = e(self.L["C0"].y_shape)
+        self.groups = None
+        if group_cap_bytes is not None:
+            self._plan_groups(group_cap_bytes, group_align_bytes)
         self._L = lib()
+
+    def dw_order(self):
+        """Layer names in the order the backward pass completes their kernel
+        gradients: head, up levels from the top, bottleneck, down levels from
+        the bottom, stem; within a block, its last layer first."""
+        blk = lambda b: [f"{b}.{l}" for l in range(self.per, 0, -1)]
+        order = ["F1x1"]
+        for d in range(1, self.levels + 1):
+            order += blk(f"U{d}") + [f"TU{d}"]
+        order += blk("B")
+        for d in range(self.levels, 0, -1):
+            order += [f"TD{d}"] + blk(f"D{d}")
+        return order + ["C0"]
+
+    def _plan_groups(self, cap, align):
+        """Gradient groups (Section 4.2) over the kernel gradients in
+        completion order, as the chain forms them: fp16 group buffers, their
+        fp32 unscaled copies, a non-finite flag per group and fp32 master
+        gradients per layer."""
+        order = self.dw_order()
+        gof, oof, gnum = grad_group_plan([self.dw[m].numel() for m in order], cap,
+                                         align, 2)
+        self.groups = [{"members": [order[j] for j in range(len(order)) if gof[j] == g],
+                        "offsets": [oof[j] for j in range(len(order)) if gof[j] == g],
+                        "numel": n} for g, n in enumerate(gnum)]
+        e = lambda n, dt: torch.empty(n, dtype=dt, device=self.dev)
+        self.gbuf16 = [e(g["numel"], F16) for g in self.groups]
+        self.gbuf32 = [e(g["numel"], torch.float32) for g in self.groups]
+        self.flags = torch.zeros(len(self.groups), dtype=torch.int32, device=self.dev)
+        self.master = {L.name: e(L.w_shape, torch.float32) for L in self.layers}
+        self._group_done_at = {g["members"][-1]: gi for gi, g in enumerate(self.groups)}
 
     @staticmethod
     def _view(s):
@@ -199,6 +234,7 @@ class _DenseProgram:
         self._dw_sid = 1 if streams > 1 else 0
         self._cp_sid = 2 if streams > 2 else 0
         self._sp = [ctypes.c_void_p(x.cuda_stream) for x in self.streams]
+        self._dw_seen = []
         self._ws_side = torch.empty(
             max(16, kernel_gradient_workspace_bytes(net.layers)), dtype=torch.uint8,
             device=net.dev) if streams > 1 else net.ws
@@ -208,7 +244,8 @@ class _DenseProgram:
         # a dependency on a call of the same stream is its stream order
         self.calls = [c._replace(deps=tuple(d for d in c.deps if self.calls[d].sid != c.sid))
                       for c in self.calls]
-        self.calls = [c._replace(args=c.args + (self._sp[c.sid],)) for c in self.calls]
+        self.calls = [c if c.fn is None else c._replace(args=c.args + (self._sp[c.sid],))
+                      for c in self.calls]
         self.final = tuple(max(j for j, c in enumerate(self.calls) if c.sid == sid)
                            for sid in range(1, len(self.streams)))
         self.step_final = self.final
@@ -308,6 +345,34 @@ class _DenseProgram:
                       (self._keep_desc(d), dy.data_ptr(), n.w[name].data_ptr(),
                        self._ptr(dx), epi, None, wsp, wsb),
                       workspace_bytes(d, OP_FWD) == 0)
+        self._dw_seen.append(name)
+        if n.groups is not None and name in n._group_done_at:
+            self._group_calls(n._group_done_at[name])
+
+    def _group_calls(self, gi):
+        """Pack, unscale with the non-finite check, unpack (Sections 4.2 and
+        6.2) of a group once its last kernel gradient is written: on the
+        kernel-gradient stream, after every member's kernel gradient."""
+        n = self.net
+        g = n.groups[gi]
+        num = g["numel"]
+        seg = lambda ts: (Segment * len(ts))(
+            *[Segment(t.data_ptr(), t.numel(), off) for t, off in zip(ts, g["offsets"])])
+        src = seg([n.dw[m] for m in g["members"]])
+        dst = seg([n.master[m] for m in g["members"]])
+        flag = n.flags[gi:gi + 1]
+        self._keep += [src, dst, flag]
+        g16, g32 = n.gbuf16[gi], n.gbuf32[gi]
+        sid = self._dw_sid
+        self._add(f"G{gi}.pack", "copy_pieces_kernel<2>", 4 * num, self._L.grad_group_pack,
+                  (src, len(g["members"]), g16.data_ptr(), num), sid=sid)
+        self._add(f"G{gi}.unscale", "unscale_vec_kernel", 6 * num,
+                  self._L.grad_unscale_check,
+                  (g16.data_ptr(), num, self._inv_scale, g32.data_ptr(), flag.data_ptr()),
+                  sid=sid)
+        self._add(f"G{gi}.unpack", "copy_pieces_kernel<4>", 8 * num,
+                  self._L.grad_group_unpack,
+                  (g32.data_ptr(), num, dst, len(g["members"])), sid=sid)
 
     def copy(self, label, src, dst, gate=None, acc=False, sid=0, deps=()):
         """Per pixel, dst.ch channels from slice src to slice dst (gated by
@@ -376,6 +441,9 @@ class _DenseProgram:
         n = self.net
         Lb = self._L
         nk = n.per * n.k
+        self._inv_scale = ctypes.c_float(1.0 / n.loss_scale)
+        if n.groups is not None:     # the step's non-finite flags start clear
+            self._add("flags.zero", "", 0, None, (n.flags.zero_,), False, sid=self._dw_sid)
         # ---- forward
         self.conv_fwd("C0", _dense(n.x), n.out["C0"], True)
         ready = (len(self.calls) - 1,)
@@ -440,10 +508,12 @@ class _DenseProgram:
         c0 = n.L["C0"].y_shape[3]
         self.copy("C0.dy", dP_src, _dense(n.dC0), gate=n.out["C0"])
         self.conv_bwd("C0", _dense(n.x), n.dC0, _dense(n.dX), acc=False)
+        assert self._dw_seen == n.dw_order(), "kernel gradients out of completion order"
 
     def set_loss_scale(self, s):
         self.net.loss_scale = float(s)
         self._head_args[3].value = s / self.net.act["F1x1"].numel()
+        self._inv_scale.value = 1.0 / s
 
     def run(self, events=None):
         """Run the step once. events: {call index: (start, end)} HIP events
@@ -456,9 +526,13 @@ class _DenseProgram:
             ev = events.get(i) if events else None
             if ev:
                 ev[0].record(s)
-            st = c.fn(*c.args)
-            if st:
-                raise FgError(c.label, st)
+            if c.fn is None:
+                with torch.cuda.stream(s):
+                    c.args[0]()
+            else:
+                st = c.fn(*c.args)
+                if st:
+                    raise FgError(c.label, st)
             if ev:
                 ev[1].record(s)
             if i in evs:

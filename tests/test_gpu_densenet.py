@@ -195,3 +195,37 @@ def test_full_densenet_step_is_deterministic_and_finite():
     for name, a in net.act.items():
         assert np.all(np.isfinite(host(a).astype(np.float32))), name
     assert np.all(np.isfinite(host(net.dX).astype(np.float32)))
+
+
+def test_densenet_gradient_groups():
+    """The dense step's gradient path: kernel gradients packed into groups
+    in completion order (bits and zero padding), unscaled with the
+    non-finite check and unpacked into fp32 master gradients, against the
+    oracle's definitions applied to the step's own kernel gradients."""
+    from oracle import grad as OG
+    layers, x, w, t = _reduced()
+    net = DenseNet(layers, w, x, loss_scale=S_RED, delta=DELTA, group_cap_bytes=48 * 1024,
+                   group_align_bytes=256)
+    assert len(net.groups) >= 3
+    order = net.dw_order()
+    assert [m for g in net.groups for m in g["members"]] == order
+    plan = OG.plan_groups([net.dw[m].numel() for m in order], 48 * 1024, 256)
+    assert [g["numel"] for g in plan] == [g["numel"] for g in net.groups]
+    net.step(dev(t))
+    torch.cuda.synchronize()
+    inv = np.float32(1.0 / S_RED)
+    flags = host(net.flags)
+    for gi, g in enumerate(net.groups):
+        g16 = host(net.gbuf16[gi]).view(np.uint16)
+        want = np.zeros(g["numel"], np.uint16)
+        src = {}
+        for m, off in zip(g["members"], g["offsets"]):
+            src[m] = host(net.dw[m]).ravel().view(np.uint16)
+            want[off:off + src[m].size] = src[m]
+        np.testing.assert_array_equal(g16, want)
+        np.testing.assert_array_equal(host(net.gbuf32[gi]).view(np.uint32),
+                                      OG.unscale(want, inv).view(np.uint32))
+        assert int(flags[gi]) == int(OG.found_nonfinite(want))
+        for m in g["members"]:
+            np.testing.assert_array_equal(host(net.master[m]).ravel().view(np.uint32),
+                                          OG.unscale(src[m], inv).view(np.uint32))
