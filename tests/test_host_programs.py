@@ -176,3 +176,26 @@ def test_dense_layout_concatenations_in_place(no_cuda, per):
         prev = seen.setdefault(key, np.zeros(sl.t.numel(), bool))
         assert not prev[e].any(), name
         prev[e] = True
+
+
+def test_dense_program_gradient_groups(no_cuda):
+    """Each group's pack, unscale and unpack follow every member's kernel
+    gradient on the kernel-gradient stream; the flags are cleared first."""
+    layers = synth.densenet_layers(n=1, h=32, c_in=32, c0=32, growth=32, levels=2,
+                                   per_block=2)
+    w = [torch.zeros(L.w_shape, dtype=torch.float16) for L in layers]
+    x = torch.zeros(layers[0].x_shape, dtype=torch.float16)
+    net = DenseNet(layers, w, x, device="cpu", group_cap_bytes=48 * 1024)
+    t = torch.zeros(layers[-1].y_shape, dtype=torch.float32)
+    for streams in (1, 2):
+        calls = net.program(t, streams=streams).calls
+        idx = {c.label: i for i, c in enumerate(calls)}
+        side = 1 if streams > 1 else 0
+        first_side = min(i for i, c in enumerate(calls) if c.sid == side)
+        assert calls[first_side].label == "flags.zero" or side == 0
+        assert idx["flags.zero"] < min(idx[f"{m}.dW"] for m in net.dw_order())
+        for gi, g in enumerate(net.groups):
+            p, u, q = idx[f"G{gi}.pack"], idx[f"G{gi}.unscale"], idx[f"G{gi}.unpack"]
+            assert p < u < q and all(calls[j].sid == side for j in (p, u, q))
+            assert max(idx[f"{m}.dW"] for m in g["members"]) < p
+            assert all(calls[idx[f"{m}.dW"]].sid == side for m in g["members"])
