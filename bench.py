@@ -41,6 +41,15 @@ MFMA_F16_PEAK_TFLOPS = 2500.0      # MI355X dense fp16 MFMA
 HBM_PEAK_GBPS = 8000.0             # MI355X HBM3E
 
 
+def paper_rates(ops_conv_per_pass, t_exec_s, t_comp_s):
+    """Sustained and Peak performance of Section 5.2 (flop/s): the three
+    convolution passes of a step (forward, kernel gradient, input gradient),
+    3 * OPS_conv, over the step's execution time t_exec and over the time its
+    convolutions compute, t_comp."""
+    total = 3.0 * ops_conv_per_pass
+    return total / t_exec_s, total / t_comp_s
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -75,6 +84,17 @@ def parse():
                          "--launches-per-step)")
     ap.add_argument("--launches-per-step", type=int, default=6,
                     help="with --summarize-trace: the kernel's launches per step")
+    ap.add_argument("--summarize-mfma", default=None, metavar="DIR",
+                    help="per-kernel MFMA utilisation table from two rocprofv3 --pmc "
+                         "runs (DIR/mfma_busy, DIR/mfma_ops)")
+    ap.add_argument("--grad-path-only", action="store_true",
+                    help="only the standalone, cache-flushed gradient-path measurement")
+    ap.add_argument("--grad-reps", type=int, default=20,
+                    help="reps per group and kernel of the gradient-path measurement")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the standalone gradient path and the small configurations")
+    ap.add_argument("--no-clocks", action="store_true",
+                    help="do not query amd-smi / rocm-smi for the clocks")
     return ap.parse_args()
 
 
@@ -188,6 +208,46 @@ def summarize_pmc(d):
         if k.startswith(("data_conv", "wgrad")):
             print(f"traffic: kernel={k} src_sha256_16={source_hash(k)} "
                   f"bytes_per_launch={int(round(mb * 1e6))}")
+
+
+def summarize_mfma(d):
+    """Per-kernel MFMA utilisation from one rocprofv3 --pmc run collecting
+    SQ_VALU_MFMA_BUSY_CYCLES, SQ_INSTS_VALU_MFMA_MOPS_F16, SQ_BUSY_CU_CYCLES
+    and GRBM_GUI_ACTIVE (a *counter_collection.csv under DIR). MFMA busy =
+    busy cycles summed over the SIMDs / (GPU-active cycles x 1024 SIMDs);
+    MFMA flops = MOPS_F16 x 512 (what the matrix cores executed, padding of
+    partial tiles included)."""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    disp = {}
+    for f in files:
+        for r in csv.DictReader(open(f)):
+            key = (f, r["Dispatch_Id"])
+            e = disp.setdefault(key, {"kernel": short_kernel_name(r["Kernel_Name"])})
+            name = r["Counter_Name"]
+            for suf in ("_sum", "_max", "_min", "_avr"):
+                if name.endswith(suf):
+                    name = name[:-len(suf)]
+            e[name] = e.get(name, 0.0) + float(r["Counter_Value"])
+    per = {}
+    for e in disp.values():
+        if "GRBM_GUI_ACTIVE" not in e or "SQ_VALU_MFMA_BUSY_CYCLES" not in e:
+            continue
+        k = per.setdefault(e["kernel"], [0, 0.0, 0.0, 0.0])
+        k[0] += 1
+        k[1] += e["GRBM_GUI_ACTIVE"]
+        k[2] += e["SQ_VALU_MFMA_BUSY_CYCLES"]
+        k[3] += e.get("SQ_INSTS_VALU_MFMA_MOPS_F16", 0.0) * 512
+    print("| kernel | dispatches | GPU-active cycles per dispatch | MFMA busy | "
+          "MFMA TFLOP per dispatch | MFMA TFLOP/s while active (2.4 GHz) |")
+    print("|---|---:|---:|---:|---:|---:|")
+    rows = sorted(per.items(), key=lambda kv: -kv[1][1])
+    for k, (n, gui, busy, fl) in rows:
+        if fl == 0:
+            continue
+        print(f"| `{k}` | {n} | {gui / n:.0f} | {100 * busy / (gui * 1024):.1f}% | "
+              f"{fl / n / 1e12:.4f} | {fl / (gui / 2.4e9) / 1e12:.0f} |")
 
 
 def op_bench(label, steps, warmup):
@@ -328,6 +388,213 @@ def cpu_baseline(layers, seconds):
                        f"{flops_done / 1e9:.1f} GFLOP algorithmic in {t_total:.1f} s")}
 
 
+def cpu_model():
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def cpu_grad_baseline(seconds):
+    """The gradient path's NumPy oracle (pack, unscale with the non-finite
+    check, unpack; single-threaded) on whole config-5 groups, repeated for
+    about `seconds`; GB/s of the same algorithmic bytes the GPU kernels are
+    credited with (4 + 6 + 8 bytes per group element)."""
+    import synth
+    from oracle import grad as G
+    layers = synth.fcn_layers()
+    numels = [L.w_numel for L in reversed(layers)]
+    plan = G.plan_groups(numels, synth.GROUP_CAP_BYTES, synth.GROUP_ALIGN_BYTES)
+    rng = np.random.default_rng(11)
+    srcs = [synth.normal(rng, (n,), 1.0) for n in numels]
+    done, t_total, groups = 0, 0.0, 0
+    while t_total < seconds and groups < 64:
+        g = plan[groups % len(plan)]
+        t0 = time.perf_counter()
+        buf = G.pack(srcs, g)
+        out, _ = G.unscale_check(buf, 1.0 / synth.LOSS_SCALE)
+        G.unpack(out, g, numels)
+        t_total += time.perf_counter() - t0
+        done += 18 * g["numel"]
+        groups += 1
+    return {"value": round(done / t_total / 1e9, 3), "unit": "GB/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"NumPy pack + unscale/check + unpack of {groups} whole gradient "
+                      f"groups of the 25 MiB plan ({done / 1e9:.2f} GB algorithmic) "
+                      f"in {t_total:.1f} s"}
+
+
+def gpu_clocks():
+    """Current SCLK / MCLK as amd-smi (or rocm-smi) prints them, or None."""
+    import subprocess
+    for cmd in (["amd-smi", "metric", "--clock"], ["rocm-smi", "--showclocks"]):
+        try:
+            r = subprocess.run(cmd, capture_output=True, text=True, timeout=20)
+        except (OSError, subprocess.TimeoutExpired):
+            continue
+        if r.returncode == 0 and r.stdout.strip():
+            keep = [ln.strip() for ln in r.stdout.splitlines()
+                    if any(k in ln.upper() for k in ("SCLK", "MCLK", "GFX_0", "MEM_0",
+                                                     "CLK:"))]
+            return {"tool": cmd[0], "lines": keep[:12]}
+    return None
+
+
+def _ev():
+    import torch
+    return torch.cuda.Event(enable_timing=True)
+
+
+def grad_path_bench(reps=20, warmup=3, flush_mib=1024):
+    """The gradient path alone on the nine 25 MiB groups of the full
+    network's weight gradients (seeded N(0,1) fp16 values): each launch of
+    pack, unscale-with-check and unpack is timed with HIP events, after a
+    write of flush_mib MiB that evicts the Infinity Cache (256 MB) and the
+    L2s, so every byte comes from HBM. Per group and kernel: median and best
+    GB/s over `reps`; per kernel: all groups' bytes over the sum of their
+    median times. The ceiling is the runtime's own device-to-device copy
+    (torch copy_) of each group's fp16 bytes, timed the same way."""
+    import torch
+
+    import paper_1909_11150_amd as fg
+    import synth
+    layers = synth.fcn_layers()
+    order = list(reversed(range(len(layers))))
+    numels = [layers[i].w_numel for i in order]
+    gof, oof, gnum = fg.grad_group_plan(numels, synth.GROUP_CAP_BYTES,
+                                        synth.GROUP_ALIGN_BYTES, 2)
+    rng = np.random.default_rng(9)
+    srcs = [torch.from_numpy(synth.normal(rng, (n,), 1.0)).cuda() for n in numels]
+    masters = [torch.empty(n, dtype=torch.float32, device="cuda") for n in numels]
+    groups = []
+    for g, n in enumerate(gnum):
+        mem = [j for j in range(len(numels)) if gof[j] == g]
+        groups.append(dict(mem=mem, off=[oof[j] for j in mem], numel=n,
+                           g16=torch.empty(n, dtype=torch.float16, device="cuda"),
+                           g32=torch.empty(n, dtype=torch.float32, device="cuda"),
+                           cpy=torch.empty(n, dtype=torch.float16, device="cuda")))
+    flags = torch.zeros(len(groups), dtype=torch.int32, device="cuda")
+    flush = torch.empty(flush_mib << 20, dtype=torch.uint8, device="cuda")
+    kinds = {
+        "pack": (4, lambda g, gi: fg.grad_group_pack([srcs[j] for j in g["mem"]],
+                                                    g["off"], g["g16"])),
+        "unscale": (6, lambda g, gi: fg.grad_unscale_check(
+            g["g16"], 1.0 / synth.LOSS_SCALE, g["g32"], flags[gi:gi + 1])),
+        "unpack": (8, lambda g, gi: fg.grad_group_unpack(
+            g["g32"], [masters[j] for j in g["mem"]], g["off"])),
+        "copy_ceiling": (4, lambda g, gi: g["cpy"].copy_(g["g16"])),
+    }
+    flush.fill_(1)
+
+    def evict():
+        # read (not write) the flush buffer: the caches then hold clean
+        # lines of it, and the timed launches pay no write-back of them
+        flush.max()
+
+    ev = {k: [[] for _ in groups] for k in kinds}
+    batch = {k: [] for k in kinds}
+    torch.cuda.synchronize()
+    for r in range(warmup + reps):
+        # all nine groups back to back after one eviction (no byte is read
+        # twice within a batch): one event pair per kernel kind
+        for k, (_, fn) in kinds.items():
+            evict()
+            e0, e1 = _ev(), _ev()
+            e0.record()
+            for gi, g in enumerate(groups):
+                fn(g, gi)
+            e1.record()
+            if r >= warmup:
+                batch[k].append((e0, e1))
+        # each group alone after its own eviction
+        for gi, g in enumerate(groups):
+            for k, (_, fn) in kinds.items():
+                evict()
+                e0, e1 = _ev(), _ev()
+                e0.record()
+                fn(g, gi)
+                e1.record()
+                if r >= warmup:
+                    ev[k][gi].append((e0, e1))
+    torch.cuda.synchronize()
+    out = {"method": f"standalone; before each timed batch or launch {flush_mib} MiB "
+                     f"are read, evicting the Infinity Cache (256 MB) and the L2s; "
+                     f"<kernel>_GBps: the nine groups' launches back to back between "
+                     f"one pair of HIP events, median of {reps} reps after {warmup} "
+                     f"warm-up; per_group: each launch alone between its own events "
+                     f"(event overhead included)",
+           "reps": reps, "flush_MiB": flush_mib, "per_group": []}
+    for k, (bpe, _) in kinds.items():
+        ts = sorted(e0.elapsed_time(e1) * 1e-3 for e0, e1 in batch[k])
+        nbytes = bpe * sum(g["numel"] for g in groups)
+        out[f"{k}_GBps"] = round(nbytes / ts[len(ts) // 2] / 1e9, 1)
+        out[f"{k}_GBps_best"] = round(nbytes / ts[0] / 1e9, 1)
+        out[f"{k}_us"] = round(ts[len(ts) // 2] * 1e6, 2)
+    for gi, g in enumerate(groups):
+        row = {"group": gi, "numel": g["numel"]}
+        for k, (bpe, _) in kinds.items():
+            ts = sorted(e0.elapsed_time(e1) * 1e-3 for e0, e1 in ev[k][gi])
+            med, best = ts[len(ts) // 2], ts[0]
+            nbytes = bpe * g["numel"]
+            row[k] = {"median_GBps": round(nbytes / med / 1e9, 1),
+                      "best_GBps": round(nbytes / best / 1e9, 1),
+                      "median_us": round(med * 1e6, 2)}
+        out["per_group"].append(row)
+    out["pack_frac_hbm"] = round(out["pack_GBps"] / HBM_PEAK_GBPS, 4)
+    out["unscale_frac_hbm"] = round(out["unscale_GBps"] / HBM_PEAK_GBPS, 4)
+    out["bytes_per_element"] = {"pack": 4, "unscale": 6, "unpack": 8, "copy_ceiling": 4}
+    return out
+
+
+def _pass_bytes(L):
+    """Minimum HBM bytes of the three passes of a layer (inputs read once,
+    output written once, a ReLU-gradient gate read once), fp16."""
+    nx, ny, nw = (int(np.prod(L.x_shape)), int(np.prod(L.y_shape)), L.w_numel)
+    return [2 * (nx + nw + ny), 2 * (ny + nw + nx), 2 * (nx + ny + nw)]
+
+
+def small_configs_bench(steps=50, warmup=5):
+    """The single conv, the encoder block and the decoder block (fwd + full
+    bwd, one stream), timed with HIP events around each whole pass; each
+    against its own roofline: the sum over its ops of max(flops / MFMA
+    peak, minimum bytes / HBM peak)."""
+    import torch
+
+    import synth
+    from paper_1909_11150_amd.fcn import Chain
+    res = []
+    for wl in (synth.single_conv(), synth.encoder_block(), synth.decoder_block()):
+        ch = Chain(wl.layers, wl.weights, wl.x)
+        ch.set_output_grad(wl.dy)
+        flops = sum(3 * L.flops for L in wl.layers)
+        roof = 0.0
+        for L in wl.layers:
+            for b in _pass_bytes(L):
+                roof += max(L.flops / (MFMA_F16_PEAK_TFLOPS * 1e12), b / (HBM_PEAK_GBPS * 1e9))
+        for _ in range(warmup):
+            ch.forward()
+            ch.backward()
+        evs = [(_ev(), _ev()) for _ in range(steps)]
+        for e0, e1 in evs:
+            e0.record()
+            ch.forward()
+            ch.backward()
+            e1.record()
+        torch.cuda.synchronize()
+        ts = sorted(e0.elapsed_time(e1) * 1e-3 for e0, e1 in evs)
+        med = ts[len(ts) // 2]
+        res.append({"config": wl.name, "gflop": round(flops / 1e9, 3),
+                    "median_us": round(med * 1e6, 2), "best_us": round(ts[0] * 1e6, 2),
+                    "tflops": round(flops / med / 1e12, 1),
+                    "roofline_us": round(roof * 1e6, 2),
+                    "frac_of_roofline": round(roof / med, 4)})
+        del ch
+    return res
+
+
 def main():
     args = parse()
     if args.summarize_stats:
@@ -335,6 +602,9 @@ def main():
         return
     if args.summarize_pmc:
         summarize_pmc(args.summarize_pmc)
+        return
+    if args.summarize_mfma:
+        summarize_mfma(args.summarize_mfma)
         return
     if args.summarize_trace:
         summarize_trace(args.summarize_trace[0], args.summarize_trace[1],
@@ -352,6 +622,10 @@ def main():
     import synth
     from paper_1909_11150_amd.fcn import AdamLARS, Chain, LossScaler
 
+    if args.grad_path_only:
+        print(json.dumps(grad_path_bench(args.grad_reps)), flush=True)
+        return
+    clocks_start = gpu_clocks() if not args.no_clocks else None
     if args.workload == "densenet":
         from paper_1909_11150_amd.densenet import DenseNet
         if args.optimizer or args.zero_copy:
@@ -376,42 +650,50 @@ def main():
     prog = ch.program(target, streams=1)
     calls = prog.calls
     torch.cuda.synchronize()
-
-    def ev():
-        return torch.cuda.Event(enable_timing=True)
+    conv = lambda k: k.startswith(("data_conv", "wgrad", "head_fwd", "head_bwd",
+                                   "head_wgrad"))
 
     for _ in range(args.warmup):
         prog.run()
     torch.cuda.synchronize()
 
-    # detail pass (untimed for `value`): events around every call
+    # detail pass (untimed for `value`): events around every call, and the
+    # library's events around every convolution call's main kernel
     det_steps = 2
-    det = [{i: (ev(), ev()) for i, c in enumerate(calls) if c.fn is not None}
+    det = [{i: (_ev(), _ev()) for i, c in enumerate(calls) if c.fn is not None}
            for _ in range(det_steps)]
-    for s_ev in det:
+    kdet = [{i: (_ev(), _ev()) for i, c in enumerate(calls) if conv(c.kernel)}
+            for _ in range(det_steps)]
+    for s_ev in det:           # call durations (events around each call)
         prog.run(s_ev)
+    for k_ev in kdet:          # main-kernel durations (the library's events)
+        prog.run(kernel_events=k_ev)
     torch.cuda.synchronize()
+    # per kernel: launches, call ms, work, main-kernel ms (per step)
     per_kernel, per_op = {}, {}
-    for s_ev in det:
+    for s_ev, k_ev in zip(det, kdet):
         for i, (e0, e1) in s_ev.items():
             c = calls[i]
             t = e0.elapsed_time(e1) / det_steps
-            k = per_kernel.setdefault(c.kernel, [0, 0.0, 0.0, c.single])
+            tk = k_ev[i][0].elapsed_time(k_ev[i][1]) / det_steps if i in k_ev else t
+            k = per_kernel.setdefault(c.kernel, [0, 0.0, 0.0, 0.0])
             k[0] += 1.0 / det_steps
             k[1] += t
             k[2] += c.work / det_steps
-            k[3] = k[3] and c.single
-            o = per_op.setdefault(c.label, [0.0, c.work, c.kernel])
+            k[3] += tk
+            o = per_op.setdefault(c.label, [0.0, c.work, c.kernel, 0.0])
             o[0] += t
-    # dominant kernel: the single-launch MFMA conv kernel with the most time
-    dom = max((k for k, v in per_kernel.items()
-               if v[3] and k.startswith(("data_conv", "wgrad"))),
-              key=lambda k: per_kernel[k][1])
+            o[3] += tk
+    # dominant kernel: the MFMA convolution kernel with the most main-kernel
+    # time per step (split variants included: the library's events exclude
+    # their reduction launch)
+    dom = max((k for k in per_kernel if k.startswith(("data_conv", "wgrad"))),
+              key=lambda k: per_kernel[k][3])
 
     # the timed program: with 3 streams, kernel gradients and the gradient
-    # path run beside the input-gradient chain, so a backward launch of the
-    # dominant kernel may share the GPU and its measured duration includes
-    # that sharing; `roofline_alone` gives the same kernel's launches in the
+    # path run beside the input-gradient chain, so a launch of the dominant
+    # kernel may share the GPU and its measured duration includes that
+    # sharing; `roofline_alone` gives the same kernel's launches in the
     # one-stream detail pass above
     prog = ch.program(target, streams=args.streams)
     calls = prog.calls
@@ -420,9 +702,14 @@ def main():
         prog.run()
     torch.cuda.synchronize()
 
-    # timed pass: K whole steps; events only around the dominant kernel
-    dom_ev = [{i: (ev(), ev()) for i in dom_idx} for _ in range(args.steps)]
-    e_start, e_end = ev(), ev()
+    # timed pass: K whole steps; the library's events only around the
+    # dominant kernel's launches
+    dom_ev = [{i: (_ev(), _ev()) for i in dom_idx} for _ in range(args.steps)]
+    for s_ev in dom_ev:          # create the events before the timed region
+        for e0, e1 in s_ev.values():
+            e0.record()
+            e1.record()
+    e_start, e_end = _ev(), _ev()
     torch.cuda.synchronize()
     if args.optimizer:
         ch.observe()
@@ -430,7 +717,7 @@ def main():
     t0 = time.perf_counter()
     e_start.record()
     for s_ev in dom_ev:
-        prog.run(s_ev)
+        prog.run(kernel_events=s_ev)
     prog.join()
     e_end.record()
     torch.cuda.synchronize()
@@ -448,18 +735,24 @@ def main():
             "peak": MFMA_F16_PEAK_TFLOPS, "unit": "TFLOP/s",
             "frac": round(achieved / MFMA_F16_PEAK_TFLOPS, 4),
             "avg_launch_us": round(avg_s * 1e6, 2), "launches_per_step": len(dom_idx),
+            "flop_per_launch": round(f_dom / n_dom),
+            "measured": "HIP events the library records around each launch of the "
+                        "kernel (fg_profile_next_launch) inside the timed region, on "
+                        "the stream it runs on; a split reduction launched after it "
+                        "is not included",
             "traffic": recorded_traffic(dom, args.workload)}
     v = per_kernel[dom]
-    alone_s = v[1] / v[0] * 1e-3
+    alone_s = v[3] / v[0] * 1e-3
     alone = v[2] / v[0] / alone_s / 1e12
     roof_alone = {"kernel": dom, "achieved": round(alone, 2), "unit": "TFLOP/s",
                   "frac": round(alone / MFMA_F16_PEAK_TFLOPS, 4),
                   "avg_launch_us": round(alone_s * 1e6, 2),
-                  "measured": "HIP events around each launch in the one-stream "
-                              "detail pass of this run (no other kernel running)"}
-    conv_ms = sum(v[1] for k, v in per_kernel.items()
-                  if k.startswith(("data_conv", "wgrad", "head_fwd", "head_bwd",
-                                   "head_wgrad")))
+                  "measured": "the library's events around each launch in the "
+                              "one-stream detail pass of this run (no other kernel "
+                              "running)"}
+    conv_ms = sum(v[1] for k, v in per_kernel.items() if conv(k))
+    conv_main_ms = sum(v[3] for k, v in per_kernel.items() if conv(k))
+    _, peak_rate = paper_rates(flops_step / 3, ms_step * 1e-3, conv_ms * 1e-3)
 
     def bw(name):
         v = per_kernel.get(name)
@@ -483,10 +776,15 @@ def main():
                    "streams": args.streams, "zero_copy_groups": args.zero_copy,
                    "optimizer": "lars_adam" if args.optimizer else None},
         "mfma_peak_frac": round(value / MFMA_F16_PEAK_TFLOPS, 4),
-        "conv_kernels_tflops": round(flops_step / (conv_ms * 1e-3) / 1e12, 2),
-        "grad_pack_GBps": bw("copy_pieces_kernel<2>"),
-        "grad_unscale_GBps": bw("unscale_vec_kernel"),
-        "grad_unpack_GBps": bw("copy_pieces_kernel<4>"),
+        "conv_kernels_tflops": round(peak_rate / 1e12, 2),
+        "conv_main_kernels_tflops": round(flops_step / (conv_main_ms * 1e-3) / 1e12, 2),
+        "conv_rates_measured": "conv_kernels_tflops: step flops over the summed durations "
+                               "of the convolution calls (split reductions included) in "
+                               "the one-stream detail pass; conv_main_kernels_tflops: over "
+                               "the summed main-kernel durations (no split reductions)",
+        "grad_pack_GBps_in_step": bw("copy_pieces_kernel<2>"),
+        "grad_unscale_GBps_in_step": bw("unscale_vec_kernel"),
+        "grad_unpack_GBps_in_step": bw("copy_pieces_kernel<4>"),
         "wall_s_timed": round(wall, 3),
         "roofline": roof,
         "roofline_alone": roof_alone,
@@ -508,14 +806,32 @@ def main():
             "loss_scale_start": scale0, "loss_scale_end": ch.loss_scale}
     if args.detail:
         det = {"per_kernel": {k: {"launches_per_step": v[0], "ms_per_step": v[1],
-                                  "work_per_step": v[2], "single_launch": v[3]}
+                                  "work_per_step": v[2], "main_kernel_ms_per_step": v[3]}
                               for k, v in per_kernel.items()},
-               "per_op": {k: {"ms": v[0], "rate": v[1] / (v[0] * 1e-3) / 1e12,
+               "per_op": {k: {"ms": v[0], "main_kernel_ms": v[3],
+                              "rate": v[1] / (v[3] * 1e-3) / 1e12,
                               "kernel": v[2]} for k, v in per_op.items()}}
         with open(args.detail, "w") as f:
             json.dump(det, f, indent=1)
+    del prog, ch
+    torch.cuda.empty_cache()
+    if args.workload == "fcn" and not args.no_extras:
+        # the gradient path alone, caches flushed (the grad-pack GB/s of the
+        # metric), and the three small configurations against their rooflines
+        gp = grad_path_bench(args.grad_reps)
+        out["grad_pack_GBps"] = gp["pack_GBps"]
+        out["grad_unscale_GBps"] = gp["unscale_GBps"]
+        out["grad_unpack_GBps"] = gp["unpack_GBps"]
+        out["grad_path"] = gp
+        out["small_configs"] = small_configs_bench()
+    if not args.no_clocks:
+        out["clocks"] = {"start": clocks_start, "end": gpu_clocks()}
     if not args.no_cpu:
-        out["cpu_baseline"] = cpu_baseline(layers, args.cpu_seconds)
+        cb = cpu_baseline(layers, args.cpu_seconds)
+        cb["cpu_model"] = cpu_model()
+        if args.workload == "fcn":
+            cb["grad_path"] = cpu_grad_baseline(args.cpu_seconds / 4)
+        out["cpu_baseline"] = cb
     print(json.dumps(out), flush=True)
 
 

@@ -31,14 +31,19 @@
  *     P = (H + 2*pad_h - R)/stride_h + 1 (floor), likewise Q.
  *   - Every device pointer (x, w, y, gate, ws, group buffers, flags, segment
  *     targets) is owned by the caller. The library never allocates or frees
- *     device memory and keeps no state between calls.
+ *     device memory and keeps no device state. Its host state is two small
+ *     records: the optimizer's per-workspace record of which layers have
+ *     norms and which are applied in the current step (lars_adam_norms /
+ *     lars_adam_apply, under a mutex), and the one-shot profiling events of
+ *     fg_profile_next_launch (per host thread).
  *   - GPU work is enqueued on `stream` (0 = the null stream) and the call
  *     returns without synchronising; results are valid once the caller has
  *     synchronised the stream. Device faults surface at that synchronisation.
  *   - Arguments are validated on the host before any HIP call:
  *       FG_EINVAL        null pointer, non-positive size, empty output,
  *                        gate missing for FG_EPI_GATE, an output aliasing an
- *                        input, an unknown enum value;
+ *                        input, a gate overlapping the output other than
+ *                        being the output itself, an unknown enum value;
  *       FG_EUNSUPPORTED  a valid shape outside what the kernels implement
  *                        (listed per call);
  *       FG_EWORKSPACE    ws_bytes below fg_conv_workspace_bytes();
@@ -215,6 +220,13 @@ fg_status grad_unscale_check(const uint16_t *group, uint64_t numel,
                              float inv_scale, float *out_f32,
                              int32_t *found_nonfinite, hipStream_t stream);
 
+/* Clears n device int32 non-finite flags (flags[0..n) = 0) with a kernel on
+ * `stream` (no memset node, so the call may sit in a captured graph). The
+ * flags grad_unscale_check and conv2d_bwd_weight_checked raise are only
+ * ever set, so a step clears them before its first check. FG_EINVAL for a
+ * null pointer or n < 1. */
+fg_status grad_flags_clear(int32_t *flags, int32_t n, hipStream_t stream);
+
 /* Fusion-buffer copy-out: dst[j] = group_f32[seg.offset + j] (bit copy) for
  * every segment; seg.ptr is the fp32 destination. Same segment rules as
  * grad_group_pack (group_numel bounds the offsets). */
@@ -237,6 +249,49 @@ fg_status relu_backward(const uint16_t *dy, const uint16_t *act,
                         uint64_t numel, uint16_t *out, hipStream_t stream);
 
 /* ---- host-only helpers (no device access) ------------------------------- */
+
+/* Backoff loss scaling (Section 6.2, Model Implementation: the loss is
+ * scaled before the gradient computation, adaptively). A step whose
+ * gradients hold a non-finite value is not applied and halves the scale
+ * (not below s_min), restarting the count of clean steps; after `interval`
+ * clean steps in a row the scale doubles (not above s_max). Powers of two
+ * keep scaling and unscaling exact. */
+typedef struct {
+    double scale;      /* the loss scale S of the next step */
+    int32_t clean;     /* clean steps since the last change of S */
+    int32_t interval;  /* clean steps before S doubles (>= 1) */
+    double s_min, s_max;
+} fg_loss_scale;
+
+/* Records one step's outcome in *s (found_nonfinite: the step's flags, any
+ * non-zero) and sets *applied to 1 if the step's update applies, else 0.
+ * FG_EINVAL for null pointers, interval < 1, or a state outside
+ * 0 < s_min <= scale <= s_max (nothing is changed then). */
+fg_status fg_loss_scale_update(fg_loss_scale *s, int32_t found_nonfinite,
+                               int32_t *applied);
+
+/* Learning rate per applied step (Section 6.2: a linear warm-up of the rate
+ * from base to about N times base for N ranks, then a staircase decay):
+ * lr(k) = base + (peak - base) * k / warmup for k < warmup, else
+ * peak * rate^floor((k - warmup) / every) (every = 0: no decay). k counts
+ * applied updates from 0. FG_EINVAL for null pointers, k < 0, negative
+ * base, peak, warmup or every, or a rate not in (0, +inf). */
+typedef struct {
+    double base, peak;
+    int64_t warmup, every;
+    double rate;
+} fg_lr_schedule;
+
+fg_status fg_lr_at(const fg_lr_schedule *s, int64_t k, double *lr);
+
+/* Profiling: the next convolution call (conv2d_fwd, conv2d_bwd_data,
+ * conv2d_bwd_weight[_checked], conv_transpose2d_fwd) made on this host
+ * thread records `start` on its stream just before its main kernel and
+ * `stop` just after it, so that the main kernel's duration can be read with
+ * hipEventElapsedTime apart from a split reduction launched after it. The
+ * events are then forgotten; calls that fail validation leave them armed.
+ * Either may be null (disarms). The caller owns the events. */
+fg_status fg_profile_next_launch(hipEvent_t start, hipEvent_t stop);
 
 /* Workspace in bytes that the given pass needs for this shape (0 if none). */
 size_t fg_conv_workspace_bytes(const fg_conv_desc *d, int op);

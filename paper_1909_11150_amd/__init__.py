@@ -28,6 +28,7 @@ ENTRY_POINTS = (
     "lars_adam_update", "lars_adam_norms", "lars_adam_apply",
     "fg_lars_adam_workspace_bytes",
     "huber_head_grad", "avg_pool2d_fwd", "avg_pool2d_bwd", "channel_slice_copy",
+    "grad_flags_clear", "fg_loss_scale_update", "fg_lr_at", "fg_profile_next_launch",
 )
 
 
@@ -43,6 +44,20 @@ class OptParams(ctypes.Structure):
     _fields_ = [("lr", ctypes.c_float), ("beta1", ctypes.c_float),
                 ("beta2", ctypes.c_float), ("eps", ctypes.c_float),
                 ("weight_decay", ctypes.c_float)]
+
+
+class LossScaleState(ctypes.Structure):
+    """fg_loss_scale: backoff loss-scale state."""
+    _fields_ = [("scale", ctypes.c_double), ("clean", ctypes.c_int32),
+                ("interval", ctypes.c_int32), ("s_min", ctypes.c_double),
+                ("s_max", ctypes.c_double)]
+
+
+class LRScheduleParams(ctypes.Structure):
+    """fg_lr_schedule."""
+    _fields_ = [("base", ctypes.c_double), ("peak", ctypes.c_double),
+                ("warmup", ctypes.c_int64), ("every", ctypes.c_int64),
+                ("rate", ctypes.c_double)]
 
 
 class LibraryNotBuilt(RuntimeError):
@@ -100,6 +115,11 @@ def lib():
         "grad_group_unpack": [vp, u64, pseg, i32, vp],
         "l2_head_grad": [vp, vp, u64, ctypes.c_double, vp, vp],
         "relu_backward": [vp, vp, u64, vp, vp],
+        "grad_flags_clear": [vp, i32, vp],
+        "fg_loss_scale_update": [ctypes.POINTER(LossScaleState), i32, ctypes.POINTER(i32)],
+        "fg_lr_at": [ctypes.POINTER(LRScheduleParams), ctypes.c_int64,
+                     ctypes.POINTER(ctypes.c_double)],
+        "fg_profile_next_launch": [vp, vp],
         "huber_head_grad": [vp, vp, u64, ctypes.c_double, ctypes.c_double, vp, vp],
         "avg_pool2d_fwd": [vp, i32, i32, i32, i32, vp, vp],
         "avg_pool2d_bwd": [vp, vp, i32, i32, i32, i32, vp, vp],
@@ -340,6 +360,38 @@ def channel_slice_copy(src, src_ld, dst, dst_ld, npix, nch, gate=None, gate_ld=0
     _check("channel_slice_copy", lib().channel_slice_copy(
         a(src), src_ld, a(gate), gate_ld, a(dst), dst_ld, npix, nch, int(accumulate),
         _s(stream)))
+
+
+def grad_flags_clear(flags, stream=None):
+    """Zero a device int32 tensor of non-finite flags with a library kernel."""
+    _check("grad_flags_clear", lib().grad_flags_clear(_p(flags), flags.numel(),
+                                                      _s(stream)))
+
+
+def profile_next_launch(start, stop):
+    """Arm two torch.cuda.Events (timing enabled) around the main kernel of
+    the next convolution call on this thread; None, None disarms."""
+    for e in (start, stop):  # torch creates an event at its first record
+        if e is not None and not e.cuda_event:
+            e.record()
+    a = None if start is None else start.cuda_event
+    b = None if stop is None else stop.cuda_event
+    _check("fg_profile_next_launch", lib().fg_profile_next_launch(a, b))
+
+
+def loss_scale_update(state, found_nonfinite):
+    """Advance a LossScaleState by one step's outcome; True if it applies."""
+    applied = ctypes.c_int32()
+    _check("fg_loss_scale_update", lib().fg_loss_scale_update(
+        ctypes.byref(state), int(bool(found_nonfinite)), ctypes.byref(applied)))
+    return bool(applied.value)
+
+
+def lr_at(params, k):
+    """Learning rate of applied step k under an LRScheduleParams."""
+    out = ctypes.c_double()
+    _check("fg_lr_at", lib().fg_lr_at(ctypes.byref(params), int(k), ctypes.byref(out)))
+    return out.value
 
 
 def relu_backward(dy, act, out, stream=None):

@@ -64,6 +64,14 @@ bool overlap(const void *a, size_t na, const void *b, size_t nb) {
   return x < y + nb && y < x + na;
 }
 
+// A ReLU-gradient gate has the output's layout and is read at each output
+// element by the thread that then writes that element: it may be the output
+// itself, but no other overlap (another workgroup could overwrite a gate
+// value before it is read).
+bool gate_ok(const void *gate, const void *out, size_t span) {
+  return gate == nullptr || gate == out || !overlap(gate, span, out, span);
+}
+
 bool sizes_ok(int64_t a, int64_t b, int64_t c) {
   return a < kMaxElems && b < kMaxElems && c < kMaxElems;
 }
@@ -370,6 +378,7 @@ fg_status conv2d_fwd(const fg_conv_desc *d, const uint16_t *x,
   if (slices_overlap(x, npx, ldx, d->c, y, npy, ldy, d->k) ||
       overlap(y, sy, w_krsc, nw * 2))
     return FG_EINVAL;
+  if (epi == FG_EPI_GATE && !gate_ok(gate, y, sy)) return FG_EINVAL;
   if ((st = check_conv_support(d)) != FG_OK) return st;
   // one input step per output position for both image axes
   if (d->stride_h != d->stride_w) return FG_EUNSUPPORTED;
@@ -414,6 +423,7 @@ fg_status conv2d_bwd_data(const fg_conv_desc *d, const uint16_t *dy,
   const size_t sx = span_bytes(npx, ld_or(d->x_ld, d->c), d->c);
   if (overlap(dx, sx, dy, ny * 2) || overlap(dx, sx, w_krsc, nw * 2))
     return FG_EINVAL;
+  if (epi == FG_EPI_GATE && !gate_ok(gate, dx, sx)) return FG_EINVAL;
   if ((st = check_conv_support(d)) != FG_OK) return st;
   if (d->stride_h != d->stride_w || d->stride_h > 2) return FG_EUNSUPPORTED;
 
@@ -456,6 +466,7 @@ fg_status conv_transpose2d_fwd(const fg_conv_desc *d, const uint16_t *x,
   const size_t sy = span_bytes(npy, ld_or(d->y_ld, d->k), d->k);
   if (overlap(y, sy, x, nx * 2) || overlap(y, sy, w_crsk, nw * 2))
     return FG_EINVAL;
+  if (epi == FG_EPI_GATE && !gate_ok(gate, y, sy)) return FG_EINVAL;
   if (!convt_supported(d)) return FG_EUNSUPPORTED;
   if ((st = check_ws(d, FG_OP_CONVT, ws, ws_bytes, x, nx * 2, w_crsk, nw * 2, y,
                      sy, gate, sy)) != FG_OK)
@@ -590,6 +601,11 @@ fg_status grad_group_unpack(const float *group_f32, uint64_t group_numel,
                 group_numel * 4))
       return FG_EINVAL;
   return launch_status(launch_unpack(group_f32, segs, nseg, stream));
+}
+
+fg_status grad_flags_clear(int32_t *flags, int32_t n, hipStream_t stream) {
+  if (!flags || n < 1) return FG_EINVAL;
+  return launch_status(launch_flags_clear(flags, n, stream));
 }
 
 fg_status grad_unscale_check(const uint16_t *group, uint64_t numel,
@@ -907,4 +923,68 @@ fg_status grad_group_plan(const uint64_t *numel, int32_t ntensors,
   return FG_OK;
 }
 
+// ---------------------------------------------------------------------------
+// Backoff loss scale and learning-rate schedule (host only).
+fg_status fg_loss_scale_update(fg_loss_scale *s, int32_t found_nonfinite,
+                               int32_t *applied) {
+  if (!s || !applied || s->interval < 1 || s->clean < 0 ||
+      !(s->s_min > 0.0 && s->s_min <= s->scale && s->scale <= s->s_max) ||
+      !std::isfinite(s->s_max))
+    return FG_EINVAL;
+  if (found_nonfinite) {
+    s->scale = std::max(s->scale * 0.5, s->s_min);
+    s->clean = 0;
+    *applied = 0;
+    return FG_OK;
+  }
+  s->clean += 1;
+  if (s->clean >= s->interval) {
+    s->scale = std::min(s->scale * 2.0, s->s_max);
+    s->clean = 0;
+  }
+  *applied = 1;
+  return FG_OK;
+}
+
+fg_status fg_lr_at(const fg_lr_schedule *s, int64_t k, double *lr) {
+  if (!s || !lr || k < 0 || !(s->base >= 0.0) || !(s->peak >= 0.0) ||
+      s->warmup < 0 || s->every < 0 || !(s->rate > 0.0) || !std::isfinite(s->rate) ||
+      !std::isfinite(s->base) || !std::isfinite(s->peak))
+    return FG_EINVAL;
+  if (k < s->warmup) {
+    *lr = s->base + (s->peak - s->base) * (double)k / (double)s->warmup;
+    return FG_OK;
+  }
+  const int64_t steps = s->every ? (k - s->warmup) / s->every : 0;
+  *lr = s->peak * std::pow(s->rate, (double)steps);
+  return FG_OK;
+}
+
+// One-shot profiling events, per host thread (see prof_begin / prof_end).
+static thread_local hipEvent_t g_prof_start = nullptr;
+static thread_local hipEvent_t g_prof_stop = nullptr;
+
+fg_status fg_profile_next_launch(hipEvent_t start, hipEvent_t stop) {
+  if (!start || !stop) {
+    g_prof_start = g_prof_stop = nullptr;
+    return FG_OK;
+  }
+  g_prof_start = start;
+  g_prof_stop = stop;
+  return FG_OK;
+}
+
 }  // extern "C"
+
+namespace fg {
+hipError_t prof_begin(hipStream_t st) {
+  return g_prof_start ? hipEventRecord(g_prof_start, st) : hipSuccess;
+}
+
+hipError_t prof_end(hipStream_t st) {
+  if (!g_prof_start) return hipSuccess;
+  const hipError_t e = hipEventRecord(g_prof_stop, st);
+  g_prof_start = g_prof_stop = nullptr;
+  return e;
+}
+}  // namespace fg

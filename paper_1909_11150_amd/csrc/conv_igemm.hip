@@ -813,12 +813,14 @@ hipError_t launch_data_conv(const DataConvArgs &a0, bool w_kmajor,
   DataConvArgs a = a0;
   const DataPlan pl = plan_data_conv(a);
   a.nsplit = pl.nsplit;
-  hipError_t e =
-      !pl.big ? (data_dma_ok(a) ? launch_data_conv_dma_small(a, w_kmajor, st)
+  hipError_t e = prof_begin(st);
+  if (e != hipSuccess) return e;
+  e = !pl.big ? (data_dma_ok(a) ? launch_data_conv_dma_small(a, w_kmajor, st)
                                 : launch_dc_tile<SmallCfg>(a, w_kmajor, st))
       : data_halo_ok(a) ? launch_data_conv_halo(a, w_kmajor, st)
       : data_dma_ok(a)  ? launch_data_conv_dma(a, w_kmajor, st)
                         : launch_dc_tile<BigCfg>(a, w_kmajor, st);
+  if (e == hipSuccess) e = prof_end(st);
   if (e != hipSuccess || a.nsplit == 1) return e;
   const int64_t len = (int64_t)a.n * a.ho * a.wo * a.co;
   hipLaunchKernelGGL(split_epilogue_kernel,
@@ -916,9 +918,10 @@ WgradPlan plan_wgrad(const fg_conv_desc &d, int32_t p, int32_t q) {
 hipError_t launch_wgrad(const WgradArgs &a, bool big, hipStream_t st) {
   const int rsc = a.r * a.s * a.c;
   const bool split = a.nsplit > 1;
+  hipError_t e = prof_begin(st);
+  if (e != hipSuccess) return e;
   if (big && wgrad_dma_ok(a)) {
-    hipError_t e = launch_wgrad_dma(a, st);
-    if (e != hipSuccess || !split) return e;
+    e = launch_wgrad_dma(a, st);
   } else if (big) {
     dim3 grid((rsc + 255) / 256, (a.k + 255) / 256, a.nsplit);
     if (split)
@@ -927,6 +930,7 @@ hipError_t launch_wgrad(const WgradArgs &a, bool big, hipStream_t st) {
     else
       hipLaunchKernelGGL((wgrad_kernel<BigCfg, false>), grid, dim3(BigCfg::NT), 0,
                          st, a);
+    e = hipGetLastError();
   } else {
     dim3 grid((rsc + 127) / 128, (a.k + 127) / 128, a.nsplit);
     if (split)
@@ -935,9 +939,10 @@ hipError_t launch_wgrad(const WgradArgs &a, bool big, hipStream_t st) {
     else
       hipLaunchKernelGGL((wgrad_kernel<SmallCfg, false>), grid,
                          dim3(SmallCfg::NT), 0, st, a);
+    e = hipGetLastError();
   }
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || a.nsplit == 1) return e;
+  if (e == hipSuccess) e = prof_end(st);
+  if (e != hipSuccess || !split) return e;
   const int64_t len = (int64_t)a.k * rsc;
   dim3 g2((unsigned)((len / 4 + 255) / 256));
   hipLaunchKernelGGL(split_reduce_kernel, g2, dim3(256), 0, st, a.part,
@@ -961,9 +966,12 @@ hipError_t launch_head_fwd(const uint16_t *x, const uint16_t *w, uint16_t *y,
   int64_t waves = (npix * L + 63) / 64;
   int64_t blocks = (waves + 3) / 4;
   if (blocks > 4096) blocks = 4096;
+  hipError_t e = prof_begin(st);
+  if (e != hipSuccess) return e;
   hipLaunchKernelGGL(head_fwd_kernel, dim3((unsigned)blocks), dim3(256), 0, st,
                      x, w, y, npix, c, L, logL, epi, gate);
-  return hipGetLastError();
+  e = hipGetLastError();
+  return e == hipSuccess ? prof_end(st) : e;
 }
 
 hipError_t launch_head_bwd_data(const uint16_t *dy, const uint16_t *w,
@@ -971,9 +979,12 @@ hipError_t launch_head_bwd_data(const uint16_t *dy, const uint16_t *w,
                                 int32_t epi, const uint16_t *gate,
                                 hipStream_t st) {
   int64_t n = npix * (c / 8);
+  hipError_t e = prof_begin(st);
+  if (e != hipSuccess) return e;
   hipLaunchKernelGGL(head_bwd_data_kernel, dim3((unsigned)((n + 255) / 256)),
                      dim3(256), 0, st, dy, w, dx, npix, c, epi, gate);
-  return hipGetLastError();
+  e = hipGetLastError();
+  return e == hipSuccess ? prof_end(st) : e;
 }
 
 static int64_t head_wgrad_blocks(int64_t npix) {
@@ -993,10 +1004,13 @@ hipError_t launch_head_wgrad(const uint16_t *x, const uint16_t *dy,
                              int32_t *flag, hipStream_t st) {
   int64_t nb = head_wgrad_blocks(npix);
   int64_t chunk = (npix + nb - 1) / nb;
+  hipError_t e = prof_begin(st);
+  if (e != hipSuccess) return e;
   hipLaunchKernelGGL(head_wgrad_kernel, dim3((unsigned)nb),
                      dim3(kHeadWgradThreads), 0, st, x, dy, npix, c, chunk,
                      ws);
-  hipError_t e = hipGetLastError();
+  e = hipGetLastError();
+  if (e == hipSuccess) e = prof_end(st);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(split_reduce_wide_kernel, dim3((unsigned)(c / 4)),
                      dim3(256), 0, st, ws, (int)nb, (int64_t)c, dw, flag);

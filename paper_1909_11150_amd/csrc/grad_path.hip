@@ -37,32 +37,46 @@ __device__ __forceinline__ int find_piece(const PieceTable &t, uint32_t b) {
 }
 
 // Bit copy of ESZ-byte elements (2: fp16 pack, 4: fp32 unpack); a piece with
-// src == 0 is zero filled.
+// src == 0 is zero filled. Every thread issues all of its 16-byte loads
+// (NV of them, 256 threads apart) before its first store, so a workgroup
+// keeps 16 KiB of reads in flight.
 template <int ESZ>
 __global__ __launch_bounds__(kGradThreads) void copy_pieces_kernel(
     PieceTable t) {
   const int pi = find_piece(t, blockIdx.x);
   const Piece pc = t.p[pi];
-  constexpr int EPV = 16 / ESZ;  // elements per 16-byte vector
-  const uint64_t per_block = (uint64_t)kPieceElems;
-  const uint64_t beg = (uint64_t)(blockIdx.x - pc.block0) * per_block;
+  constexpr int EPV = 16 / ESZ;                           // elements per vector
+  constexpr int NV = kPieceElems / (kGradThreads * EPV);  // vectors per thread
+  const uint64_t beg = (uint64_t)(blockIdx.x - pc.block0) * kPieceElems;
   if (beg >= pc.numel) return;
-  const uint64_t end = beg + per_block < pc.numel ? beg + per_block : pc.numel;
+  const uint64_t end =
+      beg + kPieceElems < pc.numel ? beg + kPieceElems : (uint64_t)pc.numel;
   if (((pc.src | pc.dst) & 15) == 0) {
-    const uint64_t nvec_end = end / EPV * EPV;
-    for (uint64_t i = beg + (uint64_t)threadIdx.x * EPV; i < nvec_end;
-         i += (uint64_t)kGradThreads * EPV) {
-      u32x4 v = pc.src ? *reinterpret_cast<const u32x4 *>(pc.src + i * ESZ)
-                       : u32x4{0, 0, 0, 0};
-      *reinterpret_cast<u32x4 *>(pc.dst + i * ESZ) = v;
+    const uint64_t nvec_end = end / EPV * EPV;  // beg is a multiple of EPV
+    u32x4 v[NV];
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+      const uint64_t i =
+          beg + ((uint64_t)j * kGradThreads + threadIdx.x) * EPV;
+      v[j] = u32x4{0, 0, 0, 0};
+      if (pc.src && i < nvec_end)
+        v[j] = *reinterpret_cast<const u32x4 *>(pc.src + i * ESZ);
     }
-    for (uint64_t i = nvec_end + threadIdx.x; i < end; i += kGradThreads) {
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+      const uint64_t i =
+          beg + ((uint64_t)j * kGradThreads + threadIdx.x) * EPV;
+      if (i < nvec_end) *reinterpret_cast<u32x4 *>(pc.dst + i * ESZ) = v[j];
+    }
+    // the last (< EPV) elements of the piece
+    const uint64_t i = nvec_end + threadIdx.x;
+    if (i < end) {
       if (ESZ == 2) {
-        uint16_t v = pc.src ? reinterpret_cast<const uint16_t *>(pc.src)[i] : 0;
-        reinterpret_cast<uint16_t *>(pc.dst)[i] = v;
+        uint16_t e = pc.src ? reinterpret_cast<const uint16_t *>(pc.src)[i] : 0;
+        reinterpret_cast<uint16_t *>(pc.dst)[i] = e;
       } else {
-        uint32_t v = pc.src ? reinterpret_cast<const uint32_t *>(pc.src)[i] : 0;
-        reinterpret_cast<uint32_t *>(pc.dst)[i] = v;
+        uint32_t e = pc.src ? reinterpret_cast<const uint32_t *>(pc.src)[i] : 0;
+        reinterpret_cast<uint32_t *>(pc.dst)[i] = e;
       }
     }
   } else {
@@ -145,20 +159,32 @@ __device__ __forceinline__ bool nonfinite16(uint32_t h) {
   return (h & 0x7C00u) == 0x7C00u;
 }
 
+// Vectors of 8 fp16 values per thread and workgroup: each thread issues its
+// kUnscaleVecs 16-byte loads (256 threads apart) before converting and
+// storing, so a workgroup keeps 16 KiB of reads in flight.
+constexpr int kUnscaleVecs = 4;
+
 __global__ __launch_bounds__(kGradThreads) void unscale_vec_kernel(
     const uint16_t *in, uint64_t nvec, float inv, float *out, int32_t *flag) {
+  const uint64_t base = (uint64_t)blockIdx.x * (kGradThreads * kUnscaleVecs);
+  u32x4 w[kUnscaleVecs];
+#pragma unroll
+  for (int j = 0; j < kUnscaleVecs; ++j) {
+    const uint64_t v = base + (uint64_t)j * kGradThreads + threadIdx.x;
+    w[j] = u32x4{0, 0, 0, 0};
+    if (v < nvec) w[j] = *reinterpret_cast<const u32x4 *>(in + v * 8);
+  }
   bool bad = false;
-  const uint64_t stride = (uint64_t)gridDim.x * kGradThreads;
-  for (uint64_t v = (uint64_t)blockIdx.x * kGradThreads + threadIdx.x;
-       v < nvec; v += stride) {
-    u32x4 w = *reinterpret_cast<const u32x4 *>(in + v * 8);
+#pragma unroll
+  for (int j = 0; j < kUnscaleVecs; ++j) {
+    const uint64_t v = base + (uint64_t)j * kGradThreads + threadIdx.x;
     f32x4 o0, o1;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      uint32_t lo = w[e] & 0xFFFFu, hi = w[e] >> 16;
+      const uint32_t lo = w[j][e] & 0xFFFFu, hi = w[j][e] >> 16;
       bad |= nonfinite16(lo) | nonfinite16(hi);
-      float a = h_to_f32((uint16_t)lo) * inv;
-      float b = h_to_f32((uint16_t)hi) * inv;
+      const float a = h_to_f32((uint16_t)lo) * inv;
+      const float b = h_to_f32((uint16_t)hi) * inv;
       if (e < 2) {
         o0[2 * e] = a;
         o0[2 * e + 1] = b;
@@ -167,12 +193,13 @@ __global__ __launch_bounds__(kGradThreads) void unscale_vec_kernel(
         o1[2 * e - 3] = b;
       }
     }
-    *reinterpret_cast<f32x4 *>(out + v * 8) = o0;
-    *reinterpret_cast<f32x4 *>(out + v * 8 + 4) = o1;
+    if (v < nvec) {
+      *reinterpret_cast<f32x4 *>(out + v * 8) = o0;
+      *reinterpret_cast<f32x4 *>(out + v * 8 + 4) = o1;
+    }
   }
-  // one store per wave that saw a non-finite value
-  if (__ballot(bad) != 0 && (threadIdx.x & 63) == __builtin_ctzll(__ballot(bad)))
-    *flag = 1;
+  // zero words past the end convert to finite values: bad is exact
+  flag_nonfinite(flag, bad);
 }
 
 __global__ __launch_bounds__(kGradThreads) void unscale_scalar_kernel(
@@ -196,8 +223,8 @@ hipError_t launch_unscale(const uint16_t *group, uint64_t numel,
   const bool vec = (((uint64_t)group % 16) == 0) && (((uint64_t)out % 16) == 0);
   uint64_t nvec = vec ? numel / 8 : 0;
   if (nvec) {
-    uint64_t blocks = (nvec + kGradThreads * 4 - 1) / (kGradThreads * 4);
-    if (blocks > 8192) blocks = 8192;
+    const uint64_t per = (uint64_t)kGradThreads * kUnscaleVecs;
+    const uint64_t blocks = (nvec + per - 1) / per;  // < 2^26 for numel < 2^31
     hipLaunchKernelGGL(unscale_vec_kernel, dim3((unsigned)blocks),
                        dim3(kGradThreads), 0, st, group, nvec, inv_scale, out,
                        flag);
@@ -215,6 +242,20 @@ hipError_t launch_unscale(const uint16_t *group, uint64_t numel,
     return hipGetLastError();
   }
   return hipSuccess;
+}
+
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kGradThreads) void flags_clear_kernel(int32_t *f,
+                                                                   int32_t n) {
+  const int32_t i = blockIdx.x * kGradThreads + threadIdx.x;
+  if (i < n) f[i] = 0;
+}
+
+hipError_t launch_flags_clear(int32_t *flags, int32_t n, hipStream_t st) {
+  hipLaunchKernelGGL(flags_clear_kernel,
+                     dim3((unsigned)((n + kGradThreads - 1) / kGradThreads)),
+                     dim3(kGradThreads), 0, st, flags, n);
+  return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------

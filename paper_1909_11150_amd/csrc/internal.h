@@ -146,6 +146,13 @@ hipError_t launch_head_wgrad(const uint16_t *x, const uint16_t *dy,
                              uint16_t *dw, int64_t npix, int32_t c,
                              float *ws, int32_t *flag, hipStream_t st);
 
+// One-shot profiling events (fg_profile_next_launch): prof_begin records the
+// armed start event on the stream, prof_end the stop event, then disarms.
+// Both do nothing when no events are armed.
+hipError_t prof_begin(hipStream_t st);
+hipError_t prof_end(hipStream_t st);
+
+hipError_t launch_flags_clear(int32_t *flags, int32_t n, hipStream_t st);
 hipError_t launch_pack(const fg_segment *segs, int32_t nseg, uint16_t *group,
                        uint64_t group_numel, hipStream_t st);
 hipError_t launch_unscale(const uint16_t *group, uint64_t numel,

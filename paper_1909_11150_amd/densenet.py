@@ -37,7 +37,7 @@ import torch
 
 from . import (EPI_ACC, EPI_NONE, EPI_RELU, OP_BWD_DATA, OP_BWD_WEIGHT, OP_CONVT,
                OP_FWD, ConvDesc, FgError, Segment, grad_group_plan, kernel_name, lib,
-               workspace_bytes)
+               profile_next_launch, workspace_bytes)
 from .fcn import (Call, chain_workspace_bytes, kernel_gradient_workspace_bytes)
 
 F16 = torch.float16
@@ -443,7 +443,8 @@ class _DenseProgram:
         nk = n.per * n.k
         self._inv_scale = ctypes.c_float(1.0 / n.loss_scale)
         if n.groups is not None:     # the step's non-finite flags start clear
-            self._add("flags.zero", "", 0, None, (n.flags.zero_,), False, sid=self._dw_sid)
+            self._add("flags.clear", "flags_clear_kernel", 0, Lb.grad_flags_clear,
+                      (n.flags.data_ptr(), n.flags.numel()), sid=self._dw_sid)
         # ---- forward
         self.conv_fwd("C0", _dense(n.x), n.out["C0"], True)
         ready = (len(self.calls) - 1,)
@@ -515,9 +516,11 @@ class _DenseProgram:
         self._head_args[3].value = s / self.net.act["F1x1"].numel()
         self._inv_scale.value = 1.0 / s
 
-    def run(self, events=None):
+    def run(self, events=None, kernel_events=None):
         """Run the step once. events: {call index: (start, end)} HIP events
-        recorded around those calls on the call's stream."""
+        recorded around those calls on the call's stream; kernel_events: the
+        same for convolution calls, recorded by the library around the call's
+        main kernel only."""
         streams, evs = self.streams, self.events
         for i, c in enumerate(self.calls):
             s = streams[c.sid]
@@ -526,6 +529,9 @@ class _DenseProgram:
             ev = events.get(i) if events else None
             if ev:
                 ev[0].record(s)
+            kev = kernel_events.get(i) if kernel_events else None
+            if kev:
+                profile_next_launch(*kev)
             if c.fn is None:
                 with torch.cuda.stream(s):
                     c.args[0]()

@@ -19,7 +19,9 @@ from collections import namedtuple
 import torch
 
 from . import (EPI_GATE, EPI_NONE, EPI_RELU, OP_BWD_DATA, OP_BWD_WEIGHT,
-               OP_CONVT, OP_FWD, ConvDesc, FgError, OptParams, Segment,
+               OP_CONVT, OP_FWD, ConvDesc, FgError, LossScaleState, LRScheduleParams,
+               OptParams, Segment, grad_flags_clear, loss_scale_update, lr_at,
+               profile_next_launch,
                GRAD_F16_SCALED, GRAD_F32, kernel_name, lib,
                conv2d_bwd_data, conv2d_bwd_weight, conv2d_bwd_weight_checked,
                conv2d_fwd,
@@ -71,37 +73,35 @@ def chain_workspace_bytes(layers):
 
 class LossScaler:
     """Backoff loss scaling (Section 6.2: the loss is scaled before the
-    gradient computation, with OpenSeq2Seq's adaptive strategy). A step whose
-    gradients hold a non-finite value is not applied; it halves the scale
-    (not below s_min) and restarts the count of clean steps. After
-    `interval` clean steps in a row the scale doubles (not above s_max).
-    Powers of two keep scaling and unscaling exact."""
+    gradient computation, with OpenSeq2Seq's adaptive strategy): the state
+    of the library's fg_loss_scale_update. A step whose gradients hold a
+    non-finite value is not applied; it halves the scale (not below s_min)
+    and restarts the count of clean steps. After `interval` clean steps in a
+    row the scale doubles (not above s_max)."""
 
     def __init__(self, scale=2.0 ** 15, interval=2000, s_min=1.0, s_max=2.0 ** 24):
         if interval < 1 or not 0 < s_min <= scale <= s_max:
             raise ValueError("need interval >= 1 and 0 < s_min <= scale <= s_max")
-        self.scale, self.interval = float(scale), int(interval)
-        self.s_min, self.s_max = float(s_min), float(s_max)
-        self.clean = 0
+        self._st = LossScaleState(float(scale), 0, int(interval), float(s_min),
+                                  float(s_max))
+
+    scale = property(lambda self: self._st.scale)
+    clean = property(lambda self: self._st.clean)
+    interval = property(lambda self: self._st.interval)
+    s_min = property(lambda self: self._st.s_min)
+    s_max = property(lambda self: self._st.s_max)
 
     def update(self, found_nonfinite):
         """Record one step's outcome; returns whether its update applied."""
-        if found_nonfinite:
-            self.scale = max(self.scale * 0.5, self.s_min)
-            self.clean = 0
-            return False
-        self.clean += 1
-        if self.clean >= self.interval:
-            self.scale = min(self.scale * 2.0, self.s_max)
-            self.clean = 0
-        return True
+        return loss_scale_update(self._st, found_nonfinite)
 
 
 class LRSchedule:
-    """Learning rate per applied step (Section 6.2): a linear warm-up from
-    `base` to `peak` (the paper's N * base for N ranks) over `warmup` steps,
-    then a staircase decay by `rate` every `every` steps (every = 0: none).
-    The step index counts applied updates from 0."""
+    """Learning rate per applied step (Section 6.2), evaluated by the
+    library's fg_lr_at: a linear warm-up from `base` to `peak` (the paper's
+    N * base for N ranks) over `warmup` steps, then a staircase decay by
+    `rate` every `every` steps (every = 0: none). The step index counts
+    applied updates from 0."""
 
     def __init__(self, base=1e-4, peak=None, warmup=0, every=0, rate=1.0):
         self.base = float(base)
@@ -109,12 +109,11 @@ class LRSchedule:
         self.warmup, self.every, self.rate = int(warmup), int(every), float(rate)
         if self.warmup < 0 or self.every < 0 or self.base < 0 or self.peak < 0:
             raise ValueError("negative schedule parameter")
+        self._p = LRScheduleParams(self.base, self.peak, self.warmup, self.every,
+                                   self.rate)
 
     def __call__(self, k):
-        if k < self.warmup:
-            return self.base + (self.peak - self.base) * k / self.warmup
-        steps = (k - self.warmup) // self.every if self.every else 0
-        return self.peak * self.rate ** steps
+        return lr_at(self._p, k)
 
 
 class AdamLARS:
@@ -167,6 +166,7 @@ class Chain:
         self.ws = torch.empty(max(chain_workspace_bytes(self.layers), 16),
                               dtype=torch.uint8, device=self.dev)
         self.groups = None
+        self.group_cap_bytes = group_cap_bytes
         if group_cap_bytes is not None:
             self._plan_groups(group_cap_bytes, group_align_bytes)
         self._nl = nl
@@ -276,7 +276,7 @@ class Chain:
 
     def backward(self, grad_path=False):
         if self.zero_copy and self.groups is not None:
-            self.flags.zero_()
+            grad_flags_clear(self.flags, stream=self.stream)
         for i in reversed(range(len(self.layers))):
             L = self.layers[i]
             dy = self.g[i + 1]
@@ -467,7 +467,8 @@ class StepProgram:
         # the non-finite flags are raised by the unscale calls (stream 2) and,
         # with zero-copy groups, by the kernel gradients (stream 1); cleared
         # after the head call, which follows the previous step's last reads
-        calls.append(Call("flags.zero", "", 0, None, (ch.flags.zero_,), False,
+        calls.append(Call("flags.clear", "flags_clear_kernel", 0, L_.grad_flags_clear,
+                          (ch.flags.data_ptr(), ch.flags.numel(), st), True,
                           sid=1 if ch.zero_copy else 2, deps=(self._head,)))
         zc = ch.zero_copy
 
@@ -636,9 +637,11 @@ class StepProgram:
         if self.params is not None:
             self.params.lr = ch.opt.lr_at(ch.applied)
 
-    def run(self, events=None):
+    def run(self, events=None, kernel_events=None):
         """Run the step once. events: {call index: (start, end)} HIP events
-        recorded around those calls on the call's stream."""
+        recorded around those calls on the call's stream; kernel_events: the
+        same for convolution calls, recorded by the library around the call's
+        main kernel only (fg_profile_next_launch)."""
         streams, evs = self.streams, self.events
         for i, c in enumerate(self.calls):
             if i == self._head:
@@ -650,6 +653,9 @@ class StepProgram:
             ev = events.get(i) if events else None
             if ev:
                 ev[0].record(s)
+            kev = kernel_events.get(i) if kernel_events else None
+            if kev:
+                profile_next_launch(*kev)
             if c.fn is None:
                 with torch.cuda.stream(s):
                     c.args[0]()

@@ -122,6 +122,21 @@ def _dist(a, b):
     return rel, ratio
 
 
+def chain_report(g16, o16, o64, what):
+    """A chained output against the oracle chain run from the same seeded
+    inputs (O16: fp16 storage at layer boundaries, O64: fp64 throughout).
+    Printed only: per-op differences (last bits, a ReLU decision on a value
+    within an ulp of zero) propagate down a chain, so chains are reported and
+    every op is gated on its own GPU inputs instead."""
+    g = np.asarray(g16, np.float64)
+    assert np.all(np.isfinite(g)), what
+    rel, ratio = _dist(g, o16)
+    rel_n, ratio_n = _dist(o16, o64)
+    print(f"{what} (chain): rel_L2 {rel:.3e} (fp16 storage {rel_n:.3e}), "
+          f"max_abs/RMS {ratio:.3e} (fp16 storage {ratio_n:.3e})")
+    return rel, ratio
+
+
 def chain_parity(g16, o16, o64, t32, what):
     """Chained outputs: rel_L2(GPU, O16) <= max(5e-3, 2 * fp16 noise), the
     noise being the larger of rel_L2(O16, O64) and rel_L2(T32, O16) (t32 may

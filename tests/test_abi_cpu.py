@@ -301,3 +301,44 @@ def test_strided_output_checks(L):
     assert bwd(head(x_ld=24)) == fg.FG_EUNSUPPORTED
     assert fwd(head(x_ld=24)) == fg.FG_EUNSUPPORTED
     assert wgt(head(x_ld=24)) == fg.FG_EUNSUPPORTED
+
+
+def test_gate_must_not_overlap_the_output(L):
+    """A ReLU-gradient gate that partly overlaps the output is refused (a
+    workgroup could overwrite gate values another one has yet to read)."""
+    d = _desc()
+    ref = ctypes.byref
+    x, w, y = FAKE, FAKE + (1 << 20), FAKE + (1 << 22)
+    assert L.conv2d_fwd(ref(d), x, w, y, fg.EPI_GATE, y + 64, None, 0,
+                        None) == fg.FG_EINVAL
+    assert L.conv2d_fwd(ref(d), x, w, y, fg.EPI_GATE, y - 64, None, 0,
+                        None) == fg.FG_EINVAL
+    dy, dx = FAKE, FAKE + (1 << 22)
+    assert L.conv2d_bwd_data(ref(d), dy, w, dx, fg.EPI_GATE, dx + 2, None, 0,
+                             None) == fg.FG_EINVAL
+    t = fg.ConvDesc.make(2, 8, 8, 16, 16, 4, 4, 2, 1)
+    yt = FAKE + (1 << 23)
+    assert L.conv_transpose2d_fwd(ref(t), FAKE, w, yt, fg.EPI_GATE, yt + 128, None,
+                                  0, None) == fg.FG_EINVAL
+
+
+def test_flags_clear_and_host_helpers_validate(L):
+    assert L.grad_flags_clear(None, 4, None) == fg.FG_EINVAL
+    assert L.grad_flags_clear(FAKE, 0, None) == fg.FG_EINVAL
+    # disarming the profiling events needs no device
+    assert L.fg_profile_next_launch(None, None) == fg.FG_OK
+    applied = ctypes.c_int32(7)
+    for bad in (fg.LossScaleState(2.0 ** 15, 0, 0, 1.0, 2.0 ** 24),      # interval
+                fg.LossScaleState(0.5, 0, 10, 1.0, 2.0 ** 24),          # below s_min
+                fg.LossScaleState(2.0 ** 25, 0, 10, 1.0, 2.0 ** 24),    # above s_max
+                fg.LossScaleState(1.0, 0, 10, 0.0, 2.0 ** 24)):         # s_min 0
+        before = bytes(bad)
+        assert L.fg_loss_scale_update(ctypes.byref(bad), 0,
+                                      ctypes.byref(applied)) == fg.FG_EINVAL
+        assert bytes(bad) == before and applied.value == 7
+    out = ctypes.c_double()
+    for bad, k in ((fg.LRScheduleParams(1e-4, 1e-3, 10, 0, 1.0), -1),
+                   (fg.LRScheduleParams(-1e-4, 1e-3, 10, 0, 1.0), 0),
+                   (fg.LRScheduleParams(1e-4, 1e-3, -1, 0, 1.0), 0),
+                   (fg.LRScheduleParams(1e-4, 1e-3, 10, 0, 0.0), 0)):
+        assert L.fg_lr_at(ctypes.byref(bad), k, ctypes.byref(out)) == fg.FG_EINVAL

@@ -192,8 +192,8 @@ def test_dense_program_gradient_groups(no_cuda):
         idx = {c.label: i for i, c in enumerate(calls)}
         side = 1 if streams > 1 else 0
         first_side = min(i for i, c in enumerate(calls) if c.sid == side)
-        assert calls[first_side].label == "flags.zero" or side == 0
-        assert idx["flags.zero"] < min(idx[f"{m}.dW"] for m in net.dw_order())
+        assert calls[first_side].label == "flags.clear" or side == 0
+        assert idx["flags.clear"] < min(idx[f"{m}.dW"] for m in net.dw_order())
         for gi, g in enumerate(net.groups):
             p, u, q = idx[f"G{gi}.pack"], idx[f"G{gi}.unscale"], idx[f"G{gi}.unpack"]
             assert p < u < q and all(calls[j].sid == side for j in (p, u, q))
