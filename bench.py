@@ -477,7 +477,7 @@ def grad_path_bench(reps=20, warmup=3, flush_mib=1024):
                            g32=torch.empty(n, dtype=torch.float32, device="cuda"),
                            cpy=torch.empty(n, dtype=torch.float16, device="cuda")))
     flags = torch.zeros(len(groups), dtype=torch.int32, device="cuda")
-    flush = torch.empty(flush_mib << 20, dtype=torch.uint8, device="cuda")
+    flush = torch.empty(flush_mib << 17, dtype=torch.int64, device="cuda")
     kinds = {
         "pack": (4, lambda g, gi: fg.grad_group_pack([srcs[j] for j in g["mem"]],
                                                     g["off"], g["g16"])),
@@ -543,9 +543,61 @@ def grad_path_bench(reps=20, warmup=3, flush_mib=1024):
                       "best_GBps": round(nbytes / best / 1e9, 1),
                       "median_us": round(med * 1e6, 2)}
         out["per_group"].append(row)
+    out["size_sweep"] = grad_size_sweep(evict, reps)
     out["pack_frac_hbm"] = round(out["pack_GBps"] / HBM_PEAK_GBPS, 4)
     out["unscale_frac_hbm"] = round(out["unscale_GBps"] / HBM_PEAK_GBPS, 4)
     out["bytes_per_element"] = {"pack": 4, "unscale": 6, "unpack": 8, "copy_ceiling": 4}
+    return out
+
+
+def grad_size_sweep(evict, reps, mib=(4, 8, 16, 32, 64, 128, 256)):
+    """Single launches of pack (one member), unscale and the runtime's copy
+    on buffers of 4 to 256 MiB of fp16, each after an eviction, HIP events
+    around each launch; a least-squares fit of the median times from 16 MiB
+    up to t = t0 + bytes / B separates the fixed cost of a launch (t0: the
+    launch, the first accesses' latency, the last wave's tail, and the
+    events) from the streaming rate B."""
+    import torch
+
+    import paper_1909_11150_amd as fg
+    n_max = max(mib) << 19
+    src = torch.randn(n_max, device="cuda").to(torch.float16)
+    dst = torch.empty(n_max, dtype=torch.float16, device="cuda")
+    o32 = torch.empty(n_max, dtype=torch.float32, device="cuda")
+    flag = torch.zeros(1, dtype=torch.int32, device="cuda")
+    kinds = {
+        "pack": (4, lambda n: fg.grad_group_pack([src[:n]], [0], dst[:n])),
+        "unscale": (6, lambda n: fg.grad_unscale_check(dst[:n], 2.0 ** -15, o32[:n], flag)),
+        "copy_ceiling": (4, lambda n: dst[:n].copy_(src[:n])),
+    }
+    evs = {(k, m): [] for k in kinds for m in mib}
+    for r in range(reps + 2):
+        for m in mib:
+            for k, (_, fn) in kinds.items():
+                evict()
+                e0, e1 = _ev(), _ev()
+                e0.record()
+                fn(m << 19)
+                e1.record()
+                if r >= 2:
+                    evs[(k, m)].append((e0, e1))
+    torch.cuda.synchronize()
+    out = {"MiB_fp16": list(mib)}
+    for k, (bpe, _) in kinds.items():
+        med = []
+        for m in mib:
+            ts = sorted(e0.elapsed_time(e1) * 1e-3 for e0, e1 in evs[(k, m)])
+            med.append(ts[len(ts) // 2])
+        nbytes = [bpe * (m << 19) for m in mib]
+        sel = [i for i, m in enumerate(mib) if m >= 16]
+        A = np.array([[1.0, nbytes[i]] for i in sel])
+        t0, inv_b = np.linalg.lstsq(A, np.array([med[i] for i in sel]), rcond=None)[0]
+        out[k] = {"median_us": [round(t * 1e6, 2) for t in med],
+                  "GBps": [round(b / t / 1e9, 1) for b, t in zip(nbytes, med)],
+                  "fixed_us": round(t0 * 1e6, 2),
+                  "stream_GBps": round(1.0 / inv_b / 1e9, 1),
+                  "stream_frac_hbm": round(1.0 / inv_b / 1e9 / HBM_PEAK_GBPS, 4)}
+    del src, dst, o32
     return out
 
 
