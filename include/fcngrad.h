@@ -185,6 +185,30 @@ fg_status conv2d_bwd_weight_checked(const fg_conv_desc *d, const uint16_t *x,
                                     int32_t *found_nonfinite, void *ws,
                                     size_t ws_bytes, hipStream_t stream);
 
+/* Size of the library's static scratch used by conv2d_bwd_weight_noalloc:
+ * one copy per GPU, held until the process ends. */
+#define FG_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/* Kernel gradient without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc). Computes what conv2d_bwd_weight computes
+ * (same validation and errors, ws aside); the fp32 split partials go to a
+ * static FG_NOALLOC_SCRATCH_BYTES (64 MiB) device array of the library instead
+ * of a caller workspace, and the split count is limited so that they fit: the
+ * result is bit-identical to conv2d_bwd_weight whenever that call's workspace
+ * (fg_conv_workspace_bytes) is at most FG_NOALLOC_SCRATCH_BYTES, and otherwise
+ * the same sum in fewer, longer split ranges (a different fp32 order).
+ * Nothing is allocated or freed (no hipMalloc, hipFree or allocating library
+ * call); the first call on a device looks up that device's copy of the scratch
+ * (FG_ELAUNCH if the runtime cannot). Every call on one GPU shares that GPU's
+ * scratch: calls that overlap in time on one GPU (other streams, other host
+ * threads) race and must be ordered by the caller. No part of the scratch needs
+ * clearing between calls. FG_EWORKSPACE if a plan would need more scratch than
+ * FG_NOALLOC_SCRATCH_BYTES (not reached by shapes the library accepts). */
+fg_status conv2d_bwd_weight_noalloc(const fg_conv_desc *d, const uint16_t *x,
+                                    const uint16_t *dy, uint16_t *dw_krsc,
+                                    hipStream_t stream);
+
 /* Transposed convolution (decoder upsampling):
  * y[n,o,u,k] = epi(sum over c and the taps (r,s) with o + ph - r = i*sh and
  * u + pw - s = j*sw for an input position (i,j), of x[n,i,j,c] *

@@ -29,7 +29,9 @@ ENTRY_POINTS = (
     "fg_lars_adam_workspace_bytes",
     "huber_head_grad", "avg_pool2d_fwd", "avg_pool2d_bwd", "channel_slice_copy",
     "grad_flags_clear", "fg_loss_scale_update", "fg_lr_at", "fg_profile_next_launch",
+    "conv2d_bwd_weight_noalloc",
 )
+NOALLOC_SCRATCH_BYTES = 64 << 20
 
 
 class OptTensor(ctypes.Structure):
@@ -109,6 +111,7 @@ def lib():
         "conv2d_bwd_data": [pdesc, vp, vp, vp, i32, vp, vp, sz, vp],
         "conv2d_bwd_weight": [pdesc, vp, vp, vp, vp, sz, vp],
         "conv2d_bwd_weight_checked": [pdesc, vp, vp, vp, vp, vp, sz, vp],
+        "conv2d_bwd_weight_noalloc": [pdesc, vp, vp, vp, vp],
         "conv_transpose2d_fwd": [pdesc, vp, vp, vp, i32, vp, vp, sz, vp],
         "grad_group_pack": [pseg, i32, vp, u64, vp],
         "grad_unscale_check": [vp, u64, ctypes.c_float, vp, vp, vp],
@@ -222,6 +225,13 @@ def conv2d_bwd_weight(desc, x, dy, dw, ws=None, stream=None):
     wp, wb = _ws(ws)
     _check("conv2d_bwd_weight", lib().conv2d_bwd_weight(
         ctypes.byref(desc), _p(x), _p(dy), _p(dw), wp, wb, _s(stream)))
+
+
+def conv2d_bwd_weight_noalloc(desc, x, dy, dw, stream=None):
+    """conv2d_bwd_weight with its split partials in the library's static
+    scratch: no workspace argument, nothing allocated."""
+    _check("conv2d_bwd_weight_noalloc", lib().conv2d_bwd_weight_noalloc(
+        ctypes.byref(desc), _p(x), _p(dy), _p(dw), _s(stream)))
 
 
 def conv2d_bwd_weight_checked(desc, x, dy, dw, found_nonfinite, ws=None,

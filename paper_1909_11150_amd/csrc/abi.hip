@@ -269,15 +269,50 @@ size_t data_ws(const fg_conv_desc *d, int op) {
 
 // Workspace present and large enough, and not overlapping the tensors
 // (byte ranges (p_i, n_i)).
-fg_status check_ws(const fg_conv_desc *d, int op, void *ws, size_t ws_bytes,
-                   const void *p0, size_t n0, const void *p1, size_t n1,
-                   const void *p2, size_t n2, const void *p3, size_t n3) {
-  const size_t need = fg_conv_workspace_bytes(d, op);
+fg_status check_ws_need(size_t need, void *ws, size_t ws_bytes,
+                        const void *p0, size_t n0, const void *p1, size_t n1,
+                        const void *p2, size_t n2, const void *p3, size_t n3) {
   if (need == 0) return FG_OK;
   if (!ws || ws_bytes < need) return FG_EWORKSPACE;
   if (overlap(ws, need, p0, n0) || overlap(ws, need, p1, n1) ||
       (p2 && overlap(ws, need, p2, n2)) || (p3 && overlap(ws, need, p3, n3)))
     return FG_EINVAL;
+  return FG_OK;
+}
+
+fg_status check_ws(const fg_conv_desc *d, int op, void *ws, size_t ws_bytes,
+                   const void *p0, size_t n0, const void *p1, size_t n1,
+                   const void *p2, size_t n2, const void *p3, size_t n3) {
+  return check_ws_need(fg_conv_workspace_bytes(d, op), ws, ws_bytes, p0, n0, p1,
+                       n1, p2, n2, p3, n3);
+}
+
+// ---- the no-allocation kernel gradient's scratch ---------------------------
+// fp32 split partials of conv2d_bwd_weight_noalloc. Each GPU the library runs
+// on holds its own copy until the process ends. In host code the array's name
+// is only a host-side stand-in: its device address on the current device is
+// looked up once per device with hipGetSymbolAddress, and only that address is
+// handed to kernels.
+static __device__ __align__(256) unsigned char scratch[FG_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices];  // device address of `scratch`, per device
+
+// Device address of `scratch` on the current device (looked up on the first
+// call on each device, with that device current).
+fg_status scratch_for_current_device(void **out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+    return FG_ELAUNCH;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p)
+      return FG_ELAUNCH;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
   return FG_OK;
 }
 
@@ -481,10 +516,12 @@ fg_status conv_transpose2d_fwd(const fg_conv_desc *d, const uint16_t *x,
   return launch_status(launch_data_conv(a, false, stream));
 }
 
+// noalloc: the split partials go to the library's static scratch (ws and
+// ws_bytes are ignored) and the plan keeps them within its size.
 static fg_status bwd_weight(const fg_conv_desc *d, const uint16_t *x,
                             const uint16_t *dy, uint16_t *dw_krsc,
                             int32_t *found_nonfinite, void *ws, size_t ws_bytes,
-                            hipStream_t stream) {
+                            hipStream_t stream, bool noalloc = false) {
   fg_status st = check_desc(d);
   if (st != FG_OK) return st;
   if (!x || !dy || !dw_krsc) return FG_EINVAL;
@@ -510,15 +547,26 @@ static fg_status bwd_weight(const fg_conv_desc *d, const uint16_t *x,
        overlap(found_nonfinite, 4, ws, ws_bytes)))
     return FG_EINVAL;
   if ((st = check_conv_support(d)) != FG_OK) return st;
-  if ((st = check_ws(d, FG_OP_BWD_WEIGHT, ws, ws_bytes, x, sx, dy, ny * 2,
-                     dw_krsc, nw * 2, nullptr, 0)) != FG_OK)
+  const size_t plan_cap = noalloc ? (size_t)FG_NOALLOC_SCRATCH_BYTES : SIZE_MAX;
+  const size_t need = d->k == 1 ? head_wgrad_ws_bytes(*d)
+                                : plan_wgrad(*d, P, Q, plan_cap).ws_bytes;
+  if (noalloc) {
+    // the library's scratch cannot overlap the caller's buffers
+    if (need > (size_t)FG_NOALLOC_SCRATCH_BYTES) return FG_EWORKSPACE;
+    ws = nullptr;
+    ws_bytes = 0;
+    if (need && (st = scratch_for_current_device(&ws)) != FG_OK) return st;
+    ws_bytes = FG_NOALLOC_SCRATCH_BYTES;
+  } else if ((st = check_ws_need(need, ws, ws_bytes, x, sx, dy, ny * 2, dw_krsc,
+                                 nw * 2, nullptr, 0)) != FG_OK) {
     return st;
+  }
 
   if (d->k == 1)
     return launch_status(launch_head_wgrad(x, dy, dw_krsc,
                                            (int64_t)d->n * d->h * d->w, d->c,
                                            (float *)ws, found_nonfinite, stream));
-  WgradPlan pl = plan_wgrad(*d, P, Q);
+  WgradPlan pl = plan_wgrad(*d, P, Q, plan_cap);
   WgradArgs a;
   memset(&a, 0, sizeof(a));
   a.x = x;
@@ -548,6 +596,12 @@ fg_status conv2d_bwd_weight_checked(const fg_conv_desc *d, const uint16_t *x,
                                     size_t ws_bytes, hipStream_t stream) {
   if (!found_nonfinite) return FG_EINVAL;
   return bwd_weight(d, x, dy, dw_krsc, found_nonfinite, ws, ws_bytes, stream);
+}
+
+fg_status conv2d_bwd_weight_noalloc(const fg_conv_desc *d, const uint16_t *x,
+                                    const uint16_t *dy, uint16_t *dw_krsc,
+                                    hipStream_t stream) {
+  return bwd_weight(d, x, dy, dw_krsc, nullptr, nullptr, 0, stream, true);
 }
 
 // ---------------------------------------------------------------------------

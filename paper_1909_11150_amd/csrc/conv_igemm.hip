@@ -744,7 +744,8 @@ static TileCost data_cost(bool dma_small) {
 constexpr TileCost kWgradCost{6.35e12, 1.3e12, 4.05e12, 6.3e-6, 4.2e-6};
 
 TileChoice choose_tiles(int64_t tiles_big, int64_t tiles_small, int64_t nk,
-                        int64_t out_elems, bool allow_big, const TileCost &cost) {
+                        int64_t out_elems, bool allow_big, const TileCost &cost,
+                        int max_split = 16) {
   TileChoice best{false, 1};
   double best_t = 1e30;
   for (int big = 0; big < 2; ++big) {
@@ -753,7 +754,7 @@ TileChoice choose_tiles(int64_t tiles_big, int64_t tiles_small, int64_t nk,
     const int64_t slots = big ? kCUs : 2 * kCUs;
     const int t = big ? 256 : 128;
     const double rate = big ? cost.rate_big : cost.rate_small;
-    for (int ns = 1; ns <= 16; ++ns) {
+    for (int ns = 1; ns <= max_split; ++ns) {
       if (ns > 1 && (nk + ns - 1) / ns < 4) break;  // >= 4 slices per split
       const int64_t waves = (tiles * ns + slots - 1) / slots;
       const int64_t nk_split = (nk + ns - 1) / ns;
@@ -870,16 +871,19 @@ const char *data_conv_kernel_name(const DataConvArgs &a, bool w_kmajor) {
   return names[pl.big][w_kmajor][(a.cr % BK) == 0][pl.nsplit > 1];
 }
 
-static TileChoice wgrad_choice(const fg_conv_desc &d, int32_t p, int32_t q) {
+// max_ws_bytes bounds the fp32 partials of a split (and so the split count).
+static TileChoice wgrad_choice(const fg_conv_desc &d, int32_t p, int32_t q,
+                               size_t max_ws_bytes) {
   const int64_t rsc = (int64_t)d.r * d.s * d.c;
   const int64_t mtot = (int64_t)d.n * p * q;
   const int64_t tb = ((rsc + 255) / 256) * ((d.k + 255) / 256);
   const int64_t ts = ((rsc + 127) / 128) * ((d.k + 127) / 128);
+  const size_t per_split = (size_t)d.k * rsc * sizeof(float);
+  const size_t cap = max_ws_bytes / per_split;
+  const int max_split = cap >= 16 ? 16 : (cap < 2 ? 1 : (int)cap);
   return choose_tiles(tb, ts, (mtot + BK - 1) / BK, (int64_t)d.k * rsc,
-                      rsc >= 256 && d.k >= 256, kWgradCost);
+                      rsc >= 256 && d.k >= 256, kWgradCost, max_split);
 }
-
-WgradPlan plan_wgrad(const fg_conv_desc &d, int32_t p, int32_t q);
 
 const char *wgrad_kernel_name(const fg_conv_desc &d) {
   int32_t p = (d.h + 2 * d.pad_h - d.r) / d.stride_h + 1;
@@ -899,9 +903,10 @@ const char *wgrad_kernel_name(const fg_conv_desc &d) {
   return names[pl.big][pl.nsplit > 1];
 }
 
-WgradPlan plan_wgrad(const fg_conv_desc &d, int32_t p, int32_t q) {
+WgradPlan plan_wgrad(const fg_conv_desc &d, int32_t p, int32_t q,
+                     size_t max_ws_bytes) {
   WgradPlan pl;
-  const TileChoice c = wgrad_choice(d, p, q);
+  const TileChoice c = wgrad_choice(d, p, q, max_ws_bytes);
   const int64_t rsc = (int64_t)d.r * d.s * d.c;
   const int64_t mtot = (int64_t)d.n * p * q;
   int64_t ns = c.nsplit;

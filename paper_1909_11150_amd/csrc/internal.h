@@ -84,7 +84,10 @@ struct WgradPlan {
   int32_t nsplit, mchunk;
   size_t ws_bytes;
 };
-WgradPlan plan_wgrad(const fg_conv_desc &d, int32_t p, int32_t q);
+// Split and tile plan of a kernel gradient; the fp32 partials of a split take
+// ws_bytes <= max_ws_bytes (fewer splits when the best plan needs more).
+WgradPlan plan_wgrad(const fg_conv_desc &d, int32_t p, int32_t q,
+                     size_t max_ws_bytes = SIZE_MAX);
 
 // The same span for the kernel gradient's x.
 __host__ __device__ inline size_t x_span_bytes(const WgradArgs &a) {

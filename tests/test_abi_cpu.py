@@ -342,3 +342,17 @@ def test_flags_clear_and_host_helpers_validate(L):
                    (fg.LRScheduleParams(1e-4, 1e-3, -1, 0, 1.0), 0),
                    (fg.LRScheduleParams(1e-4, 1e-3, 10, 0, 0.0), 0)):
         assert L.fg_lr_at(ctypes.byref(bad), k, ctypes.byref(out)) == fg.FG_EINVAL
+
+
+def test_noalloc_kernel_gradient_validates_before_any_device_call(L):
+    d = _desc()
+    ref = ctypes.byref
+    assert L.conv2d_bwd_weight_noalloc(None, FAKE, FAKE + (1 << 20), FAKE + (1 << 22),
+                                       None) == fg.FG_EINVAL
+    assert L.conv2d_bwd_weight_noalloc(ref(d), None, FAKE + (1 << 20), FAKE + (1 << 22),
+                                       None) == fg.FG_EINVAL
+    # dW aliasing x
+    assert L.conv2d_bwd_weight_noalloc(ref(d), FAKE, FAKE + (1 << 20), FAKE,
+                                       None) == fg.FG_EINVAL
+    assert L.conv2d_bwd_weight_noalloc(ref(_desc(c=12)), FAKE, FAKE + (1 << 20),
+                                       FAKE + (1 << 22), None) == fg.FG_EUNSUPPORTED
