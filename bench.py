@@ -148,22 +148,28 @@ def summarize_stats(path):
               f"{float(r['MaxNs']) / 1e3:.2f} |")
 
 
-def summarize_trace(path, kernel, per_step, timed_steps, one_stream_steps):
+def summarize_trace(path, kernel, per_step, timed_steps, warmup):
     """Launch durations of one kernel from a rocprofv3 kernel trace of the
-    default bench command: all launches, the first per_step *
-    one_stream_steps (warm-up and detail pass, one stream) and the last
-    per_step * timed_steps (the timed region)."""
+    default bench command. The step program runs warmup + 4 one-stream steps
+    (warm-up, two detail steps timing calls, two timing main kernels), then
+    warmup + timed_steps steps on the timed streams; launches of the kernel
+    by the measurements that follow (gradient path, small configurations)
+    come after those and are left out."""
     import csv
     rows = [r for r in csv.DictReader(open(path))
             if short_kernel_name(r["Kernel_Name"]) == kernel]
     rows.sort(key=lambda r: int(r["Start_Timestamp"]))
     dur = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in rows]
-    timed = dur[-per_step * timed_steps:]
-    alone = dur[:per_step * one_stream_steps]
-    print(f"`{kernel}`: {len(dur)} launches, average {sum(dur) / len(dur):.2f} us; "
-          f"one-stream steps (first {one_stream_steps}): {len(alone)} launches, average "
-          f"{sum(alone) / len(alone):.2f} us; timed region (last {timed_steps} steps): "
-          f"{len(timed)} launches, average {sum(timed) / len(timed):.2f} us")
+    one = warmup + 4
+    total = one + warmup + timed_steps
+    step_dur = dur[:per_step * total]
+    timed = step_dur[-per_step * timed_steps:]
+    alone = step_dur[per_step * warmup:per_step * one]
+    print(f"`{kernel}`: {len(step_dur)} launches in the {total} steps, average "
+          f"{sum(step_dur) / len(step_dur):.2f} us; one-stream detail steps: {len(alone)} "
+          f"launches, average {sum(alone) / len(alone):.2f} us; timed region (last "
+          f"{timed_steps} steps): {len(timed)} launches, average "
+          f"{sum(timed) / len(timed):.2f} us")
 
 
 def summarize_pmc(d):
@@ -208,15 +214,46 @@ def summarize_pmc(d):
         if k.startswith(("data_conv", "wgrad")):
             print(f"traffic: kernel={k} src_sha256_16={source_hash(k)} "
                   f"bytes_per_launch={int(round(mb * 1e6))}")
+    if os.path.isdir(os.path.join(d, "gp_FETCH_SIZE")):
+        # the standalone gradient path (--grad-path-only): per dispatch of
+        # each kernel, against its algorithmic bytes
+        # each thread of the three kernels moves 16 elements (the grid is
+        # rounded up to whole workgroups, so this is an upper bound)
+        bpe = {"copy_pieces_kernel<2>": 4, "unscale_vec_kernel": 6, "copy_pieces_kernel<4>": 8}
+
+        def algo_and_counted(run):
+            out = {}
+            for r in csv.DictReader(open(os.path.join(d, run, "run_counter_collection.csv"))):
+                k = short_kernel_name(r["Kernel_Name"])
+                if k in bpe:
+                    v = out.setdefault(k, [0, 0.0, 0.0])
+                    v[0] += 1
+                    v[1] += float(r["Counter_Value"])
+                    v[2] += int(r["Grid_Size"]) * 16 * bpe[k]
+            return out
+        gf, gw = algo_and_counted("gp_FETCH_SIZE"), algo_and_counted("gp_WRITE_SIZE")
+        print()
+        print("Standalone gradient path (`--grad-path-only`: the nine groups, each alone and "
+              "back to back, and single launches of 4 to 256 MiB), caches evicted before "
+              "each launch:")
+        print()
+        print("| kernel | dispatches | counted MB (scaled), all dispatches | algorithmic MB, "
+              "all dispatches | ratio |")
+        print("|---|---:|---:|---:|---:|")
+        for k in bpe:
+            if k in gf and k in gw:
+                mb = (gf[k][1] * fscale + gw[k][1] * wscale) * 1024 / 1e6
+                algo = gf[k][2] / 1e6
+                print(f"| `{k}` | {gf[k][0]} | {mb:.0f} | {algo:.0f} | {mb / algo:.3f} |")
 
 
 def summarize_mfma(d):
-    """Per-kernel MFMA utilisation from one rocprofv3 --pmc run collecting
-    SQ_VALU_MFMA_BUSY_CYCLES, SQ_INSTS_VALU_MFMA_MOPS_F16, SQ_BUSY_CU_CYCLES
-    and GRBM_GUI_ACTIVE (a *counter_collection.csv under DIR). MFMA busy =
-    busy cycles summed over the SIMDs / (GPU-active cycles x 1024 SIMDs);
-    MFMA flops = MOPS_F16 x 512 (what the matrix cores executed, padding of
-    partial tiles included)."""
+    """Per-kernel MFMA utilisation from one rocprofv3 --pmc run of the
+    derived MfmaUtil (MFMA-busy cycles summed over the SIMDs / (GPU-active
+    cycles x SIMDs), in %) with SQ_INSTS_VALU_MFMA_MOPS_F16 (x 512 = the
+    flops the matrix cores executed, padding of partial tiles included),
+    SQ_LDS_BANK_CONFLICT and SQ_LDS_IDX_ACTIVE (a *counter_collection.csv
+    under DIR). Averages over each kernel's dispatches."""
     import csv
     import glob
     files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
@@ -232,22 +269,22 @@ def summarize_mfma(d):
             e[name] = e.get(name, 0.0) + float(r["Counter_Value"])
     per = {}
     for e in disp.values():
-        if "GRBM_GUI_ACTIVE" not in e or "SQ_VALU_MFMA_BUSY_CYCLES" not in e:
+        if "MfmaUtil" not in e:
             continue
-        k = per.setdefault(e["kernel"], [0, 0.0, 0.0, 0.0])
+        k = per.setdefault(e["kernel"], [0, 0.0, 0.0, 0.0, 0.0])
         k[0] += 1
-        k[1] += e["GRBM_GUI_ACTIVE"]
-        k[2] += e["SQ_VALU_MFMA_BUSY_CYCLES"]
-        k[3] += e.get("SQ_INSTS_VALU_MFMA_MOPS_F16", 0.0) * 512
-    print("| kernel | dispatches | GPU-active cycles per dispatch | MFMA busy | "
-          "MFMA TFLOP per dispatch | MFMA TFLOP/s while active (2.4 GHz) |")
-    print("|---|---:|---:|---:|---:|---:|")
-    rows = sorted(per.items(), key=lambda kv: -kv[1][1])
-    for k, (n, gui, busy, fl) in rows:
+        k[1] += e["MfmaUtil"]
+        k[2] += e.get("SQ_INSTS_VALU_MFMA_MOPS_F16", 0.0) * 512
+        k[3] += e.get("SQ_LDS_BANK_CONFLICT", 0.0)
+        k[4] += e.get("SQ_LDS_IDX_ACTIVE", 0.0)
+    print("| kernel | dispatches | MFMA busy (MfmaUtil) | MFMA GFLOP per dispatch | "
+          "LDS bank-conflict cycles / LDS-active cycles |")
+    print("|---|---:|---:|---:|---:|")
+    for k, (n, util, fl, bc, act) in sorted(per.items(), key=lambda kv: -kv[1][2]):
         if fl == 0:
             continue
-        print(f"| `{k}` | {n} | {gui / n:.0f} | {100 * busy / (gui * 1024):.1f}% | "
-              f"{fl / n / 1e12:.4f} | {fl / (gui / 2.4e9) / 1e12:.0f} |")
+        conf = f"{100 * bc / act:.1f}%" if act else "-"
+        print(f"| `{k}` | {n} | {util / n:.1f}% | {fl / n / 1e9:.2f} | {conf} |")
 
 
 def op_bench(label, steps, warmup):
@@ -428,18 +465,35 @@ def cpu_grad_baseline(seconds):
 
 
 def gpu_clocks():
-    """Current SCLK / MCLK as amd-smi (or rocm-smi) prints them, or None."""
+    """Current clocks as amd-smi prints them: {section: first CLK value}
+    for the GFX (SCLK) and MEM (MCLK) sections, or the raw clock lines of
+    rocm-smi; None if neither tool answers."""
     import subprocess
-    for cmd in (["amd-smi", "metric", "--clock"], ["rocm-smi", "--showclocks"]):
-        try:
-            r = subprocess.run(cmd, capture_output=True, text=True, timeout=20)
-        except (OSError, subprocess.TimeoutExpired):
-            continue
-        if r.returncode == 0 and r.stdout.strip():
-            keep = [ln.strip() for ln in r.stdout.splitlines()
-                    if any(k in ln.upper() for k in ("SCLK", "MCLK", "GFX_0", "MEM_0",
-                                                     "CLK:"))]
-            return {"tool": cmd[0], "lines": keep[:12]}
+    try:
+        r = subprocess.run(["amd-smi", "metric", "--clock"], capture_output=True,
+                           text=True, timeout=20)
+        if r.returncode == 0:
+            out, sec = {}, None
+            for ln in r.stdout.splitlines():
+                t = ln.strip()
+                if t.endswith(":") and " " not in t:
+                    sec = t[:-1]
+                elif sec and t.startswith("CLK:") and sec not in out:
+                    out[sec] = t.split(":", 1)[1].strip()
+            keep = {k: v for k, v in out.items() if k.startswith(("GFX", "MEM"))}
+            if keep:
+                return {"tool": "amd-smi", "clk": keep}
+    except (OSError, subprocess.TimeoutExpired):
+        pass
+    try:
+        r = subprocess.run(["rocm-smi", "--showclocks"], capture_output=True, text=True,
+                           timeout=20)
+        if r.returncode == 0:
+            return {"tool": "rocm-smi",
+                    "lines": [ln.strip() for ln in r.stdout.splitlines()
+                              if "clk" in ln.lower()][:8]}
+    except (OSError, subprocess.TimeoutExpired):
+        pass
     return None
 
 
@@ -660,7 +714,7 @@ def main():
         return
     if args.summarize_trace:
         summarize_trace(args.summarize_trace[0], args.summarize_trace[1],
-                        args.launches_per_step, args.steps, args.warmup + 2)
+                        args.launches_per_step, args.steps, args.warmup)
         return
     if args.op:
         op_bench(args.op, args.steps, args.warmup)

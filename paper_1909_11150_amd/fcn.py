@@ -336,12 +336,12 @@ class Chain:
         return sum(3 * L.flops for L in self.layers)
 
     # ---- prepared step -----------------------------------------------------------
-    def program(self, target, streams=3):
+    def program(self, target, streams=3, sync_every=1):
         """The step as a list of library calls with every argument marshalled
         once (descriptors, pointers, segment tables); running it costs one
         foreign call per launch. Same calls as ``step``; see StepProgram for
         the streams."""
-        return StepProgram(self, target, streams)
+        return StepProgram(self, target, streams, sync_every)
 
 
 # algorithmic HBM bytes of the optimizer per parameter: w, m, v and the
@@ -402,7 +402,7 @@ class StepProgram:
     update, so the updates overlap the next forward pass. ``join()`` makes
     the main stream wait for everything."""
 
-    def __init__(self, ch, target, streams=3):
+    def __init__(self, ch, target, streams=3, sync_every=1):
         if ch.groups is None:
             raise ValueError("the step program needs gradient groups")
         if streams not in (1, 3):
@@ -501,36 +501,56 @@ class StepProgram:
                              fused=fused, n=sum(w.numel() for w in ch.w32))
             self._keep.append(tab)
         last_dw = {}
+
+        def emit_dw(j, dep):
+            """Kernel gradient of layer j (after the call `dep` that wrote
+            g[j + 1] or a later input gradient), then its group's path if j
+            completes a group."""
+            L = ch.layers[j]
+            if L.kind == "conv":
+                d = fwd_desc(L)
+                c = dw_call(f"{L.name}.dW", kernel_name(d, OP_BWD_WEIGHT), L.flops, d,
+                            ch.acts[j], ch.g[j + 1], j)
+            else:
+                d = convt_dx_desc(L)
+                c = dw_call(f"{L.name}.dW", kernel_name(d, OP_BWD_WEIGHT), L.flops, d,
+                            ch.g[j + 1], ch.acts[j], j)
+            calls.append(c._replace(deps=(dep,)))
+            last_dw[j] = len(calls) - 1
+            gi = ch._group_done_at.get(j)
+            if gi is not None:
+                gc = self._group_calls(ch, gi, L_, st) + self._norms_calls(ch, gi, L_, st)
+                gc[0] = gc[0]._replace(deps=(last_dw[j],))
+                calls.extend(gc)
+
+        # kernel gradients are issued sync_every layers at a time, all after
+        # the latest input gradient: the main stream then records one event
+        # per sync_every layers for the kernel-gradient stream to wait on
+        pending = []
         for i in reversed(range(nl)):
             L = ch.layers[i]
             dy = ch.g[i + 1]
             gate = i > 0 and ch.layers[i - 1].relu
             epi = EPI_GATE if gate else EPI_NONE
             gt = ptr(ch.acts[i]) if gate else None
+            pending.append(i)
+            if len(pending) >= sync_every or i == 0:
+                for j in pending:
+                    emit_dw(j, writer[i + 1])
+                pending = []
             if L.kind == "conv":
                 d = fwd_desc(L)
-                calls.append(dw_call(f"{L.name}.dW", kernel_name(d, OP_BWD_WEIGHT),
-                                     L.flops, d, ch.acts[i], dy, i))
-                last_dw[i] = len(calls) - 1
                 calls.append(Call(f"{L.name}.dx", kernel_name(d, OP_BWD_DATA),
                                   L.flops, L_.conv2d_bwd_data,
                                   (desc(d), ptr(dy), ptr(ch.w[i]), ptr(ch.g[i]), epi,
                                    gt, ws, wsb, st), one(d, OP_BWD_DATA)))
             else:
                 d = convt_dx_desc(L)
-                calls.append(dw_call(f"{L.name}.dW", kernel_name(d, OP_BWD_WEIGHT),
-                                     L.flops, d, dy, ch.acts[i], i))
-                last_dw[i] = len(calls) - 1
                 calls.append(Call(f"{L.name}.dx", kernel_name(d, OP_FWD), L.flops,
                                   L_.conv2d_fwd,
                                   (desc(d), ptr(dy), ptr(ch.w[i]), ptr(ch.g[i]), epi,
                                    gt, ws, wsb, st), one(d, OP_FWD)))
             writer[i] = len(calls) - 1
-            gi = ch._group_done_at.get(i)
-            if gi is not None:
-                gc = self._group_calls(ch, gi, L_, st) + self._norms_calls(ch, gi, L_, st)
-                gc[0] = gc[0]._replace(deps=(last_dw[i],))
-                calls += gc
         self._copy = None
         if ch.opt is not None or ch.scaler is not None:
             # the step's flags to pinned host memory once every flag is final
