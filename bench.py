@@ -93,6 +93,12 @@ def parse():
                     help="reps per group and kernel of the gradient-path measurement")
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the standalone gradient path and the small configurations")
+    ap.add_argument("--ceiling", action="store_true",
+                    help="measure the practical MFMA ceiling instead: clocks and power "
+                         "under the sustained step and under a vendor-library GEMM, and "
+                         "every pass against the vendor GEMM of the same shape")
+    ap.add_argument("--summarize-ceiling", default=None, metavar="JSON",
+                    help="turn the --ceiling JSON line into markdown tables")
     ap.add_argument("--no-clocks", action="store_true",
                     help="do not query amd-smi / rocm-smi for the clocks")
     return ap.parse_args()
@@ -502,6 +508,195 @@ def _ev():
     return torch.cuda.Event(enable_timing=True)
 
 
+def _smi_sample():
+    """One amd-smi reading: socket power (W) and the GFX clock of every
+    XCD (MHz), or None."""
+    import subprocess
+    try:
+        r = subprocess.run(["amd-smi", "metric", "-p", "-c"], capture_output=True,
+                           text=True, timeout=20)
+    except (OSError, subprocess.TimeoutExpired):
+        return None
+    if r.returncode != 0:
+        return None
+    power, gfx, sec = None, [], None
+    for ln in r.stdout.splitlines():
+        t = ln.strip()
+        if t.startswith("SOCKET_POWER:"):
+            v = t.split(":", 1)[1].split()[0]
+            power = float(v) if v.replace(".", "", 1).isdigit() else None
+        elif t.endswith(":") and " " not in t:
+            sec = t[:-1]
+        elif sec and sec.startswith("GFX") and t.startswith("CLK:"):
+            v = t.split(":", 1)[1].split()[0]
+            if v.isdigit():
+                gfx.append(int(v))
+    return {"power_W": power, "gfx_MHz": gfx} if gfx else None
+
+
+def sustained(fn, seconds, settle=1.0):
+    """Run fn (one unit of GPU work, queued) back to back for `seconds`,
+    sampling power and clocks from a second thread after `settle` seconds.
+    Returns (ms per call over the run, sample summary)."""
+    import threading
+
+    import torch
+    samples, stop = [], threading.Event()
+
+    def sampler():
+        if stop.wait(settle):
+            return
+        while not stop.is_set():
+            s = _smi_sample()
+            if s:
+                samples.append(s)
+            stop.wait(0.2)
+    th = threading.Thread(target=sampler)
+    n, t_ms = 0, 0.0
+    t0 = time.perf_counter()
+    th.start()
+    while time.perf_counter() - t0 < seconds:
+        e0, e1 = _ev(), _ev()
+        e0.record()
+        for _ in range(20):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        n += 20
+        t_ms += e0.elapsed_time(e1)
+    stop.set()
+    th.join()
+    clk = sorted(c for s in samples for c in s["gfx_MHz"])
+    pw = sorted(s["power_W"] for s in samples if s["power_W"] is not None)
+    summ = {"samples": len(samples),
+            "gfx_MHz_median": clk[len(clk) // 2] if clk else None,
+            "gfx_MHz_min": clk[0] if clk else None, "gfx_MHz_max": clk[-1] if clk else None,
+            "socket_power_W_median": pw[len(pw) // 2] if pw else None}
+    return t_ms / n, summ
+
+
+def _gemm_time(m, n, k, reps=20):
+    """Median time (s) of a vendor-library fp16 GEMM (torch.matmul, fp32
+    accumulation) of [m, k] x [k, n], row-major operands."""
+    import torch
+    a = torch.randn(m, k, device="cuda", dtype=torch.float16)
+    b = torch.randn(k, n, device="cuda", dtype=torch.float16)
+    for _ in range(3):
+        torch.matmul(a, b)
+    evs = [(_ev(), _ev()) for _ in range(reps)]
+    for e0, e1 in evs:
+        e0.record()
+        torch.matmul(a, b)
+        e1.record()
+    torch.cuda.synchronize()
+    ts = sorted(e0.elapsed_time(e1) for e0, e1 in evs)
+    del a, b
+    return ts[len(ts) // 2] * 1e-3
+
+
+def ceiling_bench():
+    """The practical MFMA ceiling of this GPU, beside the step:
+    - clocks and socket power while the three-stream step runs back to back,
+      and while a large vendor-library fp16 GEMM does;
+    - every convolution pass of the step (alone, one stream, the call's
+      whole time) against the vendor GEMM with the pass's output shape and reduction
+      length (the GEMM a convolution becomes after an explicit im2col, whose
+      own cost is not counted)."""
+    import torch
+
+    import synth
+    from paper_1909_11150_amd.fcn import Chain
+    wl = synth.fcn()
+    ch = Chain(wl.layers, wl.weights, wl.x, loss_scale=synth.LOSS_SCALE,
+               group_cap_bytes=synth.GROUP_CAP_BYTES)
+    target = torch.from_numpy(wl.target).cuda()
+    flops_step = sum(3 * L.flops for L in wl.layers)
+    prog = ch.program(target, streams=3)
+    for _ in range(3):
+        prog.run()
+    prog.join()
+
+    def step():
+        prog.run()
+        prog.join()
+    ms, clk = sustained(step, 5.0)
+    out = {"step": {"ms": round(ms, 4), "tflops": round(flops_step / ms / 1e9, 1),
+                    **clk}}
+    del prog
+    # every pass alone: events around each call (a split pass's reduction
+    # included, as the vendor GEMM's own split-K reduction is)
+    one = ch.program(target, streams=1)
+    conv = [i for i, c in enumerate(one.calls)
+            if c.kernel.startswith(("data_conv", "wgrad"))]
+    for _ in range(2):
+        one.run()
+    kev = [{i: (_ev(), _ev()) for i in conv} for _ in range(3)]
+    for k in kev:
+        one.run(events=k)
+    torch.cuda.synchronize()
+    ours = {one.calls[i].label: sorted(k[i][0].elapsed_time(k[i][1]) for k in kev)[1] * 1e-3
+            for i in conv}
+    del one, ch
+    torch.cuda.empty_cache()
+    sq = 8192
+    a = torch.randn(sq, sq, device="cuda", dtype=torch.float16)
+    b = torch.randn(sq, sq, device="cuda", dtype=torch.float16)
+    ms_g, clk_g = sustained(lambda: torch.matmul(a, b), 4.0)
+    out["gemm_8192"] = {"ms": round(ms_g, 4),
+                        "tflops": round(2 * sq ** 3 / ms_g / 1e9, 1), **clk_g}
+    del a, b
+    torch.cuda.empty_cache()
+    rows = []
+    for L in wl.layers:
+        if L.kind == "conv" and L.w_shape[0] == 1:
+            continue  # the K = 1 head runs on vector units
+        for pas, shp in (("fwd", L.y_shape), ("dx", L.x_shape), ("dW", None)):
+            if shp is None:
+                mm, nn = int(np.prod(L.w_shape)) // L.w_shape[0], L.w_shape[0]
+            else:
+                mm, nn = int(np.prod(shp[:3])), shp[3]
+            kk = L.flops // (2 * mm * nn)
+            assert 2 * mm * nn * kk == L.flops
+            t_g = _gemm_time(mm, nn, kk)
+            t_o = ours[f"{L.name}.{pas}"]
+            rows.append({"pass": f"{L.name}.{pas}", "gemm_mnk": [mm, nn, kk],
+                         "ours_us": round(t_o * 1e6, 1),
+                         "ours_tflops": round(L.flops / t_o / 1e12, 1),
+                         "gemm_us": round(t_g * 1e6, 1),
+                         "gemm_tflops": round(L.flops / t_g / 1e12, 1)})
+    out["passes"] = rows
+    t_o = sum(r["ours_us"] for r in rows)
+    t_g = sum(r["gemm_us"] for r in rows)
+    out["passes_total"] = {"ours_us": round(t_o, 1), "gemm_us": round(t_g, 1),
+                           "ours_tflops": round(flops_step / t_o / 1e6, 1),
+                           "gemm_tflops": round(flops_step / t_g / 1e6, 1)}
+    return out
+
+
+def summarize_ceiling(path):
+    with open(path) as f:
+        d = json.loads(f.read().strip().splitlines()[-1])
+    print("| run | ms per call | TFLOP/s | % of 2.5 PFLOP/s | GFX clock median (min-max), MHz "
+          "| socket power median, W | samples |")
+    print("|---|---:|---:|---:|---|---:|---:|")
+    for k, name in (("step", "encoder-decoder step, 3 streams"),
+                    ("gemm_8192", "vendor GEMM 8192 x 8192 x 8192")):
+        v = d[k]
+        print(f"| {name} | {v['ms']:.4f} | {v['tflops']:.1f} | "
+              f"{100 * v['tflops'] / MFMA_F16_PEAK_TFLOPS:.1f}% | {v['gfx_MHz_median']} "
+              f"({v['gfx_MHz_min']}-{v['gfx_MHz_max']}) | {v['socket_power_W_median']} | "
+              f"{v['samples']} |")
+    print()
+    print("| pass | GEMM M x N x K | this library, us | TFLOP/s | vendor GEMM, us | TFLOP/s "
+          "| ratio |")
+    print("|---|---|---:|---:|---:|---:|---:|")
+    for r in d["passes"] + [dict(d["passes_total"], **{"pass": "all 36", "gemm_mnk": None})]:
+        mnk = " x ".join(str(v) for v in r["gemm_mnk"]) if r["gemm_mnk"] else ""
+        print(f"| {r['pass']} | {mnk} | {r['ours_us']} | {r['ours_tflops']} | "
+              f"{r['gemm_us']} | {r['gemm_tflops']} | "
+              f"{r['gemm_us'] / r['ours_us']:.2f} |")
+
+
 def grad_path_bench(reps=20, warmup=3, flush_mib=1024):
     """The gradient path alone on the nine 25 MiB groups of the full
     network's weight gradients (seeded N(0,1) fp16 values): each launch of
@@ -712,6 +907,9 @@ def main():
     if args.summarize_mfma:
         summarize_mfma(args.summarize_mfma)
         return
+    if args.summarize_ceiling:
+        summarize_ceiling(args.summarize_ceiling)
+        return
     if args.summarize_trace:
         summarize_trace(args.summarize_trace[0], args.summarize_trace[1],
                         args.launches_per_step, args.steps, args.warmup)
@@ -730,6 +928,9 @@ def main():
 
     if args.grad_path_only:
         print(json.dumps(grad_path_bench(args.grad_reps)), flush=True)
+        return
+    if args.ceiling:
+        print(json.dumps(ceiling_bench()), flush=True)
         return
     clocks_start = gpu_clocks() if not args.no_clocks else None
     if args.workload == "densenet":
