@@ -575,12 +575,21 @@ def sustained(fn, seconds, settle=1.0):
     return t_ms / n, summ
 
 
-def _gemm_time(m, n, k, reps=20):
+def _operand(rows, cols, half_zero):
+    """fp16 N(0, 1) values, with about half of them zero when half_zero (as
+    a ReLU output or a ReLU-gated gradient has): on a power-limited GPU the
+    MFMA rate depends on how many operand bits toggle."""
+    import torch
+    a = torch.randn(rows, cols, device="cuda", dtype=torch.float16)
+    return a.relu_() if half_zero else a
+
+
+def _gemm_time(m, n, k, zero_a=False, zero_b=False, reps=20):
     """Median time (s) of a vendor-library fp16 GEMM (torch.matmul, fp32
     accumulation) of [m, k] x [k, n], row-major operands."""
     import torch
-    a = torch.randn(m, k, device="cuda", dtype=torch.float16)
-    b = torch.randn(k, n, device="cuda", dtype=torch.float16)
+    a = _operand(m, k, zero_a)
+    b = _operand(k, n, zero_b)
     for _ in range(3):
         torch.matmul(a, b)
     evs = [(_ev(), _ev()) for _ in range(reps)]
@@ -597,7 +606,8 @@ def _gemm_time(m, n, k, reps=20):
 def ceiling_bench():
     """The practical MFMA ceiling of this GPU, beside the step:
     - clocks and socket power while the three-stream step runs back to back,
-      and while a large vendor-library fp16 GEMM does;
+      and while a large vendor-library fp16 GEMM does (dense operands, and
+      one operand about half zero as after a ReLU);
     - every convolution pass of the step (alone, one stream, the call's
       whole time) against the vendor GEMM with the pass's output shape and reduction
       length (the GEMM a convolution becomes after an explicit im2col, whose
@@ -639,13 +649,14 @@ def ceiling_bench():
     del one, ch
     torch.cuda.empty_cache()
     sq = 8192
-    a = torch.randn(sq, sq, device="cuda", dtype=torch.float16)
-    b = torch.randn(sq, sq, device="cuda", dtype=torch.float16)
-    ms_g, clk_g = sustained(lambda: torch.matmul(a, b), 4.0)
-    out["gemm_8192"] = {"ms": round(ms_g, 4),
-                        "tflops": round(2 * sq ** 3 / ms_g / 1e9, 1), **clk_g}
-    del a, b
-    torch.cuda.empty_cache()
+    for key, zero_a in (("gemm_8192", False), ("gemm_8192_half_zero_a", True)):
+        a = _operand(sq, sq, zero_a)
+        b = _operand(sq, sq, False)
+        ms_g, clk_g = sustained(lambda: torch.matmul(a, b), 4.0)
+        out[key] = {"ms": round(ms_g, 4), "tflops": round(2 * sq ** 3 / ms_g / 1e9, 1),
+                    **clk_g}
+        del a, b
+        torch.cuda.empty_cache()
     rows = []
     for L in wl.layers:
         if L.kind == "conv" and L.w_shape[0] == 1:
@@ -657,7 +668,10 @@ def ceiling_bench():
                 mm, nn = int(np.prod(shp[:3])), shp[3]
             kk = L.flops // (2 * mm * nn)
             assert 2 * mm * nn * kk == L.flops
-            t_g = _gemm_time(mm, nn, kk)
+            # operands with the pass's zero fractions: the activation (or
+            # the gated output gradient) about half zero, the weights dense;
+            # the kernel gradient's two operands both about half zero
+            t_g = _gemm_time(mm, nn, kk, zero_a=True, zero_b=pas == "dW")
             t_o = ours[f"{L.name}.{pas}"]
             rows.append({"pass": f"{L.name}.{pas}", "gemm_mnk": [mm, nn, kk],
                          "ours_us": round(t_o * 1e6, 1),
@@ -680,7 +694,10 @@ def summarize_ceiling(path):
           "| socket power median, W | samples |")
     print("|---|---:|---:|---:|---|---:|---:|")
     for k, name in (("step", "encoder-decoder step, 3 streams"),
-                    ("gemm_8192", "vendor GEMM 8192 x 8192 x 8192")):
+                    ("gemm_8192", "vendor GEMM 8192 x 8192 x 8192, dense N(0,1) operands"),
+                    ("gemm_8192_half_zero_a", "the same, A about half zero")):
+        if k not in d:
+            continue
         v = d[k]
         print(f"| {name} | {v['ms']:.4f} | {v['tflops']:.1f} | "
               f"{100 * v['tflops'] / MFMA_F16_PEAK_TFLOPS:.1f}% | {v['gfx_MHz_median']} "
