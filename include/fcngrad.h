@@ -31,7 +31,10 @@
  *     P = (H + 2*pad_h - R)/stride_h + 1 (floor), likewise Q.
  *   - Every device pointer (x, w, y, gate, ws, group buffers, flags, segment
  *     targets) is owned by the caller. The library never allocates or frees
- *     device memory and keeps no device state. Its host state is two small
+ *     device memory. Its only device memory of its own is the static
+ *     scratch array of conv2d_bwd_weight_noalloc (one per GPU, loaded with
+ *     the library), and no call reads what an earlier call left there, so it
+ *     keeps no device state between calls. Its host state is two small
  *     records: the optimizer's per-workspace record of which layers have
  *     norms and which are applied in the current step (lars_adam_norms /
  *     lars_adam_apply, under a mutex), and the one-shot profiling events of
