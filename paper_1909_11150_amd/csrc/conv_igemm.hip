@@ -705,19 +705,23 @@ int64_t data_nk_max(const DataConvArgs &a) {
 }
 
 constexpr int64_t kCUs = 256;
-// flop/s of one 128x128 workgroup (two share a CU): LDS-DMA kernel and
-// register-staged kernel
-#ifndef FG_RATE_SMALL_DMA
-#define FG_RATE_SMALL_DMA 1.3e12
-#endif
-constexpr double kRateSmallDma = FG_RATE_SMALL_DMA;
+// flop/s of one 128x128 workgroup of the LDS-DMA kernel, in the units of
+// the 256x256 rate below: alone on its CU (a launch of at most one
+// workgroup per CU), and with a second one sharing the CU. Timed on the
+// network's 16x16 and 32x32 layers at forced splits: a CU holding one
+// workgroup runs 1.25x as fast as one holding two (0.39 against 0.97 us
+// per workgroup stage), so splits that double the workgroups to fill the
+// second slot lose.
+constexpr double kRateSmallDmaAlone = 2.1e12, kRateSmallDmaPaired = 0.85e12;
+// The register-staged 128x128 kernel, alone or paired.
 constexpr double kRateSmallRegs = 1.3e12;
 
 }  // namespace
 
 // Split/tile choice by an estimate of the run time: resident workgroup
 // slots per GPU (one 256x256 workgroup or two 128x128 ones per CU), the
-// per-workgroup MFMA rate each reaches (measured on MI355X), waves of
+// per-workgroup MFMA rate each reaches (measured on MI355X; for 128x128
+// tiles it depends on whether the launch fits one workgroup per CU), waves of
 // workgroups with a fixed cost per wave (prologue and tile store, which one
 // workgroup per CU cannot overlap with its MFMA work), and the fp32
 // partials a split writes and re-reads.
@@ -730,10 +734,13 @@ struct TileCost {
   double partial_bw;            // B/s for fp32 partial traffic (8 B/element)
   double split_const;           // s, the reduction launch of a split
   double wave_const;            // s per wave of workgroups
+  double rate_small_alone;      // a 128x128 workgroup with its CU to itself
 };
 // Data convolutions: rates chosen by timing the network's layers.
 static TileCost data_cost(bool dma_small) {
-  return TileCost{3.0e12, dma_small ? kRateSmallDma : kRateSmallRegs, 6.0e12, 4e-6, 0.0};
+  return dma_small ? TileCost{3.0e12, kRateSmallDmaPaired, 6.0e12, 4e-6, 0.0,
+                              kRateSmallDmaAlone}
+                   : TileCost{3.0e12, kRateSmallRegs, 6.0e12, 4e-6, 0.0, kRateSmallRegs};
 }
 // Kernel gradient: a least-squares fit of this model to the DMA kernel's
 // times on the network's twelve kernel-gradient shapes at 1-8 splits
@@ -741,7 +748,7 @@ static TileCost data_cost(bool dma_small) {
 // 6.3 us per split launch; mean error 9%). The 128x128 rate is the
 // register-staged kernel's, which only shapes too small for 256x256 tiles
 // take.
-constexpr TileCost kWgradCost{6.35e12, 1.3e12, 4.05e12, 6.3e-6, 4.2e-6};
+constexpr TileCost kWgradCost{6.35e12, 1.3e12, 4.05e12, 6.3e-6, 4.2e-6, 1.3e12};
 
 TileChoice choose_tiles(int64_t tiles_big, int64_t tiles_small, int64_t nk,
                         int64_t out_elems, bool allow_big, const TileCost &cost,
@@ -753,9 +760,11 @@ TileChoice choose_tiles(int64_t tiles_big, int64_t tiles_small, int64_t nk,
     const int64_t tiles = big ? tiles_big : tiles_small;
     const int64_t slots = big ? kCUs : 2 * kCUs;
     const int t = big ? 256 : 128;
-    const double rate = big ? cost.rate_big : cost.rate_small;
     for (int ns = 1; ns <= max_split; ++ns) {
       if (ns > 1 && (nk + ns - 1) / ns < 4) break;  // >= 4 slices per split
+      const double rate = big                 ? cost.rate_big
+                          : tiles * ns <= kCUs ? cost.rate_small_alone
+                                               : cost.rate_small;
       const int64_t waves = (tiles * ns + slots - 1) / slots;
       const int64_t nk_split = (nk + ns - 1) / ns;
       const double t_block = 2.0 * t * t * BK * (double)nk_split / rate;
