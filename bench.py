@@ -138,9 +138,14 @@ def kernel_source(kernel):
 
 
 def source_hash(kernel):
+    """Hash of the source file that defines `kernel` and of the one that
+    holds the tile and split planner (which decides the layers and splits a
+    kernel runs, and so its bytes per launch)."""
     import hashlib
-    src = os.path.join(ROOT, "paper_1909_11150_amd", "csrc", kernel_source(kernel))
-    return hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for f in dict.fromkeys((kernel_source(kernel), "conv_igemm.hip")):
+        h.update(open(os.path.join(ROOT, "paper_1909_11150_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
 
 
 def summarize_stats(path):
@@ -358,8 +363,8 @@ def recorded_traffic(kernel, workload="fcn"):
     """HBM bytes per launch of `kernel` in the workload's step, from
     profiles/<workload>_step_hbm_traffic.md (rocprofv3 FETCH_SIZE +
     WRITE_SIZE, scaled by a plain copy's reading), or None when no record
-    exists for it or the kernel's source file has changed since the counters
-    were taken."""
+    exists for it or the kernel's source file or the planner's has changed
+    since the counters were taken."""
     path = os.path.join(ROOT, "profiles", f"{workload}_step_hbm_traffic.md")
     try:
         lines = open(path).read().splitlines()
