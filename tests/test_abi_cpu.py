@@ -6,6 +6,7 @@ import json
 import os
 import re
 
+import numpy as np
 import pytest
 
 import paper_1909_11150_amd as fg
@@ -126,6 +127,31 @@ def test_workspace_query_and_shortfall(L):
                                FAKE + (1 << 32), need - 4, None) == fg.FG_EWORKSPACE
     head = fg.ConvDesc.make(4, 256, 256, 256, 1, 1, 1, 1, 0)
     assert L.fg_conv_workspace_bytes(ref(head), fg.OP_BWD_WEIGHT) > 0
+
+
+def test_small_tile_plans_keep_one_workgroup_per_cu(L):
+    """The 16x16 layers' passes on 128x128 tiles split their reduction only
+    as far as one workgroup per CU (at most 256 workgroups): such a
+    workgroup, alone on its CU, runs faster than two sharing one, so filling
+    the second slot with more splits loses."""
+    from paper_1909_11150_amd.fcn import convt_dx_desc, fwd_desc
+    layers = {l.name: l for l in synth.fcn_layers()}
+    cases = {  # pass: (descriptor, op, output shape, 128x128 tiles, expected splits)
+        "E4a.fwd": (fwd_desc(layers["E4a"]), fg.OP_FWD, layers["E4a"].y_shape, 64, 4),
+        "E4b.fwd": (fwd_desc(layers["E4b"]), fg.OP_FWD, layers["E4b"].y_shape, 64, 4),
+        "E4b.dx": (fwd_desc(layers["E4b"]), fg.OP_BWD_DATA, layers["E4b"].x_shape, 64, 4),
+        "E4a.dx": (fwd_desc(layers["E4a"]), fg.OP_BWD_DATA, layers["E4a"].x_shape, 256, 1),
+        "D4T.fwd": (fwd_desc(layers["D4T"]), fg.OP_CONVT, layers["D4T"].y_shape, 256, 1),
+    }
+    for name, (d, op, shape, tiles, splits) in cases.items():
+        kern = fg.kernel_name(d, op)
+        assert kern.startswith("data_conv_dma_kernel<128,"), (name, kern)
+        ws = L.fg_conv_workspace_bytes(ctypes.byref(d), op)
+        got = ws // (4 * int(np.prod(shape))) if ws else 1
+        assert got == splits and tiles * got <= 256, (name, got)
+    # the transposed convolution's input gradient keeps 256x256 tiles
+    assert fg.kernel_name(convt_dx_desc(layers["D4T"]), fg.OP_FWD).startswith(
+        "data_conv_dma_kernel<true")
 
 
 def test_out_dims_match_layer_table():
