@@ -524,8 +524,15 @@ def _smi_sample():
         return None
     if r.returncode != 0:
         return None
+    return parse_smi_metric(r.stdout)
+
+
+def parse_smi_metric(text):
+    """Socket power and per-XCD GFX clocks from the text of `amd-smi metric
+    -p -c`: the SOCKET_POWER line, and the CLK line of each section whose
+    header (a line like "GFX_3:") names a GFX domain. None without clocks."""
     power, gfx, sec = None, [], None
-    for ln in r.stdout.splitlines():
+    for ln in text.splitlines():
         t = ln.strip()
         if t.startswith("SOCKET_POWER:"):
             v = t.split(":", 1)[1].split()[0]
