@@ -886,15 +886,35 @@ def _pass_bytes(L):
     return [2 * (nx + nw + ny), 2 * (ny + nw + nx), 2 * (nx + ny + nw)]
 
 
+def _chain_outputs(ch):
+    import numpy as np
+    return [t.cpu().numpy().view(np.uint16).copy() for t in ch.acts[1:] + ch.g + ch.dw]
+
+
 def small_configs_bench(steps=50, warmup=5):
     """The single conv, the encoder block and the decoder block (fwd + full
     bwd, one stream), timed with HIP events around each whole pass; each
     against its own roofline: the sum over its ops of max(flops / MFMA
-    peak, minimum bytes / HBM peak)."""
+    peak, minimum bytes / HBM peak). These passes are short enough that the
+    host's launch calls bound them; the same passes captured once in a HIP
+    graph and replayed give the GPU's own time (`graph_*`), after checking
+    that every replay reproduces the eager pass bit for bit."""
+    import numpy as np
     import torch
 
     import synth
     from paper_1909_11150_amd.fcn import Chain
+
+    def timed(fn):
+        evs = [(_ev(), _ev()) for _ in range(steps)]
+        for e0, e1 in evs:
+            e0.record()
+            fn()
+            e1.record()
+        torch.cuda.synchronize()
+        ts = sorted(e0.elapsed_time(e1) * 1e-3 for e0, e1 in evs)
+        return ts[len(ts) // 2], ts[0]
+
     res = []
     for wl in (synth.single_conv(), synth.encoder_block(), synth.decoder_block()):
         ch = Chain(wl.layers, wl.weights, wl.x)
@@ -904,24 +924,45 @@ def small_configs_bench(steps=50, warmup=5):
         for L in wl.layers:
             for b in _pass_bytes(L):
                 roof += max(L.flops / (MFMA_F16_PEAK_TFLOPS * 1e12), b / (HBM_PEAK_GBPS * 1e9))
+
+        def step():
+            ch.forward()
+            ch.backward()
         for _ in range(warmup):
-            ch.forward()
-            ch.backward()
-        evs = [(_ev(), _ev()) for _ in range(steps)]
-        for e0, e1 in evs:
-            e0.record()
-            ch.forward()
-            ch.backward()
-            e1.record()
-        torch.cuda.synchronize()
-        ts = sorted(e0.elapsed_time(e1) * 1e-3 for e0, e1 in evs)
-        med = ts[len(ts) // 2]
+            step()
+        med, best = timed(step)
+        ref = _chain_outputs(ch)
+        # the same pass as a HIP graph, captured on a side stream
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step()
+        same = True
+        for _ in range(3):  # replays between eager passes and synchronisations
+            for t in ch.acts[1:] + ch.g[:-1] + ch.dw:
+                t.zero_()
+            g.replay()
+            torch.cuda.synchronize()
+            same &= all(np.array_equal(a, b) for a, b in zip(ref, _chain_outputs(ch)))
+            step()
+            torch.cuda.synchronize()
+        for _ in range(warmup):
+            g.replay()
+        gmed, gbest = timed(g.replay)
         res.append({"config": wl.name, "gflop": round(flops / 1e9, 3),
-                    "median_us": round(med * 1e6, 2), "best_us": round(ts[0] * 1e6, 2),
+                    "median_us": round(med * 1e6, 2), "best_us": round(best * 1e6, 2),
                     "tflops": round(flops / med / 1e12, 1),
                     "roofline_us": round(roof * 1e6, 2),
-                    "frac_of_roofline": round(roof / med, 4)})
-        del ch
+                    "frac_of_roofline": round(roof / med, 4),
+                    "graph_median_us": round(gmed * 1e6, 2),
+                    "graph_tflops": round(flops / gmed / 1e12, 1),
+                    "graph_frac_of_roofline": round(roof / gmed, 4),
+                    "graph_replays_bit_exact": bool(same)})
+        del g, ch
     return res
 
 
