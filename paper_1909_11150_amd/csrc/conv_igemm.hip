@@ -557,6 +557,45 @@ __global__ __launch_bounds__(256) void split_reduce_wide_kernel(
   }
 }
 
+// Same sum for a moderate number of longer partials (more than
+// kMaxSerialSplit splits): each workgroup covers 64 outputs as 16 groups of
+// 4, with 16 lanes per group; lane j adds splits j, j + 16, ... in order,
+// then a fixed-shape tree combines the 16 lane sums. (The serial sum of
+// split_reduce_kernel would wait on its many loads one by one.)
+constexpr int kMaxSerialSplit = 16;
+__global__ __launch_bounds__(256) void split_reduce_multi_kernel(
+    const float *part, int nsplit, int64_t len, uint16_t *out, int32_t *flag) {
+  __shared__ f32x4 red[16][16];  // [lane][group]
+  const int grp = threadIdx.x & 15, lane = threadIdx.x >> 4;
+  const int64_t i4 = ((int64_t)blockIdx.x * 16 + grp) * 4;
+  f32x4 s = {0.f, 0.f, 0.f, 0.f};
+  if (i4 < len)
+    for (int k = lane; k < nsplit; k += 16) {
+      const f32x4 v = *reinterpret_cast<const f32x4 *>(part + (size_t)k * len + i4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) s[e] += v[e];
+    }
+  red[lane][grp] = s;
+  __syncthreads();
+  for (int w = 8; w > 0; w >>= 1) {
+    if (lane < w) {
+      f32x4 a = red[lane][grp], b = red[lane + w][grp];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) a[e] += b[e];
+      red[lane][grp] = a;
+    }
+    __syncthreads();
+  }
+  bool bad = false;
+  if (lane == 0 && i4 < len) {
+    const f32x4 t = red[0][grp];
+    const u32x2 h = to_h4(t[0], t[1], t[2], t[3]);
+    bad = nonfinite_h2(h[0]) | nonfinite_h2(h[1]);
+    *reinterpret_cast<u32x2 *>(out + i4) = h;
+  }
+  if (flag) flag_nonfinite(flag, bad);
+}
+
 // ---------------------------------------------------------------------------
 // Single-output-channel 1x1 convolution (the network head): bandwidth-bound,
 // so no MFMA. L lanes (a power of two) cooperate on one position.
@@ -881,6 +920,13 @@ const char *data_conv_kernel_name(const DataConvArgs &a, bool w_kmajor) {
 }
 
 // max_ws_bytes bounds the fp32 partials of a split (and so the split count).
+// A kernel gradient whose R*S*C or K is below 256 (so no 256 x 256 tile)
+// with a long reduction needs many splits to fill the GPU: a 1x1 layer of
+// 128 x 64 has a single 128 x 128 tile. Such shapes may split up to
+// kMaxWgradSplit ways (at least 4 stages each); the others keep the cap of
+// 16, under which the network's layers were fitted and timed.
+constexpr int kMaxWgradSplit = 256;
+
 static TileChoice wgrad_choice(const fg_conv_desc &d, int32_t p, int32_t q,
                                size_t max_ws_bytes) {
   const int64_t rsc = (int64_t)d.r * d.s * d.c;
@@ -889,9 +935,11 @@ static TileChoice wgrad_choice(const fg_conv_desc &d, int32_t p, int32_t q,
   const int64_t ts = ((rsc + 127) / 128) * ((d.k + 127) / 128);
   const size_t per_split = (size_t)d.k * rsc * sizeof(float);
   const size_t cap = max_ws_bytes / per_split;
-  const int max_split = cap >= 16 ? 16 : (cap < 2 ? 1 : (int)cap);
-  return choose_tiles(tb, ts, (mtot + BK - 1) / BK, (int64_t)d.k * rsc,
-                      rsc >= 256 && d.k >= 256, kWgradCost, max_split);
+  const bool allow_big = rsc >= 256 && d.k >= 256;
+  const int limit = allow_big ? 16 : kMaxWgradSplit;
+  const int max_split = cap >= (size_t)limit ? limit : (cap < 2 ? 1 : (int)cap);
+  return choose_tiles(tb, ts, (mtot + BK - 1) / BK, (int64_t)d.k * rsc, allow_big,
+                      kWgradCost, max_split);
 }
 
 const char *wgrad_kernel_name(const fg_conv_desc &d) {
@@ -958,6 +1006,11 @@ hipError_t launch_wgrad(const WgradArgs &a, bool big, hipStream_t st) {
   if (e == hipSuccess) e = prof_end(st);
   if (e != hipSuccess || !split) return e;
   const int64_t len = (int64_t)a.k * rsc;
+  if (a.nsplit > kMaxSerialSplit) {
+    hipLaunchKernelGGL(split_reduce_multi_kernel, dim3((unsigned)((len + 63) / 64)),
+                       dim3(256), 0, st, a.part, a.nsplit, len, a.dw, a.flag);
+    return hipGetLastError();
+  }
   dim3 g2((unsigned)((len / 4 + 255) / 256));
   hipLaunchKernelGGL(split_reduce_kernel, g2, dim3(256), 0, st, a.part,
                      a.nsplit, len, a.dw, a.flag);

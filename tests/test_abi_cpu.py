@@ -154,6 +154,24 @@ def test_small_tile_plans_keep_one_workgroup_per_cu(L):
         "data_conv_dma_kernel<true")
 
 
+def test_kernel_gradients_without_big_tiles_split_widely(L):
+    """A kernel gradient whose R*S*C or K is below 256 has only 128x128
+    tiles, and few of them: it may split its reduction beyond 16 ways to
+    fill the GPU; shapes with 256x256 tiles (the network's layers) keep 16
+    at most."""
+    def splits(d):
+        ws = L.fg_conv_workspace_bytes(ctypes.byref(d), fg.OP_BWD_WEIGHT)
+        return ws // (4 * d.k * d.r * d.s * d.c) if ws else 1
+    one_by_one = fg.ConvDesc.make(8, 64, 64, 128, 64, 1, 1, 1, 0)  # one 128x128 tile
+    assert fg.kernel_name(one_by_one, fg.OP_BWD_WEIGHT) == "wgrad_kernel<Cfg<128, 128, 2, 2>, true>"
+    assert splits(one_by_one) > 16
+    from paper_1909_11150_amd.fcn import convt_dx_desc, fwd_desc
+    for l in synth.fcn_layers():
+        d = fwd_desc(l) if l.kind == "conv" else convt_dx_desc(l)
+        if d.k * d.r * d.s * d.c >= 256 * 256:
+            assert splits(d) <= 16, l.name
+
+
 def test_out_dims_match_layer_table():
     for L_ in synth.fcn_layers():
         n, h, w, c = L_.x_shape
