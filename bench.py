@@ -298,13 +298,49 @@ def summarize_mfma(d):
         print(f"| `{k}` | {n} | {util / n:.1f}% | {fl / n / 1e9:.2f} | {conf} |")
 
 
-def op_bench(label, steps, warmup):
-    """Time one library call in isolation on seeded full-size inputs."""
+def _op_call(label, rng):
+    """(callable, algorithmic flops, kernel name) for one pass `LAYER.fwd|dx|dW`
+    of the encoder-decoder on seeded full-size inputs."""
     import torch
 
     import paper_1909_11150_amd as fg
     import synth
     from paper_1909_11150_amd import fcn
+    name, pas = label.split(".")
+    L = {l.name: l for l in synth.fcn_layers()}[name]
+    x = torch.from_numpy(np.maximum(synth.normal(rng, L.x_shape), np.float16(0))).cuda()
+    w = torch.from_numpy(synth.normal(rng, L.w_shape, synth.he_std(L))).cuda()
+    dy = torch.from_numpy(synth.normal(rng, L.y_shape)).cuda()
+    y = torch.empty(L.y_shape, dtype=torch.float16, device="cuda")
+    dx = torch.empty(L.x_shape, dtype=torch.float16, device="cuda")
+    dw = torch.empty(L.w_shape, dtype=torch.float16, device="cuda")
+    ws = torch.empty(max(16, fcn.chain_workspace_bytes([L])), dtype=torch.uint8,
+                     device="cuda")
+    d, dd = fcn.fwd_desc(L), fcn.convt_dx_desc(L)
+    conv = L.kind == "conv"
+    calls = {
+        "fwd": (lambda: fg.conv2d_fwd(d, x, w, y, fg.EPI_RELU, None, ws),
+                fg.kernel_name(d, fg.OP_FWD)) if conv else
+               (lambda: fg.conv_transpose2d_fwd(d, x, w, y, fg.EPI_RELU, None, ws),
+                fg.kernel_name(d, fg.OP_CONVT)),
+        "dx": (lambda: fg.conv2d_bwd_data(d, dy, w, dx, fg.EPI_GATE, x, ws),
+               fg.kernel_name(d, fg.OP_BWD_DATA)) if conv else
+              (lambda: fg.conv2d_fwd(dd, dy, w, dx, fg.EPI_GATE, x, ws),
+               fg.kernel_name(dd, fg.OP_FWD)),
+        "dW": (lambda: fg.conv2d_bwd_weight(d, x, dy, dw, ws),
+               fg.kernel_name(d, fg.OP_BWD_WEIGHT)) if conv else
+              (lambda: fg.conv2d_bwd_weight(dd, dy, x, dw, ws),
+               fg.kernel_name(dd, fg.OP_BWD_WEIGHT)),
+    }
+    fn, kern = calls[pas]
+    return fn, L.flops, kern
+
+
+def op_bench(label, steps, warmup):
+    """Time one library call in isolation on seeded full-size inputs."""
+    import torch
+
+    import paper_1909_11150_amd as fg
     rng = np.random.default_rng(5)
     if label == "copy":
         n = 128 * 1024 * 1024  # 256 MiB of fp16 in, 256 MiB out
@@ -313,34 +349,8 @@ def op_bench(label, steps, warmup):
         fn = lambda: fg.grad_group_pack([src], [0], dst)
         work, unit, kern = 4 * n, "GB/s", "copy_pieces_kernel<2>"
     else:
-        name, pas = label.split(".")
-        L = {l.name: l for l in synth.fcn_layers()}[name]
-        x = torch.from_numpy(np.maximum(synth.normal(rng, L.x_shape), np.float16(0))).cuda()
-        w = torch.from_numpy(synth.normal(rng, L.w_shape, synth.he_std(L))).cuda()
-        dy = torch.from_numpy(synth.normal(rng, L.y_shape)).cuda()
-        y = torch.empty(L.y_shape, dtype=torch.float16, device="cuda")
-        dx = torch.empty(L.x_shape, dtype=torch.float16, device="cuda")
-        dw = torch.empty(L.w_shape, dtype=torch.float16, device="cuda")
-        ws = torch.empty(max(16, fcn.chain_workspace_bytes([L])), dtype=torch.uint8,
-                         device="cuda")
-        d, dd = fcn.fwd_desc(L), fcn.convt_dx_desc(L)
-        conv = L.kind == "conv"
-        calls = {
-            "fwd": (lambda: fg.conv2d_fwd(d, x, w, y, fg.EPI_RELU, None, ws),
-                    fg.kernel_name(d, fg.OP_FWD)) if conv else
-                   (lambda: fg.conv_transpose2d_fwd(d, x, w, y, fg.EPI_RELU, None, ws),
-                    fg.kernel_name(d, fg.OP_CONVT)),
-            "dx": (lambda: fg.conv2d_bwd_data(d, dy, w, dx, fg.EPI_GATE, x, ws),
-                   fg.kernel_name(d, fg.OP_BWD_DATA)) if conv else
-                  (lambda: fg.conv2d_fwd(dd, dy, w, dx, fg.EPI_GATE, x, ws),
-                   fg.kernel_name(dd, fg.OP_FWD)),
-            "dW": (lambda: fg.conv2d_bwd_weight(d, x, dy, dw, ws),
-                   fg.kernel_name(d, fg.OP_BWD_WEIGHT)) if conv else
-                  (lambda: fg.conv2d_bwd_weight(dd, dy, x, dw, ws),
-                   fg.kernel_name(dd, fg.OP_BWD_WEIGHT)),
-        }
-        fn, kern = calls[pas]
-        work, unit = L.flops, "TFLOP/s"
+        fn, work, kern = _op_call(label, rng)
+        unit = "TFLOP/s"
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
@@ -615,6 +625,10 @@ def _gemm_time(m, n, k, zero_a=False, zero_b=False, reps=20):
     return ts[len(ts) // 2] * 1e-3
 
 
+SUSTAINED_PASSES = ("E1b.fwd", "E2b.dx", "E1b.dW", "D1T.dW")
+NOMINAL_GFX_MHZ = 2400  # the clock the published MFMA peak assumes
+
+
 def ceiling_bench():
     """The practical MFMA ceiling of this GPU, beside the step:
     - clocks and socket power while the three-stream step runs back to back,
@@ -691,6 +705,25 @@ def ceiling_bench():
                          "gemm_us": round(t_g * 1e6, 1),
                          "gemm_tflops": round(L.flops / t_g / 1e12, 1)})
     out["passes"] = rows
+    # four large passes back to back, each alone: the clock each one gets,
+    # and its rate against the peak scaled to that clock
+    rng = np.random.default_rng(5)
+    sus = []
+    for label in SUSTAINED_PASSES:
+        fn, fl, kern = _op_call(label, rng)
+        for _ in range(3):
+            fn()
+        ms_p, clk_p = sustained(fn, 3.0)
+        tf = fl / ms_p / 1e9
+        at_clk = (MFMA_F16_PEAK_TFLOPS * clk_p["gfx_MHz_median"] / NOMINAL_GFX_MHZ
+                  if clk_p["gfx_MHz_median"] else None)
+        sus.append({"pass": label, "kernel": kern, "us": round(ms_p * 1e3, 1),
+                    "tflops": round(tf, 1),
+                    "frac_of_peak_at_clock": round(tf / at_clk, 3) if at_clk else None,
+                    **clk_p})
+        del fn
+        torch.cuda.empty_cache()
+    out["sustained_passes"] = sus
     t_o = sum(r["ours_us"] for r in rows)
     t_g = sum(r["gemm_us"] for r in rows)
     out["passes_total"] = {"ours_us": round(t_o, 1), "gemm_us": round(t_g, 1),
@@ -715,6 +748,15 @@ def summarize_ceiling(path):
               f"{100 * v['tflops'] / MFMA_F16_PEAK_TFLOPS:.1f}% | {v['gfx_MHz_median']} "
               f"({v['gfx_MHz_min']}-{v['gfx_MHz_max']}) | {v['socket_power_W_median']} | "
               f"{v['samples']} |")
+    if "sustained_passes" in d:
+        print()
+        print("| pass, back to back | kernel | us per call | TFLOP/s | GFX clock median "
+              "(min-max), MHz | socket power median, W | fraction of the peak at that clock |")
+        print("|---|---|---:|---:|---|---:|---:|")
+        for v in d["sustained_passes"]:
+            print(f"| {v['pass']} | `{v['kernel']}` | {v['us']} | {v['tflops']} | "
+                  f"{v['gfx_MHz_median']} ({v['gfx_MHz_min']}-{v['gfx_MHz_max']}) | "
+                  f"{v['socket_power_W_median']} | {v['frac_of_peak_at_clock']} |")
     print()
     print("| pass | GEMM M x N x K | this library, us | TFLOP/s | vendor GEMM, us | TFLOP/s "
           "| ratio |")

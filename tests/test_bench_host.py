@@ -101,3 +101,30 @@ def test_traffic_record_is_keyed_by_kernel_and_planner_sources(tmp_path, monkeyp
     # an edit to the planner's file invalidates the record
     (csrc / "conv_igemm.hip").write_bytes(b"// edited\n" + (csrc / "conv_igemm.hip").read_bytes())
     assert bench.recorded_traffic(k) is None
+
+
+def test_ceiling_summary_prints_every_section(tmp_path, capsys):
+    """summarize_ceiling turns the --ceiling JSON line into the three tables
+    of the committed ceiling profile; the total row's ratio is the vendor
+    time over this library's."""
+    clk = {"samples": 9, "gfx_MHz_median": 1920, "gfx_MHz_min": 1850, "gfx_MHz_max": 2010,
+           "socket_power_W_median": 1398.0}
+    d = {"step": {"ms": 5.2, "tflops": 1060.0, **clk},
+         "gemm_8192": {"ms": 0.86, "tflops": 1280.0, **clk},
+         "passes": [{"pass": "E1b.fwd", "gemm_mnk": [65536, 512, 4608], "ours_us": 226.9,
+                     "ours_tflops": 1362.9, "gemm_us": 264.8, "gemm_tflops": 1167.8}],
+         "passes_total": {"ours_us": 200.0, "gemm_us": 250.0, "ours_tflops": 1.0,
+                          "gemm_tflops": 1.0},
+         "sustained_passes": [{"pass": "E1b.dW", "kernel": "wgrad_dma_kernel<true>",
+                               "us": 251.0, "tflops": 1232.0, "frac_of_peak_at_clock": 0.616,
+                               **clk}]}
+    path = tmp_path / "ceiling.json"
+    path.write_text("warm-up text\n" + json.dumps(d) + "\n")
+    bench.summarize_ceiling(str(path))
+    out = capsys.readouterr().out
+    assert "| encoder-decoder step, 3 streams | 5.2000 | 1060.0 | 42.4% | 1920 (1850-2010)" in out
+    assert "the same, A about half zero" not in out  # absent runs are left out
+    assert "| E1b.dW | `wgrad_dma_kernel<true>` | 251.0 | 1232.0 | 1920 (1850-2010) " \
+           "| 1398.0 | 0.616 |" in out
+    assert "| E1b.fwd | 65536 x 512 x 4608 | 226.9 |" in out
+    assert out.rstrip().endswith("| 1.25 |")
