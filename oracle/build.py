@@ -13,12 +13,15 @@ OUT = os.path.join(HERE, "liboracle_conv.so")
 
 
 def build(verbose=False):
+    # a temporary name of this process's own, renamed into place: builds in
+    # concurrent processes (parallel test workers) do not clobber each other
+    tmp = f"{OUT}.{os.getpid()}.tmp"
     cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11",
-           "-fno-fast-math", "-ffp-contract=off", SRC, "-o", OUT + ".tmp"]
+           "-fno-fast-math", "-ffp-contract=off", SRC, "-o", tmp]
     if verbose:
         print(" ".join(cmd))
     subprocess.run(cmd, check=True)
-    os.replace(OUT + ".tmp", OUT)
+    os.replace(tmp, OUT)
     return OUT
 
 

@@ -54,12 +54,12 @@ def build(verbose=False, jobs=None):
             failed.append(src)
     if failed:
         raise RuntimeError(f"hipcc failed for {failed}")
-    cmd = [hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o",
-           LIB + ".tmp"]
+    tmp = f"{LIB}.{os.getpid()}.tmp"  # renamed into place when linked
+    cmd = [hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(LIB + ".tmp", LIB)
+    os.replace(tmp, LIB)
     return LIB
 
 
