@@ -400,3 +400,10 @@ def test_noalloc_kernel_gradient_validates_before_any_device_call(L):
                                        None) == fg.FG_EINVAL
     assert L.conv2d_bwd_weight_noalloc(ref(_desc(c=12)), FAKE, FAKE + (1 << 20),
                                        FAKE + (1 << 22), None) == fg.FG_EUNSUPPORTED
+
+
+def test_random_shape_sweep_reaches_every_kernel_family(L):
+    """The seeded shapes of the GPU sweep take every convolution kernel
+    family, non-square kernels, strided input gradients and empty phases."""
+    import test_gpu_sweep
+    test_gpu_sweep.check_coverage()
