@@ -228,3 +228,69 @@ def test_random_shape_convt_parity(t):
     if epi != "none":
         ref = _epilogue(ref, epi, g)
     conv_parity(got, ref, f"{name} {epi} ({kern})")
+
+
+SLICED = CASES[::4]
+
+
+@pytest.mark.parametrize("case", SLICED, ids=[_name(c) for c in SLICED])
+def test_random_shape_channel_slices(case):
+    """The same pass with its output in a channel slice of a wider buffer
+    (pixel stride = channels + 8a, slice at channel 8b, b <= a), and the
+    forward pass and kernel gradient reading x from such a slice (the
+    layouts a dense block's concatenation uses): the slice holds the dense
+    call's bits and every other channel keeps its own."""
+    op, (n, h, w, c, k, r, s, st, pd) = case
+    name = _name(case)
+    rng = np.random.default_rng(zlib.crc32(("slice" + name).encode()))
+    p, q = _out(h, pd, r, st), _out(w, pd, s, st)
+    a_in, a_out = (int(v) for v in rng.integers(0, 4, size=2))
+    b_in, b_out = int(rng.integers(0, a_in + 1)), int(rng.integers(0, a_out + 1))
+    ld_in, ld_out = c + 8 * a_in, (k if op != DX else c) + 8 * a_out
+    dense = fg.ConvDesc.make(n, h, w, c, k, r, s, st, pd)
+    # the output's pixel stride: y_ld for the forward pass, x_ld for the
+    # input gradient; x read from a slice by the forward pass and kernel gradient
+    if op == FWD:
+        sliced = fg.ConvDesc.make(n, h, w, c, k, r, s, st, pd, x_ld=ld_in, y_ld=ld_out)
+    elif op == DX:
+        sliced = fg.ConvDesc.make(n, h, w, c, k, r, s, st, pd, x_ld=ld_out)
+    else:
+        sliced = fg.ConvDesc.make(n, h, w, c, k, r, s, st, pd, x_ld=ld_in)
+    kern = fg.kernel_name(dense, op)
+    assert fg.kernel_name(sliced, op) == kern
+    print(f"{name}: {kern}, in ld {ld_in} at {8 * b_in}, out ld {ld_out} at {8 * b_out}",
+          flush=True)
+    x = synth.uniform(rng, (n, h, w, c))
+    W = synth.normal(rng, (k, r, s, c), np.sqrt(2.0 / (r * s * c)))
+    dy = synth.uniform(rng, (n, p, q, k))
+    # the wide input: x in channels [8 b_in, 8 b_in + c), other channels random
+    wide_in = synth.uniform(rng, (n, h, w, ld_in))
+    wide_in[..., 8 * b_in:8 * b_in + c] = x
+    x_wide = dev(wide_in)
+    x_slice = x_wide.view(-1)[8 * b_in:]  # the slice's first element
+    if op == DW:
+        ref, got = empty16(W.shape), empty16(W.shape)
+        fg.conv2d_bwd_weight(dense, dev(x), dev(dy), ref, workspace(dense, op))
+        fg.conv2d_bwd_weight(sliced, x_slice, dev(dy), got, workspace(sliced, op))
+        assert np.array_equal(host(got).view(np.uint16), host(ref).view(np.uint16)), name
+        return
+    oshape = (n, p, q, k) if op == FWD else (n, h, w, c)
+    och = oshape[3]
+    fill = synth.uniform(rng, oshape[:3] + (ld_out,))
+    out_wide = dev(fill)
+    out_slice = out_wide.view(-1)[8 * b_out:]
+    ref = empty16(oshape)
+    if op == FWD:
+        fg.conv2d_fwd(dense, dev(x), dev(W), ref, fg.EPI_RELU, None, workspace(dense, op))
+        fg.conv2d_fwd(sliced, x_slice, dev(W), out_slice, fg.EPI_RELU, None,
+                      workspace(sliced, op))
+    else:
+        fg.conv2d_bwd_data(dense, dev(dy), dev(W), ref, fg.EPI_NONE, None,
+                           workspace(dense, op))
+        fg.conv2d_bwd_data(sliced, dev(dy), dev(W), out_slice, fg.EPI_NONE, None,
+                           workspace(sliced, op))
+    got = host(out_wide).view(np.uint16)
+    inside = np.zeros(ld_out, bool)
+    inside[8 * b_out:8 * b_out + och] = True
+    assert np.array_equal(got[..., inside], host(ref).view(np.uint16)), name
+    assert np.array_equal(got[..., ~inside], fill.view(np.uint16)[..., ~inside]), name
