@@ -11,7 +11,7 @@ that the planner's choices meet shapes nobody picked: empty output phases of
 strided input gradients, images smaller than the kernel, single-tile and
 ragged tiles, split and unsplit reductions. Small cases are compared in
 full; large ones (on the LDS-DMA, halo and split kernels) on sampled outputs
-plus all corners. The parity rule is the one every convolution test uses
+plus all corners; each call is made twice and must give the same bits. The parity rule is the one every convolution test uses
 (rel_L2 <= 5e-3 and max_abs <= 2e-2 * RMS against the fp64 oracle on the
 same fp16 inputs).
 """
@@ -158,8 +158,9 @@ def test_random_shape_parity(case):
     if op == FWD:
         out = empty16((n, p, q, k))
         gate = synth.uniform(rng, out.shape) if epi == "gate" else None
-        fg.conv2d_fwd(d, dev(x), dev(W), out, EPI[epi],
-                      dev(gate) if gate is not None else None, ws)
+        call = lambda o: fg.conv2d_fwd(d, dev(x), dev(W), o, EPI[epi],
+                                       dev(gate) if gate is not None else None, ws)
+        call(out)
         if full:
             ref = oracle.conv2d_fwd(x, W, st, pd)
         else:
@@ -168,8 +169,9 @@ def test_random_shape_parity(case):
     elif op == DX:
         out = empty16(x.shape)
         gate = synth.uniform(rng, out.shape) if epi == "gate" else None
-        fg.conv2d_bwd_data(d, dev(dy), dev(W), out, EPI[epi],
-                           dev(gate) if gate is not None else None, ws)
+        call = lambda o: fg.conv2d_bwd_data(d, dev(dy), dev(W), o, EPI[epi],
+                                            dev(gate) if gate is not None else None, ws)
+        call(out)
         if full:
             ref = oracle.conv2d_bwd_data(dy, W, x.shape, st, pd)
         else:
@@ -177,13 +179,19 @@ def test_random_shape_parity(case):
             ref = oracle.conv2d_bwd_data_points(dy, W, x.shape, idx, st, pd)
     else:
         out = empty16(W.shape)
-        fg.conv2d_bwd_weight(d, dev(x), dev(dy), out, ws)
+        call = lambda o: fg.conv2d_bwd_weight(d, dev(x), dev(dy), o, ws)
+        call(out)
         if full:
             ref = oracle.conv2d_bwd_weight(x, dy, r, s, st, pd)
         else:
             idx = sample_indices(out.shape, SAMPLES, rng)
             ref = oracle.conv2d_bwd_weight_points(x, dy, r, s, idx, st, pd)
     got = host(out)
+    # a second call, into a fresh buffer, gives the same bits (every sum in
+    # a fixed order, split reductions included)
+    again = empty16(out.shape)
+    call(again)
+    assert np.array_equal(host(again).view(np.uint16), got.view(np.uint16)), _name(case)
     if not full:
         got = got.ravel()[idx]
     if epi != "none":
