@@ -302,3 +302,44 @@ def test_random_shape_channel_slices(case):
     inside[8 * b_out:8 * b_out + och] = True
     assert np.array_equal(got[..., inside], host(ref).view(np.uint16)), name
     assert np.array_equal(got[..., ~inside], fill.view(np.uint16)[..., ~inside]), name
+
+
+def draw_heads(seed=20191127, count=12):
+    """The K = 1 head (1x1, stride 1, no padding; its own bandwidth kernels):
+    (n, h, w, c) with c any multiple of 8 up to 2048."""
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < count:
+        t = (int(rng.integers(1, 5)), int(rng.integers(1, 300)), int(rng.integers(1, 300)),
+             8 * int(rng.integers(1, 257)))
+        if np.prod(t) <= 1 << 25:  # host memory of the fp64 oracle
+            out.append(t)
+    return out
+
+
+HEADS = draw_heads()
+
+
+@pytest.mark.parametrize("t", HEADS, ids=[f"head-n{n}-{h}x{w}-c{c}" for n, h, w, c in HEADS])
+def test_random_head_parity(t):
+    """Forward (ReLU'd activations as the head's input), input gradient
+    gated by the activations (one product per output: the oracle rounded
+    once to fp16, exactly) and kernel gradient (a sum over every position)."""
+    n, h, w, c = t
+    rng = np.random.default_rng(zlib.crc32(f"head{t}".encode()))
+    x = np.maximum(synth.uniform(rng, (n, h, w, c)), np.float16(0))
+    W = synth.normal(rng, (1, 1, 1, c), np.sqrt(2.0 / c))
+    dy = synth.uniform(rng, (n, h, w, 1))
+    d = fg.ConvDesc.make(n, h, w, c, 1, 1, 1, 1, 0)
+    print(f"head {t}: {fg.kernel_name(d, FWD)}, {fg.kernel_name(d, DX)}, "
+          f"{fg.kernel_name(d, DW)}", flush=True)
+    y = empty16((n, h, w, 1))
+    fg.conv2d_fwd(d, dev(x), dev(W), y, fg.EPI_NONE, None, workspace(d, FWD))
+    conv_parity(host(y), oracle.conv2d_fwd(x, W, 1, 0), f"head fwd {t}")
+    dx = empty16(x.shape)
+    fg.conv2d_bwd_data(d, dev(dy), dev(W), dx, fg.EPI_GATE, dev(x), workspace(d, DX))
+    ref = oracle.conv2d_bwd_data(dy, W, x.shape, 1, 0, epi="gate", gate=x)
+    np.testing.assert_array_equal(host(dx), ref.astype(np.float16))  # +0 == -0
+    dw = empty16(W.shape)
+    fg.conv2d_bwd_weight(d, dev(x), dev(dy), dw, workspace(d, DW))
+    conv_parity(host(dw), oracle.conv2d_bwd_weight(x, dy, 1, 1, 1, 0), f"head dW {t}")
