@@ -55,6 +55,10 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--settle-steps", type=int, default=200,
+                    help="untimed steps of the timed program run back to back before the "
+                         "warm-up steps (the first steps after the one-stream detail pass "
+                         "run 1-1.4%% slower than the steady state)")
     ap.add_argument("--no-cpu", action="store_true",
                     help="skip the CPU oracle baseline leg")
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
@@ -159,20 +163,21 @@ def summarize_stats(path):
               f"{float(r['MaxNs']) / 1e3:.2f} |")
 
 
-def summarize_trace(path, kernel, per_step, timed_steps, warmup):
+def summarize_trace(path, kernel, per_step, timed_steps, warmup, settle):
     """Launch durations of one kernel from a rocprofv3 kernel trace of the
     default bench command. The step program runs warmup + 4 one-stream steps
     (warm-up, two detail steps timing calls, two timing main kernels), then
-    warmup + timed_steps steps on the timed streams; launches of the kernel
-    by the measurements that follow (gradient path, small configurations)
-    come after those and are left out."""
+    settle + warmup + timed_steps steps on the timed streams; launches
+    of the kernel by the measurements that follow (single steps, the clock
+    sampling, gradient path, small configurations) come after those and are
+    left out."""
     import csv
     rows = [r for r in csv.DictReader(open(path))
             if short_kernel_name(r["Kernel_Name"]) == kernel]
     rows.sort(key=lambda r: int(r["Start_Timestamp"]))
     dur = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in rows]
     one = warmup + 4
-    total = one + warmup + timed_steps
+    total = one + settle + warmup + timed_steps
     step_dur = dur[:per_step * total]
     timed = step_dur[-per_step * timed_steps:]
     alone = step_dur[per_step * warmup:per_step * one]
@@ -626,6 +631,7 @@ def _gemm_time(m, n, k, zero_a=False, zero_b=False, reps=20):
 
 
 SUSTAINED_PASSES = ("E1b.fwd", "E2b.dx", "E1b.dW", "D1T.dW")
+STEP_STAT_REPS = 20
 NOMINAL_GFX_MHZ = 2400  # the clock the published MFMA peak assumes
 
 
@@ -1024,7 +1030,7 @@ def main():
         return
     if args.summarize_trace:
         summarize_trace(args.summarize_trace[0], args.summarize_trace[1],
-                        args.launches_per_step, args.steps, args.warmup)
+                        args.launches_per_step, args.steps, args.warmup, args.settle_steps)
         return
     if args.op:
         op_bench(args.op, args.steps, args.warmup)
@@ -1117,6 +1123,14 @@ def main():
     prog = ch.program(target, streams=args.streams)
     calls = prog.calls
     dom_idx = [i for i, c in enumerate(calls) if c.kernel == dom]
+    # settle: SETTLE_STEPS steps back to back (about a second) before the
+    # warm-up steps; the first steps after the one-stream detail pass run
+    # 1-1.4% slower than the steady state a training run is in
+    for i in range(args.settle_steps):
+        prog.run()
+        if i % 10 == 9:
+            prog.join()
+            torch.cuda.synchronize()
     for _ in range(args.warmup):
         prog.run()
     torch.cuda.synchronize()
@@ -1205,6 +1219,7 @@ def main():
         "grad_unscale_GBps_in_step": bw("unscale_vec_kernel"),
         "grad_unpack_GBps_in_step": bw("copy_pieces_kernel<4>"),
         "wall_s_timed": round(wall, 3),
+        "settle_steps_before_warmup": args.settle_steps,
         "roofline": roof,
         "roofline_alone": roof_alone,
     }
@@ -1223,6 +1238,24 @@ def main():
             "apply_overlap": "per layer, beside the next step's forward pass",
             "timed_updates_applied": ch.applied - applied0,
             "loss_scale_start": scale0, "loss_scale_end": ch.loss_scale}
+    # spread of single steps, after the timed region: each step between its
+    # own events on the main stream, its side streams joined before the end
+    # event (so no step overlaps the next, unlike the timed region's)
+    per_step = []
+    for _ in range(STEP_STAT_REPS):
+        e0, e1 = _ev(), _ev()
+        e0.record()
+        prog.run()
+        prog.join()
+        e1.record()
+        per_step.append((e0, e1))
+    torch.cuda.synchronize()
+    st = sorted(e0.elapsed_time(e1) for e0, e1 in per_step)
+    out["step_ms_stats"] = {
+        "reps": STEP_STAT_REPS, "median": round(st[len(st) // 2], 4),
+        "min": round(st[0], 4), "max": round(st[-1], 4),
+        "measured": "after the timed region: single steps, each between its own HIP "
+                    "events with its side streams joined, so no step overlaps the next"}
     under_load = None
     if not args.no_clocks:
         # clocks and power while the timed program runs back to back (after

@@ -52,12 +52,12 @@ def test_smi_parser_takes_socket_power_and_gfx_clocks_only():
 
 def test_trace_summary_separates_detail_and_timed_launches(tmp_path, capsys):
     """A kernel with 2 launches per step: warm-up 1 + 4 one-stream detail
-    steps, then 1 warm-up and 3 timed steps; launches after those (other
-    measurements) are left out."""
+    steps, then the settle steps, 1 warm-up and 3 timed steps; launches after
+    those (other measurements) are left out."""
     per, warm, timed = 2, 1, 3
     one = warm + 4
-    total = one + warm + timed
-    durs = ([10.0] * per * warm + [20.0] * per * 4 + [30.0] * per * warm +
+    total = one + 6 + warm + timed
+    durs = ([10.0] * per * warm + [20.0] * per * 4 + [25.0] * per * 6 + [30.0] * per * warm +
             [40.0] * per * timed + [99.0] * 5)
     path = tmp_path / "trace.csv"
     t = 1_000_000
@@ -70,7 +70,7 @@ def test_trace_summary_separates_detail_and_timed_launches(tmp_path, capsys):
             w.writerow(["fg::split_reduce_kernel(float const*, int, long, unsigned short*, "
                         "int*)", t + 100_000, t + 105_000])
             t += 200_000
-    bench.summarize_trace(str(path), "wgrad_dma_kernel<true>", per, timed, warm)
+    bench.summarize_trace(str(path), "wgrad_dma_kernel<true>", per, timed, warm, 6)
     out = capsys.readouterr().out
     assert f"{per * total} launches in the {total} steps" in out
     assert "one-stream detail steps: 8 launches, average 20.00 us" in out
