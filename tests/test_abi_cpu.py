@@ -407,3 +407,46 @@ def test_random_shape_sweep_reaches_every_kernel_family(L):
     family, non-square kernels, strided input gradients and empty phases."""
     import test_gpu_sweep
     test_gpu_sweep.check_coverage()
+
+
+def test_plain_c_consumer_builds_and_plans(L, tmp_path):
+    """The header compiles as C11 (gcc, warnings as errors) and a C program
+    linked against the library gets the oracle's group plan, the output
+    sizes, the workspace and kernel the binding reports, and FG_EINVAL for
+    null pointers; no GPU is touched."""
+    import shutil
+    import subprocess
+    import numpy as np
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("gcc not found")
+    exe = str(tmp_path / "abi_consumer")
+    libdir = os.path.dirname(fg.LIB_PATH)
+    subprocess.run([gcc, "-std=c11", "-Wall", "-Wextra", "-Werror",
+                    "-D__HIP_PLATFORM_AMD__", "-I", os.path.join(ROOT, "include"),
+                    "-I", "/opt/rocm/include",
+                    os.path.join(ROOT, "tests", "c_consumer", "abi_consumer.c"),
+                    "-L", libdir, "-lfcngrad", f"-Wl,-rpath,{libdir}", "-o", exe],
+                   check=True, timeout=120)
+    rng = np.random.default_rng(11)
+    numels = [int(v) for v in rng.integers(1, 200_000, size=40)]
+    cap, align = 1 << 20, 256
+    r = subprocess.run([exe, str(cap), str(align)], input=" ".join(map(str, numels)),
+                       capture_output=True, text=True, timeout=60, check=True)
+    lines = r.stdout.splitlines()
+    plan = G.plan_groups(numels, cap, align)
+    assert lines[0] == f"plan {len(plan)}"
+    want = {}
+    for gi, p in enumerate(plan):
+        for m, off in zip(p["members"], p["offsets"]):
+            want[m] = f"{gi} {off}"
+    assert lines[1:1 + len(numels)] == [want[i] for i in range(len(numels))]
+    rest = lines[1 + len(numels):]
+    assert rest[:len(plan)] == [str(p["numel"]) for p in plan]
+    kv = dict(ln.split(" ", 1) for ln in rest[len(plan):])
+    d = fg.ConvDesc.make(4, 256, 256, 256, 512, 3, 3, 2, 1)
+    assert kv["out_dims"] == "128 128 256 256"
+    assert kv["ws"] == str(fg.workspace_bytes(d, fg.OP_BWD_WEIGHT))
+    assert kv["kernel"] == fg.kernel_name(d, fg.OP_BWD_WEIGHT)
+    assert kv["einval"] == "OK"
+    assert kv["status"] == fg.status_string(fg.FG_EUNSUPPORTED)
