@@ -1036,8 +1036,9 @@ def main():
         op_bench(args.op, args.steps, args.warmup)
         return
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; "
-                          "--gpus must be 1 (multi-GPU sharding is design-only)"}))
+        print(json.dumps({"error": "the benchmark runs on one GPU only; --gpus must be 1 "
+                          "(the library and its step driver implement one GPU's share of "
+                          "the data-parallel step; sharding across GPUs is not built)"}))
         sys.exit(2)
     import torch
 
