@@ -232,7 +232,9 @@ fg_status conv_transpose2d_fwd(const fg_conv_desc *d, const uint16_t *x,
  * segment, and every element of [0, group_numel) not covered by a segment
  * is set to 0x0000. segs: host array of nseg (1..FG_MAX_SEGMENTS) fp16
  * sources, read during the call only; segments must lie inside the group
- * and must not overlap each other (FG_EINVAL). group: group_numel fp16. */
+ * and must not overlap each other (FG_EINVAL). A segment may have no
+ * elements (its ptr may then be NULL): it copies nothing, and its place is
+ * zero-filled like any uncovered element. group: group_numel fp16. */
 fg_status grad_group_pack(const fg_segment *segs, int32_t nseg,
                           uint16_t *group, uint64_t group_numel,
                           hipStream_t stream);
@@ -256,7 +258,9 @@ fg_status grad_flags_clear(int32_t *flags, int32_t n, hipStream_t stream);
 
 /* Fusion-buffer copy-out: dst[j] = group_f32[seg.offset + j] (bit copy) for
  * every segment; seg.ptr is the fp32 destination. Same segment rules as
- * grad_group_pack (group_numel bounds the offsets). */
+ * grad_group_pack (group_numel bounds the offsets); the destinations of
+ * non-empty segments must not overlap each other (FG_EINVAL), and a segment
+ * with no elements writes nothing. */
 fg_status grad_group_unpack(const float *group_f32, uint64_t group_numel,
                             const fg_segment *segs, int32_t nseg,
                             hipStream_t stream);

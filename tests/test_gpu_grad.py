@@ -184,3 +184,39 @@ def test_relu_backward_bit_exact():
     fg.relu_backward(dev(dy), dev(a), out)
     np.testing.assert_array_equal(host(out).view(np.uint16),
                                   G.relu_backward(dy, a).view(np.uint16))
+
+
+def test_empty_members():
+    """Members with no elements (allowed, null or not): pack copies the
+    others and zero-fills every uncovered element, the empty members
+    included; unpack writes only the non-empty destinations; a group of
+    empty members only packs to zeros and unpacks nothing."""
+    rng = np.random.default_rng(12)
+    numels = [0, 5, 0, 1000, 0]
+    srcs = [_rand16(rng, n) for n in numels]
+    offsets = [0, 8, 16, 24, 1030]
+    grp = {"members": list(range(5)), "offsets": offsets, "numel": 1040}
+    dsrc = [dev(s.view(np.int16)) if s.size else torch.empty(0, dtype=torch.int16,
+                                                              device="cuda")
+            for s in srcs]
+    gbuf = torch.full((1040,), 0x5555, dtype=torch.int16, device="cuda")
+    fg.grad_group_pack(dsrc, offsets, gbuf)
+    ref = G.pack(srcs, grp)
+    np.testing.assert_array_equal(host(gbuf).view(np.uint16), ref)
+    g32 = torch.empty(1040, dtype=torch.float32, device="cuda")
+    flag = torch.zeros(1, dtype=torch.int32, device="cuda")
+    fg.grad_unscale_check(gbuf, INV, g32, flag)
+    dsts = [torch.full((n,), float("nan"), dtype=torch.float32, device="cuda")
+            for n in numels]
+    fg.grad_group_unpack(g32, dsts, offsets)
+    r32, _ = G.unscale_check(ref, INV)
+    for m, v in G.unpack(r32, grp, numels).items():
+        np.testing.assert_array_equal(host(dsts[m]).view(np.uint32), v.view(np.uint32))
+    # only empty members
+    g2 = torch.full((64,), 0x5555, dtype=torch.int16, device="cuda")
+    empty = [torch.empty(0, dtype=torch.int16, device="cuda")] * 2
+    fg.grad_group_pack(empty, [0, 32], g2)
+    assert not host(g2).any()
+    e32 = [torch.empty(0, dtype=torch.float32, device="cuda")] * 2
+    fg.grad_group_unpack(torch.zeros(64, dtype=torch.float32, device="cuda"), e32, [0, 32])
+    torch.cuda.synchronize()
