@@ -125,6 +125,7 @@ COPY_KIB = 256 * 1024  # bytes read (and written) by `--op copy`, in KiB
 def short_kernel_name(name):
     """rocprofv3 kernel name -> the name fg.kernel_name() reports."""
     import re
+    name = name.replace("(anonymous namespace)::", "")
     name = name.split("(")[0].replace("void ", "")
     name = name.replace("fg::dma::", "").replace("fg::", "")
     # the pipeline configuration: dropped, except a tile size other than 256
@@ -635,6 +636,32 @@ STEP_STAT_REPS = 20
 NOMINAL_GFX_MHZ = 2400  # the clock the published MFMA peak assumes
 
 
+MFMA_LOOP_BLOCKS, MFMA_LOOP_ITERS = 512, 60000  # 2 waves per SIMD, ~15 ms a launch
+
+
+def mfma_loop_bench(seconds=2.0):
+    """The library's register-only MFMA loop (fg_mfma_loop, random fp16
+    operands about half zero) run back to back: the fp16 MFMA rate this GPU
+    sustains with no memory traffic, and its clock and power meanwhile."""
+    import torch
+
+    import paper_1909_11150_amd as fg
+    out = torch.empty(MFMA_LOOP_BLOCKS * 256, dtype=torch.float32, device="cuda")
+    fn = lambda: fg.mfma_loop(out, MFMA_LOOP_BLOCKS, MFMA_LOOP_ITERS)
+    for _ in range(3):
+        fn()
+    torch.cuda.synchronize()
+    ms, clk = sustained(fn, seconds)
+    work = MFMA_LOOP_BLOCKS * MFMA_LOOP_ITERS * fg.MFMA_LOOP_FLOPS_PER_BLOCK_ITER
+    tf = work / ms / 1e9
+    return {"tflops": round(tf, 1), "frac_of_peak": round(tf / MFMA_F16_PEAK_TFLOPS, 4),
+            "ms_per_launch": round(ms, 3), **clk,
+            "measured": f"fg_mfma_loop ({MFMA_LOOP_BLOCKS} workgroups of 4 waves, "
+                        f"{MFMA_LOOP_ITERS} iterations of 8 v_mfma_f32_32x32x16_f16 from "
+                        f"registers, random fp16 operands about half zero) back to back for "
+                        f"{seconds} s"}
+
+
 def ceiling_bench():
     """The practical MFMA ceiling of this GPU, beside the step:
     - clocks and socket power while the three-stream step runs back to back,
@@ -680,6 +707,10 @@ def ceiling_bench():
             for i in conv}
     del one, ch
     torch.cuda.empty_cache()
+    ml = mfma_loop_bench(4.0)
+    out["mfma_loop"] = {"ms": ml["ms_per_launch"], "tflops": ml["tflops"],
+                        **{k: ml[k] for k in ("samples", "gfx_MHz_median", "gfx_MHz_min",
+                                              "gfx_MHz_max", "socket_power_W_median")}}
     sq = 8192
     for key, zero_a in (("gemm_8192", False), ("gemm_8192_half_zero_a", True)):
         a = _operand(sq, sq, zero_a)
@@ -745,6 +776,8 @@ def summarize_ceiling(path):
           "| socket power median, W | samples |")
     print("|---|---:|---:|---:|---|---:|---:|")
     for k, name in (("step", "encoder-decoder step, 3 streams"),
+                    ("mfma_loop", "register-only MFMA loop (fg_mfma_loop), operands about "
+                                  "half zero"),
                     ("gemm_8192", "vendor GEMM 8192 x 8192 x 8192, dense N(0,1) operands"),
                     ("gemm_8192_half_zero_a", "the same, A about half zero")):
         if k not in d:
@@ -1286,6 +1319,9 @@ def main():
         out["grad_unpack_GBps"] = gp["unpack_GBps"]
         out["grad_path"] = gp
         out["small_configs"] = small_configs_bench()
+        ml = mfma_loop_bench()
+        out["mfma_loop"] = ml
+        out["value_frac_of_mfma_loop"] = round(out["value"] / ml["tflops"], 4)
     if not args.no_clocks:
         out["clocks"] = {"start": clocks_start, "end": gpu_clocks(),
                          "under_load": under_load,

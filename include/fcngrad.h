@@ -315,6 +315,23 @@ typedef struct {
 
 fg_status fg_lr_at(const fg_lr_schedule *s, int64_t k, double *lr);
 
+/* Measurement: the sustained fp16 MFMA rate of this GPU, the on-chip
+ * ceiling against which the convolutions' rates (Section 5.2, Sustained and
+ * Peak) can be read beside the nominal peak. Launches `blocks` workgroups of
+ * 4 waves; every wave runs `iters` iterations of 8 v_mfma_f32_32x32x16_f16
+ * from registers only (4 accumulator chains, no memory traffic in the loop),
+ * then each of its threads writes one float, the sum of its accumulators, to
+ * out[blockIdx * 256 + thread] (device, blocks * 256 floats, owned by the
+ * caller). Work: blocks * iters * 2^20 flops. Operands are hashed from the
+ * thread, operand and element indices, about half zero: operands = 0 gives
+ * random fp16 values in (-1, 1), which draw the power of real data;
+ * operands = 1 gives integers in -2..2, whose sums stay exact in fp32.
+ * FG_EINVAL for a null out, blocks or iters < 1, another operands value, or
+ * blocks * iters above FG_MFMA_LOOP_MAX_WORK (about 0.1 s of work). */
+#define FG_MFMA_LOOP_MAX_WORK (1LL << 28)
+fg_status fg_mfma_loop(float *out, int32_t blocks, int32_t iters, int32_t operands,
+                       hipStream_t stream);
+
 /* Profiling: the next convolution call (conv2d_fwd, conv2d_bwd_data,
  * conv2d_bwd_weight[_checked], conv_transpose2d_fwd) made on this host
  * thread records `start` on its stream just before its main kernel and

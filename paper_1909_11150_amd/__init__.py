@@ -29,8 +29,10 @@ ENTRY_POINTS = (
     "fg_lars_adam_workspace_bytes",
     "huber_head_grad", "avg_pool2d_fwd", "avg_pool2d_bwd", "channel_slice_copy",
     "grad_flags_clear", "fg_loss_scale_update", "fg_lr_at", "fg_profile_next_launch",
-    "conv2d_bwd_weight_noalloc",
+    "conv2d_bwd_weight_noalloc", "fg_mfma_loop",
 )
+MFMA_LOOP_MAX_WORK = 1 << 28  # blocks * iters accepted by fg_mfma_loop
+MFMA_LOOP_FLOPS_PER_BLOCK_ITER = 1 << 20
 NOALLOC_SCRATCH_BYTES = 64 << 20
 
 
@@ -123,6 +125,7 @@ def lib():
         "fg_lr_at": [ctypes.POINTER(LRScheduleParams), ctypes.c_int64,
                      ctypes.POINTER(ctypes.c_double)],
         "fg_profile_next_launch": [vp, vp],
+        "fg_mfma_loop": [vp, i32, i32, i32, vp],
         "huber_head_grad": [vp, vp, u64, ctypes.c_double, ctypes.c_double, vp, vp],
         "avg_pool2d_fwd": [vp, i32, i32, i32, i32, vp, vp],
         "avg_pool2d_bwd": [vp, vp, i32, i32, i32, i32, vp, vp],
@@ -387,6 +390,15 @@ def profile_next_launch(start, stop):
     a = None if start is None else start.cuda_event
     b = None if stop is None else stop.cuda_event
     _check("fg_profile_next_launch", lib().fg_profile_next_launch(a, b))
+
+
+def mfma_loop(out, blocks, iters, operands=0, stream=None):
+    """Register-only MFMA chains (fg_mfma_loop): out is a float32 device
+    tensor of at least blocks * 256 elements; blocks * iters * 2^20 flops."""
+    if (not out.is_floating_point() or out.element_size() != 4
+            or out.numel() < blocks * 256):
+        raise ValueError("fg_mfma_loop needs blocks * 256 float32 outputs")
+    _check("fg_mfma_loop", lib().fg_mfma_loop(_p(out), blocks, iters, operands, _s(stream)))
 
 
 def loss_scale_update(state, found_nonfinite):

@@ -1018,6 +1018,14 @@ fg_status fg_lr_at(const fg_lr_schedule *s, int64_t k, double *lr) {
 static thread_local hipEvent_t g_prof_start = nullptr;
 static thread_local hipEvent_t g_prof_stop = nullptr;
 
+fg_status fg_mfma_loop(float *out, int32_t blocks, int32_t iters, int32_t operands,
+                       hipStream_t stream) {
+  if (!out || blocks < 1 || iters < 1 || (operands != 0 && operands != 1) ||
+      (int64_t)blocks * iters > FG_MFMA_LOOP_MAX_WORK)
+    return FG_EINVAL;
+  return launch_status(launch_mfma_loop(out, blocks, iters, operands, stream));
+}
+
 fg_status fg_profile_next_launch(hipEvent_t start, hipEvent_t stop) {
   if (!start || !stop) {
     g_prof_start = g_prof_stop = nullptr;

@@ -155,6 +155,11 @@ hipError_t launch_head_wgrad(const uint16_t *x, const uint16_t *dy,
 hipError_t prof_begin(hipStream_t st);
 hipError_t prof_end(hipStream_t st);
 
+// Register-only MFMA chains (fg_mfma_loop): blocks x 256 threads, each
+// writing one float to out.
+hipError_t launch_mfma_loop(float *out, int32_t blocks, int32_t iters, int32_t mode,
+                            hipStream_t st);
+
 hipError_t launch_flags_clear(int32_t *flags, int32_t n, hipStream_t st);
 hipError_t launch_pack(const fg_segment *segs, int32_t nseg, uint16_t *group,
                        uint64_t group_numel, hipStream_t st);

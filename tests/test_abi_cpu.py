@@ -450,3 +450,19 @@ def test_plain_c_consumer_builds_and_plans(L, tmp_path):
     assert kv["kernel"] == fg.kernel_name(d, fg.OP_BWD_WEIGHT)
     assert kv["einval"] == "OK"
     assert kv["status"] == fg.status_string(fg.FG_EUNSUPPORTED)
+
+
+def test_mfma_loop_argument_checks(L):
+    """fg_mfma_loop rejects its bad arguments on the host (nothing is
+    launched; the pointer below is never dereferenced)."""
+    ok = fg.FG_EINVAL
+    assert L.fg_mfma_loop(None, 1, 1, 0, None) == ok
+    assert L.fg_mfma_loop(FAKE, 0, 1, 0, None) == ok
+    assert L.fg_mfma_loop(FAKE, 1, 0, 0, None) == ok
+    assert L.fg_mfma_loop(FAKE, 1, 1, 2, None) == ok
+    assert L.fg_mfma_loop(FAKE, 1 << 15, (fg.MFMA_LOOP_MAX_WORK >> 15) + 1, 0, None) == ok
+    import torch
+    with pytest.raises(ValueError):
+        fg.mfma_loop(torch.empty(255, dtype=torch.float32), 1, 1)
+    with pytest.raises(ValueError):
+        fg.mfma_loop(torch.empty(256, dtype=torch.float16), 1, 1)

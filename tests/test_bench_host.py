@@ -128,3 +128,18 @@ def test_ceiling_summary_prints_every_section(tmp_path, capsys):
            "| 1398.0 | 0.616 |" in out
     assert "| E1b.fwd | 65536 x 512 x 4608 | 226.9 |" in out
     assert out.rstrip().endswith("| 1.25 |")
+
+
+def test_kernel_names_from_the_trace_match_the_library_names():
+    """rocprofv3's demangled names map to the names fg_conv_kernel_name
+    reports: namespaces and arguments dropped, the pipeline configuration
+    dropped unless its tile is not 256, anonymous namespaces too."""
+    f = bench.short_kernel_name
+    assert f("void fg::dma::wgrad_dma_kernel<fg::dma::K<32, 4, 2, 4, 256>, true>"
+             "(fg::WgradArgs, fg::dma::WgradDiv, fg::dma::TileMap)") == "wgrad_dma_kernel<true>"
+    assert f("void fg::dma::data_conv_dma_kernel<fg::dma::K<32, 5, 2, 2, 128>, false, true>"
+             "(fg::DataConvArgs, fg::dma::TileMap)") == "data_conv_dma_kernel<128, false, true>"
+    assert f("fg::(anonymous namespace)::mfma_loop_kernel(float*, int, int)") == \
+        "mfma_loop_kernel"
+    assert f("fg::split_reduce_kernel(float const*, int, long, unsigned short*, int*)") == \
+        "split_reduce_kernel"
